@@ -1,0 +1,456 @@
+"""Plain CPU oracle of Sphinx's selective partial-denoising step.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import or run this module.  It shares
+no code with the HIP path (``paper_2511_18672_amd``) and imports nothing from
+it; the only module both sides use is ``workloads`` (seeded inputs, no method
+arithmetic).
+
+Everything is numpy in float64.  It is slow and meant to be checked by eye
+against the paper (Sphinx, arXiv 2511.18672):
+
+* Alg. 1 ("Sphinx Inference"), partial-denoising loop: noise is injected into
+  the clean latents at the start step (``add_noise``), the frames whose start
+  step has been reached form the active set ``A_u = 1[k <= u]``, and the
+  denoiser updates only the active frames (``D.partial_step``) restricted to
+  the mask ``M``.
+* Sec. 5.3 (spatially selective refinement): only positions inside the binary
+  mask are forwarded to the diffusion model; confident regions bypass the
+  partial denoising entirely and keep their values.
+* Sec. 3 (hybrid proposal): the regression output, with controlled noise
+  injected, replaces Gaussian-noise initialisation and partial denoising
+  removes the added noise.
+* Sec. 6: 1000-step training schedule sampled with 50 inference steps; opacity
+  threshold 0.5 with strict "below" comparison.
+
+Where the paper is silent (sampler, beta schedule, timestep spacing, denoiser
+architecture, threshold semantics, attention context), this module follows the
+readings listed in the design notes (sampler DDIM eta=0 with eps-prediction,
+linear betas 1e-4..2e-2, trailing grid from the start index, DiT-style adaLN
+blocks with (1+gate) residuals, strict ``u > thr`` with NaN unselected,
+attention over the selected tokens of one request).
+
+Precision modes:
+  ``precision="fp64"``  -- every value in float64 (the "truth").
+  ``precision="model"`` -- float64 arithmetic, but for a bf16 model the
+      operands that the model declares as bf16 are rounded to bf16
+      (round-to-nearest-even) exactly where the model stores them: the
+      adaLN-modulated LayerNorm outputs fed to the QKV and MLP1 GEMMs, q, k, v,
+      the attention output, and the GELU output fed to MLP2.  Weights and
+      latents are bf16 values already.  Residual stream, statistics, softmax,
+      conditioning, noise prediction and the DDIM update stay float64.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+T_TRAIN = 1000
+BETA_START = 1e-4
+BETA_END = 2e-2
+LN_EPS = 1e-6
+TEMB_DIM = 256
+TOKEN_DIM = 16
+
+
+# ----------------------------------------------------------------------------
+# number format: bfloat16 round-to-nearest-even on float64 data
+# ----------------------------------------------------------------------------
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Nearest bfloat16 value (ties to even) of each element, returned as float64.
+
+    bfloat16 keeps the float32 exponent and the top 7 stored mantissa bits.
+    The value is first rounded to float32 (RNE), then the low 16 bits of the
+    float32 pattern are rounded away with ties to even.  NaN stays NaN.
+    """
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    bits = f.view(np.uint32).astype(np.uint64)
+    lsb = (bits >> 16) & 1
+    rounded = ((bits + 0x7FFF + lsb) >> 16) << 16
+    out = rounded.astype(np.uint32).view(np.float32).astype(np.float64)
+    nan = np.isnan(f)
+    if nan.any():
+        out[nan] = np.nan
+    return out
+
+
+# ----------------------------------------------------------------------------
+# noise schedule and sampler (reading: linear betas, DDIM eta = 0)
+# ----------------------------------------------------------------------------
+def betas() -> np.ndarray:
+    """Linear beta schedule over the 1000 training timesteps."""
+    i = np.arange(T_TRAIN, dtype=np.float64)
+    return BETA_START + (BETA_END - BETA_START) * i / (T_TRAIN - 1)
+
+
+def alpha_bar() -> np.ndarray:
+    """Cumulative product of (1 - beta_i), i <= t, for t = 0..999."""
+    return np.cumprod(1.0 - betas())
+
+
+def abar_at(t: int, ab: Optional[np.ndarray] = None) -> float:
+    """alpha_bar at timestep t; t = -1 denotes the clean end point (alpha_bar = 1)."""
+    if t < 0:
+        return 1.0
+    ab = alpha_bar() if ab is None else ab
+    return float(ab[t])
+
+
+def timestep_grid(s_max: int, n: int) -> List[int]:
+    """The n+1 timesteps visited by n steps starting at index s_max.
+
+    tau_i = floor((n - i)(s_max + 1) / n) - 1, so tau_0 = s_max and tau_n = -1.
+    At s_max = 499, n = 25 this is the last 25 entries of a 50-step grid with
+    spacing 20 (the paper's S = 50 with refinement starting at k = 25).
+    """
+    return [((n - i) * (s_max + 1)) // n - 1 for i in range(n + 1)]
+
+
+def injection_coeffs(t: int, ab=None):
+    """(a, b) with add_noise(z0, t) = a*z0 + b*eps: a = sqrt(abar_t), b = sqrt(1 - abar_t)."""
+    a_t = abar_at(t, ab)
+    return np.sqrt(a_t), np.sqrt(1.0 - a_t)
+
+
+def ddim_coeffs(t: int, t_next: int, ab=None):
+    """(c1, c2) of the deterministic DDIM update x' = c1*x + c2*eps_hat.
+
+    x0_hat = (x - sqrt(1-abar)*eps_hat)/sqrt(abar);
+    x'     = sqrt(abar')*x0_hat + sqrt(1-abar')*eps_hat.
+    """
+    a, an = abar_at(t, ab), abar_at(t_next, ab)
+    c1 = np.sqrt(an / a)
+    c2 = np.sqrt(1.0 - an) - np.sqrt(an * (1.0 - a) / a)
+    return c1, c2
+
+
+@dataclass
+class StepPlan:
+    active: np.ndarray  # bool [G]
+    newly: np.ndarray  # bool [G]
+    tau: np.ndarray  # int [G] (timestep of the frame's request at this step; -1 if idle)
+    a: np.ndarray  # float64 [G]
+    b: np.ndarray
+    c1: np.ndarray
+    c2: np.ndarray
+
+
+def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Sequence[int]) -> List[StepPlan]:
+    """Per-step, per-frame schedule (Alg. 1 loop with a per-frame start step).
+
+    Each request walks its own grid from s_max = max of its frames' start
+    indices.  Frame f is active at step i iff tau_i <= s_f (it has reached its
+    own start); on its first active step it is newly active and receives
+    add_noise at level tau_i.  A request takes part in global step i iff
+    i < nsteps[r].
+    """
+    ab = alpha_bar()
+    G = int(sum(frames_per_req))
+    total = int(max(nsteps))
+    out = []
+    for i in range(total):
+        p = StepPlan(np.zeros(G, bool), np.zeros(G, bool), np.full(G, -1, np.int64),
+                     np.ones(G), np.zeros(G), np.ones(G), np.zeros(G))
+        g0 = 0
+        for r, F in enumerate(frames_per_req):
+            n = int(nsteps[r])
+            if i < n:
+                s = s_start[g0:g0 + F]
+                grid = timestep_grid(int(max(s)), n)
+                t, tn = grid[i], grid[i + 1]
+                c1, c2 = ddim_coeffs(t, tn, ab)
+                for f in range(F):
+                    g = g0 + f
+                    p.tau[g] = t
+                    if t <= s[f]:
+                        p.active[g] = True
+                        p.newly[g] = (i == 0) or (grid[i - 1] > s[f])
+                        p.c1[g], p.c2[g] = c1, c2
+                        if p.newly[g]:
+                            p.a[g], p.b[g] = injection_coeffs(t, ab)
+            g0 += F
+        out.append(p)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# token geometry
+# ----------------------------------------------------------------------------
+@dataclass
+class TokenInfo:
+    req: np.ndarray  # request of each token
+    gframe: np.ndarray  # global frame index
+    f: np.ndarray  # frame index inside its request
+    y: np.ndarray
+    x: np.ndarray
+
+
+def token_info(requests) -> TokenInfo:
+    req, gfr, ff, yy, xx = [], [], [], [], []
+    g0 = 0
+    for r, q in enumerate(requests):
+        hp, wp = q.h // 2, q.w // 2
+        f, y, x = np.meshgrid(np.arange(q.frames), np.arange(hp), np.arange(wp), indexing="ij")
+        req.append(np.full(f.size, r))
+        gfr.append(g0 + f.ravel())
+        ff.append(f.ravel())
+        yy.append(y.ravel())
+        xx.append(x.ravel())
+        g0 += q.frames
+    cat = lambda a: np.concatenate(a).astype(np.int64)
+    return TokenInfo(cat(req), cat(gfr), cat(ff), cat(yy), cat(xx))
+
+
+def patchify(latent: np.ndarray, requests) -> np.ndarray:
+    """NCHW latents of all requests -> [N][16] token rows, value order c*4 + py*2 + px."""
+    rows, e0 = [], 0
+    for q in requests:
+        n = q.frames * 4 * q.h * q.w
+        z = np.asarray(latent[e0:e0 + n], dtype=np.float64).reshape(q.frames, 4, q.h // 2, 2, q.w // 2, 2)
+        rows.append(z.transpose(0, 2, 4, 1, 3, 5).reshape(-1, TOKEN_DIM))
+        e0 += n
+    return np.concatenate(rows, axis=0)
+
+
+def unpatchify(tokens: np.ndarray, requests) -> np.ndarray:
+    """Inverse of patchify."""
+    out, t0 = [], 0
+    for q in requests:
+        n = q.frames * (q.h // 2) * (q.w // 2)
+        z = tokens[t0:t0 + n].reshape(q.frames, q.h // 2, q.w // 2, 4, 2, 2)
+        out.append(z.transpose(0, 3, 1, 4, 2, 5).ravel())
+        t0 += n
+    return np.concatenate(out)
+
+
+# ----------------------------------------------------------------------------
+# mask and compaction (Sec. 5.3 mask; Alg. 1 opacity mask 1[O < tau_o])
+# ----------------------------------------------------------------------------
+def select(u: np.ndarray, thr_tok: np.ndarray, active_tok: np.ndarray, tok_offset: np.ndarray):
+    """Selected-token mask and its stable compaction.
+
+    mask[t] = active(t) and u[t] > thr(t)  (strict; NaN compares false).
+    idx     = ascending positions with mask = 1.
+    cu_sel  = number of selected tokens before each request boundary.
+    """
+    mask = np.logical_and(active_tok, np.asarray(u) > np.asarray(thr_tok))
+    idx = np.flatnonzero(mask).astype(np.int64)
+    cu = np.array([np.count_nonzero(mask[:o]) for o in tok_offset], dtype=np.int64)
+    return mask, idx, cu, int(idx.size)
+
+
+# ----------------------------------------------------------------------------
+# denoiser pieces
+# ----------------------------------------------------------------------------
+def linear(x, w, b):
+    """y = x W^T + b with W stored [out][in]."""
+    return x @ np.asarray(w, np.float64).T + np.asarray(b, np.float64)
+
+
+def silu(z):
+    return z / (1.0 + np.exp(-z))
+
+
+def gelu_tanh(z):
+    return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+
+
+def layer_norm(h):
+    """Normalise each row to zero mean and unit (biased) variance, eps 1e-6, no affine."""
+    mu = h.mean(axis=-1, keepdims=True)
+    var = ((h - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (h - mu) / np.sqrt(var + LN_EPS)
+
+
+def timestep_embedding(tau: np.ndarray) -> np.ndarray:
+    """[len(tau)][256]: cos(tau*w_k) for k < 128, then sin(tau*w_k); w_k = 10^4^(-k/128)."""
+    half = TEMB_DIM // 2
+    w = np.exp(-np.log(1e4) * np.arange(half) / half)
+    arg = np.asarray(tau, np.float64)[:, None] * w[None, :]
+    return np.concatenate([np.cos(arg), np.sin(arg)], axis=1)
+
+
+def position_embedding(f, y, x, D: int) -> np.ndarray:
+    """[n][D]: [Ty(y) || Tx(x)] + Tf(f).
+
+    Ty(y) = [sin(y v_k)]_{k<D/4} || [cos(y v_k)]_{k<D/4}, v_k = 10^4^(-k/(D/4)); Tx likewise
+    over x; Tf(f) = [sin(f m_k)]_{k<D/2} || [cos(f m_k)]_{k<D/2}, m_k = 10^4^(-k/(D/2)).
+    """
+    q = D // 4
+    nu = 1e4 ** (-np.arange(q) / q)
+    mu = 1e4 ** (-np.arange(D // 2) / (D // 2))
+    ay = np.asarray(y, np.float64)[:, None] * nu
+    ax = np.asarray(x, np.float64)[:, None] * nu
+    af = np.asarray(f, np.float64)[:, None] * mu
+    spatial = np.concatenate([np.sin(ay), np.cos(ay), np.sin(ax), np.cos(ax)], axis=1)
+    return spatial + np.concatenate([np.sin(af), np.cos(af)], axis=1)
+
+
+def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048):
+    """Non-causal softmax(q k^T / sqrt(d)) v per head, each query attending to
+    the keys of its own segment only (segments = contiguous row ranges seg[r]..seg[r+1])."""
+    n, D = q.shape
+    d = D // heads
+    scale = 1.0 / np.sqrt(d)
+    out = np.zeros((n, D))
+    for r in range(len(seg) - 1):
+        s0, s1 = int(seg[r]), int(seg[r + 1])
+        if s1 <= s0:
+            continue
+        for h in range(heads):
+            cols = slice(h * d, (h + 1) * d)
+            kh, vh = k[s0:s1, cols], v[s0:s1, cols]
+            for c0 in range(s0, s1, chunk):
+                c1 = min(s1, c0 + chunk)
+                s = (q[c0:c1, cols] @ kh.T) * scale
+                s -= s.max(axis=1, keepdims=True)
+                p = np.exp(s)
+                p /= p.sum(axis=1, keepdims=True)
+                out[c0:c1, cols] = p @ vh
+    return out
+
+
+@dataclass
+class Model:
+    D: int
+    heads: int
+    mlp: int
+    L: int
+    dtype: str
+    weights: Dict[str, np.ndarray]
+
+
+def model_from_workload(wl) -> Model:
+    m = wl.model
+    return Model(m.D, m.heads, m.mlp, m.L, m.dtype, wl.weights)
+
+
+def conditioning(model: Model, tau: np.ndarray) -> np.ndarray:
+    """c = W_t2 SiLU(W_t1 temb(tau) + b_t1) + b_t2, one row per timestep."""
+    w = model.weights
+    return linear(silu(linear(timestep_embedding(tau), w["t1_w"], w["t1_b"])), w["t2_w"], w["t2_b"])
+
+
+def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.ndarray,
+            precision: str = "model") -> np.ndarray:
+    """Noise prediction eps_hat [n][16] for packed tokens x [n][16].
+
+    Tokens carry their in-request frame f, grid position (y, xx) and their
+    frame's timestep tau_tok; attention runs inside each segment.
+    """
+    w = model.weights
+    D, H = model.D, model.heads
+    rnd = round_bf16 if (precision == "model" and model.dtype == "bf16") else (lambda a: a)
+    # conditioning, per distinct timestep (identical for equal timesteps)
+    taus, inv = np.unique(np.asarray(tau_tok), return_inverse=True)
+    c = silu(conditioning(model, taus))
+    h = linear(x, w["pe_w"], w["pe_b"]) + position_embedding(f, y, xx, D)
+    for l in range(model.L):
+        mod = linear(c, w[f"b{l}.ada_w"], w[f"b{l}.ada_b"])[inv]
+        sh1, sc1, g1, sh2, sc2, g2 = (mod[:, i * D:(i + 1) * D] for i in range(6))
+        a = rnd(layer_norm(h) * (1.0 + sc1) + sh1)
+        qkv = linear(a, w[f"b{l}.qkv_w"], w[f"b{l}.qkv_b"])
+        q, k, v = rnd(qkv[:, :D]), rnd(qkv[:, D:2 * D]), rnd(qkv[:, 2 * D:])
+        o = rnd(attention(q, k, v, H, seg))
+        h = h + (1.0 + g1) * linear(o, w[f"b{l}.o_w"], w[f"b{l}.o_b"])
+        a2 = rnd(layer_norm(h) * (1.0 + sc2) + sh2)
+        m = rnd(gelu_tanh(linear(a2, w[f"b{l}.fc1_w"], w[f"b{l}.fc1_b"])))
+        h = h + (1.0 + g2) * linear(m, w[f"b{l}.fc2_w"], w[f"b{l}.fc2_b"])
+    fm = linear(c, w["fada_w"], w["fada_b"])[inv]
+    shf, scf = fm[:, :D], fm[:, D:]
+    return linear(layer_norm(h) * (1.0 + scf) + shf, w["out_w"], w["out_b"])
+
+
+# ----------------------------------------------------------------------------
+# one step and the whole refinement loop
+# ----------------------------------------------------------------------------
+@dataclass
+class StepResult:
+    mask: np.ndarray
+    idx: np.ndarray
+    cu_sel: np.ndarray
+    n_sel: int
+    x_in: np.ndarray  # gathered (and injected) token rows
+    eps_hat: np.ndarray
+    x_out: np.ndarray  # after the DDIM update
+    state: np.ndarray  # NCHW state after scatter
+
+
+def per_token(values_per_frame: np.ndarray, info: TokenInfo) -> np.ndarray:
+    return np.asarray(values_per_frame)[info.gframe]
+
+
+def step(wl, model: Model, state: np.ndarray, plan: StepPlan, precision: str = "model",
+         denoiser=None, info: Optional[TokenInfo] = None) -> StepResult:
+    """One partial-denoising step: select, compact, gather(+inject), denoise, DDIM, scatter."""
+    info = token_info(wl.requests) if info is None else info
+    tok_off = wl.tok_offset
+    mask, idx, cu, n = select(wl.u, per_token(wl.thr, info), per_token(plan.active, info), tok_off)
+    state = np.array(state, dtype=np.float64, copy=True)
+    if n == 0:
+        z = np.zeros((0, TOKEN_DIM))
+        return StepResult(mask, idx, cu, 0, z, z, z, state)
+    P = patchify(state, wl.requests)
+    E = patchify(wl.eps, wl.requests)
+    g = info.gframe[idx]
+    a, b = plan.a[g][:, None], plan.b[g][:, None]
+    x = a * P[idx] + b * E[idx]
+    seg = np.concatenate([cu, [n]])
+    den = denoiser or denoise
+    eps_hat = den(model, x, info.f[idx], info.y[idx], info.x[idx], plan.tau[g], seg, precision)
+    x_out = plan.c1[g][:, None] * x + plan.c2[g][:, None] * eps_hat
+    P[idx] = x_out
+    return StepResult(mask, idx, cu, n, x, eps_hat, x_out, unpatchify(P, wl.requests))
+
+
+def refine(wl, precision: str = "model", denoiser=None, trace: bool = False, steps: Optional[int] = None):
+    """Run the whole partial-denoising loop; returns the final NCHW state (float64)
+    and, with trace=True, the list of per-step results."""
+    model = model_from_workload(wl)
+    plans = plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    info = token_info(wl.requests)
+    state = np.asarray(wl.z0, dtype=np.float64).copy()
+    out = []
+    for i, p in enumerate(plans[: steps if steps is not None else len(plans)]):
+        res = step(wl, model, state, p, precision, denoiser, info)
+        state = res.state
+        if trace:
+            out.append(res)
+    return (state, out) if trace else state
+
+
+def refine_dense(wl, precision: str = "model", denoiser=None):
+    """Dense partial denoising of every token of every frame, with no mask, no
+    gather and no scatter: the whole latent is noised at the start step and the
+    denoiser sees all tokens of each request.  Defined for workloads whose frames
+    of a request share one start index."""
+    model = model_from_workload(wl)
+    info = token_info(wl.requests)
+    ab = alpha_bar()
+    P = patchify(wl.z0, wl.requests)
+    E = patchify(wl.eps, wl.requests)
+    seg = np.asarray(wl.tok_offset, dtype=np.int64)
+    g0, t0 = 0, 0
+    grids = []
+    for r, q in enumerate(wl.requests):
+        s = wl.s_start[g0:g0 + q.frames]
+        assert (s == s[0]).all(), "dense path needs one start index per request"
+        grids.append(timestep_grid(int(s[0]), int(wl.nsteps[r])))
+        a, b = injection_coeffs(grids[-1][0], ab)
+        P[t0:t0 + q.tokens] = a * P[t0:t0 + q.tokens] + b * E[t0:t0 + q.tokens]
+        g0 += q.frames
+        t0 += q.tokens
+    den = denoiser or denoise
+    for i in range(int(max(wl.nsteps))):
+        live = [r for r in range(wl.R) if i < wl.nsteps[r]]
+        rows = np.concatenate([np.arange(seg[r], seg[r + 1]) for r in live])
+        tau = np.array([grids[r][i] for r in range(wl.R)])[info.req[rows]]
+        sub = np.concatenate([[0], np.cumsum([seg[r + 1] - seg[r] for r in live])])
+        eps_hat = den(model, P[rows], info.f[rows], info.y[rows], info.x[rows], tau, sub, precision)
+        c = np.array([ddim_coeffs(grids[r][i], grids[r][i + 1], ab) if i < wl.nsteps[r] else (1.0, 0.0)
+                      for r in range(wl.R)])
+        c1, c2 = c[info.req[rows], 0][:, None], c[info.req[rows], 1][:, None]
+        P[rows] = c1 * P[rows] + c2 * eps_hat
+    return unpatchify(P, wl.requests)
