@@ -1,0 +1,186 @@
+"""Throughput of the selective partial-denoising step on one MI355X.
+
+A step is one pass of the whole hot path over one batch: select + compact the
+mask, gather with noise injection, the denoiser on the gathered tokens with the
+DDIM update, and scatter back (all through the C ABI of libsphinx.so).  The
+default workload is the headline configuration: 14 frames of a 4x72x128 bf16
+latent (576x1024 views), 32256 tokens, Gaussian-blob uncertainty, 30 %
+selected (9677 tokens), a 12-block D=1024 denoiser with 16 heads of 64 and an
+MLP of 4096, 25 DDIM steps from t_start 0.5; step k runs schedule step
+k mod 25.  Inputs are seeded synthetic latents and random-init weights.
+
+Prints one JSON line: refined tokens*steps/s over the timed steps, the roofline
+of the dominant kernel (attention) from HIP events recorded on its stream over
+the timed region, per-kernel-class times, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+METRIC = "refined tokens·steps/s + MFMA util, 14-frame 576×1024 latent, 30% selected"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=25)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="headline", choices=["headline", "small", "frame_region", "batched"])
+    ap.add_argument("--rho", type=float, default=None, help="selected fraction (headline only)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--select-every-step", type=int, default=1,
+                    help="1: run mask+compaction in every step (default); 0: only when the active set changes")
+    return ap.parse_args()
+
+
+def traffic_entry(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source (else None)."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("|") and line.count("|") >= 3:
+            parts = [p.strip() for p in line.strip().strip("|").split("|")]
+            if len(parts) >= 2:
+                fields[parts[0]] = parts[1]
+    src = os.path.join(ROOT, "paper_2511_18672_amd", "csrc", fields.get("source", "attention.hip"))
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16] if os.path.exists(src) else None
+    if fields.get("source_sha256_16") != digest:
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl) -> dict:
+    """The oracle (numpy fp64, unmodified) on a bounded sample: one step of the
+    same workload through a one-block denoiser, scaled to the full depth."""
+    import oracle as O
+    import workloads as W
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        cores = max([d.get("num_threads", 1) for d in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    m = wl.model
+    one = W.ModelCfg(D=m.D, heads=m.heads, head_dim=m.head_dim, mlp=m.mlp, L=1, dtype=m.dtype)
+    sample = W.Workload(name=wl.name, model=one, requests=wl.requests, u=wl.u, thr=wl.thr, s_start=wl.s_start,
+                        nsteps=wl.nsteps, z0=wl.z0, eps=wl.eps,
+                        weights={k: v for k, v in wl.weights.items() if not k.startswith("b") or k.startswith("b0.")})
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    model = O.model_from_workload(sample)
+    t0 = time.perf_counter()
+    res = O.step(sample, model, wl.z0, plans[0], "model")
+    dt = time.perf_counter() - t0
+    per_step = dt * m.L  # blocks dominate; embedding and final projection counted L times (conservative)
+    return {"value": res.n_sel / per_step, "unit": "refined tokens·steps/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"one step ({res.n_sel} selected tokens) through a 1-block copy of the denoiser, "
+                      f"{dt:.1f} s, scaled x{m.L} blocks"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              f"(the selective-refinement step is built and measured on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2511_18672_amd as S
+    import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.config == "headline":
+        wl = W.headline(rho=args.rho) if args.rho is not None else W.headline()
+    else:
+        wl = W.CONFIGS[args.config]()
+    t_setup = time.perf_counter()
+    R = S.from_workload(wl)
+    R.reset()
+    stream = torch.cuda.current_stream()
+    force = bool(args.select_every_step)
+    for i in range(args.warmup):
+        R.step(i, force_select=force)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    S.sphinx_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    refined = 0
+    for i in range(args.warmup, args.warmup + args.steps):
+        refined += R.step(i, force_select=force)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    timing = S.sphinx_timing_read()
+    S.sphinx_timing_enable(False)
+
+    ms_per_step = 1e3 * wall / args.steps
+    value = refined / wall
+    n = R.n_sel
+    D, L, mlp = wl.model.D, wl.model.L, wl.model.mlp
+    cu = R.cu_host
+    seg = np.diff(cu).astype(np.float64)
+    attn_flop = 4.0 * D * float((seg ** 2).sum())
+    gemm_flop = {"gemm_qkv": 2.0 * n * D * 3 * D, "gemm_out": 2.0 * n * D * D, "gemm_mlp1": 2.0 * n * D * mlp,
+                 "gemm_mlp2": 2.0 * n * mlp * D}
+    kernels = {}
+    for k, (cnt, ms) in timing.items():
+        if cnt == 0:
+            continue
+        avg_us = 1e3 * ms / cnt
+        e = {"launches": cnt, "avg_us": round(avg_us, 2), "ms_per_step": round(ms / args.steps, 4)}
+        if k == "attention":
+            e["tflops"] = round(attn_flop / (avg_us * 1e-6) / 1e12, 1)
+        if k in gemm_flop:
+            e["tflops"] = round(gemm_flop[k] / (avg_us * 1e-6) / 1e12, 1)
+        kernels[k] = e
+    cnt, ms = timing["attention"]
+    avg_s = ms / cnt / 1e3
+    achieved = attn_flop / avg_s / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_entry("attention", args.config),
+                "kernel": "k_attn_bf16 (varlen flash attention, head_dim 64)",
+                "algorithmic_flop_per_launch": attn_flop}
+    step_flop = L * (attn_flop + sum(gemm_flop.values()))
+    mfma_util = step_flop / (ms_per_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
+
+    out = {"metric": METRIC, "value": round(value, 1), "unit": "refined tokens·steps/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded latents, blob uncertainty map, random-init weights)",
+           "config": {"workload": f"{wl.name}: {wl.G} frames, {wl.N} tokens, {n} selected, "
+                                  f"D{D} H{wl.model.heads}x{wl.model.head_dim} L{L} MLP{mlp}, "
+                                  f"{int(wl.max_steps)}-step DDIM schedule",
+                      "selected_tokens": int(n), "tokens": int(wl.N), "select_every_step": force},
+           "mfma_util_step": round(mfma_util, 4),
+           "roofline": roofline, "kernels": kernels, "setup_s": round(setup_s, 1)}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

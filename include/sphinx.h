@@ -1,0 +1,221 @@
+/*
+ * sphinx.h -- C ABI of the selective partial-denoising step on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The library implements the inner loop of Sphinx's inference algorithm
+ * (Sphinx, arXiv 2511.18672, Alg. 1 "Sphinx Inference", partial-denoising
+ * loop; Sec. 5.3 spatially selective refinement): a per-token uncertainty map
+ * is thresholded into a binary mask, the selected latent tokens are
+ * stream-compacted and gathered with noise injected at the frame's start step,
+ * the transformer denoiser runs on the gathered tokens only, the DDIM update is
+ * applied, and the result is scattered back while unselected tokens keep their
+ * values.  Sampler, schedule and denoiser architecture are not fixed by the
+ * paper; the library uses deterministic DDIM (eta = 0, eps-prediction), a
+ * linear beta schedule 1e-4..2e-2 over 1000 steps and a DiT-style adaLN
+ * transformer with joint attention over the selected tokens of each request.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Plain C types only.  Pointers marked "dev" are device (HBM) pointers,
+ *    "host" are host pointers.  `stream` is a hipStream_t passed as void*
+ *    (NULL = the default stream).  Every call only enqueues work on `stream`
+ *    unless stated otherwise.
+ *  - The caller owns every buffer.  No call allocates device memory; scratch
+ *    space comes from a caller-provided workspace whose size a *_bytes query
+ *    returns.  Device pointers must be 16-byte aligned.
+ *  - Requests are concatenated.  Request r covers global tokens
+ *    [tok_offset, tok_offset + frames*(h/2)*(w/2)) and global frames
+ *    [frame_offset, frame_offset + frames); both offsets must equal the running
+ *    sums over the preceding requests.  At most SPHINX_MAX_REQUESTS requests.
+ *  - Token t of a request is t = f*(h/2)*(w/2) + y*(w/2) + x (patch 2x2).
+ *    Latents are NCHW per request, [frames][4][h][w], request r starting at
+ *    element 16*tok_offset.  A token's 16 values are ordered c*4 + py*2 + px.
+ *  - Arguments are validated before any HIP call, so every error path is
+ *    reachable without a GPU; an invalid call enqueues nothing.  No exception
+ *    or abort crosses the ABI.  SPHINX_E_HIP reports a failed launch or copy.
+ */
+#ifndef SPHINX_H
+#define SPHINX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPHINX_MAX_REQUESTS 64
+#define SPHINX_TOKEN_DIM 16 /* 4 latent channels x 2 x 2 patch */
+#define SPHINX_TEMB_DIM 256 /* sinusoidal timestep embedding width */
+#define SPHINX_TRAIN_STEPS 1000
+
+typedef enum {
+  SPHINX_OK = 0,
+  SPHINX_E_INVALID = 1,     /* null required pointer, bad size, misalignment, inconsistent offsets */
+  SPHINX_E_UNSUPPORTED = 2, /* valid but not implemented (head_dim, dtype, sizes) */
+  SPHINX_E_WORKSPACE = 3,   /* workspace too small */
+  SPHINX_E_HIP = 4          /* a HIP launch or copy failed */
+} sphinx_status;
+
+typedef enum { SPHINX_F32 = 0, SPHINX_BF16 = 1 } sphinx_dtype;
+
+typedef struct {
+  int32_t frames;       /* F >= 1 */
+  int32_t h, w;         /* latent height and width, even, h/2 and w/2 <= 1024 */
+  int32_t frame_offset; /* first global frame of the request */
+  int64_t tok_offset;   /* first global token of the request */
+} sphinx_request;
+
+/* Denoiser description.  `weights` is a caller-owned device blob whose layout
+ * sphinx_model_param() defines; it is only read. */
+typedef struct {
+  int32_t D;        /* hidden size, = heads * head_dim */
+  int32_t heads;
+  int32_t head_dim; /* 64 for bf16 models; 16..64 for f32 models */
+  int32_t mlp;      /* MLP hidden size */
+  int32_t L;        /* number of blocks */
+  sphinx_dtype dtype; /* storage and GEMM-operand type of weights/activations */
+  const void* weights; /* dev */
+} sphinx_model_desc;
+
+/* Parameter tensors of the blob.  Matrices are row-major [out][in]
+ * (y = x W^T + b).  The adaLN projections of all blocks and the final adaLN
+ * projection are stored as one matrix COND_W [(6L+2)D][D]: rows
+ * [6D*l, 6D*(l+1)) belong to block l and give (shift1, scale1, gate1, shift2,
+ * scale2, gate2); the last 2D rows give the final (shift, scale). */
+typedef enum {
+  SPHINX_P_PE_W = 0,  /* [D][16]     patch embedding */
+  SPHINX_P_PE_B,      /* [D] */
+  SPHINX_P_T1_W,      /* [D][256]    timestep MLP, first layer */
+  SPHINX_P_T1_B,      /* [D] */
+  SPHINX_P_T2_W,      /* [D][D]      timestep MLP, second layer */
+  SPHINX_P_T2_B,      /* [D] */
+  SPHINX_P_COND_W,    /* [(6L+2)D][D] adaLN projections, all blocks + final */
+  SPHINX_P_COND_B,    /* [(6L+2)D] */
+  SPHINX_P_QKV_W,     /* per block [3D][D] */
+  SPHINX_P_QKV_B,     /* per block [3D] */
+  SPHINX_P_O_W,       /* per block [D][D] */
+  SPHINX_P_O_B,       /* per block [D] */
+  SPHINX_P_FC1_W,     /* per block [mlp][D] */
+  SPHINX_P_FC1_B,     /* per block [mlp] */
+  SPHINX_P_FC2_W,     /* per block [D][mlp] */
+  SPHINX_P_FC2_B,     /* per block [D] */
+  SPHINX_P_OUT_W,     /* [16][D]     final projection to the noise prediction */
+  SPHINX_P_OUT_B,     /* [16] */
+  SPHINX_P_COUNT
+} sphinx_param;
+
+/* Human-readable name of a status code (static string). */
+const char* sphinx_status_string(sphinx_status s);
+
+/* Total blob size in bytes for a model description (weights pointer ignored). */
+sphinx_status sphinx_model_blob_bytes(const sphinx_model_desc* m, size_t* bytes);
+
+/* Byte offset and element count of parameter `p` (of block `block` for the
+ * per-block tensors, block ignored otherwise).  Every tensor starts on a
+ * 256-byte boundary; elements have the model dtype. */
+sphinx_status sphinx_model_param(const sphinx_model_desc* m, sphinx_param p, int32_t block,
+                                 size_t* offset_bytes, size_t* count);
+
+/* Schedule of step `step` (0-based) for all frames, computed on the host in
+ * double precision (Alg. 1 partial-denoising loop with per-frame start steps).
+ * Request r walks the timestep grid tau_i = floor((n-i)(s+1)/n) - 1,
+ * i = 0..n (n = nsteps[r], s = the largest start index among its frames),
+ * with alpha_bar(-1) = 1.  Frame f is active at step i iff tau_i <= s_f and
+ * i < n; on its first active step it is newly active and add_noise applies
+ * a = sqrt(abar(tau_i)), b = sqrt(1 - abar(tau_i)); otherwise a = 1, b = 0.
+ * The DDIM coefficients of the step are c1 = sqrt(abar'/abar) and
+ * c2 = sqrt(1-abar') - sqrt(abar'(1-abar)/abar) with abar = abar(tau_i),
+ * abar' = abar(tau_{i+1}).  Outputs are host arrays [G] (G = total frames):
+ * active/newly (0/1), tau (timestep fed to the denoiser), a, b, c1, c2.
+ * Inactive frames get tau of their request's step (or -1 when the request has
+ * finished), a = 1, b = 0, c1 = 1, c2 = 0.  Pure host code. */
+sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int32_t* s_start /*host[G]*/,
+                               const int32_t* nsteps /*host[R]*/, int32_t step, uint8_t* active,
+                               uint8_t* newly, int32_t* tau, float* a, float* b, float* c1, float* c2);
+
+/* Workspace bytes needed by sphinx_select_mask for N tokens. */
+sphinx_status sphinx_select_workspace_bytes(int64_t N, size_t* bytes);
+
+/* Selection mask and its stable compaction (Alg. 1 opacity mask
+ * 1[O < tau_o] with u = -O; Sec. 5.3: only masked positions are forwarded).
+ *   mask[t] = active[frame(t)] && (uncert[t] > thr[frame(t)])   (strict, NaN -> 0)
+ *   idx[0..n_sel)  = the selected t in ascending order,
+ *   cu_sel[r]      = number of selected tokens before request r, cu_sel[R] = n_sel.
+ * uncert: dev float [N]; thr: dev float [G]; active: dev uint8 [G] or NULL (all
+ * active); mask: dev uint8 [N] out; idx: dev int32 [N] out; cu_sel: dev int32
+ * [R+1] out.  If cu_sel_host (host int32 [R+1]) is non-NULL the call copies
+ * cu_sel back and synchronizes `stream` once (its only host synchronization).
+ * Bit-exact and deterministic. */
+sphinx_status sphinx_select_mask(const sphinx_request* reqs, int32_t R, const float* uncert, const float* thr,
+                                 const uint8_t* active, uint8_t* mask, int32_t* idx, int32_t* cu_sel,
+                                 int32_t* cu_sel_host, void* ws, size_t ws_bytes, void* stream);
+
+/* Gather with noise injection (Alg. 1 add_noise on the selected tokens).
+ *   x_sel[j][k] = a[g] * z[k] + b[g] * eps[k]   for token idx[j] of frame g,
+ * z and eps read from the NCHW latents `state` / `eps` (dtype f32 or bf16).
+ * eps may be NULL: then the noise term is dropped.  a, b: dev float [G];
+ * idx: dev int32 [n_sel]; x_sel: dev float [n_sel][16] out.  n_sel = 0 is a
+ * no-op.  Every idx[j] must lie in [0, N). */
+sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, const void* state, sphinx_dtype state_dtype,
+                            const void* eps, sphinx_dtype eps_dtype, const int32_t* idx, int32_t n_sel,
+                            const float* a, const float* b, float* x_sel, void* stream);
+
+/* Workspace bytes of sphinx_refine_step for up to max_sel selected tokens. */
+sphinx_status sphinx_refine_workspace_bytes(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                            int64_t max_sel, size_t* bytes);
+
+/* One denoiser pass over the gathered tokens plus the DDIM update,
+ * in place on x_sel (Alg. 1 D.partial_step on the masked tokens).
+ *   eps_hat = Denoiser(x_sel, positions, tau);  x_sel <- c1[g] x_sel + c2[g] eps_hat
+ * Attention is non-causal over the selected tokens of the same request:
+ * rows [cu_sel_host[r], cu_sel_host[r+1]) form segment r.  idx: dev int32
+ * [n_sel] (positions of the rows); tau: dev int32 [G] timestep per frame;
+ * c1, c2: dev float [G]; x_sel: dev float [n_sel][16] in/out; cu_sel_host:
+ * host int32 [R+1] with cu_sel_host[R] = n_sel.  n_sel = 0 is a no-op.
+ * bf16 models compute GEMMs and attention with bf16 operands and fp32
+ * accumulation; residual stream, statistics, softmax and the update are fp32. */
+sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                 const int32_t* idx, int32_t n_sel, const int32_t* cu_sel_host,
+                                 const int32_t* tau, const float* c1, const float* c2, float* x_sel, void* ws,
+                                 size_t ws_bytes, void* stream);
+
+/* Scatter and blend (Sec. 3 and 5.3: confident regions keep their values).
+ *   z_out = z_in with token idx[j] replaced by x_sel[j]   (j < n_sel)
+ * z_in == z_out scatters in place (dtypes must match); otherwise z_in is first
+ * copied to z_out with dtype conversion (bf16 outputs round to nearest even).
+ * x_sel: dev float [n_sel][16]; z_in, z_out: dev NCHW latents of all requests. */
+sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const float* x_sel, const int32_t* idx,
+                                   int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, void* z_out,
+                                   sphinx_dtype out_dtype, void* stream);
+
+/* Profiling aid (outside the method).  While enabled, every launch of a kernel
+ * class is bracketed by two HIP events recorded on the stream of the launch;
+ * sphinx_timing_read waits for the recorded events and returns the number of
+ * launches and their summed GPU time since timing was last enabled.  Events are
+ * created on first use and reused; nothing is allocated on the device.  The
+ * timing state is process-wide and guarded by a mutex. */
+typedef enum {
+  SPHINX_K_SELECT = 0, /* mask + compaction (three kernels, one bracket) */
+  SPHINX_K_GATHER,
+  SPHINX_K_COND,       /* timestep/adaLN conditioning, position tables, token metadata */
+  SPHINX_K_EMBED,
+  SPHINX_K_LN,         /* adaLN LayerNorm before QKV and MLP1 */
+  SPHINX_K_GEMM_QKV,
+  SPHINX_K_ATTENTION,
+  SPHINX_K_GEMM_OUT,
+  SPHINX_K_GEMM_MLP1,
+  SPHINX_K_GEMM_MLP2,
+  SPHINX_K_FINAL,      /* final LayerNorm + projection + DDIM update */
+  SPHINX_K_SCATTER,
+  SPHINX_K_COUNT
+} sphinx_kernel_class;
+
+sphinx_status sphinx_timing_enable(int32_t on);
+sphinx_status sphinx_timing_read(sphinx_kernel_class k, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPHINX_H */

@@ -386,7 +386,7 @@ def step(wl, model: Model, state: np.ndarray, plan: StepPlan, precision: str = "
          denoiser=None, info: Optional[TokenInfo] = None) -> StepResult:
     """One partial-denoising step: select, compact, gather(+inject), denoise, DDIM, scatter."""
     info = token_info(wl.requests) if info is None else info
-    tok_off = wl.tok_offset
+    tok_off = wl.tok_offset[:-1]  # request starts
     mask, idx, cu, n = select(wl.u, per_token(wl.thr, info), per_token(plan.active, info), tok_off)
     state = np.array(state, dtype=np.float64, copy=True)
     if n == 0:

@@ -1,0 +1,99 @@
+// Device-side helpers shared by the gfx950 kernels of the selective-refinement
+// step: the request table passed by value to every kernel, token-position
+// decoding, bf16 conversion and wave64 reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sphinx.h"
+
+namespace sphinx {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kWave = 64;
+
+// Request geometry, passed by value (kernarg segment) to every kernel.
+struct ReqTable {
+  int32_t R;
+  int32_t frames[SPHINX_MAX_REQUESTS];
+  int32_t h[SPHINX_MAX_REQUESTS];
+  int32_t w[SPHINX_MAX_REQUESTS];
+  int32_t frame_off[SPHINX_MAX_REQUESTS + 1];
+  int64_t tok_off[SPHINX_MAX_REQUESTS + 1];  // tok_off[R] = N
+};
+
+struct TokPos {
+  int r, f, y, x, g;  // request, frame in request, patch row, patch column, global frame
+  int64_t elem;       // NCHW element index of (c=0, py=0, px=0) of the token
+  int plane;          // h*w of the request (stride between channels)
+  int w;              // latent width (stride between rows)
+};
+
+__device__ __forceinline__ int find_request(const ReqTable& T, int64_t t) {
+  int lo = 0, hi = T.R - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (T.tok_off[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ TokPos decode_token(const ReqTable& T, int64_t t) {
+  TokPos p;
+  p.r = find_request(T, t);
+  const uint32_t loc = (uint32_t)(t - T.tok_off[p.r]);
+  const uint32_t wp = (uint32_t)T.w[p.r] >> 1, hp = (uint32_t)T.h[p.r] >> 1;
+  const uint32_t tpf = hp * wp;
+  const uint32_t f = loc / tpf;
+  const uint32_t rem = loc - f * tpf;
+  const uint32_t y = rem / wp;
+  p.f = (int)f;
+  p.y = (int)y;
+  p.x = (int)(rem - y * wp);
+  p.g = T.frame_off[p.r] + p.f;
+  p.w = T.w[p.r];
+  p.plane = T.h[p.r] * T.w[p.r];
+  p.elem = 16 * T.tok_off[p.r] + ((int64_t)p.f * 4) * p.plane + (int64_t)(2 * p.y) * p.w + 2 * p.x;
+  return p;
+}
+
+__device__ __forceinline__ float bf2f(bf16 v) { return (float)v; }
+__device__ __forceinline__ bf16 f2bf(float v) { return (bf16)v; }  // round to nearest even
+
+template <typename T> __device__ __forceinline__ float load_as_f32(const T* p, int64_t i);
+template <> __device__ __forceinline__ float load_as_f32<float>(const float* p, int64_t i) { return p[i]; }
+template <> __device__ __forceinline__ float load_as_f32<bf16>(const bf16* p, int64_t i) { return (float)p[i]; }
+
+template <typename T> __device__ __forceinline__ T store_from_f32(float v);
+template <> __device__ __forceinline__ float store_from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 store_from_f32<bf16>(float v) { return (bf16)v; }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, kWave));
+  return v;
+}
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1)); }
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+
+__device__ __forceinline__ float gelu_tanh(float z) {
+  const float k0 = 0.7978845608028654f, k1 = 0.044715f;
+  return 0.5f * z * (1.0f + tanhf(k0 * (z + k1 * z * z * z)));
+}
+
+}  // namespace sphinx

@@ -1,0 +1,175 @@
+// GEMMs of the denoiser blocks: C[M][N] = A[M][K] W[N][K]^T + b with a fused
+// epilogue:
+//   EPI_BIAS  : out = C                         (QKV projection)      -> bf16/fp32
+//   EPI_GELU  : out = GELU_tanh(C)              (MLP first layer)     -> bf16/fp32
+//   EPI_GATED : h  += (1 + gate[row]) * C       (out-proj, MLP second layer; fp32 residual)
+// M = selected tokens (ragged), N, K multiples of the tile sizes.
+//
+// bf16 path (gfx950 MFMA): block tile 128x128, K step 64, 256 threads = 4 waves
+// in a 2x2 grid, each wave a 64x64 tile of 2x2 v_mfma_f32_32x32x16_bf16.  A and
+// W are both K-contiguous, so every operand fragment is one 16-byte LDS read.
+// LDS rows are padded by 16 bytes against bank conflicts; two LDS buffers let
+// the global loads of the next K step overlap the MFMAs of the current one.
+// Rows past M load zeros and are not stored.
+//
+// fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
+#include "kernels.hpp"
+
+namespace sphinx {
+
+namespace {
+template <int EPI, typename OT>
+__device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float v) {
+  if constexpr (EPI == EPI_GATED) {
+    float* h = reinterpret_cast<float*>(e.out);
+    const int64_t o = (int64_t)m * e.ldo + n;
+    h[o] = fmaf(1.0f + e.gate[(int64_t)e.crow[m] * e.ldg + n], v, h[o]);
+  } else {
+    if constexpr (EPI == EPI_GELU) v = gelu_tanh(v);
+    reinterpret_cast<OT*>(e.out)[(int64_t)m * e.ldo + n] = store_from_f32<OT>(v);
+  }
+}
+
+constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
+
+template <int EPI>
+__global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                                      const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {
+  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * LDK];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int lrow = tid >> 3, lch = (tid & 7) * 8;
+  const int g = lane >> 5, r32 = lane & 31;
+  bf16x8 ra[4], rb[4];
+  const bf16x8 zero = {};
+
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = lrow + 32 * i;
+      const int m = m0 + r;
+      ra[i] = (m < M) ? *reinterpret_cast<const bf16x8*>(A + (int64_t)m * K + k0 + lch) : zero;
+      rb[i] = *reinterpret_cast<const bf16x8*>(W + (int64_t)(n0 + r) * K + k0 + lch);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = lrow + 32 * i;
+      *reinterpret_cast<bf16x8*>(&sA[buf][r * LDK + lch]) = ra[i];
+      *reinterpret_cast<bf16x8*>(&sB[buf][r * LDK + lch]) = rb[i];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+  const int KT = K / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < KT) gload((kt + 1) * BK);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      bf16x8 af[2], bw[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8*>(&sA[buf][(wm * 64 + i * 32 + r32) * LDK + ks * 16 + g * 8]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        bw[j] = *reinterpret_cast<const bf16x8*>(&sB[buf][(wn * 64 + j * 32 + r32) * LDK + ks * 16 + g * 8]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // accumulator (i, j) register r holds row 8*(r/4) + 4*g + r%4, column r32 of its 32x32 block
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = n0 + wn * 64 + j * 32 + r32;
+    const float bv = (float)bias[n];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
+        if (m < M) epi_store<EPI, bf16>(e, m, n, acc[i][j][r] + bv);
+      }
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, const float* __restrict__ W,
+                                                  const float* __restrict__ bias, int M, int N, int K, GemmEpi e) {
+  __shared__ float sA[16][65];
+  __shared__ float sB[16][65];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int li = tid + 256 * q;
+      const int r = li >> 4, k = li & 15;
+      sA[k][r] = (m0 + r < M) ? A[(int64_t)(m0 + r) * K + k0 + k] : 0.0f;
+      sB[k][r] = W[(int64_t)(n0 + r) * K + k0 + k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = sA[k][ty + 16 * i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = sB[k][tx + 16 * j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + ty + 16 * i;
+    if (m >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx + 16 * j;
+      epi_store<EPI, float>(e, m, n, acc[i][j] + bias[n]);
+    }
+  }
+}
+}  // namespace
+
+hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
+                       const GemmEpi& e, hipStream_t s) {
+  if (dt == SPHINX_BF16) {
+    const dim3 grid(N / BN, (M + BM - 1) / BM);
+    const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
+    if (epi == EPI_BIAS) k_gemm_bf16<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    else if (epi == EPI_GELU) k_gemm_bf16<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    else k_gemm_bf16<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+  } else {
+    const dim3 grid(N / 64, (M + 63) / 64);
+    const float *a = (const float*)A, *w = (const float*)W, *b = (const float*)bias;
+    if (epi == EPI_BIAS) k_gemm_f32<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    else if (epi == EPI_GELU) k_gemm_f32<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    else k_gemm_f32<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sphinx

@@ -1,0 +1,73 @@
+// Internal launchers of the gfx950 kernels.  Callers (api.cpp) validate every
+// argument and size before calling; the launchers only enqueue work on the
+// given stream and return hipGetLastError().
+#pragma once
+
+#include "common.hpp"
+
+namespace sphinx {
+
+enum { EPI_BIAS = 0, EPI_GELU = 1, EPI_GATED = 2 };
+
+struct GemmEpi {
+  void* out;             // EPI_BIAS/EPI_GELU: activation buffer; EPI_GATED: fp32 residual h
+  int ldo;
+  const float* gate;     // EPI_GATED: gate rows (conditioning row of each token)
+  int ldg;
+  const int32_t* crow;   // EPI_GATED: conditioning row of each token
+};
+
+// Attention segments (one per request with selected tokens).
+struct SegTable {
+  int nseg;                                  // non-empty segments, longest first
+  int start[SPHINX_MAX_REQUESTS];
+  int len[SPHINX_MAX_REQUESTS];
+  int tile_prefix[SPHINX_MAX_REQUESTS + 1];  // prefix sums of 128-query tiles
+  int nseg_by_start;                         // non-empty segments in row order
+  int start_sorted[SPHINX_MAX_REQUESTS];
+  int len_sorted[SPHINX_MAX_REQUESTS];
+};
+
+constexpr int kAttnQueryTile = 128;
+
+// select.hip
+size_t select_ws_bytes(int64_t N);
+hipError_t launch_select(const ReqTable& T, int64_t N, const float* u, const float* thr, const uint8_t* active,
+                         uint8_t* mask, int32_t* idx, int32_t* cu_sel, void* ws, hipStream_t s);
+
+// gather_scatter.hip
+hipError_t launch_gather(const ReqTable& T, const void* state, sphinx_dtype sdt, const void* eps, sphinx_dtype edt,
+                         const int32_t* idx, int n, const float* a, const float* b, float* x, hipStream_t s);
+hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, void* out, sphinx_dtype odt,
+                          hipStream_t s);
+hipError_t launch_convert(const void* in, sphinx_dtype idt, void* out, sphinx_dtype odt, int64_t count,
+                          hipStream_t s);
+
+// cond.hip
+hipError_t launch_cond_rows(const int32_t* tau, int G, int32_t* fmap, int32_t* utau, int32_t* U, hipStream_t s);
+hipError_t launch_temb(const int32_t* utau, const int32_t* U, int Gmax, float* temb, hipStream_t s);
+hipError_t launch_rowgemm(const float* X, int ldx, const int32_t* U, int K, const void* W, const void* b,
+                          sphinx_dtype wdt, int N, bool silu_out, float* out, int ldo, hipStream_t s);
+hipError_t launch_pos_tables(int D, int hp, int wp, int nf, float* Ty, float* Tx, float* Tf, hipStream_t s);
+hipError_t launch_token_meta(const ReqTable& T, const int32_t* idx, int n, const int32_t* fmap, int32_t* gframe,
+                             int32_t* crow, int32_t* posc, hipStream_t s);
+
+// rowwise.hip
+hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const void* pe_b, sphinx_dtype wdt,
+                        const float* Ty, const float* Tx, const float* Tf, const int32_t* posc, float* h,
+                        hipStream_t s);
+hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
+                         const int32_t* crow, void* out, sphinx_dtype odt, hipStream_t s);
+hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
+                        const int32_t* crow, const int32_t* gframe, const void* out_w, const void* out_b,
+                        sphinx_dtype wdt, const float* c1, const float* c2, float* x, hipStream_t s);
+
+// gemm.hip
+hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
+                       const GemmEpi& e, hipStream_t s);
+
+// attention.hip
+hipError_t launch_attention(sphinx_dtype dt, const void* qkv, void* o, int D, int heads, int head_dim, int n,
+                            const SegTable& S, hipStream_t s);
+
+}  // namespace sphinx

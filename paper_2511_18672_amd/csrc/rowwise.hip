@@ -1,0 +1,176 @@
+// Row-wise kernels of the denoiser:
+//  * k_embed   h = x W_pe^T + b_pe + [Ty(y) || Tx(x)] + Tf(f)          (fp32)
+//  * k_ln_mod  a = LN(h) * (1 + scale[row]) + shift[row]  -> bf16/fp32  (one wave per row)
+//  * k_final   eps_hat = (LN(h) (1 + scale) + shift) W_out^T + b_out, then the
+//              DDIM update x <- c1 x + c2 eps_hat in place (one wave per row;
+//              the 16 outputs are reduced with a butterfly reduce-scatter).
+// LayerNorm: biased variance, eps 1e-6, no affine; statistics in fp32 from the
+// row held in registers (two passes over registers, one read of HBM).
+#include "kernels.hpp"
+
+namespace sphinx {
+
+namespace {
+constexpr int kTPB = 256;
+constexpr int kRowsPerBlock = kTPB / kWave;
+constexpr int kMaxPer = 32;  // D <= 2048
+
+template <typename WT>
+__global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int n, int D, const WT* __restrict__ pe_w,
+                                                const WT* __restrict__ pe_b, const float* __restrict__ Ty,
+                                                const float* __restrict__ Tx, const float* __restrict__ Tf,
+                                                const int32_t* __restrict__ posc, float* __restrict__ h) {
+  const int64_t gid = (int64_t)blockIdx.x * kTPB + threadIdx.x;
+  if (gid >= (int64_t)n * D) return;
+  const int j = (int)(gid / D), c = (int)(gid % D);
+  const int pc = posc[j];
+  const int f = pc >> 20, y = (pc >> 10) & 1023, xx = pc & 1023;
+  const float* xr = x + (int64_t)j * 16;
+  float v = load_as_f32(pe_b, c);
+#pragma unroll
+  for (int k = 0; k < 16; ++k) v = fmaf(xr[k], load_as_f32(pe_w, (int64_t)c * 16 + k), v);
+  const int half = D / 2;
+  v += (c < half) ? Ty[(int64_t)y * half + c] : Tx[(int64_t)xx * half + (c - half)];
+  v += Tf[(int64_t)f * D + c];
+  h[gid] = v;
+}
+
+// Loads the row into registers and returns (mean, rstd).
+__device__ __forceinline__ void row_stats(const float* __restrict__ hr, int D, int lane, float (&v)[kMaxPer],
+                                          float& mu, float& rstd) {
+  const int per = D / kWave;
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i)
+    if (i < per) {
+      v[i] = hr[i * kWave + lane];
+      s += v[i];
+    }
+  mu = wave_sum(s) / (float)D;
+  float s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i)
+    if (i < per) {
+      const float d = v[i] - mu;
+      s2 = fmaf(d, d, s2);
+    }
+  rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
+}
+
+template <typename OT>
+__global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, int n, int D,
+                                                 const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
+                                                 const int32_t* __restrict__ crow, OT* __restrict__ out) {
+  const int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
+  if (row >= n) return;
+  const int lane = lane_id();
+  float v[kMaxPer];
+  float mu, rstd;
+  row_stats(h + (int64_t)row * D, D, lane, v, mu, rstd);
+  const float* m = mod + (int64_t)crow[row] * ldm;
+  OT* o = out + (int64_t)row * D;
+  const int per = D / kWave;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i)
+    if (i < per) {
+      const int c = i * kWave + lane;
+      o[c] = store_from_f32<OT>(fmaf((v[i] - mu) * rstd, 1.0f + m[sc_off + c], m[sh_off + c]));
+    }
+}
+
+template <typename WT>
+__global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int n, int D,
+                                                const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
+                                                const int32_t* __restrict__ crow, const int32_t* __restrict__ gframe,
+                                                const WT* __restrict__ out_w, const WT* __restrict__ out_b,
+                                                const float* __restrict__ c1, const float* __restrict__ c2,
+                                                float* __restrict__ x) {
+  extern __shared__ unsigned char s_raw[];
+  WT* s_w = reinterpret_cast<WT*>(s_raw);  // [16][D]
+  for (int i = threadIdx.x; i < 16 * D; i += kTPB) s_w[i] = out_w[i];
+  __syncthreads();
+  const int lane = lane_id();
+  const int per = D / kWave;
+  for (int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave); row < n;
+       row += gridDim.x * kRowsPerBlock) {
+    float v[kMaxPer];
+    float mu, rstd;
+    row_stats(h + (int64_t)row * D, D, lane, v, mu, rstd);
+    const float* m = mod + (int64_t)crow[row] * ldm;
+    float acc[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) acc[k] = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i)
+      if (i < per) {
+        const int c = i * kWave + lane;
+        const float a = fmaf((v[i] - mu) * rstd, 1.0f + m[sc_off + c], m[sh_off + c]);
+#pragma unroll
+        for (int k = 0; k < 16; ++k) acc[k] = fmaf(a, load_as_f32(s_w, (int64_t)k * D + c), acc[k]);
+      }
+    // butterfly reduce-scatter: after the four halving steps lane holds output
+    // k = 8*b5 + 4*b4 + 2*b3 + b2 (b = lane bits), summed over lanes that differ
+    // in those bits; the last two steps sum over lane bits 1 and 0.
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const int mask = 32 >> st;
+      const int cnt = 16 >> st;
+      const bool up = (lane & mask) != 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (i < cnt / 2) {
+          const float send = up ? acc[i] : acc[i + cnt / 2];
+          const float keep = up ? acc[i + cnt / 2] : acc[i];
+          acc[i] = keep + __shfl_xor(send, mask, kWave);
+        }
+    }
+    float e = acc[0];
+    e += __shfl_xor(e, 2, kWave);
+    e += __shfl_xor(e, 1, kWave);
+    if ((lane & 3) == 0) {
+      const int k = ((lane >> 5) & 1) * 8 + ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1);
+      const float eps_hat = e + load_as_f32(out_b, k);
+      const int g = gframe[row];
+      float* xp = x + (int64_t)row * 16 + k;
+      *xp = fmaf(c2[g], eps_hat, c1[g] * *xp);
+    }
+  }
+}
+}  // namespace
+
+hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const void* pe_b, sphinx_dtype wdt,
+                        const float* Ty, const float* Tx, const float* Tf, const int32_t* posc, float* h,
+                        hipStream_t s) {
+  const int g = (int)(((int64_t)n * D + kTPB - 1) / kTPB);
+  if (wdt == SPHINX_BF16)
+    k_embed<bf16><<<g, kTPB, 0, s>>>(x, n, D, (const bf16*)pe_w, (const bf16*)pe_b, Ty, Tx, Tf, posc, h);
+  else
+    k_embed<float><<<g, kTPB, 0, s>>>(x, n, D, (const float*)pe_w, (const float*)pe_b, Ty, Tx, Tf, posc, h);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
+                         const int32_t* crow, void* out, sphinx_dtype odt, hipStream_t s) {
+  const int g = (n + kRowsPerBlock - 1) / kRowsPerBlock;
+  if (odt == SPHINX_BF16)
+    k_ln_mod<bf16><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
+  else
+    k_ln_mod<float><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
+  return hipGetLastError();
+}
+
+hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
+                        const int32_t* crow, const int32_t* gframe, const void* out_w, const void* out_b,
+                        sphinx_dtype wdt, const float* c1, const float* c2, float* x, hipStream_t s) {
+  const int rows_blocks = (n + kRowsPerBlock - 1) / kRowsPerBlock;
+  const int g = rows_blocks < 1024 ? rows_blocks : 1024;
+  if (wdt == SPHINX_BF16)
+    k_final<bf16><<<g, kTPB, 16 * D * sizeof(bf16), s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe,
+                                                         (const bf16*)out_w, (const bf16*)out_b, c1, c2, x);
+  else
+    k_final<float><<<g, kTPB, 16 * D * sizeof(float), s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe,
+                                                           (const float*)out_w, (const float*)out_b, c1, c2, x);
+  return hipGetLastError();
+}
+
+}  // namespace sphinx

@@ -1,0 +1,145 @@
+"""Driver of the partial-denoising loop on one GPU (Alg. 1 loop with per-frame
+start steps and the selective mask of Sec. 5.3).
+
+``Refiner`` owns the device buffers of one batch of packed requests and runs,
+for each step: ``sphinx_select_mask`` (whenever the set of active frames
+changes, or every step when asked), ``sphinx_gather``, ``sphinx_refine_step``
+and ``sphinx_scatter_blend``.  Python only sequences the calls; every value is
+computed by libsphinx.so.  The per-step schedule comes from
+``sphinx_plan_step`` (library host code) and is uploaded once.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+
+def _torch_dtype(name: str):
+    return torch.bfloat16 if name == "bf16" else torch.float32
+
+
+def pack_weights(cfg, weights: Dict[str, np.ndarray], device="cuda") -> torch.Tensor:
+    """Place named parameters into the library's blob layout and upload it.
+
+    ``weights`` uses the names ``pe_w, pe_b, t1_w, t1_b, t2_w, t2_b,
+    b{l}.{ada_w, ada_b, qkv_w, qkv_b, o_w, o_b, fc1_w, fc1_b, fc2_w, fc2_b},
+    fada_w, fada_b, out_w, out_b`` with matrices [out][in]."""
+    desc = B.model_desc(cfg)
+    tdt = _torch_dtype(cfg.dtype)
+    esz = 2 if cfg.dtype == "bf16" else 4
+    blob = torch.zeros(B.sphinx_model_blob_bytes(desc) // esz, dtype=tdt)
+
+    def put(param: str, block: int, arr: np.ndarray, elem0: int = 0):
+        off, cnt = B.sphinx_model_param(desc, param, block)
+        flat = torch.from_numpy(np.ascontiguousarray(arr, dtype=np.float32).ravel()).to(tdt)
+        assert elem0 + flat.numel() <= cnt, (param, block)
+        start = off // esz + elem0
+        blob[start:start + flat.numel()] = flat
+
+    D, L = cfg.D, cfg.L
+    for p in ("pe_w", "pe_b", "t1_w", "t1_b", "t2_w", "t2_b", "out_w", "out_b"):
+        put(p.upper(), 0, weights[p])
+    for l in range(L):
+        put("COND_W", 0, weights[f"b{l}.ada_w"], 6 * D * l * D)
+        put("COND_B", 0, weights[f"b{l}.ada_b"], 6 * D * l)
+        for p in ("qkv_w", "qkv_b", "o_w", "o_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b"):
+            put(p.upper(), l, weights[f"b{l}.{p}"])
+    put("COND_W", 0, weights["fada_w"], 6 * D * L * D)
+    put("COND_B", 0, weights["fada_b"], 6 * D * L)
+    return blob.to(device)
+
+
+class Refiner:
+    """Selective partial denoising of one batch of packed requests on one GPU."""
+
+    def __init__(self, requests: Sequence, cfg, blob: torch.Tensor, s_start: np.ndarray, nsteps: np.ndarray,
+                 u: np.ndarray, thr: np.ndarray, z0: np.ndarray, eps: np.ndarray, device="cuda",
+                 max_sel: Optional[int] = None):
+        if not torch.cuda.is_available():
+            raise RuntimeError("Refiner needs a GPU: the selective-refinement step has no CPU path")
+        B.lib()
+        self.shapes = list(requests)
+        self.reqs = B.make_requests(self.shapes)
+        self.cfg = cfg
+        self.blob = blob
+        self.desc = B.model_desc(cfg, blob.data_ptr())
+        self.N = sum(r.frames * (r.h // 2) * (r.w // 2) for r in self.shapes)
+        self.G = sum(r.frames for r in self.shapes)
+        self.R = len(self.shapes)
+        self.dt = B.dtype_code(cfg.dtype)
+        tdt = _torch_dtype(cfg.dtype)
+        dev = torch.device(device)
+        self.z0 = torch.from_numpy(np.ascontiguousarray(z0, np.float32)).to(tdt).to(dev)
+        self.eps = torch.from_numpy(np.ascontiguousarray(eps, np.float32)).to(tdt).to(dev)
+        self.u = torch.from_numpy(np.ascontiguousarray(u, np.float32)).to(dev)
+        self.thr = torch.from_numpy(np.ascontiguousarray(thr, np.float32)).to(dev)
+        self.state = torch.empty(16 * self.N, dtype=torch.float32, device=dev)
+        self.mask = torch.empty(self.N, dtype=torch.uint8, device=dev)
+        self.idx = torch.empty(self.N, dtype=torch.int32, device=dev)
+        self.cu_sel = torch.empty(self.R + 1, dtype=torch.int32, device=dev)
+        self.max_sel = self.N if max_sel is None else int(max_sel)
+        self.x_sel = torch.empty(16 * self.max_sel, dtype=torch.float32, device=dev)
+        self.ws_sel = torch.empty(B.sphinx_select_workspace_bytes(self.N), dtype=torch.uint8, device=dev)
+        self.ws = torch.empty(B.sphinx_refine_workspace_bytes(self.desc, self.reqs, self.max_sel),
+                              dtype=torch.uint8, device=dev)
+        self.total_steps = int(np.max(nsteps))
+        plans = [B.sphinx_plan_step(self.reqs, s_start, nsteps, i) for i in range(self.total_steps)]
+        self.plan_host = {k: np.stack([p[k] for p in plans]) for k in plans[0]}
+        self.plan = {k: torch.from_numpy(v).to(dev) for k, v in self.plan_host.items()}
+        self._active_key = None
+        self.n_sel = 0
+        self.cu_host = None
+
+    def reset(self, stream=None):
+        """state <- fp32(z0) (a dtype-converting copy through scatter_blend with no tokens)."""
+        B.sphinx_scatter_blend(self.reqs, None, None, 0, self.z0, self.dt, self.state, B.F32, stream)
+        self._active_key = None
+
+    def select(self, k: int, stream=None) -> int:
+        self.cu_host = B.sphinx_select_mask(self.reqs, self.u, self.thr, self.plan["active"][k], self.mask,
+                                            self.idx, self.cu_sel, self.ws_sel, True, stream)
+        self.n_sel = int(self.cu_host[-1])
+        if self.n_sel > self.max_sel:
+            raise RuntimeError(f"{self.n_sel} selected tokens exceed the buffers sized for {self.max_sel}")
+        self._active_key = self.plan_host["active"][k].copy()
+        return self.n_sel
+
+    def step(self, i: int, force_select: bool = False, stream=None) -> int:
+        """One partial-denoising step (schedule index i modulo the schedule length)."""
+        k = i % self.total_steps
+        if force_select or self._active_key is None or not np.array_equal(self.plan_host["active"][k],
+                                                                          self._active_key):
+            self.select(k, stream)
+        n = self.n_sel
+        if n == 0:
+            return 0
+        P = self.plan
+        B.sphinx_gather(self.reqs, self.state, B.F32, self.eps, self.dt, self.idx, n, P["a"][k], P["b"][k],
+                        self.x_sel, stream)
+        B.sphinx_refine_step(self.desc, self.reqs, self.idx, n, self.cu_host, P["tau"][k], P["c1"][k],
+                             P["c2"][k], self.x_sel, self.ws, stream)
+        B.sphinx_scatter_blend(self.reqs, self.x_sel, self.idx, n, self.state, B.F32, self.state, B.F32, stream)
+        return n
+
+    def run(self, stream=None) -> torch.Tensor:
+        """The whole schedule from z0; returns the fp32 state (NCHW of all requests)."""
+        self.reset(stream)
+        for i in range(self.total_steps):
+            self.step(i, stream=stream)
+        return self.state
+
+    def output(self, dtype: str = "bf16", stream=None) -> torch.Tensor:
+        """The state converted to the latent dtype (bf16 rounds to nearest even)."""
+        out = torch.empty(16 * self.N, dtype=_torch_dtype(dtype), device=self.state.device)
+        B.sphinx_scatter_blend(self.reqs, None, None, 0, self.state, B.F32, out, B.dtype_code(dtype), stream)
+        return out
+
+
+def from_workload(wl, device="cuda", **kw) -> Refiner:
+    """Refiner for a ``workloads.Workload`` (seeded inputs and weights)."""
+    blob = pack_weights(wl.model, wl.weights, device)
+    return Refiner(wl.requests, wl.model, blob, wl.s_start, wl.nsteps, wl.u, wl.thr, wl.z0, wl.eps, device, **kw)

@@ -1,0 +1,154 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/sphinx.h, validates arguments before any HIP call, lays
+out the weight blob consistently, and its host-side step schedule equals the
+oracle's."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+S = pytest.importorskip("paper_2511_18672_amd")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(S.binding.LIB_PATH):
+        pytest.skip("libsphinx.so not built")
+    return S.lib()
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "sphinx.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(sphinx_\w+)\s*\(", text, re.M)))
+
+
+def test_exports_every_declared_symbol(L):
+    declared = header_functions()
+    assert len(declared) >= 10
+    for name in declared:
+        assert hasattr(L, name), name
+    assert sorted(S.EXPORTED) == declared
+
+
+def test_status_strings(L):
+    assert S.sphinx_status_string(0) == "ok"
+    assert S.sphinx_status_string(3) == "workspace too small"
+    assert S.sphinx_status_string(99) == "unknown status"
+
+
+def _reqs(shapes):
+    return S.make_requests([W.Request(*s) for s in shapes])
+
+
+def test_request_validation(L):
+    P = ctypes.c_void_p
+    reqs = _reqs([(2, 8, 8)])
+    out = ctypes.c_size_t()
+    assert L.sphinx_select_workspace_bytes(0, ctypes.byref(out)) == INVALID
+    # bad offsets
+    bad = _reqs([(2, 8, 8), (1, 4, 4)])
+    bad[1].tok_offset = 5
+    assert L.sphinx_gather(bad, 2, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == INVALID
+    # odd latent size
+    odd = _reqs([(1, 7, 8)])
+    assert L.sphinx_gather(odd, 1, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == INVALID
+    # too many requests
+    many = _reqs([(1, 2, 2)] * 65)
+    assert L.sphinx_gather(many, 65, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == UNSUPPORTED
+    # n_sel beyond N, null pointers, misalignment
+    assert L.sphinx_gather(reqs, 1, P(256), 0, None, 0, P(256), 33, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(reqs, 1, None, 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(reqs, 1, P(258), 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(reqs, 1, P(256), 7, None, 0, P(256), 3, P(256), P(256), P(256), None) == UNSUPPORTED
+    # n_sel = 0 is a no-op that touches no pointer
+    assert L.sphinx_gather(reqs, 1, None, 0, None, 0, None, 0, None, None, None, None) == OK
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, P(256), 0, None) == OK
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, P(256), 1, None) == INVALID
+
+
+def test_select_validation(L):
+    P = ctypes.c_void_p
+    reqs = _reqs([(2, 8, 8)])
+    args = [P(256)] * 6
+    assert L.sphinx_select_mask(reqs, 1, *args, None, P(256), 0, None) == WORKSPACE
+    assert L.sphinx_select_mask(reqs, 1, None, *args[1:], None, P(256), 1 << 20, None) == INVALID
+    assert L.sphinx_select_mask(reqs, 1, P(260), *args[1:], None, P(256), 1 << 20, None) == INVALID
+    assert L.sphinx_select_mask(reqs, 0, *args, None, P(256), 1 << 20, None) == INVALID
+
+
+def test_model_validation(L):
+    out = ctypes.c_size_t()
+    ok = S.model_desc(W.SMALL_MODEL, 256)
+    assert L.sphinx_model_blob_bytes(ctypes.byref(ok), ctypes.byref(out)) == OK
+    for kw, code in [(dict(head_dim=72, heads=8, D=576), UNSUPPORTED), (dict(D=500), INVALID),
+                     (dict(dtype=7), UNSUPPORTED), (dict(L=0), INVALID), (dict(mlp=100), UNSUPPORTED)]:
+        d = S.model_desc(W.SMALL_MODEL, 256)
+        for k, v in kw.items():
+            setattr(d, k, v)
+        assert L.sphinx_model_blob_bytes(ctypes.byref(d), ctypes.byref(out)) == code, kw
+    # fp32 models: head_dim up to 64, D <= 512
+    d = S.model_desc(W.TINY_MODEL, 256)
+    assert L.sphinx_model_blob_bytes(ctypes.byref(d), ctypes.byref(out)) == OK
+
+
+def test_refine_validation(L):
+    P = ctypes.c_void_p
+    reqs = _reqs([(2, 8, 8)])
+    d = S.model_desc(W.TINY_MODEL, 256)
+    cu = (ctypes.c_int32 * 2)(0, 5)
+    need = ctypes.c_size_t()
+    assert L.sphinx_refine_workspace_bytes(ctypes.byref(d), reqs, 1, 5, ctypes.byref(need)) == OK
+    assert need.value > 0
+    args = lambda n, cu_, ws_bytes: (ctypes.byref(d), reqs, 1, P(256), n, cu_, P(256), P(256), P(256), P(256),
+                                     P(256), ws_bytes, None)
+    assert L.sphinx_refine_step(*args(5, cu, need.value - 1)) == WORKSPACE
+    assert L.sphinx_refine_step(*args(4, cu, need.value)) == INVALID  # cu_sel[R] != n_sel
+    assert L.sphinx_refine_step(*args(5, None, need.value)) == INVALID
+    cu0 = (ctypes.c_int32 * 2)(0, 0)
+    assert L.sphinx_refine_step(ctypes.byref(d), reqs, 1, None, 0, cu0, None, None, None, None, None, 0,
+                                None) == OK
+    over = (ctypes.c_int32 * 2)(0, 40)
+    assert L.sphinx_refine_step(*args(40, over, need.value)) == INVALID
+
+
+@pytest.mark.parametrize("cfg", [W.TINY_MODEL, W.SMALL_MODEL, W.HEADLINE_MODEL])
+def test_blob_layout(L, cfg):
+    d = S.model_desc(cfg, 256)
+    total = S.sphinx_model_blob_bytes(d)
+    esz = 2 if cfg.dtype == "bf16" else 4
+    spans = []
+    for p in S.binding.PARAMS:
+        blocks = range(cfg.L) if p[:3] in ("QKV", "O_W", "O_B", "FC1", "FC2") else [0]
+        for l in blocks:
+            off, cnt = S.sphinx_model_param(d, p, l)
+            assert off % 256 == 0
+            spans.append((off, off + cnt * esz))
+    spans.sort()
+    assert all(a[1] <= b[0] for a, b in zip(spans, spans[1:]))
+    assert spans[-1][1] <= total
+    expect = sum(int(np.prod(s)) for _, s in W.weight_shapes(cfg))
+    assert sum((b - a) // esz for a, b in spans) == expect
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "headline", "frame_region", "batched"])
+def test_plan_matches_oracle(L, name):
+    import oracle as O
+
+    wl = W.CONFIGS[name](with_weights=False)
+    reqs = S.make_requests(wl.requests)
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    for i, p in enumerate(plans):
+        q = S.plan_step(reqs, wl.s_start, wl.nsteps, i)
+        assert np.array_equal(q["active"].astype(bool), p.active), i
+        assert np.array_equal(q["newly"].astype(bool), p.newly), i
+        assert np.array_equal(q["tau"], p.tau), i
+        for k in ("a", "b", "c1", "c2"):
+            ref = getattr(p, k).astype(np.float32)
+            assert np.array_equal(q[k], ref) or np.abs(q[k] - ref).max() <= 2 * np.spacing(np.abs(ref)).max(), (i, k)

@@ -1,0 +1,262 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+* masks, indices and compaction: bit-exact;
+* latents: max-abs error <= 1e-4 (fp32 model) / 2e-2 (bf16 model) against the
+  oracle in its model precision (bf16 operands where the model stores bf16);
+* full-size shapes: every kernel at the headline launch configuration against
+  the oracle (one block deep), plus properties that hold at any size for the
+  12-block headline and the packed four-request batch.
+Each test prints the errors it measured.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+from pins import MICRO_BF16
+
+torch = pytest.importorskip("torch")
+S = pytest.importorskip("paper_2511_18672_amd")
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+MID_BF16 = W.ModelCfg(D=128, heads=2, head_dim=64, mlp=512, L=2, dtype="bf16")
+
+
+def _dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.cuda()
+
+
+def gpu_select(wl, active):
+    N = wl.N
+    reqs = S.make_requests(wl.requests)
+    mask = torch.empty(N, dtype=torch.uint8, device="cuda")
+    idx = torch.full((N,), -7, dtype=torch.int32, device="cuda")
+    cu = torch.empty(wl.R + 1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(S.sphinx_select_workspace_bytes(N), dtype=torch.uint8, device="cuda")
+    act = None if active is None else _dev(np.asarray(active, np.uint8))
+    cu_host = S.sphinx_select_mask(reqs, _dev(wl.u), _dev(wl.thr), act, mask, idx, cu, ws)
+    n = int(cu_host[-1])
+    return mask.cpu().numpy().astype(bool), idx[:n].cpu().numpy(), cu_host, cu.cpu().numpy()
+
+
+def check_select(wl, active):
+    info = O.token_info(wl.requests)
+    act_tok = np.ones(wl.N, bool) if active is None else np.asarray(active, bool)[info.gframe]
+    mask, idx, cu, n = O.select(wl.u, wl.thr[info.gframe], act_tok, wl.tok_offset[:-1])
+    gm, gi, gcu, gcu_dev = gpu_select(wl, active)
+    assert np.array_equal(gm, mask)
+    assert np.array_equal(gi, idx)
+    assert list(gcu) == list(cu) + [n]
+    assert np.array_equal(gcu, gcu_dev)
+    return n
+
+
+@pytest.mark.parametrize("name", ["tiny", "small", "headline", "frame_region", "batched"])
+def test_select_bitexact_configs(name):
+    wl = W.CONFIGS[name](with_weights=False)
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    seen = set()
+    for p in plans:
+        key = tuple(p.active)
+        if key in seen:
+            continue
+        seen.add(key)
+        n = check_select(wl, p.active.astype(np.uint8))
+        print(f"[select] {name} active={int(p.active.sum())}/{wl.G} n_sel={n}")
+    check_select(wl, None)
+
+
+def test_select_edge_cases():
+    rng = np.random.default_rng(21)
+    shapes = [W.Request(3, 6, 10), W.Request(1, 2, 2), W.Request(5, 18, 6), W.Request(2, 64, 66)]
+    wl = W.custom("edge", MICRO_BF16, shapes, [0.5] * 4, [0.5] * 4, [1] * 4, with_weights=False)
+    specials = np.array([np.nan, np.inf, -np.inf, 0.5, 0.5, 0.25], np.float32)
+    wl.u = np.where(rng.random(wl.N) < 0.2, rng.choice(specials, wl.N), wl.u).astype(np.float32)
+    wl.thr = rng.choice(np.array([0.5, 0.25, -np.inf, np.inf, np.nan], np.float32), wl.G)
+    for active in [None, (rng.random(wl.G) < 0.5).astype(np.uint8), np.zeros(wl.G, np.uint8)]:
+        n = check_select(wl, active)
+        print(f"[select] edge N={wl.N} n_sel={n}")
+    # large ragged input spanning many 4096-token chunks
+    big = W.custom("big", MICRO_BF16, [W.Request(37, 130, 98), W.Request(3, 10, 2)], [0.3, 0.9], [0.5, 0.5],
+                   [1, 1], u_recipe="uniform", with_weights=False)
+    n = check_select(big, None)
+    print(f"[select] big N={big.N} n_sel={n}")
+
+
+def test_gather_scatter():
+    wl = W.custom("gs", MICRO_BF16, [W.Request(3, 8, 12), W.Request(2, 6, 4)], [0.5, 0.3], [0.5, 0.5], [1, 1],
+                  with_weights=False)
+    rng = np.random.default_rng(3)
+    state = rng.standard_normal(16 * wl.N).astype(np.float32)
+    a = rng.random(wl.G).astype(np.float32)
+    b = (rng.random(wl.G) * (rng.random(wl.G) < 0.6)).astype(np.float32)
+    _, idx, cu, _ = gpu_select(wl, None)
+    n = len(idx)
+    reqs = S.make_requests(wl.requests)
+    x = torch.empty(16 * n, dtype=torch.float32, device="cuda")
+    S.sphinx_gather(reqs, _dev(state), S.F32, _dev(wl.eps, torch.bfloat16), S.BF16, _dev(idx.astype(np.int32)), n,
+                    _dev(a), _dev(b), x)
+    info = O.token_info(wl.requests)
+    P, E = O.patchify(state, wl.requests), O.patchify(wl.eps, wl.requests)
+    g = info.gframe[idx]
+    ref = a[g].astype(np.float64)[:, None] * P[idx] + b[g].astype(np.float64)[:, None] * E[idx]
+    err = np.abs(x.cpu().numpy().reshape(n, 16) - ref).max()
+    print(f"[gather] n={n} max_abs={err:.3e}")
+    assert err <= 1e-6 * max(1.0, np.abs(ref).max())
+    # scatter in place: selected tokens replaced exactly, the rest untouched
+    xs = rng.standard_normal(16 * n).astype(np.float32)
+    st = _dev(state)
+    S.sphinx_scatter_blend(reqs, _dev(xs), _dev(idx.astype(np.int32)), n, st, S.F32, st, S.F32)
+    Pexp = P.copy()
+    Pexp[idx] = xs.reshape(n, 16)
+    assert np.array_equal(st.cpu().numpy(), O.unpatchify(Pexp, wl.requests).astype(np.float32))
+    # out of place with conversion to bf16 (round to nearest even)
+    out = torch.empty(16 * wl.N, dtype=torch.bfloat16, device="cuda")
+    S.sphinx_scatter_blend(reqs, _dev(xs), _dev(idx.astype(np.int32)), n, _dev(state), S.F32, out, S.BF16)
+    expect = torch.from_numpy(O.unpatchify(Pexp, wl.requests).astype(np.float32)).to(torch.bfloat16)
+    assert torch.equal(out.cpu(), expect)
+
+
+def run_gpu(wl, trace=False, steps=None):
+    R = S.from_workload(wl)
+    R.reset()
+    states = [R.state.cpu().numpy().astype(np.float64)] if trace else None
+    sels = []
+    for i in range(steps or R.total_steps):
+        R.step(i)
+        sels.append((R.n_sel, R.idx[:R.n_sel].cpu().numpy().copy(), R.cu_host.copy()))
+        if trace:
+            states.append(R.state.cpu().numpy().astype(np.float64))
+    torch.cuda.synchronize()
+    return R, states, sels
+
+
+def _report(tag, got, ref, truth=None):
+    err = np.abs(got - ref).max()
+    msg = f"[{tag}] max_abs vs oracle(model precision) = {err:.3e}"
+    if truth is not None:
+        msg += f"; vs oracle(fp64) = {np.abs(got - truth).max():.3e}"
+    print(msg)
+    return err
+
+
+def check_end_to_end(wl, teacher_forced=True):
+    R, states, sels = run_gpu(wl, trace=teacher_forced)
+    got = R.state.cpu().numpy().astype(np.float64)
+    ref, trace = O.refine(wl, precision="model", trace=True)
+    for i, (res, (n, idx, cu)) in enumerate(zip(trace, sels)):
+        assert n == res.n_sel and np.array_equal(idx, res.idx), i
+        assert list(cu) == list(res.cu_sel) + [res.n_sel], i
+    truth = O.refine(wl, precision="fp64") if wl.model.dtype == "bf16" and wl.N <= 4096 else None
+    err = _report(f"{wl.name} end-to-end {len(trace)} steps", got, ref, truth)
+    assert err <= TOL[wl.model.dtype]
+    assert np.isfinite(got).all()
+    if teacher_forced:
+        model = O.model_from_workload(wl)
+        plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+        info = O.token_info(wl.requests)
+        worst = 0.0
+        for i, p in enumerate(plans):
+            res = O.step(wl, model, states[i], p, "model", info=info)
+            worst = max(worst, np.abs(states[i + 1] - res.state).max())
+        print(f"[{wl.name}] teacher-forced per-step max_abs = {worst:.3e}")
+        assert worst <= TOL[wl.model.dtype]
+    return R
+
+
+def test_tiny_end_to_end():
+    R = check_end_to_end(W.tiny())
+    out = R.output("f32").cpu().numpy()
+    assert np.array_equal(out, R.state.cpu().numpy())
+
+
+def test_small_end_to_end():
+    check_end_to_end(W.small())
+
+
+def test_multi_request_ragged_staggered():
+    wl = W.custom("ragged", MID_BF16, [W.Request(3, 24, 20), W.Request(2, 10, 14), W.Request(1, 4, 4)],
+                  [0.6, 0.9, 0.5], [("uniform", 0.3, 0.7), 0.5, 0.2], [6, 4, 3])
+    check_end_to_end(wl)
+
+
+def test_empty_mask_is_identity():
+    wl = W.custom("empty", MID_BF16, [W.Request(2, 16, 16)], [0.3], [0.5], [3])
+    wl.thr[:] = np.inf
+    R, _, sels = run_gpu(wl)
+    assert all(n == 0 for n, _, _ in sels)
+    assert np.array_equal(R.state.cpu().numpy(), wl.z0)
+    # one empty request next to a refined one: the empty one stays bit-exact
+    wl2 = W.custom("half_empty", MID_BF16, [W.Request(2, 16, 16), W.Request(1, 8, 8)], [0.3, 0.5], [0.5, 0.5],
+                   [3, 3])
+    wl2.thr[2:] = np.inf
+    R2 = check_end_to_end(wl2, teacher_forced=False)
+    e0 = 16 * wl2.tok_offset[1]
+    assert np.array_equal(R2.state.cpu().numpy()[e0:], wl2.z0[e0:])
+
+
+def test_all_selected_equals_dense():
+    wl = W.custom("dense", MID_BF16, [W.Request(2, 16, 16), W.Request(1, 12, 8)], [1.0, 1.0], [0.5, 0.3], [3, 2])
+    assert np.isneginf(wl.thr).all()
+    R, _, _ = run_gpu(wl)
+    got = R.state.cpu().numpy().astype(np.float64)
+    dense = O.refine_dense(wl, precision="model")
+    assert _report("all-selected vs dense oracle", got, dense) <= TOL["bf16"]
+
+
+def test_headline_shape_one_block_step():
+    """Every kernel at the headline launch configuration (9677 of 32256 tokens,
+    D 1024, 16 heads, MLP 4096), one block deep so the oracle can follow."""
+    model = W.ModelCfg(D=1024, heads=16, head_dim=64, mlp=4096, L=1, dtype="bf16")
+    wl = W.headline(model=model)
+    R, states, sels = run_gpu(wl, trace=True, steps=1)
+    assert sels[0][0] == 9677
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    res = O.step(wl, O.model_from_workload(wl), wl.z0, plans[0], "model")
+    assert np.array_equal(sels[0][1], res.idx)
+    assert _report("headline L=1 step 0", states[1], res.state) <= TOL["bf16"]
+
+
+def test_headline_full_depth_properties():
+    """12-block headline step: deterministic, unselected tokens untouched,
+    finite, and only selected tokens move."""
+    wl = W.headline()
+    R, states, sels = run_gpu(wl, trace=True, steps=2)
+    R2, states2, _ = run_gpu(wl, trace=True, steps=2)
+    assert np.array_equal(states[2], states2[2]), "two runs differ"
+    idx = sels[0][1]
+    P0 = O.patchify(states[0], wl.requests)
+    P2 = O.patchify(states[2], wl.requests)
+    keep = np.ones(wl.N, bool)
+    keep[idx] = False
+    assert np.array_equal(P2[keep], P0[keep])
+    assert np.isfinite(P2).all()
+    print(f"[headline] 12 blocks, n_sel={len(idx)}, mean |dx| selected={np.abs(P2[idx] - P0[idx]).mean():.3f}")
+
+
+def test_batched_packed_equals_separate():
+    """Four requests packed varlen into one launch give the same result as each
+    request alone (segment isolation), at the full batched shape."""
+    wl = W.batched()
+    R, _, _ = run_gpu(wl, steps=1)
+    packed = R.state.cpu().numpy()
+    del R
+    worst = 0.0
+    for r, q in enumerate(wl.requests):
+        one = W.Workload(name=f"r{r}", model=wl.model, requests=[q],
+                         u=wl.u[wl.tok_offset[r]:wl.tok_offset[r + 1]],
+                         thr=wl.thr[wl.frame_offset[r]:wl.frame_offset[r + 1]],
+                         s_start=wl.s_start[wl.frame_offset[r]:wl.frame_offset[r + 1]],
+                         nsteps=wl.nsteps[r:r + 1], z0=wl.z0[16 * wl.tok_offset[r]:16 * wl.tok_offset[r + 1]],
+                         eps=wl.eps[16 * wl.tok_offset[r]:16 * wl.tok_offset[r + 1]], weights=wl.weights)
+        Rr, _, _ = run_gpu(one, steps=1)
+        sep = Rr.state.cpu().numpy()
+        worst = max(worst, float(np.abs(sep - packed[16 * wl.tok_offset[r]:16 * wl.tok_offset[r + 1]]).max()))
+        del Rr
+    print(f"[batched] packed vs separate max_abs = {worst:.3e}")
+    assert worst <= 1e-5
