@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--config", default="headline", choices=["headline", "small", "frame_region", "batched"])
     ap.add_argument("--rho", type=float, default=None, help="selected fraction (headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", default="step", choices=["step", "copy"],
+                    help="step: the hot path; copy: a plain 1 GiB fp32 copy through scatter_blend (no tokens), "
+                         "used to calibrate HBM byte counters and to measure achievable bandwidth")
     ap.add_argument("--select-every-step", type=int, default=1,
                     help="1: run mask+compaction in every step (default); 0: only when the active set changes")
     return ap.parse_args()
@@ -98,8 +101,39 @@ def cpu_baseline(wl) -> dict:
                       f"{dt:.1f} s, scaled x{m.L} blocks"}
 
 
+def copy_mode(args):
+    """Plain device copy of 2^28 fp32 values (1 GiB read + 1 GiB written) through
+    scatter_blend with no selected tokens, which is one grid-stride copy kernel."""
+    import torch
+
+    import paper_2511_18672_amd as S
+    import workloads as W
+
+    reqs = S.make_requests([W.Request(256, 512, 512)])
+    n = 16 * 256 * 256 * 256
+    src = torch.randn(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        S.sphinx_scatter_blend(reqs, None, None, 0, src, S.F32, dst, S.F32)
+    torch.cuda.synchronize()
+    S.sphinx_timing_enable(True)
+    for _ in range(args.steps):
+        S.sphinx_scatter_blend(reqs, None, None, 0, src, S.F32, dst, S.F32)
+    torch.cuda.synchronize()
+    cnt, ms = S.sphinx_timing_read()["scatter"]
+    S.sphinx_timing_enable(False)
+    assert torch.equal(src, dst)
+    nbytes = 2 * 4 * n
+    avg_s = ms / cnt / 1e3
+    print(json.dumps({"mode": "copy", "bytes_per_launch": nbytes, "launches": cnt, "avg_us": round(avg_s * 1e6, 2),
+                      "GB/s": round(nbytes / avg_s / 1e9, 1), "frac_of_8TBs": round(nbytes / avg_s / 8e12, 4)}),
+          flush=True)
+
+
 def main():
     args = parse()
+    if args.mode == "copy" and args.gpus == 1:
+        return copy_mode(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               f"(the selective-refinement step is built and measured on a single MI355X)", file=sys.stderr)

@@ -12,12 +12,18 @@
 //  * P^T stays in registers and is fed directly as the B operand of
 //    O^T = V^T P^T.  The MFMA sums over k-slots; a slot (g = lane/32, j) of
 //    P^T holds key 16*half + 8*(j/4) + 4*g + j%4 of the 32-key block, and the
-//    V^T A-operand is read with the same key permutation (two 8-byte LDS reads);
+//    V^T tile is stored with the same key permutation inside each 16-key group,
+//    so each A-operand fragment is one 16-byte LDS read;
 //  * the output O^T lands with the query on the lane, so the final 1/l
 //    normalisation is lane-local;
 //  * softmax in base 2 with the 1/sqrt(d) scale folded into log2(e)/sqrt(d);
-//    P is rounded to bf16 for the PV product, the running sum uses fp32 P.
-// Workgroups of the longest segment are scheduled first.
+//    the running max is only moved (and O, l rescaled) when a tile raises it
+//    by more than 8 in log2 units, so P <= 2^8; P is rounded to bf16 for the PV
+//    product and the row sum adds the same rounded values (v_dot2 with ones);
+//  * only the last key tile of a segment is masked; K/V tiles are double
+//    buffered in LDS, the next tile's global loads overlapping this tile.
+// Workgroups of the longest segment are scheduled first, and the linear
+// workgroup order is remapped so that each XCD works on whole heads.
 //
 // fp32 path (fp32 models, head_dim <= 64): one thread per (query, head).
 #include "kernels.hpp"
@@ -30,19 +36,110 @@ constexpr int AK = 64;   // keys per LDS tile
 constexpr int HD = 64;   // head_dim of the bf16 path
 constexpr int KLD = HD + 8;
 constexpr int VLD = AK + 8;
+constexpr float kRescaleLog2 = 8.0f;  // rescale only when the running max grows by > 2^8
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Column of key k in a V^T row.  Inside each group of 16 keys the order is
+// 0-3, 8-11, 4-7, 12-15, so the eight keys that lane group g feeds to one
+// PV k-step (4g..4g+3 and 8+4g..8+4g+3) are contiguous: one 16-byte read.
+__device__ __forceinline__ int vcol(int k) { return (k & ~15) | (k & 3) | ((k & 8) >> 1) | ((k & 4) << 1); }
+
+struct AttnSmem {
+  bf16 k[2][AK * KLD];  // K tile, [key][d]
+  bf16 v[2][HD * VLD];  // V tile transposed, [d][vcol(key)]
+};
+
+// One 64-key tile for the 32 queries of this wave.  Scores are S^T = K Q^T:
+// s[kb][r] is key 32*kb + 8*(r/4) + 4*g + r%4 against query r32 of the wave.
+template <bool MASK>
+__device__ __forceinline__ void attn_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
+                                          const bf16x8 (&qf)[4], int g, int r32, int kbase, int L,
+                                          float scale_log2, float& m_run, float& l_run, f32x16 (&oacc)[2]) {
+  f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&sK[r32 * KLD + ks * 16 + g * 8]);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&sK[(32 + r32) * KLD + ks * 16 + g * 8]);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
+  }
+  if (MASK) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = kbase + (r >> 2) * 8 + g * 4 + (r & 3);
+      if (key >= L) s0[r] = -INFINITY;
+      if (key + 32 >= L) s1[r] = -INFINITY;
+    }
+  }
+  float m4[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float t = fmaxf(fmaxf(s0[4 * q], s0[4 * q + 1]), s0[4 * q + 2]);
+    t = fmaxf(fmaxf(t, s0[4 * q + 3]), s1[4 * q]);
+    t = fmaxf(fmaxf(t, s1[4 * q + 1]), s1[4 * q + 2]);
+    m4[q] = fmaxf(t, s1[4 * q + 3]);
+  }
+  float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
+  // lanes l and l^32 hold the same query and see the same mx: same decision
+  if (mx > m_run + kRescaleLog2) {
+    const float alpha = fast_exp2(m_run - mx);
+    l_run *= alpha;
+    oacc[0] *= alpha;
+    oacc[1] *= alpha;
+    m_run = mx;
+  }
+  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+  bf16x8 pf[2][2];
+  float psum = 0.0f;
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = hf * 8 + 2 * i;
+      bf16x2 a, b;
+      a[0] = (bf16)fast_exp2(fmaf(s0[r], scale_log2, -m_run));
+      a[1] = (bf16)fast_exp2(fmaf(s0[r + 1], scale_log2, -m_run));
+      b[0] = (bf16)fast_exp2(fmaf(s1[r], scale_log2, -m_run));
+      b[1] = (bf16)fast_exp2(fmaf(s1[r + 1], scale_log2, -m_run));
+      psum = __builtin_amdgcn_fdot2_f32_bf16(a, ones, psum, false);
+      psum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, psum, false);
+      pf[0][hf][2 * i] = a[0];
+      pf[0][hf][2 * i + 1] = a[1];
+      pf[1][hf][2 * i] = b[0];
+      pf[1][hf][2 * i + 1] = b[1];
+    }
+  l_run += psum;
+  // O^T += V^T P^T; P^T k-slot (g, j) of half hf is key 16*hf + 8*(j/4) + 4*g + j%4
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int db = 0; db < 2; ++db) {
+        const bf16x8 vf =
+            *reinterpret_cast<const bf16x8*>(&sV[(db * 32 + r32) * VLD + kb * 32 + hf * 16 + g * 8]);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
+      }
+}
+
 __global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D,
-                                                      float scale_log2, SegTable S) {
-  __shared__ __attribute__((aligned(16))) bf16 sK[AK * KLD];
-  __shared__ __attribute__((aligned(16))) bf16 sV[HD * VLD];
+                                                      int heads, float scale_log2, SegTable S) {
+  __shared__ __attribute__((aligned(16))) AttnSmem sm;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
-  const int head = blockIdx.y;
+  // Workgroups are dealt to the 8 XCDs round-robin by linear id.  Renumber them
+  // so that each XCD receives a contiguous range of (head, query tile) work,
+  // i.e. whole heads, keeping a head's K and V in that XCD's L2.
+  const int ntiles = S.tile_prefix[S.nseg];
+  const int work = ntiles * heads;
+  int lid = (int)blockIdx.x;
+  if (work % 8 == 0) lid = (lid & 7) * (work >> 3) + (lid >> 3);
+  const int head = lid / ntiles, tile = lid - head * ntiles;
   int s = 0;
-  while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= (int)blockIdx.x) ++s;
-  const int qt = (int)blockIdx.x - S.tile_prefix[s];
+  while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
+  const int qt = tile - S.tile_prefix[s];
   const int seg0 = S.start[s], L = S.len[s];
   const int64_t ld = 3 * (int64_t)D;
   const bf16* Qg = qkv + head * HD;
@@ -56,87 +153,52 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ q
   for (int ks = 0; ks < 4; ++ks)
     qf[ks] = (ql < L) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(seg0 + ql) * ld + ks * 16 + g * 8) : zero8;
 
+  // loader roles: K rows (tid>>3) and 32+(tid>>3), 16-byte chunk tid&7;
+  // V key pair (2p, 2p+1), 8-wide d chunk c.  Rows past the segment end are
+  // clamped to its last key: their scores are masked to -inf, so they get
+  // weight exactly 0 and their (finite) values never contribute.
+  const int krow = tid >> 3, kch = (tid & 7) * 8;
+  const int vp = tid & 31, vc = tid >> 5;
+  const bf16* kbase_ptr = Kg + (int64_t)seg0 * ld + kch;
+  const bf16* vbase_ptr = Vg + (int64_t)seg0 * ld + vc * 8;
+  bf16x8 rk[2], rv[2];
+  auto gload = [&](int kbase) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int key = min(kbase + krow + 32 * i, L - 1);
+      rk[i] = *reinterpret_cast<const bf16x8*>(kbase_ptr + (int64_t)key * ld);
+      const int vk = min(kbase + 2 * vp + i, L - 1);
+      rv[i] = *reinterpret_cast<const bf16x8*>(vbase_ptr + (int64_t)vk * ld);
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) *reinterpret_cast<bf16x8*>(&sm.k[buf][(krow + 32 * i) * KLD + kch]) = rk[i];
+    const int col = vcol(2 * vp);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      bf16x2 pr;
+      pr[0] = rv[0][i];
+      pr[1] = rv[1][i];
+      *reinterpret_cast<bf16x2*>(&sm.v[buf][(vc * 8 + i) * VLD + col]) = pr;
+    }
+  };
+
   f32x16 oacc[2] = {f32x16{}, f32x16{}};
   float m_run = -INFINITY, l_run = 0.0f;
   const int nkt = (L + AK - 1) / AK;
+  const int nfull = L / AK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
-    const int kbase = kt * AK;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int key = (tid >> 3) + 32 * i, ch = (tid & 7) * 8;
-      const bf16x8 v = (kbase + key < L)
-                           ? *reinterpret_cast<const bf16x8*>(Kg + (int64_t)(seg0 + kbase + key) * ld + ch)
-                           : zero8;
-      *reinterpret_cast<bf16x8*>(&sK[key * KLD + ch]) = v;
-    }
-    {
-      const int p = tid & 31, c = tid >> 5;
-      const int k0 = kbase + 2 * p;
-      const bf16x8 v0 = (k0 < L) ? *reinterpret_cast<const bf16x8*>(Vg + (int64_t)(seg0 + k0) * ld + c * 8) : zero8;
-      const bf16x8 v1 =
-          (k0 + 1 < L) ? *reinterpret_cast<const bf16x8*>(Vg + (int64_t)(seg0 + k0 + 1) * ld + c * 8) : zero8;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        bf16x2 pr;
-        pr[0] = v0[i];
-        pr[1] = v1[i];
-        *reinterpret_cast<bf16x2*>(&sV[(c * 8 + i) * VLD + 2 * p]) = pr;
-      }
-    }
-    __syncthreads();
-
-    f32x16 sacc[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      sacc[kb] = f32x16{};
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[(kb * 32 + r32) * KLD + ks * 16 + g * 8]);
-        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], sacc[kb], 0, 0, 0);
-      }
-    }
-    // sacc[kb][r] = score of key kbase + 32*kb + 8*(r/4) + 4*g + r%4 with query r32
-    if (kbase + AK > L) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (kbase + kb * 32 + (r >> 2) * 8 + g * 4 + (r & 3) >= L) sacc[kb][r] = -INFINITY;
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float m_new = fmaxf(m_run, mx * scale_log2);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
-    float psum = 0.0f;
-    bf16x8 pf[2][2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pv = fast_exp2(fmaf(sacc[kb][r], scale_log2, -m_new));
-        psum += pv;
-        pf[kb][r >> 3][r & 7] = (bf16)pv;
-      }
-    l_run = fmaf(l_run, alpha, psum);
-#pragma unroll
-    for (int db = 0; db < 2; ++db) oacc[db] *= alpha;
-#pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const bf16* vrow = &sV[(db * 32 + r32) * VLD + kb * 32 + hf * 16 + g * 4];
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 8);
-          const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
-        }
+    const int buf = kt & 1;
+    if (kt + 1 < nkt) gload((kt + 1) * AK);
+    if (kt < nfull)
+      attn_tile<false>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
+    else
+      attn_tile<true>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
+    if (kt + 1 < nkt) sstore(buf ^ 1);
     __syncthreads();
   }
   l_run += __shfl_xor(l_run, 32, kWave);
@@ -200,8 +262,7 @@ hipError_t launch_attention(sphinx_dtype dt, const void* qkv, void* o, int D, in
                             const SegTable& S, hipStream_t s) {
   if (dt == SPHINX_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
-    const dim3 grid(S.tile_prefix[S.nseg], heads);
-    k_attn_bf16<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, scale_log2, S);
+    k_attn_bf16<<<S.tile_prefix[S.nseg] * heads, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
   } else {
     const float scale = 1.0f / sqrtf((float)head_dim);
     k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>((const float*)qkv, (float*)o, D, head_dim, heads, n, scale, S);

@@ -10,7 +10,8 @@
 // W are both K-contiguous, so every operand fragment is one 16-byte LDS read.
 // LDS rows are padded by 16 bytes against bank conflicts; two LDS buffers let
 // the global loads of the next K step overlap the MFMAs of the current one.
-// Rows past M load zeros and are not stored.
+// Rows past M load zeros and are not stored.  The epilogue stages the fp32
+// tile in LDS and finishes it with 16-byte row-contiguous loads and stores.
 //
 // fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
 #include "kernels.hpp"
@@ -31,12 +32,17 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 }
 
 constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
+constexpr int CLD = BN + 4;  // fp32 staging row of the epilogue
+constexpr int kGemmSmem = 2 * (BM + BN) * LDK * 2;
+static_assert(BM * CLD * 4 <= kGemmSmem, "epilogue staging must fit in the operand buffers");
 
 template <int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                       const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * LDK];
+  // one LDS block: two A and two B operand buffers, reused as the fp32 C tile
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kGemmSmem];
+  bf16(*sA)[BM * LDK] = reinterpret_cast<bf16(*)[BM * LDK]>(smem);
+  bf16(*sB)[BN * LDK] = reinterpret_cast<bf16(*)[BN * LDK]>(smem + 2 * BM * LDK * sizeof(bf16));
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
@@ -95,18 +101,70 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
     __syncthreads();
   }
 
-  // accumulator (i, j) register r holds row 8*(r/4) + 4*g + r%4, column r32 of its 32x32 block
+  // Epilogue through LDS: each wave parks its 64x64 fp32 tile (register r of
+  // block (i, j) is row 8*(r/4) + 4*g + r%4, column r32), then every thread
+  // finishes 4-wide row segments with coalesced 16-byte loads and stores.
+  float* sC = reinterpret_cast<float*>(smem);  // [BM][CLD], reuses the operand buffers
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + wn * 64 + j * 32 + r32;
-    const float bv = (float)bias[n];
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 64 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3);
-        if (m < M) epi_store<EPI, bf16>(e, m, n, acc[i][j][r] + bv);
+      for (int r = 0; r < 16; ++r)
+        sC[(wm * 64 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * CLD + wn * 64 + j * 32 + r32] = acc[i][j][r];
+  __syncthreads();
+  const int c4 = (tid & 31) * 4;  // column inside the tile
+  const int n = n0 + c4;
+  float4 bv;
+  {
+    const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n);
+    bv = make_float4((float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]);
+  }
+#pragma unroll
+  for (int q0 = 0; q0 < BM / 8; q0 += 4) {
+    float4 v[4], hv[4], gv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int row = (q0 + u) * 8 + (tid >> 5);
+      const int m = m0 + row;
+      v[u] = *reinterpret_cast<const float4*>(&sC[row * CLD + c4]);
+      v[u].x += bv.x;
+      v[u].y += bv.y;
+      v[u].z += bv.z;
+      v[u].w += bv.w;
+      if constexpr (EPI == EPI_GATED) {
+        if (m < M) {
+          hv[u] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(e.out) + (int64_t)m * e.ldo + n);
+          gv[u] = *reinterpret_cast<const float4*>(e.gate + (int64_t)e.crow[m] * e.ldg + n);
+        }
       }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int m = m0 + (q0 + u) * 8 + (tid >> 5);
+      if (m >= M) continue;
+      if constexpr (EPI == EPI_GATED) {
+        float4 h = hv[u];
+        h.x = fmaf(1.0f + gv[u].x, v[u].x, h.x);
+        h.y = fmaf(1.0f + gv[u].y, v[u].y, h.y);
+        h.z = fmaf(1.0f + gv[u].z, v[u].z, h.z);
+        h.w = fmaf(1.0f + gv[u].w, v[u].w, h.w);
+        *reinterpret_cast<float4*>(reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n) = h;
+      } else {
+        if constexpr (EPI == EPI_GELU) {
+          v[u].x = gelu_tanh(v[u].x);
+          v[u].y = gelu_tanh(v[u].y);
+          v[u].z = gelu_tanh(v[u].z);
+          v[u].w = gelu_tanh(v[u].w);
+        }
+        bf16x4 o;
+        o[0] = (bf16)v[u].x;
+        o[1] = (bf16)v[u].y;
+        o[2] = (bf16)v[u].z;
+        o[3] = (bf16)v[u].w;
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
+      }
+    }
   }
 }
 

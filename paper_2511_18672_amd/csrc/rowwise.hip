@@ -57,24 +57,102 @@ __device__ __forceinline__ void row_stats(const float* __restrict__ hr, int D, i
   rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
 }
 
-template <typename OT>
+template <int V> struct VecF;
+template <> struct VecF<1> {
+  typedef float T;
+  static __device__ __forceinline__ float get(const T& v, int i) { return v; }
+};
+template <> struct VecF<2> {
+  typedef float2 T;
+  static __device__ __forceinline__ float get(const T& v, int i) { return i == 0 ? v.x : v.y; }
+};
+template <> struct VecF<4> {
+  typedef float4 T;
+  static __device__ __forceinline__ float get(const T& v, int i) {
+    return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
+  }
+};
+
+template <typename OT, int V> struct VecStore;
+template <typename OT> struct VecStore<OT, 1> {
+  static __device__ __forceinline__ void put(OT* p, const float (&v)[1]) { *p = store_from_f32<OT>(v[0]); }
+};
+template <> struct VecStore<float, 2> {
+  static __device__ __forceinline__ void put(float* p, const float (&v)[2]) {
+    *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+  }
+};
+template <> struct VecStore<float, 4> {
+  static __device__ __forceinline__ void put(float* p, const float (&v)[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+};
+template <> struct VecStore<bf16, 2> {
+  static __device__ __forceinline__ void put(bf16* p, const float (&v)[2]) {
+    bf16x2 o;
+    o[0] = (bf16)v[0];
+    o[1] = (bf16)v[1];
+    *reinterpret_cast<bf16x2*>(p) = o;
+  }
+};
+template <> struct VecStore<bf16, 4> {
+  static __device__ __forceinline__ void put(bf16* p, const float (&v)[4]) {
+    bf16x4 o;
+    o[0] = (bf16)v[0];
+    o[1] = (bf16)v[1];
+    o[2] = (bf16)v[2];
+    o[3] = (bf16)v[3];
+    *reinterpret_cast<bf16x4*>(p) = o;
+  }
+};
+
+// One wave per row; lane handles V consecutive values per 64*V-wide chunk, so
+// every load and store of a wave is one contiguous 256*V- (fp32) or 128*V-byte run.
+template <typename OT, int V>
 __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, int n, int D,
                                                  const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
                                                  const int32_t* __restrict__ crow, OT* __restrict__ out) {
+  typedef typename VecF<V>::T VT;
+  constexpr int kMaxChunks = kMaxPer / V;
   const int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
   if (row >= n) return;
   const int lane = lane_id();
-  float v[kMaxPer];
-  float mu, rstd;
-  row_stats(h + (int64_t)row * D, D, lane, v, mu, rstd);
+  const int chunks = D / (kWave * V);
+  const float* hr = h + (int64_t)row * D;
+  VT v[kMaxChunks];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxChunks; ++i)
+    if (i < chunks) {
+      v[i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+#pragma unroll
+      for (int e = 0; e < V; ++e) s += VecF<V>::get(v[i], e);
+    }
+  const float mu = wave_sum(s) / (float)D;
+  float s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxChunks; ++i)
+    if (i < chunks) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        const float d = VecF<V>::get(v[i], e) - mu;
+        s2 = fmaf(d, d, s2);
+      }
+    }
+  const float rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
   const float* m = mod + (int64_t)crow[row] * ldm;
   OT* o = out + (int64_t)row * D;
-  const int per = D / kWave;
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i)
-    if (i < per) {
-      const int c = i * kWave + lane;
-      o[c] = store_from_f32<OT>(fmaf((v[i] - mu) * rstd, 1.0f + m[sc_off + c], m[sh_off + c]));
+  for (int i = 0; i < kMaxChunks; ++i)
+    if (i < chunks) {
+      const int c = (i * kWave + lane) * V;
+      const VT sh = *reinterpret_cast<const VT*>(m + sh_off + c);
+      const VT sc = *reinterpret_cast<const VT*>(m + sc_off + c);
+      float r[V];
+#pragma unroll
+      for (int e = 0; e < V; ++e)
+        r[e] = fmaf((VecF<V>::get(v[i], e) - mu) * rstd, 1.0f + VecF<V>::get(sc, e), VecF<V>::get(sh, e));
+      VecStore<OT, V>::put(o + c, r);
     }
 }
 
@@ -152,10 +230,18 @@ hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const vo
 hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
                          const int32_t* crow, void* out, sphinx_dtype odt, hipStream_t s) {
   const int g = (n + kRowsPerBlock - 1) / kRowsPerBlock;
-  if (odt == SPHINX_BF16)
-    k_ln_mod<bf16><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
-  else
-    k_ln_mod<float><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
+  // 16-byte vectors need every row and every modulation chunk on a 16-byte boundary
+  const bool v4 = (D % (kWave * 4) == 0) && (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
+  const bool v2 = (D % (kWave * 2) == 0) && (ldm % 2 == 0) && (sh_off % 2 == 0) && (sc_off % 2 == 0);
+  if (odt == SPHINX_BF16) {
+    if (v4) k_ln_mod<bf16, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
+    else if (v2) k_ln_mod<bf16, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
+    else k_ln_mod<bf16, 1><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
+  } else {
+    if (v4) k_ln_mod<float, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
+    else if (v2) k_ln_mod<float, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
+    else k_ln_mod<float, 1><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
+  }
   return hipGetLastError();
 }
 
