@@ -8,9 +8,10 @@
 // bf16 path (gfx950 MFMA): block tile 128x128, K step 64, 256 threads = 4 waves
 // in a 2x2 grid, each wave a 64x64 tile of 2x2 v_mfma_f32_32x32x16_bf16.  A and
 // W are both K-contiguous, so every operand fragment is one 16-byte LDS read.
-// LDS rows are padded by 16 bytes against bank conflicts; two LDS buffers let
-// the global loads of the next K step overlap the MFMAs of the current one.
-// Rows past M load zeros and are not stored.  The epilogue stages the fp32
+// LDS rows are padded by 16 bytes against bank conflicts.  Global loads run
+// two K steps ahead (two register sets, two LDS buffers, K loop unrolled by
+// two), which hides the L2/HBM latency behind the MFMAs.  Rows past M are
+// clamped to the last row and not stored.  The epilogue stages the fp32
 // tile in LDS and finishes it with 16-byte row-contiguous loads and stores.
 //
 // fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
@@ -48,19 +49,26 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int lrow = tid >> 3, lch = (tid & 7) * 8;
   const int g = lane >> 5, r32 = lane & 31;
-  bf16x8 ra[4], rb[4];
-  const bf16x8 zero = {};
-
-  auto gload = [&](int k0) {
+  // Row pointers of this thread's four A and four W rows.  Rows past M are
+  // clamped to M-1: they are computed like any other row and never stored.
+  const bf16* pa[4];
+  const bf16* pw[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = lrow + 32 * i;
+    pa[i] = A + (int64_t)min(m0 + r, M - 1) * K + lch;
+    pw[i] = W + (int64_t)(n0 + r) * K + lch;
+  }
+  // Two register sets: the global loads run two K steps ahead of the MFMAs.
+  bf16x8 ra0[4], rb0[4], ra1[4], rb1[4];
+  auto gload = [&](int k0, bf16x8 (&ra)[4], bf16x8 (&rb)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = lrow + 32 * i;
-      const int m = m0 + r;
-      ra[i] = (m < M) ? *reinterpret_cast<const bf16x8*>(A + (int64_t)m * K + k0 + lch) : zero;
-      rb[i] = *reinterpret_cast<const bf16x8*>(W + (int64_t)(n0 + r) * K + k0 + lch);
+      ra[i] = *reinterpret_cast<const bf16x8*>(pa[i] + k0);
+      rb[i] = *reinterpret_cast<const bf16x8*>(pw[i] + k0);
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](int buf, const bf16x8 (&ra)[4], const bf16x8 (&rb)[4]) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int r = lrow + 32 * i;
@@ -74,14 +82,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-
-  const int KT = K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * BK);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 af[2], bw[2];
@@ -97,7 +98,25 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
         for (int j = 0; j < 2; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < KT) sstore(buf ^ 1);
+  };
+
+  // K loop unrolled by two so that LDS buffers and register sets are static:
+  // even steps read LDS buffer 0 (register set 0 was stored there), odd steps
+  // buffer 1 (set 1).
+  const int KT = K / BK;
+  gload(0, ra0, rb0);
+  if (KT > 1) gload(BK, ra1, rb1);
+  sstore(0, ra0, rb0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; kt += 2) {
+    if (kt + 2 < KT) gload((kt + 2) * BK, ra0, rb0);
+    compute(0);
+    if (kt + 1 < KT) sstore(1, ra1, rb1);
+    __syncthreads();
+    if (kt + 1 >= KT) break;
+    if (kt + 3 < KT) gload((kt + 3) * BK, ra1, rb1);
+    compute(1);
+    if (kt + 2 < KT) sstore(0, ra0, rb0);
     __syncthreads();
   }
 
