@@ -71,7 +71,7 @@ typedef struct {
 typedef struct {
   int32_t D;        /* hidden size, = heads * head_dim */
   int32_t heads;
-  int32_t head_dim; /* 64 for bf16 models; 16..64 for f32 models */
+  int32_t head_dim; /* 64 or 72 for bf16 models; up to 64 for f32 models */
   int32_t mlp;      /* MLP hidden size */
   int32_t L;        /* number of blocks */
   sphinx_dtype dtype; /* storage and GEMM-operand type of weights/activations */

@@ -52,7 +52,8 @@ sphinx_status check_model(const sphinx_model_desc* m) {
   if ((int64_t)m->heads * m->head_dim != m->D) return SPHINX_E_INVALID;
   if (!valid_dtype(m->dtype)) return SPHINX_E_UNSUPPORTED;
   if (m->dtype == SPHINX_BF16) {
-    if (m->head_dim != 64 || m->D % 128 != 0 || m->mlp % 128 != 0 || m->D > 2048) return SPHINX_E_UNSUPPORTED;
+    if ((m->head_dim != 64 && m->head_dim != 72) || m->D % 128 != 0 || m->mlp % 128 != 0 || m->D > 2048)
+      return SPHINX_E_UNSUPPORTED;
   } else {
     if (m->head_dim > 64 || m->D % 64 != 0 || m->mlp % 64 != 0 || m->D > 512) return SPHINX_E_UNSUPPORTED;
   }

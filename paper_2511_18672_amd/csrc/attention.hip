@@ -2,7 +2,7 @@
 // (joint spatio-temporal attention of the denoiser blocks restricted to the
 // gathered tokens, Sec. 5.3 / Alg. 1 partial_step on the masked tokens).
 //
-// bf16 path, head_dim 64, gfx950 MFMA (flash-attention style, online softmax):
+// bf16 path, head_dim 64 or 72, gfx950 MFMA (flash-attention style, online softmax):
 //  * one workgroup = 128 queries of one segment and one head, 4 waves x 32
 //    queries; K/V tiles of 64 keys are staged in LDS (K row-major, V
 //    transposed to [d][key]);
@@ -24,6 +24,8 @@
 //    buffered in LDS, the next tile's global loads overlapping this tile.
 // Workgroups of the longest segment are scheduled first, and the linear
 // workgroup order is remapped so that each XCD works on whole heads.
+// head_dim 72 pads QK^T to 5 k-steps of 16 (d 72..79 zero) and computes O^T in
+// three 32-row blocks (rows 72..95 are computed from zero V^T rows and dropped).
 //
 // fp32 path (fp32 models, head_dim <= 64): one thread per (query, head).
 #include "kernels.hpp"
@@ -33,10 +35,21 @@ namespace sphinx {
 namespace {
 constexpr int AQ = 128;  // queries per workgroup
 constexpr int AK = 64;   // keys per LDS tile
-constexpr int HD = 64;   // head_dim of the bf16 path
-constexpr int KLD = HD + 8;
 constexpr int VLD = AK + 8;
 constexpr float kRescaleLog2 = 8.0f;  // rescale only when the running max grows by > 2^8
+static_assert(AQ == kAttnQueryTile, "host tile size must match the kernel");
+
+// Head-dimension dependent shape: HD = 64 or 72.
+template <int HD>
+struct AttnShape {
+  static constexpr int KS = (HD + 15) / 16;  // 16-deep k steps of QK^T (d padded with zeros)
+  static constexpr int DB = (HD + 31) / 32;  // 32-row blocks of O^T (rows past HD unused)
+  static constexpr int KCH = HD / 8;         // 16-byte chunks of one q/k/v row
+  static constexpr int KLD = KS * 16 + 8;    // K tile row stride (bf16)
+  static constexpr int VROWS = DB * 32;      // rows of the V^T tile
+  static constexpr int KLOADS = (AK * KCH + 255) / 256;       // K chunks per thread
+  static constexpr int VLOADS = ((AK / 2) * KCH + 255) / 256;  // V key-pair chunks per thread
+};
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -45,22 +58,25 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // PV k-step (4g..4g+3 and 8+4g..8+4g+3) are contiguous: one 16-byte read.
 __device__ __forceinline__ int vcol(int k) { return (k & ~15) | (k & 3) | ((k & 8) >> 1) | ((k & 4) << 1); }
 
+template <int HD>
 struct AttnSmem {
-  bf16 k[2][AK * KLD];  // K tile, [key][d]
-  bf16 v[2][HD * VLD];  // V tile transposed, [d][vcol(key)]
+  bf16 k[2][AK * AttnShape<HD>::KLD];        // K tile, [key][d], d >= HD zero
+  bf16 v[2][AttnShape<HD>::VROWS * VLD];     // V tile transposed, [d][vcol(key)], d >= HD zero
 };
 
 // One 64-key tile for the 32 queries of this wave.  Scores are S^T = K Q^T:
 // s[kb][r] is key 32*kb + 8*(r/4) + 4*g + r%4 against query r32 of the wave.
-template <bool MASK>
+template <int HD, bool MASK>
 __device__ __forceinline__ void attn_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
-                                          const bf16x8 (&qf)[4], int g, int r32, int kbase, int L,
-                                          float scale_log2, float& m_run, float& l_run, f32x16 (&oacc)[2]) {
+                                          const bf16x8 (&qf)[AttnShape<HD>::KS], int g, int r32, int kbase, int L,
+                                          float scale_log2, float& m_run, float& l_run,
+                                          f32x16 (&oacc)[AttnShape<HD>::DB]) {
+  typedef AttnShape<HD> SH;
   f32x16 s0 = f32x16{}, s1 = f32x16{};
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&sK[r32 * KLD + ks * 16 + g * 8]);
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&sK[(32 + r32) * KLD + ks * 16 + g * 8]);
+  for (int ks = 0; ks < SH::KS; ++ks) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&sK[r32 * SH::KLD + ks * 16 + g * 8]);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&sK[(32 + r32) * SH::KLD + ks * 16 + g * 8]);
     s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
   }
@@ -86,8 +102,8 @@ __device__ __forceinline__ void attn_tile(const bf16* __restrict__ sK, const bf1
   if (mx > m_run + kRescaleLog2) {
     const float alpha = fast_exp2(m_run - mx);
     l_run *= alpha;
-    oacc[0] *= alpha;
-    oacc[1] *= alpha;
+#pragma unroll
+    for (int db = 0; db < SH::DB; ++db) oacc[db] *= alpha;
     m_run = mx;
   }
   const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
@@ -117,16 +133,17 @@ __device__ __forceinline__ void attn_tile(const bf16* __restrict__ sK, const bf1
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-      for (int db = 0; db < 2; ++db) {
+      for (int db = 0; db < SH::DB; ++db) {
         const bf16x8 vf =
             *reinterpret_cast<const bf16x8*>(&sV[(db * 32 + r32) * VLD + kb * 32 + hf * 16 + g * 8]);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
       }
 }
 
-__global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D,
-                                                      int heads, float scale_log2, SegTable S) {
-  __shared__ __attribute__((aligned(16))) AttnSmem sm;
+template <int HD>
+__device__ __forceinline__ void attn_body(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D, int heads,
+                                          float scale_log2, const SegTable& S, AttnSmem<HD>& sm) {
+  typedef AttnShape<HD> SH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
   // Workgroups are dealt to the 8 XCDs round-robin by linear id.  Renumber them
@@ -147,44 +164,83 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ q
   const bf16* Vg = qkv + 2 * D + head * HD;
   const bf16x8 zero8 = {};
 
-  const int ql = qt * AQ + wave * 32 + r32;
-  bf16x8 qf[4];
+  // d columns past HD stay zero in both LDS buffers for the whole kernel
+  if (SH::KS * 16 != HD) {
+    for (int i = tid; i < 2 * AK; i += 256) {
+      const int b = i / AK, key = i % AK;
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
-    qf[ks] = (ql < L) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(seg0 + ql) * ld + ks * 16 + g * 8) : zero8;
+      for (int d = HD; d < SH::KS * 16; ++d) sm.k[b][key * SH::KLD + d] = (bf16)0.0f;
+    }
+  }
+  if (SH::VROWS != HD) {
+    for (int i = tid; i < 2 * (SH::VROWS - HD) * VLD; i += 256) {
+      const int b = i / ((SH::VROWS - HD) * VLD), rem = i % ((SH::VROWS - HD) * VLD);
+      sm.v[b][HD * VLD + rem] = (bf16)0.0f;
+    }
+  }
 
-  // loader roles: K rows (tid>>3) and 32+(tid>>3), 16-byte chunk tid&7;
-  // V key pair (2p, 2p+1), 8-wide d chunk c.  Rows past the segment end are
-  // clamped to its last key: their scores are masked to -inf, so they get
-  // weight exactly 0 and their (finite) values never contribute.
-  const int krow = tid >> 3, kch = (tid & 7) * 8;
-  const int vp = tid & 31, vc = tid >> 5;
-  const bf16* kbase_ptr = Kg + (int64_t)seg0 * ld + kch;
-  const bf16* vbase_ptr = Vg + (int64_t)seg0 * ld + vc * 8;
-  bf16x8 rk[2], rv[2];
+  const int ql = qt * AQ + wave * 32 + r32;
+  bf16x8 qf[SH::KS];
+#pragma unroll
+  for (int ks = 0; ks < SH::KS; ++ks) {
+    const int d0 = ks * 16 + g * 8;
+    qf[ks] = (ql < L && d0 < HD) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(seg0 + ql) * ld + d0) : zero8;
+  }
+
+  // Loaders: K as (key, 16-byte chunk) and V as (key pair, chunk) work items
+  // spread over the 256 threads.  Rows past the segment end are clamped to its
+  // last key: their scores are masked to -inf, so they get weight exactly 0 and
+  // their (finite) values never contribute.
+  const bf16* kptr = Kg + (int64_t)seg0 * ld;
+  const bf16* vptr = Vg + (int64_t)seg0 * ld;
+  bf16x8 rk[SH::KLOADS], rv[2 * SH::VLOADS];
   auto gload = [&](int kbase) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int key = min(kbase + krow + 32 * i, L - 1);
-      rk[i] = *reinterpret_cast<const bf16x8*>(kbase_ptr + (int64_t)key * ld);
-      const int vk = min(kbase + 2 * vp + i, L - 1);
-      rv[i] = *reinterpret_cast<const bf16x8*>(vbase_ptr + (int64_t)vk * ld);
+    for (int i = 0; i < SH::KLOADS; ++i) {
+      const int c = tid + 256 * i;
+      if (c < AK * SH::KCH) {
+        const int key = min(kbase + c / SH::KCH, L - 1);
+        rk[i] = *reinterpret_cast<const bf16x8*>(kptr + (int64_t)key * ld + (c % SH::KCH) * 8);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < SH::VLOADS; ++i) {
+      const int c = tid + 256 * i;
+      if (c < (AK / 2) * SH::KCH) {
+        const int p = c % 32, vc = c / 32;
+        const int k0 = min(kbase + 2 * p, L - 1), k1 = min(kbase + 2 * p + 1, L - 1);
+        rv[2 * i] = *reinterpret_cast<const bf16x8*>(vptr + (int64_t)k0 * ld + vc * 8);
+        rv[2 * i + 1] = *reinterpret_cast<const bf16x8*>(vptr + (int64_t)k1 * ld + vc * 8);
+      }
     }
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) *reinterpret_cast<bf16x8*>(&sm.k[buf][(krow + 32 * i) * KLD + kch]) = rk[i];
-    const int col = vcol(2 * vp);
+    for (int i = 0; i < SH::KLOADS; ++i) {
+      const int c = tid + 256 * i;
+      if (c < AK * SH::KCH)
+        *reinterpret_cast<bf16x8*>(&sm.k[buf][(c / SH::KCH) * SH::KLD + (c % SH::KCH) * 8]) = rk[i];
+    }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      bf16x2 pr;
-      pr[0] = rv[0][i];
-      pr[1] = rv[1][i];
-      *reinterpret_cast<bf16x2*>(&sm.v[buf][(vc * 8 + i) * VLD + col]) = pr;
+    for (int i = 0; i < SH::VLOADS; ++i) {
+      const int c = tid + 256 * i;
+      if (c < (AK / 2) * SH::KCH) {
+        const int p = c % 32, vc = c / 32;
+        const int col = vcol(2 * p);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          bf16x2 pr;
+          pr[0] = rv[2 * i][e];
+          pr[1] = rv[2 * i + 1][e];
+          *reinterpret_cast<bf16x2*>(&sm.v[buf][(vc * 8 + e) * VLD + col]) = pr;
+        }
+      }
     }
   };
 
-  f32x16 oacc[2] = {f32x16{}, f32x16{}};
+  f32x16 oacc[SH::DB];
+#pragma unroll
+  for (int db = 0; db < SH::DB; ++db) oacc[db] = f32x16{};
   float m_run = -INFINITY, l_run = 0.0f;
   const int nkt = (L + AK - 1) / AK;
   const int nfull = L / AK;
@@ -195,9 +251,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ q
     const int buf = kt & 1;
     if (kt + 1 < nkt) gload((kt + 1) * AK);
     if (kt < nfull)
-      attn_tile<false>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
+      attn_tile<HD, false>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
     else
-      attn_tile<true>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
+      attn_tile<HD, true>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
     if (kt + 1 < nkt) sstore(buf ^ 1);
     __syncthreads();
   }
@@ -206,15 +262,30 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ q
     const float inv = 1.0f / l_run;
     bf16* orow = o + (int64_t)(seg0 + ql) * D + head * HD;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < SH::DB; ++db)
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
-        bf16x4 ov;
+        const int d = db * 32 + rr * 8 + g * 4;  // output rows d .. d+3 of this register group
+        if (d < HD) {
+          bf16x4 ov;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) ov[t] = (bf16)(oacc[db][rr * 4 + t] * inv);
-        *reinterpret_cast<bf16x4*>(orow + db * 32 + rr * 8 + g * 4) = ov;
+          for (int t = 0; t < 4; ++t) ov[t] = (bf16)(oacc[db][rr * 4 + t] * inv);
+          *reinterpret_cast<bf16x4*>(orow + d) = ov;
+        }
       }
   }
+}
+
+__global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D,
+                                                      int heads, float scale_log2, SegTable S) {
+  __shared__ __attribute__((aligned(16))) AttnSmem<64> sm;
+  attn_body<64>(qkv, o, D, heads, scale_log2, S, sm);
+}
+
+__global__ __launch_bounds__(256, 2) void k_attn_bf16_d72(const bf16* __restrict__ qkv, bf16* __restrict__ o,
+                                                          int D, int heads, float scale_log2, SegTable S) {
+  __shared__ __attribute__((aligned(16))) AttnSmem<72> sm;
+  attn_body<72>(qkv, o, D, heads, scale_log2, S, sm);
 }
 
 constexpr int kF32Max = 64;
@@ -262,7 +333,11 @@ hipError_t launch_attention(sphinx_dtype dt, const void* qkv, void* o, int D, in
                             const SegTable& S, hipStream_t s) {
   if (dt == SPHINX_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
-    k_attn_bf16<<<S.tile_prefix[S.nseg] * heads, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
+    const int grid = S.tile_prefix[S.nseg] * heads;
+    if (head_dim == 64)
+      k_attn_bf16<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
+    else
+      k_attn_bf16_d72<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
   } else {
     const float scale = 1.0f / sqrtf((float)head_dim);
     k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>((const float*)qkv, (float*)o, D, head_dim, heads, n, scale, S);

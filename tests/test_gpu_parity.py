@@ -260,3 +260,58 @@ def test_batched_packed_equals_separate():
         del Rr
     print(f"[batched] packed vs separate max_abs = {worst:.3e}")
     assert worst <= 1e-5
+
+
+XL1 = W.ModelCfg(D=1152, heads=16, head_dim=72, mlp=4608, L=1, dtype="bf16")
+
+
+def test_frame_region_small_end_to_end_d72():
+    """head_dim 72 (the DiT-XL-like denoiser) end to end on a reduced
+    frame+region workload: 21 frames, top-8 fully refined, the rest 15 %,
+    per-frame start times, 25 steps on one shared grid."""
+    wl = W.build("frame_region_small", W.ModelCfg(D=1152, heads=16, head_dim=72, mlp=4608, L=2, dtype="bf16"),
+                 [W.Request(21, 16, 16)], ["blobs"], [("frames_top_then_rho", 8, 0.15)],
+                 [("uniform", 0.3, 0.7)], [25])
+    check_end_to_end(wl, teacher_forced=False)
+
+
+def test_frame_region_full_shape_one_block_step():
+    """Frame+region at its full shape (21 x 64x64 latent) with a one-block
+    head_dim-72 denoiser: run until every frame is active, then compare the
+    next step teacher-forced with the oracle."""
+    wl = W.frame_region(model=XL1)
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    k = next(i for i, p in enumerate(plans) if p.active.all())
+    R, states, sels = run_gpu(wl, trace=True, steps=k + 1)
+    assert sels[k][0] == 10194
+    res = O.step(wl, O.model_from_workload(wl), states[k], plans[k], "model")
+    assert np.array_equal(sels[k][1], res.idx)
+    assert _report(f"frame_region L=1 step {k} (teacher-forced)", states[k + 1], res.state) <= TOL["bf16"]
+
+
+def test_frame_region_full_depth_properties():
+    """28-block head_dim-72 denoiser at the full frame+region shape: two
+    steps, deterministic, unselected tokens untouched, finite."""
+    wl = W.frame_region()
+    _, s1, sel1 = run_gpu(wl, trace=True, steps=2)
+    _, s2, _ = run_gpu(wl, trace=True, steps=2)
+    assert np.array_equal(s1[2], s2[2])
+    P0, P2 = O.patchify(s1[0], wl.requests), O.patchify(s1[2], wl.requests)
+    moved = np.zeros(wl.N, bool)
+    for n, idx, _ in sel1:
+        moved[idx] = True
+    assert np.array_equal(P2[~moved], P0[~moved])
+    assert np.isfinite(P2).all()
+    print(f"[frame_region] 28 blocks, n_sel per step {[n for n, _, _ in sel1]}")
+
+
+def test_batched_full_shape_one_block_step():
+    """The four-request batch at its full shape (30 925 selected tokens in four
+    segments of 154 .. 12 902) with a one-block denoiser, against the oracle."""
+    model = W.ModelCfg(D=1024, heads=16, head_dim=64, mlp=4096, L=1, dtype="bf16")
+    wl = W.batched(model=model)
+    R, states, sels = run_gpu(wl, trace=True, steps=1)
+    assert sels[0][0] == 30925 and list(np.diff(sels[0][2])) == [154, 9677, 12902, 8192]
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    res = O.step(wl, O.model_from_workload(wl), wl.z0, plans[0], "model")
+    assert _report("batched L=1 step 0", states[1], res.state) <= TOL["bf16"]
