@@ -40,9 +40,11 @@ def parse():
     ap.add_argument("--config", default="headline", choices=["headline", "small", "frame_region", "batched"])
     ap.add_argument("--rho", type=float, default=None, help="selected fraction (headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", default="step", choices=["step", "copy"],
+    ap.add_argument("--mode", default="step", choices=["step", "copy", "sweep"],
                     help="step: the hot path; copy: a plain 1 GiB fp32 copy through scatter_blend (no tokens), "
-                         "used to calibrate HBM byte counters and to measure achievable bandwidth")
+                         "used to calibrate HBM byte counters and to measure achievable bandwidth; sweep: "
+                         "mask/compaction, gather and scatter at 2^20..2^26 tokens against the HBM roofline")
+    ap.add_argument("--sweep-log2", default="20,22,24,26", help="token counts of the sweep (log2)")
     ap.add_argument("--select-every-step", type=int, default=1,
                     help="1: run mask+compaction in every step (default); 0: only when the active set changes")
     return ap.parse_args()
@@ -130,8 +132,96 @@ def copy_mode(args):
           flush=True)
 
 
+def sweep_mode(args):
+    """HBM roofline of the memory-bound kernels at large token counts.
+
+    One request of F frames of a 4x512x512 latent (2^16 tokens per frame),
+    30 % selected, with two selection recipes: uniform random (worst case for
+    the gathers: selected tokens are isolated) and Gaussian blobs at the
+    headline map's density (clustered).  Algorithmic bytes per launch:
+      select  : 4 N (u) + N (mask) + 4 n_sel (idx)
+      gather  : n_sel (4 idx + 64 state + 64 x_sel) [+ 32 n_sel bf16 noise when injecting]
+      scatter : n_sel (4 idx + 64 x_sel + 64 state)
+    """
+    import torch
+
+    import paper_2511_18672_amd as S
+    import workloads as W
+
+    torch.manual_seed(5)
+    for lg in [int(x) for x in args.sweep_log2.split(",")]:
+        N = 1 << lg
+        F = N >> 16
+        reqs = S.make_requests([W.Request(F, 512, 512)])
+        state = torch.randn(16 * N, dtype=torch.float32, device="cuda")
+        eps = torch.randn(16 * N, dtype=torch.bfloat16, device="cuda")
+        mask = torch.empty(N, dtype=torch.uint8, device="cuda")
+        idx = torch.empty(N, dtype=torch.int32, device="cuda")
+        cu = torch.empty(2, dtype=torch.int32, device="cuda")
+        ws = torch.empty(S.sphinx_select_workspace_bytes(N), dtype=torch.uint8, device="cuda")
+        ones = torch.ones(F, dtype=torch.float32, device="cuda")
+        zeros = torch.zeros(F, dtype=torch.float32, device="cuda")
+        bvals = torch.full((F,), 0.5, dtype=torch.float32, device="cuda")
+        for recipe in ("uniform", "blobs"):
+            if recipe == "uniform":
+                u = torch.rand(N, device="cuda")
+            else:
+                # the headline recipe (20 blobs of sigma 8 per 72x128 latent) at the
+                # same density: 20 * (512*512)/(72*128) = 569 centres per frame
+                yy = (2 * torch.arange(256, device="cuda", dtype=torch.float32) + 0.5)
+                u = torch.zeros(F, 256, 256, device="cuda")
+                for f in range(F):
+                    c = torch.rand(569, 2, device="cuda") * 512
+                    for c0 in range(0, 569, 64):
+                        cc = c[c0:c0 + 64]
+                        d2 = (yy[None, :, None] - cc[:, 0, None, None]) ** 2 + (yy[None, None, :] - cc[:, 1, None, None]) ** 2
+                        u[f] += torch.exp(-d2 / 128.0).sum(0)
+                u = (u + 0.1 * torch.rand_like(u)).reshape(-1)
+            thr = torch.full((F,), float(torch.quantile(u[:1 << 24].float(), 0.7)), device="cuda")
+            cu_host = S.sphinx_select_mask(reqs, u, thr, None, mask, idx, cu, ws)
+            n = int(cu_host[-1])
+            x = torch.empty(16 * n, dtype=torch.float32, device="cuda")
+            reps = max(3, args.steps)
+            S.sphinx_timing_enable(True)
+            for _ in range(reps):
+                S.sphinx_select_mask(reqs, u, thr, None, mask, idx, cu, ws, readback=False)
+            for _ in range(reps):
+                S.sphinx_gather(reqs, state, S.F32, eps, S.BF16, idx, n, ones, zeros, x)
+            torch.cuda.synchronize()
+            t1 = S.sphinx_timing_read()
+            S.sphinx_timing_enable(True)
+            for _ in range(reps):
+                S.sphinx_gather(reqs, state, S.F32, eps, S.BF16, idx, n, ones, bvals, x)
+            torch.cuda.synchronize()
+            t2 = S.sphinx_timing_read()
+            S.sphinx_timing_enable(True)
+            for _ in range(reps):
+                S.sphinx_scatter_blend(reqs, x, idx, n, state, S.F32, state, S.F32)
+            torch.cuda.synchronize()
+            t3 = S.sphinx_timing_read()
+            S.sphinx_timing_enable(False)
+
+            def rate(tm, key, nbytes):
+                cnt, ms = tm[key]
+                us = 1e3 * ms / cnt
+                gbs = nbytes / (us * 1e-6) / 1e9
+                return {"avg_us": round(us, 2), "GB/s": round(gbs, 1), "frac_of_8TBs": round(gbs / PEAK_HBM_GBS, 4),
+                        "bytes": nbytes}
+            out = {"mode": "sweep", "tokens": N, "recipe": recipe, "selected": n,
+                   "select": rate(t1, "select", 5 * N + 4 * n),
+                   "gather": rate(t1, "gather", 132 * n),
+                   "gather_inject": rate(t2, "gather", 164 * n),
+                   "scatter": rate(t3, "scatter", 132 * n)}
+            print(json.dumps(out), flush=True)
+            del x
+        del state, eps, mask, idx, ws
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
+    if args.mode == "sweep" and args.gpus == 1:
+        return sweep_mode(args)
     if args.mode == "copy" and args.gpus == 1:
         return copy_mode(args)
     if args.gpus != 1:

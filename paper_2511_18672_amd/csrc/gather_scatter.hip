@@ -2,10 +2,10 @@
 // scatter/blend back into the NCHW latents (Sec. 3, Sec. 5.3: confident
 // regions keep their values).
 //
-// One thread moves one (channel, patch-row) pair of a token: 2 horizontally
-// adjacent latent values, i.e. 8 threads per token.  Neighbouring selected
-// tokens along x are neighbours in memory, so a wave touches contiguous runs of
-// the latent planes, and writes to x_sel ([n][16] fp32) are contiguous.
+// One thread moves one token: its position is decoded once, its 16 values are
+// eight 8-byte (channel, patch-row) pairs in the latent planes and one
+// 64-byte row of x_sel ([n][16] fp32).  Neighbouring selected tokens along x
+// are neighbours in memory, so a wave touches contiguous runs of each plane.
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -35,43 +35,65 @@ template <> struct Pair<bf16> {
   }
 };
 
+// One thread per selected token: decode its position once, read its 8 (c, py)
+// pairs of 2 values from the latent planes, write its 64-byte x_sel row as
+// four 16-byte stores.
 template <typename ST, typename ET>
 __global__ __launch_bounds__(kTPB) void k_gather(ReqTable T, const ST* __restrict__ state, const ET* __restrict__ eps,
                                                  const int32_t* __restrict__ idx, int n, const float* __restrict__ a,
                                                  const float* __restrict__ b, float* __restrict__ x) {
-  const int64_t gid = (int64_t)blockIdx.x * kTPB + threadIdx.x;
-  const int64_t j = gid >> 3;
-  const int p = (int)(gid & 7);
+  const int64_t j = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   if (j >= n) return;
   const int32_t t = idx[j];
   if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is read
   const TokPos tp = decode_token(T, t);
-  const int c = p >> 1, py = p & 1;
-  const int64_t e = tp.elem + (int64_t)c * tp.plane + (int64_t)py * tp.w;
-  const float2 z = Pair<ST>::load(state, e);
   const float av = a[tp.g], bv = b[tp.g];
-  float2 r = make_float2(av * z.x, av * z.y);
-  if (eps != nullptr && bv != 0.0f) {
-    const float2 nz = Pair<ET>::load(eps, e);
-    r.x = fmaf(bv, nz.x, r.x);
-    r.y = fmaf(bv, nz.y, r.y);
+  const bool inject = eps != nullptr && bv != 0.0f;
+  float v[16];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const int64_t e = tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
+    const float2 z = Pair<ST>::load(state, e);
+    v[2 * p] = av * z.x;
+    v[2 * p + 1] = av * z.y;
   }
-  *reinterpret_cast<float2*>(x + j * 16 + p * 2) = r;
+  if (inject) {
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      const int64_t e = tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
+      const float2 nz = Pair<ET>::load(eps, e);
+      v[2 * p] = fmaf(bv, nz.x, v[2 * p]);
+      v[2 * p + 1] = fmaf(bv, nz.y, v[2 * p + 1]);
+    }
+  }
+  float4* xr = reinterpret_cast<float4*>(x + j * 16);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) xr[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
 }
 
 template <typename OT>
 __global__ __launch_bounds__(kTPB) void k_scatter(ReqTable T, const float* __restrict__ x,
                                                   const int32_t* __restrict__ idx, int n, OT* __restrict__ out) {
-  const int64_t gid = (int64_t)blockIdx.x * kTPB + threadIdx.x;
-  const int64_t j = gid >> 3;
-  const int p = (int)(gid & 7);
+  const int64_t j = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   if (j >= n) return;
   const int32_t t = idx[j];
   if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is written
   const TokPos tp = decode_token(T, t);
-  const int c = p >> 1, py = p & 1;
-  const int64_t e = tp.elem + (int64_t)c * tp.plane + (int64_t)py * tp.w;
-  Pair<OT>::store(out, e, *reinterpret_cast<const float2*>(x + j * 16 + p * 2));
+  const float4* xr = reinterpret_cast<const float4*>(x + j * 16);
+  float v[16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 f = xr[q];
+    v[4 * q] = f.x;
+    v[4 * q + 1] = f.y;
+    v[4 * q + 2] = f.z;
+    v[4 * q + 3] = f.w;
+  }
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    const int64_t e = tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
+    Pair<OT>::store(out, e, make_float2(v[2 * p], v[2 * p + 1]));
+  }
 }
 
 template <typename IT, typename OT>
@@ -85,7 +107,7 @@ inline int grid_for(int64_t threads) { return (int)((threads + kTPB - 1) / kTPB)
 
 hipError_t launch_gather(const ReqTable& T, const void* state, sphinx_dtype sdt, const void* eps, sphinx_dtype edt,
                          const int32_t* idx, int n, const float* a, const float* b, float* x, hipStream_t s) {
-  const int g = grid_for((int64_t)n * 8);
+  const int g = grid_for(n);
   if (sdt == SPHINX_F32 && edt == SPHINX_F32)
     k_gather<float, float><<<g, kTPB, 0, s>>>(T, (const float*)state, (const float*)eps, idx, n, a, b, x);
   else if (sdt == SPHINX_F32 && edt == SPHINX_BF16)
@@ -99,7 +121,7 @@ hipError_t launch_gather(const ReqTable& T, const void* state, sphinx_dtype sdt,
 
 hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, void* out, sphinx_dtype odt,
                           hipStream_t s) {
-  const int g = grid_for((int64_t)n * 8);
+  const int g = grid_for(n);
   if (odt == SPHINX_F32)
     k_scatter<float><<<g, kTPB, 0, s>>>(T, x, idx, n, (float*)out);
   else

@@ -22,11 +22,14 @@ constexpr int kTPB = 256;
 constexpr int kGroups = 4;                      // float4 groups per thread
 constexpr int kChunk = kTPB * kGroups * 4;      // 4096 tokens per workgroup
 
-__device__ __forceinline__ bool select_one(const ReqTable& T, int64_t t, float u, const float* __restrict__ thr,
-                                           const uint8_t* __restrict__ active) {
-  const TokPos p = decode_token(T, t);
-  const bool act = active ? (active[p.g] != 0) : true;
-  return act && (u > thr[p.g]);
+// Global frame of token t and the first token of the next frame.
+__device__ __forceinline__ void frame_of(const ReqTable& T, int64_t t, int& g, int64_t& next) {
+  const int r = find_request(T, t);
+  const uint32_t loc = (uint32_t)(t - T.tok_off[r]);
+  const uint32_t tpf = (uint32_t)(T.h[r] >> 1) * (uint32_t)(T.w[r] >> 1);
+  const uint32_t f = loc / tpf;
+  g = T.frame_off[r] + (int)f;
+  next = T.tok_off[r] + (int64_t)(f + 1) * tpf;
 }
 
 __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, const float* __restrict__ u,
@@ -47,12 +50,29 @@ __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, co
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] = (t0 + e < N) ? u[t0 + e] : 0.0f;
     }
+    // one frame lookup per group of 4 (a second one only when the group
+    // straddles a frame boundary)
     uint32_t packed = 0;
+    if (t0 < N) {
+      int g;
+      int64_t next;
+      frame_of(T, t0, g, next);
+      float th = thr[g];
+      bool act = active ? (active[g] != 0) : true;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const bool m = (t0 + e < N) && select_one(T, t0 + e, v[e], thr, active);
-      packed |= (uint32_t)m << (8 * e);
-      cnt += m;
+      for (int e = 0; e < 4; ++e) {
+        const int64_t t = t0 + e;
+        if (t < N) {
+          if (t >= next) {
+            frame_of(T, t, g, next);
+            th = thr[g];
+            act = active ? (active[g] != 0) : true;
+          }
+          const bool m = act && (v[e] > th);
+          packed |= (uint32_t)m << (8 * e);
+          cnt += m;
+        }
+      }
     }
     if (t0 + 3 < N) {
       *reinterpret_cast<uint32_t*>(mask + t0) = packed;
