@@ -44,6 +44,8 @@ def parse():
                     help="step: the hot path; copy: a plain 1 GiB fp32 copy through scatter_blend (no tokens), "
                          "used to calibrate HBM byte counters and to measure achievable bandwidth; sweep: "
                          "mask/compaction, gather and scatter at 2^20..2^26 tokens against the HBM roofline")
+    ap.add_argument("--layout", default="tokens", choices=["tokens", "nchw"],
+                    help="layout of the fp32 state of record and the noise")
     ap.add_argument("--sweep-log2", default="20,22,24,26", help="token counts of the sweep (log2)")
     ap.add_argument("--select-every-step", type=int, default=1,
                     help="1: run mask+compaction in every step (default); 0: only when the active set changes")
@@ -116,11 +118,11 @@ def copy_mode(args):
     src = torch.randn(n, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
     for _ in range(2):
-        S.sphinx_scatter_blend(reqs, None, None, 0, src, S.F32, dst, S.F32)
+        S.sphinx_scatter_blend(reqs, None, None, 0, src, S.F32, S.NCHW, dst, S.F32, S.NCHW)
     torch.cuda.synchronize()
     S.sphinx_timing_enable(True)
     for _ in range(args.steps):
-        S.sphinx_scatter_blend(reqs, None, None, 0, src, S.F32, dst, S.F32)
+        S.sphinx_scatter_blend(reqs, None, None, 0, src, S.F32, S.NCHW, dst, S.F32, S.NCHW)
     torch.cuda.synchronize()
     cnt, ms = S.sphinx_timing_read()["scatter"]
     S.sphinx_timing_enable(False)
@@ -138,7 +140,8 @@ def sweep_mode(args):
     One request of F frames of a 4x512x512 latent (2^16 tokens per frame),
     30 % selected, with two selection recipes: uniform random (worst case for
     the gathers: selected tokens are isolated) and Gaussian blobs at the
-    headline map's density (clustered).  Algorithmic bytes per launch:
+    headline map's density (clustered), for NCHW and token-major latents.
+    Algorithmic bytes per launch:
       select  : 4 N (u) + N (mask) + 4 n_sel (idx)
       gather  : n_sel (4 idx + 64 state + 64 x_sel) [+ 32 n_sel bf16 noise when injecting]
       scatter : n_sel (4 idx + 64 x_sel + 64 state)
@@ -182,24 +185,6 @@ def sweep_mode(args):
             n = int(cu_host[-1])
             x = torch.empty(16 * n, dtype=torch.float32, device="cuda")
             reps = max(3, args.steps)
-            S.sphinx_timing_enable(True)
-            for _ in range(reps):
-                S.sphinx_select_mask(reqs, u, thr, None, mask, idx, cu, ws, readback=False)
-            for _ in range(reps):
-                S.sphinx_gather(reqs, state, S.F32, eps, S.BF16, idx, n, ones, zeros, x)
-            torch.cuda.synchronize()
-            t1 = S.sphinx_timing_read()
-            S.sphinx_timing_enable(True)
-            for _ in range(reps):
-                S.sphinx_gather(reqs, state, S.F32, eps, S.BF16, idx, n, ones, bvals, x)
-            torch.cuda.synchronize()
-            t2 = S.sphinx_timing_read()
-            S.sphinx_timing_enable(True)
-            for _ in range(reps):
-                S.sphinx_scatter_blend(reqs, x, idx, n, state, S.F32, state, S.F32)
-            torch.cuda.synchronize()
-            t3 = S.sphinx_timing_read()
-            S.sphinx_timing_enable(False)
 
             def rate(tm, key, nbytes):
                 cnt, ms = tm[key]
@@ -207,11 +192,32 @@ def sweep_mode(args):
                 gbs = nbytes / (us * 1e-6) / 1e9
                 return {"avg_us": round(us, 2), "GB/s": round(gbs, 1), "frac_of_8TBs": round(gbs / PEAK_HBM_GBS, 4),
                         "bytes": nbytes}
+
+            S.sphinx_timing_enable(True)
+            for _ in range(reps):
+                S.sphinx_select_mask(reqs, u, thr, None, mask, idx, cu, ws, readback=False)
+            torch.cuda.synchronize()
             out = {"mode": "sweep", "tokens": N, "recipe": recipe, "selected": n,
-                   "select": rate(t1, "select", 5 * N + 4 * n),
-                   "gather": rate(t1, "gather", 132 * n),
-                   "gather_inject": rate(t2, "gather", 164 * n),
-                   "scatter": rate(t3, "scatter", 132 * n)}
+                   "select": rate(S.sphinx_timing_read(), "select", 5 * N + 4 * n)}
+            for lay_name, lay in (("nchw", S.NCHW), ("tokens", S.TOKENS)):
+                S.sphinx_timing_enable(True)
+                for _ in range(reps):
+                    S.sphinx_gather(reqs, lay, state, S.F32, eps, S.BF16, idx, n, ones, zeros, x)
+                torch.cuda.synchronize()
+                t1 = S.sphinx_timing_read()
+                S.sphinx_timing_enable(True)
+                for _ in range(reps):
+                    S.sphinx_gather(reqs, lay, state, S.F32, eps, S.BF16, idx, n, ones, bvals, x)
+                torch.cuda.synchronize()
+                t2 = S.sphinx_timing_read()
+                S.sphinx_timing_enable(True)
+                for _ in range(reps):
+                    S.sphinx_scatter_blend(reqs, x, idx, n, state, S.F32, lay, state, S.F32, lay)
+                torch.cuda.synchronize()
+                t3 = S.sphinx_timing_read()
+                out[lay_name] = {"gather": rate(t1, "gather", 132 * n), "gather_inject": rate(t2, "gather", 164 * n),
+                                 "scatter": rate(t3, "scatter", 132 * n)}
+            S.sphinx_timing_enable(False)
             print(json.dumps(out), flush=True)
             del x
         del state, eps, mask, idx, ws
@@ -239,7 +245,7 @@ def main():
     else:
         wl = W.CONFIGS[args.config]()
     t_setup = time.perf_counter()
-    R = S.from_workload(wl)
+    R = S.from_workload(wl, layout=S.TOKENS if args.layout == "tokens" else S.NCHW)
     R.reset()
     stream = torch.cuda.current_stream()
     force = bool(args.select_every_step)
@@ -296,7 +302,8 @@ def main():
            "config": {"workload": f"{wl.name}: {wl.G} frames, {wl.N} tokens, {n} selected, "
                                   f"D{D} H{wl.model.heads}x{wl.model.head_dim} L{L} MLP{mlp}, "
                                   f"{int(wl.max_steps)}-step DDIM schedule",
-                      "selected_tokens": int(n), "tokens": int(wl.N), "select_every_step": force},
+                      "selected_tokens": int(n), "tokens": int(wl.N), "select_every_step": force,
+                      "state_layout": args.layout},
            "mfma_util_step": round(mfma_util, 4),
            "roofline": roofline, "kernels": kernels, "setup_s": round(setup_s, 1)}
     if not args.no_cpu_baseline:

@@ -28,8 +28,13 @@
  *    [frame_offset, frame_offset + frames); both offsets must equal the running
  *    sums over the preceding requests.  At most SPHINX_MAX_REQUESTS requests.
  *  - Token t of a request is t = f*(h/2)*(w/2) + y*(w/2) + x (patch 2x2).
- *    Latents are NCHW per request, [frames][4][h][w], request r starting at
- *    element 16*tok_offset.  A token's 16 values are ordered c*4 + py*2 + px.
+ *    A token's 16 values are ordered c*4 + py*2 + px.  Latents come in one of
+ *    two layouts (sphinx_layout), both 16*N elements with request r starting
+ *    at element 16*tok_offset:
+ *      SPHINX_LAYOUT_NCHW    per request [frames][4][h][w] (the VAE's layout);
+ *      SPHINX_LAYOUT_TOKENS  [N][16]: token t's 16 values at 16*t, the layout
+ *                            of an x_sel row, so gathering or scattering a
+ *                            token moves one contiguous 64-byte row (f32).
  *  - Arguments are validated before any HIP call, so every error path is
  *    reachable without a GPU; an invalid call enqueues nothing.  No exception
  *    or abort crosses the ABI.  SPHINX_E_HIP reports a failed launch or copy.
@@ -58,6 +63,8 @@ typedef enum {
 } sphinx_status;
 
 typedef enum { SPHINX_F32 = 0, SPHINX_BF16 = 1 } sphinx_dtype;
+
+typedef enum { SPHINX_LAYOUT_NCHW = 0, SPHINX_LAYOUT_TOKENS = 1 } sphinx_layout;
 
 typedef struct {
   int32_t frames;       /* F >= 1 */
@@ -153,13 +160,13 @@ sphinx_status sphinx_select_mask(const sphinx_request* reqs, int32_t R, const fl
 
 /* Gather with noise injection (Alg. 1 add_noise on the selected tokens).
  *   x_sel[j][k] = a[g] * z[k] + b[g] * eps[k]   for token idx[j] of frame g,
- * z and eps read from the NCHW latents `state` / `eps` (dtype f32 or bf16).
- * eps may be NULL: then the noise term is dropped.  a, b: dev float [G];
- * idx: dev int32 [n_sel]; x_sel: dev float [n_sel][16] out.  n_sel = 0 is a
- * no-op.  Every idx[j] must lie in [0, N). */
-sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, const void* state, sphinx_dtype state_dtype,
-                            const void* eps, sphinx_dtype eps_dtype, const int32_t* idx, int32_t n_sel,
-                            const float* a, const float* b, float* x_sel, void* stream);
+ * z and eps read from the latents `state` / `eps` (dtype f32 or bf16), both in
+ * `layout`.  eps may be NULL: then the noise term is dropped.  a, b: dev float
+ * [G]; idx: dev int32 [n_sel]; x_sel: dev float [n_sel][16] out.  n_sel = 0
+ * is a no-op.  An idx[j] outside [0, N) leaves row j unwritten. */
+sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, sphinx_layout layout, const void* state,
+                            sphinx_dtype state_dtype, const void* eps, sphinx_dtype eps_dtype, const int32_t* idx,
+                            int32_t n_sel, const float* a, const float* b, float* x_sel, void* stream);
 
 /* Workspace bytes of sphinx_refine_step for up to max_sel selected tokens. */
 sphinx_status sphinx_refine_workspace_bytes(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
@@ -182,12 +189,15 @@ sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_reques
 
 /* Scatter and blend (Sec. 3 and 5.3: confident regions keep their values).
  *   z_out = z_in with token idx[j] replaced by x_sel[j]   (j < n_sel)
- * z_in == z_out scatters in place (dtypes must match); otherwise z_in is first
- * copied to z_out with dtype conversion (bf16 outputs round to nearest even).
- * x_sel: dev float [n_sel][16]; z_in, z_out: dev NCHW latents of all requests. */
+ * z_in == z_out scatters in place (dtype and layout must match); otherwise
+ * z_in is first copied to z_out with dtype and layout conversion (bf16 outputs
+ * round to nearest even), so n_sel = 0 converts between layouts and dtypes.
+ * x_sel: dev float [n_sel][16]; z_in, z_out: dev latents of all requests in
+ * the given layouts; the two buffers must not partially overlap.  An idx[j]
+ * outside [0, N) is skipped. */
 sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const float* x_sel, const int32_t* idx,
-                                   int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, void* z_out,
-                                   sphinx_dtype out_dtype, void* stream);
+                                   int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, sphinx_layout in_layout,
+                                   void* z_out, sphinx_dtype out_dtype, sphinx_layout out_layout, void* stream);
 
 /* Profiling aid (outside the method).  While enabled, every launch of a kernel
  * class is bracketed by two HIP events recorded on the stream of the launch;

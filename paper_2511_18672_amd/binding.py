@@ -17,6 +17,7 @@ import numpy as np
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsphinx.so")
 
 F32, BF16 = 0, 1
+NCHW, TOKENS = 0, 1  # sphinx_layout
 MAX_REQUESTS = 64
 STATUS_NAMES = {0: "SPHINX_OK", 1: "SPHINX_E_INVALID", 2: "SPHINX_E_UNSUPPORTED", 3: "SPHINX_E_WORKSPACE",
                 4: "SPHINX_E_HIP"}
@@ -66,12 +67,14 @@ def lib() -> ctypes.CDLL:
         "sphinx_plan_step": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, P, P, P, P, P, P]),
         "sphinx_select_workspace_bytes": (c_int32, [c_int64, POINTER(c_size_t)]),
         "sphinx_select_mask": (c_int32, [POINTER(Request), c_int32, P, P, P, P, P, P, P, P, c_size_t, P]),
-        "sphinx_gather": (c_int32, [POINTER(Request), c_int32, P, c_int32, P, c_int32, P, c_int32, P, P, P, P]),
+        "sphinx_gather": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P, P,
+                                    P]),
         "sphinx_refine_workspace_bytes": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, c_int64,
                                                     POINTER(c_size_t)]),
         "sphinx_refine_step": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, P, c_int32, P, P, P, P,
                                          P, P, c_size_t, P]),
-        "sphinx_scatter_blend": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, c_int32, P, c_int32, P]),
+        "sphinx_scatter_blend": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, c_int32, c_int32, P, c_int32,
+                                           c_int32, P]),
         "sphinx_timing_enable": (c_int32, [c_int32]),
         "sphinx_timing_read": (c_int32, [c_int32, POINTER(c_int64), POINTER(ctypes.c_double)]),
     }
@@ -175,10 +178,11 @@ def sphinx_select_mask(reqs, uncert, thr, active, mask, idx, cu_sel, ws, readbac
     return host
 
 
-def sphinx_gather(reqs, state, state_dtype: int, eps, eps_dtype: int, idx, n_sel: int, a, b, x_sel, stream=None):
+def sphinx_gather(reqs, layout: int, state, state_dtype: int, eps, eps_dtype: int, idx, n_sel: int, a, b, x_sel,
+                  stream=None):
     _check("sphinx_gather", lib().sphinx_gather(
-        reqs, len(reqs), _ptr(state), state_dtype, _ptr(eps), eps_dtype, _ptr(idx), n_sel, _ptr(a), _ptr(b),
-        _ptr(x_sel), _stream(stream)))
+        reqs, len(reqs), layout, _ptr(state), state_dtype, _ptr(eps), eps_dtype, _ptr(idx), n_sel, _ptr(a),
+        _ptr(b), _ptr(x_sel), _stream(stream)))
 
 
 def sphinx_refine_workspace_bytes(desc: ModelDesc, reqs, max_sel: int) -> int:
@@ -196,10 +200,11 @@ def sphinx_refine_step(desc: ModelDesc, reqs, idx, n_sel: int, cu_sel_host: np.n
         _ptr(x_sel), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
-def sphinx_scatter_blend(reqs, x_sel, idx, n_sel: int, z_in, in_dtype: int, z_out, out_dtype: int, stream=None):
+def sphinx_scatter_blend(reqs, x_sel, idx, n_sel: int, z_in, in_dtype: int, in_layout: int, z_out, out_dtype: int,
+                         out_layout: int, stream=None):
     _check("sphinx_scatter_blend", lib().sphinx_scatter_blend(
-        reqs, len(reqs), _ptr(x_sel), _ptr(idx), n_sel, _ptr(z_in), in_dtype, _ptr(z_out), out_dtype,
-        _stream(stream)))
+        reqs, len(reqs), _ptr(x_sel), _ptr(idx), n_sel, _ptr(z_in), in_dtype, in_layout, _ptr(z_out), out_dtype,
+        out_layout, _stream(stream)))
 
 
 def sphinx_timing_enable(on: bool = True):

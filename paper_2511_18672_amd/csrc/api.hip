@@ -17,6 +17,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 inline size_t esize(sphinx_dtype d) { return d == SPHINX_BF16 ? 2 : 4; }
 inline bool valid_dtype(sphinx_dtype d) { return d == SPHINX_F32 || d == SPHINX_BF16; }
+inline bool valid_layout(sphinx_layout l) { return l == SPHINX_LAYOUT_NCHW || l == SPHINX_LAYOUT_TOKENS; }
+inline size_t dtype_bytes(sphinx_dtype d) { return d == SPHINX_F32 ? 4 : 2; }
 
 sphinx_status build_table(const sphinx_request* reqs, int32_t R, ReqTable* T, int64_t* N, int32_t* G) {
   if (reqs == nullptr || R < 1) return SPHINX_E_INVALID;
@@ -363,22 +365,22 @@ sphinx_status sphinx_select_mask(const sphinx_request* reqs, int32_t R, const fl
   return SPHINX_OK;
 }
 
-sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, const void* state, sphinx_dtype state_dtype,
-                            const void* eps, sphinx_dtype eps_dtype, const int32_t* idx, int32_t n_sel,
-                            const float* a, const float* b, float* x_sel, void* stream) {
+sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, sphinx_layout layout, const void* state,
+                            sphinx_dtype state_dtype, const void* eps, sphinx_dtype eps_dtype, const int32_t* idx,
+                            int32_t n_sel, const float* a, const float* b, float* x_sel, void* stream) {
   ReqTable T;
   int64_t N;
   int32_t G;
   sphinx_status st = build_table(reqs, R, &T, &N, &G);
   if (st != SPHINX_OK) return st;
   if (n_sel < 0 || n_sel > N) return SPHINX_E_INVALID;
-  if (!valid_dtype(state_dtype) || !valid_dtype(eps_dtype)) return SPHINX_E_UNSUPPORTED;
+  if (!valid_dtype(state_dtype) || !valid_dtype(eps_dtype) || !valid_layout(layout)) return SPHINX_E_UNSUPPORTED;
   if (n_sel == 0) return SPHINX_OK;
   if (!state || !idx || !a || !b || !x_sel) return SPHINX_E_INVALID;
   if (!aligned(state, 16) || (eps && !aligned(eps, 16)) || !aligned(idx, 16) || !aligned(x_sel, 16))
     return SPHINX_E_INVALID;
   Bracket br(SPHINX_K_GATHER, (hipStream_t)stream);
-  return hip_status(launch_gather(T, state, state_dtype, eps, eps_dtype, idx, n_sel, a, b, x_sel,
+  return hip_status(launch_gather(T, layout, state, state_dtype, eps, eps_dtype, idx, n_sel, a, b, x_sel,
                                   (hipStream_t)stream));
 }
 
@@ -525,23 +527,29 @@ sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_reques
 }
 
 sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const float* x_sel, const int32_t* idx,
-                                   int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, void* z_out,
-                                   sphinx_dtype out_dtype, void* stream) {
+                                   int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, sphinx_layout in_layout,
+                                   void* z_out, sphinx_dtype out_dtype, sphinx_layout out_layout, void* stream) {
   ReqTable T;
   int64_t N;
   int32_t G;
   sphinx_status st = build_table(reqs, R, &T, &N, &G);
   if (st != SPHINX_OK) return st;
   if (!valid_dtype(in_dtype) || !valid_dtype(out_dtype)) return SPHINX_E_UNSUPPORTED;
+  if (!valid_layout(in_layout) || !valid_layout(out_layout)) return SPHINX_E_UNSUPPORTED;
   if (n_sel < 0 || n_sel > N || z_in == nullptr || z_out == nullptr) return SPHINX_E_INVALID;
   if (!aligned(z_in, 16) || !aligned(z_out, 16)) return SPHINX_E_INVALID;
   if (n_sel > 0 && (!x_sel || !idx || !aligned(x_sel, 16) || !aligned(idx, 16))) return SPHINX_E_INVALID;
   const bool in_place = (z_in == (const void*)z_out);
-  if (in_place && in_dtype != out_dtype) return SPHINX_E_INVALID;
+  if (in_place && (in_dtype != out_dtype || in_layout != out_layout)) return SPHINX_E_INVALID;
+  if (!in_place) {
+    const uintptr_t i0 = (uintptr_t)z_in, i1 = i0 + (uintptr_t)(16 * N) * dtype_bytes(in_dtype);
+    const uintptr_t o0 = (uintptr_t)z_out, o1 = o0 + (uintptr_t)(16 * N) * dtype_bytes(out_dtype);
+    if (i0 < o1 && o0 < i1) return SPHINX_E_INVALID;  // partial overlap
+  }
   hipStream_t s = (hipStream_t)stream;
   Bracket br(SPHINX_K_SCATTER, s);
-  if (!in_place) SPHINX_TRY(launch_convert(z_in, in_dtype, z_out, out_dtype, 16 * N, s));
-  if (n_sel > 0) SPHINX_TRY(launch_scatter(T, x_sel, idx, n_sel, z_out, out_dtype, s));
+  if (!in_place) SPHINX_TRY(launch_convert(T, z_in, in_dtype, in_layout, z_out, out_dtype, out_layout, s));
+  if (n_sel > 0) SPHINX_TRY(launch_scatter(T, x_sel, idx, n_sel, z_out, out_dtype, out_layout, s));
   return SPHINX_OK;
 }
 

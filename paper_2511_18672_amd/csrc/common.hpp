@@ -45,6 +45,14 @@ __device__ __forceinline__ int find_request(const ReqTable& T, int64_t t) {
   return lo;
 }
 
+// Global frame of token t (the part of decode_token that token-major latents need).
+__device__ __forceinline__ int frame_of_token(const ReqTable& T, int64_t t) {
+  const int r = find_request(T, t);
+  const uint32_t loc = (uint32_t)(t - T.tok_off[r]);
+  const uint32_t tpf = ((uint32_t)T.h[r] >> 1) * ((uint32_t)T.w[r] >> 1);
+  return T.frame_off[r] + (int)(loc / tpf);
+}
+
 __device__ __forceinline__ TokPos decode_token(const ReqTable& T, int64_t t) {
   TokPos p;
   p.r = find_request(T, t);

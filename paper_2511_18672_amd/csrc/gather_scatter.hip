@@ -1,11 +1,15 @@
 // Gather with noise injection (Alg. 1 add_noise on the selected tokens) and
-// scatter/blend back into the NCHW latents (Sec. 3, Sec. 5.3: confident
-// regions keep their values).
+// scatter/blend back into the latents (Sec. 3, Sec. 5.3: confident regions
+// keep their values), for NCHW and token-major latents.
 //
-// One thread moves one token: its position is decoded once, its 16 values are
-// eight 8-byte (channel, patch-row) pairs in the latent planes and one
-// 64-byte row of x_sel ([n][16] fp32).  Neighbouring selected tokens along x
-// are neighbours in memory, so a wave touches contiguous runs of each plane.
+// NCHW: one thread moves one token.  Its position is decoded once; its 16
+// values are eight 8-byte (channel, patch-row) pairs in the latent planes and
+// one 64-byte row of x_sel ([n][16] fp32).  Neighbouring selected tokens along
+// x are neighbours in memory, so a wave touches contiguous runs of each plane.
+//
+// Token-major: a token is one contiguous row (64 B in f32, 32 B in bf16) at
+// 16*t, in the order of an x_sel row.  Four lanes move one token, four values
+// each, so one wave instruction covers 16 whole rows on both sides.
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -13,55 +17,76 @@ namespace sphinx {
 namespace {
 constexpr int kTPB = 256;
 
-template <typename T> struct Pair;
-template <> struct Pair<float> {
-  static __device__ __forceinline__ float2 load(const float* p, int64_t e) {
+template <typename T> struct Vec;
+template <> struct Vec<float> {
+  static __device__ __forceinline__ float2 load2(const float* p, int64_t e) {
     return *reinterpret_cast<const float2*>(p + e);
   }
-  static __device__ __forceinline__ void store(float* p, int64_t e, float2 v) {
+  static __device__ __forceinline__ void store2(float* p, int64_t e, float2 v) {
     *reinterpret_cast<float2*>(p + e) = v;
   }
+  static __device__ __forceinline__ float4 load4(const float* p, int64_t e) {
+    return *reinterpret_cast<const float4*>(p + e);
+  }
+  static __device__ __forceinline__ void store4(float* p, int64_t e, float4 v) {
+    *reinterpret_cast<float4*>(p + e) = v;
+  }
 };
-template <> struct Pair<bf16> {
-  static __device__ __forceinline__ float2 load(const bf16* p, int64_t e) {
+template <> struct Vec<bf16> {
+  static __device__ __forceinline__ float2 load2(const bf16* p, int64_t e) {
     const bf16x2 v = *reinterpret_cast<const bf16x2*>(p + e);
     return make_float2((float)v[0], (float)v[1]);
   }
-  static __device__ __forceinline__ void store(bf16* p, int64_t e, float2 v) {
+  static __device__ __forceinline__ void store2(bf16* p, int64_t e, float2 v) {
     bf16x2 o;
     o[0] = (bf16)v.x;
     o[1] = (bf16)v.y;
     *reinterpret_cast<bf16x2*>(p + e) = o;
   }
+  static __device__ __forceinline__ float4 load4(const bf16* p, int64_t e) {
+    const bf16x2* q = reinterpret_cast<const bf16x2*>(p + e);
+    const bf16x2 v0 = q[0], v1 = q[1];
+    return make_float4((float)v0[0], (float)v0[1], (float)v1[0], (float)v1[1]);
+  }
+  static __device__ __forceinline__ void store4(bf16* p, int64_t e, float4 v) {
+    bf16x2 o0, o1;
+    o0[0] = (bf16)v.x;
+    o0[1] = (bf16)v.y;
+    o1[0] = (bf16)v.z;
+    o1[1] = (bf16)v.w;
+    bf16x2* q = reinterpret_cast<bf16x2*>(p + e);
+    q[0] = o0;
+    q[1] = o1;
+  }
 };
 
-// One thread per selected token: decode its position once, read its 8 (c, py)
-// pairs of 2 values from the latent planes, write its 64-byte x_sel row as
-// four 16-byte stores.
+// Element offset of pair p = (c, py) = (p >> 1, p & 1) of a decoded NCHW token.
+__device__ __forceinline__ int64_t nchw_pair(const TokPos& tp, int p) {
+  return tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
+}
+
 template <typename ST, typename ET>
-__global__ __launch_bounds__(kTPB) void k_gather(ReqTable T, const ST* __restrict__ state, const ET* __restrict__ eps,
-                                                 const int32_t* __restrict__ idx, int n, const float* __restrict__ a,
-                                                 const float* __restrict__ b, float* __restrict__ x) {
+__global__ __launch_bounds__(kTPB) void k_gather_nchw(ReqTable T, const ST* __restrict__ state,
+                                                      const ET* __restrict__ eps, const int32_t* __restrict__ idx,
+                                                      int n, const float* __restrict__ a,
+                                                      const float* __restrict__ b, float* __restrict__ x) {
   const int64_t j = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   if (j >= n) return;
   const int32_t t = idx[j];
   if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is read
   const TokPos tp = decode_token(T, t);
   const float av = a[tp.g], bv = b[tp.g];
-  const bool inject = eps != nullptr && bv != 0.0f;
   float v[16];
 #pragma unroll
   for (int p = 0; p < 8; ++p) {
-    const int64_t e = tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
-    const float2 z = Pair<ST>::load(state, e);
+    const float2 z = Vec<ST>::load2(state, nchw_pair(tp, p));
     v[2 * p] = av * z.x;
     v[2 * p + 1] = av * z.y;
   }
-  if (inject) {
+  if (eps != nullptr && bv != 0.0f) {
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
-      const int64_t e = tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
-      const float2 nz = Pair<ET>::load(eps, e);
+      const float2 nz = Vec<ET>::load2(eps, nchw_pair(tp, p));
       v[2 * p] = fmaf(bv, nz.x, v[2 * p]);
       v[2 * p + 1] = fmaf(bv, nz.y, v[2 * p + 1]);
     }
@@ -71,9 +96,33 @@ __global__ __launch_bounds__(kTPB) void k_gather(ReqTable T, const ST* __restric
   for (int q = 0; q < 4; ++q) xr[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
 }
 
+// Token-major gather: lane i moves values 4*(i%4) .. 4*(i%4)+3 of token i/4.
+template <typename ST, typename ET>
+__global__ __launch_bounds__(kTPB) void k_gather_tok(ReqTable T, const ST* __restrict__ state,
+                                                     const ET* __restrict__ eps, const int32_t* __restrict__ idx,
+                                                     int n, const float* __restrict__ a,
+                                                     const float* __restrict__ b, float* __restrict__ x) {
+  const int64_t i = (int64_t)blockIdx.x * kTPB + threadIdx.x;
+  const int64_t j = i >> 2;
+  if (j >= n) return;
+  const int q = (int)(i & 3);
+  const int32_t t = idx[j];
+  if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is read
+  const int g = frame_of_token(T, t);
+  const float av = a[g], bv = b[g];
+  const int64_t e = 16 * (int64_t)t + 4 * q;
+  const float4 z = Vec<ST>::load4(state, e);
+  float4 v = make_float4(av * z.x, av * z.y, av * z.z, av * z.w);
+  if (eps != nullptr && bv != 0.0f) {
+    const float4 nz = Vec<ET>::load4(eps, e);
+    v = make_float4(fmaf(bv, nz.x, v.x), fmaf(bv, nz.y, v.y), fmaf(bv, nz.z, v.z), fmaf(bv, nz.w, v.w));
+  }
+  reinterpret_cast<float4*>(x)[i] = v;
+}
+
 template <typename OT>
-__global__ __launch_bounds__(kTPB) void k_scatter(ReqTable T, const float* __restrict__ x,
-                                                  const int32_t* __restrict__ idx, int n, OT* __restrict__ out) {
+__global__ __launch_bounds__(kTPB) void k_scatter_nchw(ReqTable T, const float* __restrict__ x,
+                                                       const int32_t* __restrict__ idx, int n, OT* __restrict__ out) {
   const int64_t j = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   if (j >= n) return;
   const int32_t t = idx[j];
@@ -90,57 +139,114 @@ __global__ __launch_bounds__(kTPB) void k_scatter(ReqTable T, const float* __res
     v[4 * q + 3] = f.w;
   }
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const int64_t e = tp.elem + (int64_t)(p >> 1) * tp.plane + (int64_t)(p & 1) * tp.w;
-    Pair<OT>::store(out, e, make_float2(v[2 * p], v[2 * p + 1]));
-  }
+  for (int p = 0; p < 8; ++p) Vec<OT>::store2(out, nchw_pair(tp, p), make_float2(v[2 * p], v[2 * p + 1]));
 }
 
+template <typename OT>
+__global__ __launch_bounds__(kTPB) void k_scatter_tok(int64_t N, const float* __restrict__ x,
+                                                      const int32_t* __restrict__ idx, int n, OT* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * kTPB + threadIdx.x;
+  const int64_t j = i >> 2;
+  if (j >= n) return;
+  const int32_t t = idx[j];
+  if (t < 0 || t >= N) return;  // out-of-range index: nothing is written
+  Vec<OT>::store4(out, 16 * (int64_t)t + 4 * (i & 3), reinterpret_cast<const float4*>(x)[i]);
+}
+
+// Same-layout copy with dtype conversion, two values per step.
 template <typename IT, typename OT>
 __global__ __launch_bounds__(kTPB) void k_convert(const IT* __restrict__ in, OT* __restrict__ out, int64_t pairs) {
   for (int64_t i = (int64_t)blockIdx.x * kTPB + threadIdx.x; i < pairs; i += (int64_t)gridDim.x * kTPB)
-    Pair<OT>::store(out, 2 * i, Pair<IT>::load(in, 2 * i));
+    Vec<OT>::store2(out, 2 * i, Vec<IT>::load2(in, 2 * i));
 }
 
-inline int grid_for(int64_t threads) { return (int)((threads + kTPB - 1) / kTPB); }
+// Layout change NCHW <-> token-major with dtype conversion, one token per
+// thread (a whole-latent conversion, done once per run at its ends).
+template <typename IT, typename OT, bool TO_TOKENS>
+__global__ __launch_bounds__(kTPB) void k_relayout(ReqTable T, const IT* __restrict__ in, OT* __restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * kTPB + threadIdx.x;
+  if (t >= T.tok_off[T.R]) return;
+  const TokPos tp = decode_token(T, t);
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    if (TO_TOKENS)
+      Vec<OT>::store2(out, 16 * t + 2 * p, Vec<IT>::load2(in, nchw_pair(tp, p)));
+    else
+      Vec<OT>::store2(out, nchw_pair(tp, p), Vec<IT>::load2(in, 16 * t + 2 * p));
+  }
+}
+
+inline unsigned grid_for(int64_t threads) { return (unsigned)((threads + kTPB - 1) / kTPB); }
+
+template <typename ST, typename ET>
+void gather_typed(const ReqTable& T, sphinx_layout lay, const void* state, const void* eps, const int32_t* idx,
+                  int n, const float* a, const float* b, float* x, hipStream_t s) {
+  if (lay == SPHINX_LAYOUT_TOKENS)
+    k_gather_tok<ST, ET><<<grid_for(4 * (int64_t)n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a,
+                                                                   b, x);
+  else
+    k_gather_nchw<ST, ET><<<grid_for(n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a, b, x);
+}
+
+template <typename IT, typename OT>
+void convert_typed(const ReqTable& T, int64_t N, const void* in, sphinx_layout il, void* out, sphinx_layout ol,
+                   hipStream_t s) {
+  if (il == ol) {
+    const int64_t pairs = 8 * N;
+    k_convert<IT, OT><<<(unsigned)std::min<int64_t>(grid_for(pairs), 8192), kTPB, 0, s>>>((const IT*)in, (OT*)out,
+                                                                                          pairs);
+  } else if (ol == SPHINX_LAYOUT_TOKENS) {
+    k_relayout<IT, OT, true><<<grid_for(N), kTPB, 0, s>>>(T, (const IT*)in, (OT*)out);
+  } else {
+    k_relayout<IT, OT, false><<<grid_for(N), kTPB, 0, s>>>(T, (const IT*)in, (OT*)out);
+  }
+}
 }  // namespace
 
-hipError_t launch_gather(const ReqTable& T, const void* state, sphinx_dtype sdt, const void* eps, sphinx_dtype edt,
-                         const int32_t* idx, int n, const float* a, const float* b, float* x, hipStream_t s) {
-  const int g = grid_for(n);
+hipError_t launch_gather(const ReqTable& T, sphinx_layout lay, const void* state, sphinx_dtype sdt, const void* eps,
+                         sphinx_dtype edt, const int32_t* idx, int n, const float* a, const float* b, float* x,
+                         hipStream_t s) {
   if (sdt == SPHINX_F32 && edt == SPHINX_F32)
-    k_gather<float, float><<<g, kTPB, 0, s>>>(T, (const float*)state, (const float*)eps, idx, n, a, b, x);
+    gather_typed<float, float>(T, lay, state, eps, idx, n, a, b, x, s);
   else if (sdt == SPHINX_F32 && edt == SPHINX_BF16)
-    k_gather<float, bf16><<<g, kTPB, 0, s>>>(T, (const float*)state, (const bf16*)eps, idx, n, a, b, x);
+    gather_typed<float, bf16>(T, lay, state, eps, idx, n, a, b, x, s);
   else if (sdt == SPHINX_BF16 && edt == SPHINX_F32)
-    k_gather<bf16, float><<<g, kTPB, 0, s>>>(T, (const bf16*)state, (const float*)eps, idx, n, a, b, x);
+    gather_typed<bf16, float>(T, lay, state, eps, idx, n, a, b, x, s);
   else
-    k_gather<bf16, bf16><<<g, kTPB, 0, s>>>(T, (const bf16*)state, (const bf16*)eps, idx, n, a, b, x);
+    gather_typed<bf16, bf16>(T, lay, state, eps, idx, n, a, b, x, s);
   return hipGetLastError();
 }
 
 hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, void* out, sphinx_dtype odt,
-                          hipStream_t s) {
-  const int g = grid_for(n);
-  if (odt == SPHINX_F32)
-    k_scatter<float><<<g, kTPB, 0, s>>>(T, x, idx, n, (float*)out);
-  else
-    k_scatter<bf16><<<g, kTPB, 0, s>>>(T, x, idx, n, (bf16*)out);
+                          sphinx_layout lay, hipStream_t s) {
+  const int64_t N = T.tok_off[T.R];
+  if (lay == SPHINX_LAYOUT_TOKENS) {
+    const unsigned g = grid_for(4 * (int64_t)n);
+    if (odt == SPHINX_F32)
+      k_scatter_tok<float><<<g, kTPB, 0, s>>>(N, x, idx, n, (float*)out);
+    else
+      k_scatter_tok<bf16><<<g, kTPB, 0, s>>>(N, x, idx, n, (bf16*)out);
+  } else {
+    const unsigned g = grid_for(n);
+    if (odt == SPHINX_F32)
+      k_scatter_nchw<float><<<g, kTPB, 0, s>>>(T, x, idx, n, (float*)out);
+    else
+      k_scatter_nchw<bf16><<<g, kTPB, 0, s>>>(T, x, idx, n, (bf16*)out);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_convert(const void* in, sphinx_dtype idt, void* out, sphinx_dtype odt, int64_t count,
-                          hipStream_t s) {
-  const int64_t pairs = count / 2;
-  const int g = (int)std::min<int64_t>(grid_for(pairs), 8192);
+hipError_t launch_convert(const ReqTable& T, const void* in, sphinx_dtype idt, sphinx_layout il, void* out,
+                          sphinx_dtype odt, sphinx_layout ol, hipStream_t s) {
+  const int64_t N = T.tok_off[T.R];
   if (idt == SPHINX_F32 && odt == SPHINX_F32)
-    k_convert<float, float><<<g, kTPB, 0, s>>>((const float*)in, (float*)out, pairs);
+    convert_typed<float, float>(T, N, in, il, out, ol, s);
   else if (idt == SPHINX_F32 && odt == SPHINX_BF16)
-    k_convert<float, bf16><<<g, kTPB, 0, s>>>((const float*)in, (bf16*)out, pairs);
+    convert_typed<float, bf16>(T, N, in, il, out, ol, s);
   else if (idt == SPHINX_BF16 && odt == SPHINX_F32)
-    k_convert<bf16, float><<<g, kTPB, 0, s>>>((const bf16*)in, (float*)out, pairs);
+    convert_typed<bf16, float>(T, N, in, il, out, ol, s);
   else
-    k_convert<bf16, bf16><<<g, kTPB, 0, s>>>((const bf16*)in, (bf16*)out, pairs);
+    convert_typed<bf16, bf16>(T, N, in, il, out, ol, s);
   return hipGetLastError();
 }
 

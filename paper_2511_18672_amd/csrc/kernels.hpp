@@ -36,12 +36,13 @@ hipError_t launch_select(const ReqTable& T, int64_t N, const float* u, const flo
                          uint8_t* mask, int32_t* idx, int32_t* cu_sel, void* ws, hipStream_t s);
 
 // gather_scatter.hip
-hipError_t launch_gather(const ReqTable& T, const void* state, sphinx_dtype sdt, const void* eps, sphinx_dtype edt,
-                         const int32_t* idx, int n, const float* a, const float* b, float* x, hipStream_t s);
+hipError_t launch_gather(const ReqTable& T, sphinx_layout lay, const void* state, sphinx_dtype sdt, const void* eps,
+                         sphinx_dtype edt, const int32_t* idx, int n, const float* a, const float* b, float* x,
+                         hipStream_t s);
 hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, void* out, sphinx_dtype odt,
-                          hipStream_t s);
-hipError_t launch_convert(const void* in, sphinx_dtype idt, void* out, sphinx_dtype odt, int64_t count,
-                          hipStream_t s);
+                          sphinx_layout lay, hipStream_t s);
+hipError_t launch_convert(const ReqTable& T, const void* in, sphinx_dtype idt, sphinx_layout il, void* out,
+                          sphinx_dtype odt, sphinx_layout ol, hipStream_t s);
 
 // cond.hip
 hipError_t launch_cond_rows(const int32_t* tau, int G, int32_t* fmap, int32_t* utau, int32_t* U, hipStream_t s);

@@ -5,22 +5,23 @@
 //   idx     = ascending t with mask[t] = 1
 //   cu_sel  = selected count before each request start, cu_sel[R] = n_sel
 //
-// Reduce-then-scan over chunks of 4096 tokens (256 threads x 4 groups of
-// 4 consecutive tokens, float4 loads):
-//   1. k_select_count  writes mask (uchar4) and one count per chunk,
+// Reduce-then-scan over chunks of 4096 tokens; every thread owns 16
+// consecutive tokens (64 contiguous bytes of u, 16 bytes of mask):
+//   1. k_select_count  writes the mask and one count per chunk,
 //   2. k_select_scan   exclusive scan of the chunk counts (one workgroup),
-//   3. k_select_write  ranks each selected token inside its chunk with wave64
-//      ballots + mbcnt and writes idx; it also writes cu_sel at request starts.
-// The order inside a chunk is (group, wave, lane, element) = token order, so
-// idx comes out ascending without any sort and the result is deterministic.
+//   3. k_select_write  ranks the selected tokens of a chunk with a wave64 scan
+//      of per-thread counts, stages their indices in LDS and stores them
+//      contiguously; it also writes cu_sel at request starts.
+// Thread order is token order, so idx comes out ascending without a sort and
+// the result is deterministic.
 #include "kernels.hpp"
 
 namespace sphinx {
 
 namespace {
 constexpr int kTPB = 256;
-constexpr int kGroups = 4;                      // float4 groups per thread
-constexpr int kChunk = kTPB * kGroups * 4;      // 4096 tokens per workgroup
+constexpr int kPer = 16;              // consecutive tokens per thread
+constexpr int kChunk = kTPB * kPer;   // 4096 tokens per workgroup
 
 // Global frame of token t and the first token of the next frame.
 __device__ __forceinline__ void frame_of(const ReqTable& T, int64_t t, int& g, int64_t& next) {
@@ -32,56 +33,65 @@ __device__ __forceinline__ void frame_of(const ReqTable& T, int64_t t, int& g, i
   next = T.tok_off[r] + (int64_t)(f + 1) * tpf;
 }
 
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int y = __shfl_up(v, d, kWave);
+    if (lane >= d) v += y;
+  }
+  return v;
+}
+
 __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, const float* __restrict__ u,
                                                       const float* __restrict__ thr,
                                                       const uint8_t* __restrict__ active, uint8_t* __restrict__ mask,
                                                       int32_t* __restrict__ blk_cnt) {
   __shared__ int s_cnt[kTPB / kWave];
-  const int64_t base = (int64_t)blockIdx.x * kChunk;
+  const int64_t t0 = (int64_t)blockIdx.x * kChunk + (int64_t)threadIdx.x * kPer;
   int cnt = 0;
+  if (t0 < N) {
+    const bool full = t0 + kPer <= N;
+    float v[kPer];
+    if (full) {
 #pragma unroll
-  for (int gi = 0; gi < kGroups; ++gi) {
-    const int64_t t0 = base + ((int64_t)gi * kTPB + threadIdx.x) * 4;
-    float v[4];
-    if (t0 + 3 < N) {
-      const float4 q = *reinterpret_cast<const float4*>(u + t0);
-      v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+      for (int q = 0; q < kPer / 4; ++q) {
+        const float4 f = reinterpret_cast<const float4*>(u + t0)[q];
+        v[4 * q] = f.x;
+        v[4 * q + 1] = f.y;
+        v[4 * q + 2] = f.z;
+        v[4 * q + 3] = f.w;
+      }
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (t0 + e < N) ? u[t0 + e] : 0.0f;
+      for (int e = 0; e < kPer; ++e) v[e] = (t0 + e < N) ? u[t0 + e] : 0.0f;
     }
-    // one frame lookup per group of 4 (a second one only when the group
-    // straddles a frame boundary)
-    uint32_t packed = 0;
-    if (t0 < N) {
-      int g;
-      int64_t next;
-      frame_of(T, t0, g, next);
-      float th = thr[g];
-      bool act = active ? (active[g] != 0) : true;
+    // one frame lookup per thread, another only where its tokens cross a frame
+    int g;
+    int64_t next;
+    frame_of(T, t0, g, next);
+    float th = thr[g];
+    bool act = active ? (active[g] != 0) : true;
+    uint32_t w[kPer / 4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int64_t t = t0 + e;
-        if (t < N) {
-          if (t >= next) {
-            frame_of(T, t, g, next);
-            th = thr[g];
-            act = active ? (active[g] != 0) : true;
-          }
-          const bool m = act && (v[e] > th);
-          packed |= (uint32_t)m << (8 * e);
-          cnt += m;
+    for (int e = 0; e < kPer; ++e) {
+      const int64_t t = t0 + e;
+      if (t < N) {
+        if (t >= next) {
+          frame_of(T, t, g, next);
+          th = thr[g];
+          act = active ? (active[g] != 0) : true;
         }
+        const bool m = act && (v[e] > th);
+        w[e >> 2] |= (uint32_t)m << (8 * (e & 3));
+        cnt += m;
       }
     }
-    if (t0 + 3 < N) {
-      *reinterpret_cast<uint32_t*>(mask + t0) = packed;
+    if (full) {
+      *reinterpret_cast<uint4*>(mask + t0) = make_uint4(w[0], w[1], w[2], w[3]);
     } else {
-      for (int e = 0; e < 4; ++e)
-        if (t0 + e < N) mask[t0 + e] = (uint8_t)((packed >> (8 * e)) & 1u);
+      for (int e = 0; e < kPer; ++e)
+        if (t0 + e < N) mask[t0 + e] = (uint8_t)((w[e >> 2] >> (8 * (e & 3))) & 1u);
     }
   }
-  // block sum
   for (int m = 32; m >= 1; m >>= 1) cnt += __shfl_xor(cnt, m, kWave);
   if (lane_id() == 0) s_cnt[threadIdx.x / kWave] = cnt;
   __syncthreads();
@@ -102,13 +112,8 @@ __global__ __launch_bounds__(1024) void k_select_scan(const int32_t* __restrict_
   int local = 0;
   for (int i = 0; i < per; ++i)
     if (b0 + i < nblk) local += blk_cnt[b0 + i];
-  // inclusive wave scan of `local`
-  int incl = local;
   const int lane = lane_id();
-  for (int d = 1; d < kWave; d <<= 1) {
-    const int y = __shfl_up(incl, d, kWave);
-    if (lane >= d) incl += y;
-  }
+  const int incl = wave_incl_scan(local, lane);
   if (lane == kWave - 1) s_part[threadIdx.x / kWave] = incl;
   __syncthreads();
   int wave_base = 0;
@@ -130,54 +135,47 @@ __global__ __launch_bounds__(1024) void k_select_scan(const int32_t* __restrict_
 __global__ __launch_bounds__(kTPB) void k_select_write(ReqTable T, int64_t N, const uint8_t* __restrict__ mask,
                                                       const int32_t* __restrict__ blk_off, int32_t* __restrict__ idx,
                                                       int32_t* __restrict__ cu_sel) {
-  __shared__ int s_wcnt[kGroups][kTPB / kWave];
-  const int64_t base = (int64_t)blockIdx.x * kChunk;
+  __shared__ int s_wtot[kTPB / kWave];
+  __shared__ int32_t s_idx[kChunk];
+  const int64_t t0 = (int64_t)blockIdx.x * kChunk + (int64_t)threadIdx.x * kPer;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  uint32_t bits[kGroups];
-  int lane_prefix[kGroups];
-#pragma unroll
-  for (int gi = 0; gi < kGroups; ++gi) {
-    const int64_t t0 = base + ((int64_t)gi * kTPB + threadIdx.x) * 4;
-    uint32_t packed = 0;
-    if (t0 + 3 < N) {
-      packed = *reinterpret_cast<const uint32_t*>(mask + t0);
-    } else {
-      for (int e = 0; e < 4; ++e)
-        if (t0 + e < N) packed |= (uint32_t)(mask[t0 + e] & 1u) << (8 * e);
-    }
-    bits[gi] = packed;
-    int before = 0, total = 0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint64_t b = __ballot((packed >> (8 * e)) & 1u);
-      before += __popcll(b & ((1ull << lane) - 1ull));
-      total += __popcll(b);
-    }
-    lane_prefix[gi] = before;
-    if (lane == 0) s_wcnt[gi][wave] = total;
+  uint32_t w[kPer / 4] = {0u, 0u, 0u, 0u};
+  if (t0 + kPer <= N) {
+    const uint4 m4 = *reinterpret_cast<const uint4*>(mask + t0);
+    w[0] = m4.x;
+    w[1] = m4.y;
+    w[2] = m4.z;
+    w[3] = m4.w;
+  } else {
+    for (int e = 0; e < kPer; ++e)
+      if (t0 + e < N) w[e >> 2] |= (uint32_t)(mask[t0 + e] & 1u) << (8 * (e & 3));
   }
+  // mask bytes are 0 or 1: fold the 4 bytes of each word into 4 bits
+  uint32_t bits = 0;
+#pragma unroll
+  for (int q = 0; q < kPer / 4; ++q)
+    bits |= ((w[q] & 1u) | ((w[q] >> 7) & 2u) | ((w[q] >> 14) & 4u) | ((w[q] >> 21) & 8u)) << (4 * q);
+  const int cnt = __popc(bits);
+  const int incl = wave_incl_scan(cnt, lane);
+  if (lane == kWave - 1) s_wtot[wave] = incl;
   __syncthreads();
-  int run = blk_off[blockIdx.x];
-#pragma unroll
-  for (int gi = 0; gi < kGroups; ++gi) {
-    int wbase = run;
-    for (int w = 0; w < wave; ++w) wbase += s_wcnt[gi][w];
-    int gtot = 0;
-    for (int w = 0; w < kTPB / kWave; ++w) gtot += s_wcnt[gi][w];
-    const int64_t t0 = base + ((int64_t)gi * kTPB + threadIdx.x) * 4;
-    int pos = wbase + lane_prefix[gi];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int64_t t = t0 + e;
-      if (t < N) {
-        for (int r = 0; r < T.R; ++r)
-          if (T.tok_off[r] == t) cu_sel[r] = pos;
-      }
-      if ((bits[gi] >> (8 * e)) & 1u) idx[pos++] = (int32_t)t;
-    }
-    run += gtot;
+  int lpos = incl - cnt;
+  for (int i = 0; i < wave; ++i) lpos += s_wtot[i];
+  int btot = 0;
+  for (int i = 0; i < kTPB / kWave; ++i) btot += s_wtot[i];
+  const int boff = blk_off[blockIdx.x];
+  for (int r = 0; r < T.R; ++r) {
+    const int64_t s = T.tok_off[r];
+    if (s >= t0 && s < t0 + kPer && s < N)
+      cu_sel[r] = boff + lpos + __popc(bits & ((1u << (uint32_t)(s - t0)) - 1u));
   }
+  int p = lpos;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e)
+    if ((bits >> e) & 1u) s_idx[p++] = (int32_t)(t0 + e);
+  __syncthreads();
+  for (int i = threadIdx.x; i < btot; i += kTPB) idx[boff + i] = s_idx[i];
 }
 }  // namespace
 

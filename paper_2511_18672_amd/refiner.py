@@ -7,6 +7,11 @@ changes, or every step when asked), ``sphinx_gather``, ``sphinx_refine_step``
 and ``sphinx_scatter_blend``.  Python only sequences the calls; every value is
 computed by libsphinx.so.  The per-step schedule comes from
 ``sphinx_plan_step`` (library host code) and is uploaded once.
+
+The fp32 state of record and the noise live token-major by default (token t's
+16 values contiguous at 16*t), so each gathered or scattered token is one
+contiguous row; the NCHW latents are converted once at ``reset`` and back in
+``output``.  ``layout=B.NCHW`` keeps them NCHW throughout (same arithmetic).
 """
 from __future__ import annotations
 
@@ -58,7 +63,7 @@ class Refiner:
 
     def __init__(self, requests: Sequence, cfg, blob: torch.Tensor, s_start: np.ndarray, nsteps: np.ndarray,
                  u: np.ndarray, thr: np.ndarray, z0: np.ndarray, eps: np.ndarray, device="cuda",
-                 max_sel: Optional[int] = None):
+                 max_sel: Optional[int] = None, layout: int = B.TOKENS):
         if not torch.cuda.is_available():
             raise RuntimeError("Refiner needs a GPU: the selective-refinement step has no CPU path")
         B.lib()
@@ -73,11 +78,18 @@ class Refiner:
         self.dt = B.dtype_code(cfg.dtype)
         tdt = _torch_dtype(cfg.dtype)
         dev = torch.device(device)
+        self.layout = int(layout)
         self.z0 = torch.from_numpy(np.ascontiguousarray(z0, np.float32)).to(tdt).to(dev)
-        self.eps = torch.from_numpy(np.ascontiguousarray(eps, np.float32)).to(tdt).to(dev)
+        eps_nchw = torch.from_numpy(np.ascontiguousarray(eps, np.float32)).to(tdt).to(dev)
+        if self.layout == B.NCHW:
+            self.eps = eps_nchw
+        else:  # noise in the state's layout, converted once
+            self.eps = torch.empty_like(eps_nchw)
+            B.sphinx_scatter_blend(self.reqs, None, None, 0, eps_nchw, self.dt, B.NCHW, self.eps, self.dt,
+                                   self.layout)
         self.u = torch.from_numpy(np.ascontiguousarray(u, np.float32)).to(dev)
         self.thr = torch.from_numpy(np.ascontiguousarray(thr, np.float32)).to(dev)
-        self.state = torch.empty(16 * self.N, dtype=torch.float32, device=dev)
+        self.z = torch.empty(16 * self.N, dtype=torch.float32, device=dev)  # state of record, in self.layout
         self.mask = torch.empty(self.N, dtype=torch.uint8, device=dev)
         self.idx = torch.empty(self.N, dtype=torch.int32, device=dev)
         self.cu_sel = torch.empty(self.R + 1, dtype=torch.int32, device=dev)
@@ -95,8 +107,9 @@ class Refiner:
         self.cu_host = None
 
     def reset(self, stream=None):
-        """state <- fp32(z0) (a dtype-converting copy through scatter_blend with no tokens)."""
-        B.sphinx_scatter_blend(self.reqs, None, None, 0, self.z0, self.dt, self.state, B.F32, stream)
+        """state <- fp32(z0) (a converting copy through scatter_blend with no tokens)."""
+        B.sphinx_scatter_blend(self.reqs, None, None, 0, self.z0, self.dt, B.NCHW, self.z, B.F32, self.layout,
+                               stream)
         self._active_key = None
 
     def select(self, k: int, stream=None) -> int:
@@ -118,11 +131,12 @@ class Refiner:
         if n == 0:
             return 0
         P = self.plan
-        B.sphinx_gather(self.reqs, self.state, B.F32, self.eps, self.dt, self.idx, n, P["a"][k], P["b"][k],
-                        self.x_sel, stream)
+        B.sphinx_gather(self.reqs, self.layout, self.z, B.F32, self.eps, self.dt, self.idx, n, P["a"][k],
+                        P["b"][k], self.x_sel, stream)
         B.sphinx_refine_step(self.desc, self.reqs, self.idx, n, self.cu_host, P["tau"][k], P["c1"][k],
                              P["c2"][k], self.x_sel, self.ws, stream)
-        B.sphinx_scatter_blend(self.reqs, self.x_sel, self.idx, n, self.state, B.F32, self.state, B.F32, stream)
+        B.sphinx_scatter_blend(self.reqs, self.x_sel, self.idx, n, self.z, B.F32, self.layout, self.z, B.F32,
+                               self.layout, stream)
         return n
 
     def run(self, stream=None) -> torch.Tensor:
@@ -133,10 +147,16 @@ class Refiner:
         return self.state
 
     def output(self, dtype: str = "bf16", stream=None) -> torch.Tensor:
-        """The state converted to the latent dtype (bf16 rounds to nearest even)."""
-        out = torch.empty(16 * self.N, dtype=_torch_dtype(dtype), device=self.state.device)
-        B.sphinx_scatter_blend(self.reqs, None, None, 0, self.state, B.F32, out, B.dtype_code(dtype), stream)
+        """The state as NCHW latents of the given dtype (bf16 rounds to nearest even)."""
+        out = torch.empty(16 * self.N, dtype=_torch_dtype(dtype), device=self.z.device)
+        B.sphinx_scatter_blend(self.reqs, None, None, 0, self.z, B.F32, self.layout, out, B.dtype_code(dtype),
+                               B.NCHW, stream)
         return out
+
+    @property
+    def state(self) -> torch.Tensor:
+        """A fp32 NCHW copy of the state of record (a new tensor on every access)."""
+        return self.output("f32")
 
 
 def from_workload(wl, device="cuda", **kw) -> Refiner:

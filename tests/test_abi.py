@@ -55,22 +55,30 @@ def test_request_validation(L):
     # bad offsets
     bad = _reqs([(2, 8, 8), (1, 4, 4)])
     bad[1].tok_offset = 5
-    assert L.sphinx_gather(bad, 2, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(bad, 2, 0, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == INVALID
     # odd latent size
     odd = _reqs([(1, 7, 8)])
-    assert L.sphinx_gather(odd, 1, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(odd, 1, 0, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == INVALID
     # too many requests
     many = _reqs([(1, 2, 2)] * 65)
-    assert L.sphinx_gather(many, 65, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == UNSUPPORTED
+    assert L.sphinx_gather(many, 65, 0, P(256), 0, None, 0, P(256), 1, P(256), P(256), P(256), None) == UNSUPPORTED
     # n_sel beyond N, null pointers, misalignment
-    assert L.sphinx_gather(reqs, 1, P(256), 0, None, 0, P(256), 33, P(256), P(256), P(256), None) == INVALID
-    assert L.sphinx_gather(reqs, 1, None, 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == INVALID
-    assert L.sphinx_gather(reqs, 1, P(258), 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == INVALID
-    assert L.sphinx_gather(reqs, 1, P(256), 7, None, 0, P(256), 3, P(256), P(256), P(256), None) == UNSUPPORTED
+    assert L.sphinx_gather(reqs, 1, 0, P(256), 0, None, 0, P(256), 33, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(reqs, 1, 0, None, 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(reqs, 1, 0, P(258), 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == INVALID
+    assert L.sphinx_gather(reqs, 1, 0, P(256), 7, None, 0, P(256), 3, P(256), P(256), P(256), None) == UNSUPPORTED
     # n_sel = 0 is a no-op that touches no pointer
-    assert L.sphinx_gather(reqs, 1, None, 0, None, 0, None, 0, None, None, None, None) == OK
-    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, P(256), 0, None) == OK
-    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, P(256), 1, None) == INVALID
+    assert L.sphinx_gather(reqs, 1, 0, None, 0, None, 0, None, 0, None, None, None, None) == OK
+    assert L.sphinx_gather(reqs, 1, 2, P(256), 0, None, 0, P(256), 3, P(256), P(256), P(256), None) == UNSUPPORTED
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, 0, P(256), 0, 0, None) == OK
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, 1, P(256), 0, 1, None) == OK
+    # in place needs equal dtype and layout
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, 0, P(256), 1, 0, None) == INVALID
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, 0, P(256), 0, 1, None) == INVALID
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, 3, P(1 << 20), 0, 0, None) == UNSUPPORTED
+    # 32 tokens x 16 f32 = 2048 bytes: buffers 256 bytes apart overlap partially
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(256), 0, 0, P(512), 0, 1, None) == INVALID
+    assert L.sphinx_scatter_blend(reqs, 1, None, None, 0, P(4096), 0, 0, P(3584), 1, 0, None) == INVALID
 
 
 def test_select_validation(L):

@@ -88,7 +88,13 @@ def test_select_edge_cases():
     print(f"[select] big N={big.N} n_sel={n}")
 
 
-def test_gather_scatter():
+def _in_layout(nchw, tokens_2d, layout):
+    """The same latents in `layout` (tokens_2d: [N][16] in patch order)."""
+    return nchw if layout == S.NCHW else np.ascontiguousarray(tokens_2d).ravel()
+
+
+@pytest.mark.parametrize("layout", [S.NCHW, S.TOKENS], ids=["nchw", "tokens"])
+def test_gather_scatter(layout):
     wl = W.custom("gs", MICRO_BF16, [W.Request(3, 8, 12), W.Request(2, 6, 4)], [0.5, 0.3], [0.5, 0.5], [1, 1],
                   with_weights=False)
     rng = np.random.default_rng(3)
@@ -97,29 +103,58 @@ def test_gather_scatter():
     b = (rng.random(wl.G) * (rng.random(wl.G) < 0.6)).astype(np.float32)
     _, idx, cu, _ = gpu_select(wl, None)
     n = len(idx)
+    print(f"[gather_scatter] layout={layout} n={n} N={wl.N}", flush=True)
     reqs = S.make_requests(wl.requests)
-    x = torch.empty(16 * n, dtype=torch.float32, device="cuda")
-    S.sphinx_gather(reqs, _dev(state), S.F32, _dev(wl.eps, torch.bfloat16), S.BF16, _dev(idx.astype(np.int32)), n,
-                    _dev(a), _dev(b), x)
-    info = O.token_info(wl.requests)
     P, E = O.patchify(state, wl.requests), O.patchify(wl.eps, wl.requests)
+    state_l = _in_layout(state, P.astype(np.float32), layout)
+    eps_l = _in_layout(wl.eps, E.astype(np.float32), layout)
+    x = torch.empty(16 * n, dtype=torch.float32, device="cuda")
+    S.sphinx_gather(reqs, layout, _dev(state_l), S.F32, _dev(eps_l, torch.bfloat16), S.BF16,
+                    _dev(idx.astype(np.int32)), n, _dev(a), _dev(b), x)
+    info = O.token_info(wl.requests)
+    Eb = torch.from_numpy(E.astype(np.float32)).to(torch.bfloat16).double().numpy()
     g = info.gframe[idx]
-    ref = a[g].astype(np.float64)[:, None] * P[idx] + b[g].astype(np.float64)[:, None] * E[idx]
+    ref = a[g].astype(np.float64)[:, None] * P[idx] + b[g].astype(np.float64)[:, None] * Eb[idx]
     err = np.abs(x.cpu().numpy().reshape(n, 16) - ref).max()
     print(f"[gather] n={n} max_abs={err:.3e}")
     assert err <= 1e-6 * max(1.0, np.abs(ref).max())
+    # eps = NULL drops the noise term
+    S.sphinx_gather(reqs, layout, _dev(state_l), S.F32, None, S.BF16, _dev(idx.astype(np.int32)), n, _dev(a),
+                    _dev(b), x)
+    assert np.array_equal(x.cpu().numpy().reshape(n, 16), (a[g][:, None] * P[idx].astype(np.float32)))
     # scatter in place: selected tokens replaced exactly, the rest untouched
     xs = rng.standard_normal(16 * n).astype(np.float32)
-    st = _dev(state)
-    S.sphinx_scatter_blend(reqs, _dev(xs), _dev(idx.astype(np.int32)), n, st, S.F32, st, S.F32)
+    st = _dev(state_l)
+    S.sphinx_scatter_blend(reqs, _dev(xs), _dev(idx.astype(np.int32)), n, st, S.F32, layout, st, S.F32, layout)
     Pexp = P.copy()
     Pexp[idx] = xs.reshape(n, 16)
-    assert np.array_equal(st.cpu().numpy(), O.unpatchify(Pexp, wl.requests).astype(np.float32))
-    # out of place with conversion to bf16 (round to nearest even)
+    exp_nchw = O.unpatchify(Pexp, wl.requests).astype(np.float32)
+    assert np.array_equal(st.cpu().numpy(), _in_layout(exp_nchw, Pexp.astype(np.float32), layout))
+    # out of place into the other layout with conversion to bf16 (round to nearest even)
+    other = S.TOKENS if layout == S.NCHW else S.NCHW
     out = torch.empty(16 * wl.N, dtype=torch.bfloat16, device="cuda")
-    S.sphinx_scatter_blend(reqs, _dev(xs), _dev(idx.astype(np.int32)), n, _dev(state), S.F32, out, S.BF16)
-    expect = torch.from_numpy(O.unpatchify(Pexp, wl.requests).astype(np.float32)).to(torch.bfloat16)
+    S.sphinx_scatter_blend(reqs, _dev(xs), _dev(idx.astype(np.int32)), n, _dev(state_l), S.F32, layout, out, S.BF16,
+                           other)
+    expect = torch.from_numpy(_in_layout(exp_nchw, Pexp.astype(np.float32), other)).to(torch.bfloat16)
     assert torch.equal(out.cpu(), expect)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_layout_conversion_roundtrip(dt):
+    """NCHW -> tokens -> NCHW with n_sel = 0 is a bit-exact permutation."""
+    reqs_w = [W.Request(3, 10, 6), W.Request(1, 64, 66), W.Request(2, 2, 2)]
+    reqs = S.make_requests(reqs_w)
+    N = sum(r.frames * (r.h // 2) * (r.w // 2) for r in reqs_w)
+    tdt = torch.float32 if dt == "f32" else torch.bfloat16
+    code = S.F32 if dt == "f32" else S.BF16
+    z = torch.from_numpy(np.random.default_rng(5).standard_normal(16 * N).astype(np.float32)).to(tdt)
+    zt = torch.empty_like(z, device="cuda")
+    back = torch.empty_like(z, device="cuda")
+    S.sphinx_scatter_blend(reqs, None, None, 0, z.cuda(), code, S.NCHW, zt, code, S.TOKENS)
+    S.sphinx_scatter_blend(reqs, None, None, 0, zt, code, S.TOKENS, back, code, S.NCHW)
+    expect_t = O.patchify(z.float().numpy(), reqs_w).astype(np.float32).ravel()
+    assert np.array_equal(zt.float().cpu().numpy(), expect_t)
+    assert torch.equal(back.cpu(), z)
 
 
 def run_gpu(wl, trace=False, steps=None):
@@ -171,8 +206,19 @@ def check_end_to_end(wl, teacher_forced=True):
 
 def test_tiny_end_to_end():
     R = check_end_to_end(W.tiny())
-    out = R.output("f32").cpu().numpy()
-    assert np.array_equal(out, R.state.cpu().numpy())
+    f32 = R.output("f32")
+    assert torch.equal(R.output("bf16"), f32.to(torch.bfloat16))
+    # the NCHW state of record runs the same arithmetic: bit-identical result
+    Rn = S.from_workload(W.tiny(), layout=S.NCHW)
+    assert Rn.layout == S.NCHW
+    Rn.run()
+    assert torch.equal(Rn.state, f32)
+
+
+def test_layouts_bit_identical_bf16():
+    wl = W.custom("layouts", MID_BF16, [W.Request(2, 16, 12), W.Request(1, 10, 10)], [0.6, 0.4], [0.5, 0.3], [3, 2])
+    Rt, Rn = S.from_workload(wl), S.from_workload(wl, layout=S.NCHW)
+    assert torch.equal(Rt.run(), Rn.run())
 
 
 def test_small_end_to_end():
