@@ -26,8 +26,14 @@
 // workgroup order is remapped so that each XCD works on whole heads.
 // head_dim 72 pads QK^T to 5 k-steps of 16 (d 72..79 zero) and computes O^T in
 // three 32-row blocks (rows 72..95 are computed from zero V^T rows and dropped).
+// head_dim 64 runs a software-pipelined form of the same computation with
+// direct global->LDS copies (k_attn_bf16_dma, described with its code); the
+// kernel above remains for head_dim 64 inputs too large for its 32-bit offsets.
 //
 // fp32 path (fp32 models, head_dim <= 64): one thread per (query, head).
+
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -288,6 +294,398 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16_d72(const bf16* __restrict
   attn_body<72>(qkv, o, D, heads, scale_log2, S, sm);
 }
 
+__device__ __forceinline__ float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Row max of one 64-key tile in log2 units (scores s0: keys 0..31, s1: keys
+// 32..63 of the tile, slot r = key 8*(r/4) + 4*g + r%4; lanes l and l^32 hold
+// the two halves of the same query's keys).
+template <bool MASK>
+__device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kbase, int L, float scale_log2) {
+  if (MASK) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int key = kbase + (r >> 2) * 8 + g * 4 + (r & 3);
+      if (key >= L) s0[r] = -INFINITY;
+      if (key + 32 >= L) s1[r] = -INFINITY;
+    }
+  }
+  float m4[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    float t = fmaxf(fmaxf(s0[4 * q], s0[4 * q + 1]), s0[4 * q + 2]);
+    t = fmaxf(fmaxf(t, s0[4 * q + 3]), s1[4 * q]);
+    t = fmaxf(fmaxf(t, s1[4 * q + 1]), s1[4 * q + 2]);
+    m4[q] = fmaxf(t, s1[4 * q + 3]);
+  }
+  return max_across_halves(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * scale_log2;
+}
+
+// Probabilities exp2(s * scale - m) of one tile, rounded to bf16 in P^T
+// operand order; their row sum (of the rounded values) is added to l_run.
+__device__ __forceinline__ void tile_probs(const f32x16& s0, const f32x16& s1, float scale_log2, float m_run,
+                                           float& l_run, bf16x8 (&pf)[2][2]) {
+  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+  float psum = 0.0f;
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = hf * 8 + 2 * i;
+      bf16x2 a, b;
+      a[0] = (bf16)fast_exp2(fmaf(s0[r], scale_log2, -m_run));
+      a[1] = (bf16)fast_exp2(fmaf(s0[r + 1], scale_log2, -m_run));
+      b[0] = (bf16)fast_exp2(fmaf(s1[r], scale_log2, -m_run));
+      b[1] = (bf16)fast_exp2(fmaf(s1[r + 1], scale_log2, -m_run));
+      psum = __builtin_amdgcn_fdot2_f32_bf16(a, ones, psum, false);
+      psum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, psum, false);
+      pf[0][hf][2 * i] = a[0];
+      pf[0][hf][2 * i + 1] = a[1];
+      pf[1][hf][2 * i] = b[0];
+      pf[1][hf][2 * i + 1] = b[1];
+    }
+  l_run += psum;
+}
+
+// Moves the running max to mx where it grew by more than 2^kRescaleLog2 and
+// returns the factor for O (exactly 1, exp2(0), on lanes that keep theirs).
+__device__ __forceinline__ float raise_max(float mx, float& m_run, float& l_run) {
+  const float m_new = (mx > m_run + kRescaleLog2) ? mx : m_run;
+  const float alpha = fast_exp2(m_run - m_new);
+  l_run *= alpha;
+  m_run = m_new;
+  return alpha;
+}
+
+// ---------------------------------------------------------------------------
+// head_dim 64, software-pipelined, with direct global->LDS copies
+// (global_load_lds_dwordx4) and the LDS transpose read (ds_read_b64_tr_b16).
+//  * Iteration t of the key loop issues QK(t+1) (8 MFMAs on the next K tile)
+//    and PV(t-1) (8 MFMAs with the probabilities kept from the previous
+//    iteration) while computing the softmax of tile t, whose scores came from
+//    the previous iteration.  Neither MFMA group depends on that softmax, so
+//    the region is one straight-line block: all fragment reads first, then 16
+//    steps of one MFMA and one pair of probabilities, fenced so the compiler
+//    keeps the order.  The running max moves branch-free; O is rescaled (a
+//    wave-uniform branch taken only when some lane's max moved) between
+//    PV(t-1) and PV(t), at the start of the next iteration.  The floating-point
+//    operations and their order are those of attn_body<64>: results are
+//    bit-identical.
+//  * K and V tiles are stored unpadded, 64 rows of 128 B, with the 16-byte
+//    chunks of row r permuted: K chunk c at c ^ ((r >> 1) & 7), V chunk c at
+//    c ^ 2(r & 3).  LDS has 64 four-byte banks and serves a 16-byte read to 16
+//    lanes per pass; a 128-byte row covers half the banks, so the 16 rows of
+//    one ds_read_b128 pass (same chunk) must spread over both halves and all
+//    eight chunk slots, which the K permutation does; the V permutation does
+//    the same for the four rows of each transpose-read lane group.
+//  * Each wave copies 8 rows per instruction: lane i of copy n writes the 16
+//    bytes at row 8(2w + n) + i/8, slot i%8 of the tile and reads them from
+//    the global chunk that the permutation puts there: no registers, no LDS
+//    stores and no VALU transposition.
+//  * The V^T A fragment of a 32-row block db is two transpose reads: within a
+//    16-lane group, output lane i gets element i%4 of what input lane
+//    4e + i/4 addressed, so input lane j addresses V row (key) 4g + j/4 (+8
+//    for the second read) at d = 32 db + 16 (b & 1) + 4 (j % 4), b = lane/16;
+//    this gives each lane the 8 keys of its P^T k-slots for d = 32 db + l%32.
+//  * Tiles live in 3-slot rings: the copies issued in iteration t land by the
+//    end of iteration t+1 (a per-wave vmcnt wait that leaves the newest copies
+//    in flight, then the workgroup barrier; no memory fence).
+namespace dma {
+constexpr int kTileBytes = AK * 64 * 2;  // 8 KB
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kRing = 3;  // tiles in flight per operand
+
+struct Smem {
+  char k[kRing][kTileBytes];
+  char v[kRing][kTileBytes];
+};
+
+__device__ __forceinline__ bf16x8 tr_pair(const char* p0, const char* p1) {
+  const v4s a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p0);
+  const v4s b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p1);
+  const v4s r[2] = {a, b};
+  return *reinterpret_cast<const bf16x8*>(r);
+}
+
+// Per-lane byte offsets inside a tile (loop invariant).
+struct LaneOff {
+  int k[4];   // QK A fragment, k-step ks, key rows 0..31 (rows 32..63: +4096)
+  int v[2];   // PV A fragment, block db, first transpose read (second: +1024)
+};
+
+__device__ __forceinline__ LaneOff lane_offsets(int lane) {
+  LaneOff o;
+  const int r32 = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) o.k[ks] = r32 * 128 + (((2 * ks + g) ^ ((r32 >> 1) & 7)) << 4);
+  const int j = lane & 15, b = lane >> 4;
+  const int row = 4 * g + (j >> 2);
+#pragma unroll
+  for (int db = 0; db < 2; ++db) {
+    const int byte = 64 * db + 32 * (b & 1) + 8 * (j & 3);
+    const int chunk = (byte >> 4) ^ (2 * (row & 3));
+    o.v[db] = row * 128 + (chunk << 4) + (byte & 8);
+  }
+  return o;
+}
+
+__device__ __forceinline__ void qk(const char* sK, const LaneOff& lo, const bf16x8 (&qf)[4], f32x16& s0,
+                                   f32x16& s1) {
+  s0 = f32x16{};
+  s1 = f32x16{};
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks]);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks] + 4096);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
+  }
+}
+
+// O^T += V^T P^T; P^T k-slot (g, j) of (kb, hf) is key 32 kb + 16 hf + 8 (j/4) + 4 g + j%4.
+__device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16x8 (&pf)[2][2],
+                                   f32x16 (&oacc)[2]) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int db = 0; db < 2; ++db) {
+        const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
+        const bf16x8 vf = tr_pair(p, p + 8 * 128);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
+      }
+}
+
+// One iteration's MFMA work interleaved by hand with the softmax of the
+// previous tile: all fragment reads first, then 16 steps of one MFMA
+// (QK(t+1) for steps 0..7, PV(t-1) for steps 8..15) and one pair of
+// probabilities (two exponentials, one bf16 pack, one row-sum dot product),
+// each step fenced so the compiler keeps the order.
+__device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff& lo, const bf16x8 (&qf)[4],
+                                       const f32x16& c0, const f32x16& c1, float scale_log2, float m_run,
+                                       float& l_run, const bf16x8 (&pp)[2][2], bf16x8 (&pn)[2][2], f32x16& n0,
+                                       f32x16& n1, f32x16 (&oacc)[2]) {
+  bf16x8 kf[4][2];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    kf[ks][0] = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks]);
+    kf[ks][1] = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks] + 4096);
+  }
+  bf16x8 vf[2][2][2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int db = 0; db < 2; ++db) {
+        const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
+        vf[kb][hf][db] = tr_pair(p, p + 8 * 128);
+      }
+  __builtin_amdgcn_sched_barrier(0);
+  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+  float psum = 0.0f;
+  n0 = f32x16{};
+  n1 = f32x16{};
+#pragma unroll
+  for (int st = 0; st < 16; ++st) {
+    if (st < 8) {
+      const int ks = st >> 1;
+      if (st & 1)
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][1], qf[ks], n1, 0, 0, 0);
+      else
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][0], qf[ks], n0, 0, 0, 0);
+    } else {
+      const int kb = (st - 8) >> 2, hf = ((st - 8) >> 1) & 1, db = (st - 8) & 1;
+      oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kb][hf][db], pp[kb][hf], oacc[db], 0, 0, 0);
+    }
+    // probability pair st: half hf, pair i, score block w (s0 or s1)
+    const int hf = st >> 3, i = (st >> 1) & 3, w = st & 1;
+    const int r = hf * 8 + 2 * i;
+    const f32x16& sc = w ? c1 : c0;
+    bf16x2 pr;
+    pr[0] = (bf16)fast_exp2(fmaf(sc[r], scale_log2, -m_run));
+    pr[1] = (bf16)fast_exp2(fmaf(sc[r + 1], scale_log2, -m_run));
+    psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, psum, false);
+    pn[w][hf][2 * i] = pr[0];
+    pn[w][hf][2 * i + 1] = pr[1];
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  l_run += psum;
+}
+}  // namespace dma
+
+__device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D, int heads,
+                                              float scale_log2, const SegTable& S, dma::Smem& sm) {
+  constexpr int HD = 64;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5, r32 = lane & 31;
+  const int ntiles = S.tile_prefix[S.nseg];
+  const int work = ntiles * heads;
+  int lid = (int)blockIdx.x;
+  if (work % 8 == 0) lid = (lid & 7) * (work >> 3) + (lid >> 3);
+  const int head = lid / ntiles, tile = lid - head * ntiles;
+  int s = 0;
+  while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
+  const int qt = tile - S.tile_prefix[s];
+  const int seg0 = S.start[s], L = S.len[s];
+  const int ld = 3 * D;
+  const bf16x8 zero8 = {};
+
+  // V buffer 2 (that of "tile -1") starts all zero: the first iteration's PV
+  // multiplies it by zero probabilities.
+  for (int i = tid; i < dma::kTileBytes / 16; i += 256) reinterpret_cast<bf16x8*>(sm.v[2])[i] = zero8;
+
+  const int ql = qt * AQ + wave * 32 + r32;
+  bf16x8 qf[4];
+  const bf16* Qg = qkv + (int64_t)seg0 * ld + head * HD;
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks)
+    qf[ks] = (ql < L) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)ql * ld + ks * 16 + g * 8) : zero8;
+
+  // Copy sources: lane i of copy n (n = 0, 1) fills row 8(2 wave + n) + i/8,
+  // slot i%8 of a tile.  Element offsets from the segment's first key, rows
+  // clamped to the last key of the segment.
+  const bf16* Kg = qkv + (int64_t)seg0 * ld + D + head * HD;
+  const bf16* Vg = qkv + (int64_t)seg0 * ld + 2 * D + head * HD;
+  int koff[2], voff[2], klast[2], vlast[2];
+#pragma unroll
+  for (int n = 0; n < 2; ++n) {
+    const int row = 8 * (2 * wave + n) + (lane >> 3);
+    const int kc = (lane & 7) ^ ((row >> 1) & 7), vc = (lane & 7) ^ (2 * (row & 3));
+    koff[n] = row * ld + kc * 8;
+    voff[n] = row * ld + vc * 8;
+    klast[n] = (L - 1) * ld + kc * 8;
+    vlast[n] = (L - 1) * ld + vc * 8;
+  }
+  auto copy_k = [&](int kbase, int buf) {
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+      __builtin_amdgcn_global_load_lds(Kg + min(koff[n] + kbase * ld, klast[n]),
+                                       (dma::lds_void*)(sm.k[buf] + (2 * wave + n) * 1024), 16, 0, 0);
+  };
+  auto copy_v = [&](int kbase, int buf) {
+#pragma unroll
+    for (int n = 0; n < 2; ++n)
+      __builtin_amdgcn_global_load_lds(Vg + min(voff[n] + kbase * ld, vlast[n]),
+                                       (dma::lds_void*)(sm.v[buf] + (2 * wave + n) * 1024), 16, 0, 0);
+  };
+  // Barrier after this wave's LDS operations and all but its newest `keep`
+  // copies (the copies issued in the current iteration stay in flight); no
+  // memory fence is needed beyond that (the LDS reads of the iteration have
+  // all been consumed by MFMAs).  The empty asm statements keep the compiler
+  // from moving memory operations across the barrier.
+  auto land = [&](auto keep) {
+    if (decltype(keep)::value == 4)
+      __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4) lgkmcnt(0)
+    else
+      __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+  using Keep4 = std::integral_constant<int, 4>;
+  using Keep0 = std::integral_constant<int, 0>;
+
+  const dma::LaneOff lo = dma::lane_offsets(lane);
+  f32x16 oacc[2] = {f32x16{}, f32x16{}};
+  float m_run = -INFINITY, l_run = 0.0f;
+  const int nkt = (L + AK - 1) / AK;
+
+  // Tile j of K and of V lives in ring slot j % 3.  Iteration t: softmax of
+  // tile t, QK(t+1), PV(t-1); copies K(t+3) (clamped to the last tile: a
+  // harmless duplicate near the end) and V(t+1), which land by the end of
+  // iteration t+1.  The running max moves branch-free; the factor for O
+  // (exactly 1 unless some lane's max moved) is applied at the start of the
+  // next iteration, i.e. after PV(t-1) and before PV(t).
+  float alpha = 1.0f;
+  auto rescale_o = [&]() {
+    if (__ballot(alpha != 1.0f) != 0) {
+      oacc[0] *= alpha;
+      oacc[1] *= alpha;
+    }
+  };
+  int slot = 0;  // t % 3
+  auto iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, bf16x8 (&pp)[2][2],
+                  bf16x8 (&pn)[2][2]) {
+    const int s1 = slot == 2 ? 0 : slot + 1, s2 = slot == 0 ? 2 : slot - 1;  // (t+1) % 3, (t-1) % 3
+    copy_k(min(t + 3, nkt - 1) * AK, slot);
+    copy_v((t + 1) * AK, s1);
+    const float a_new = raise_max(tile_max<false>(c0, c1, g, t * AK, L, scale_log2), m_run, l_run);
+    rescale_o();
+    alpha = a_new;
+    dma::region(sm.k[s1], sm.v[s2], lo, qf, c0, c1, scale_log2, m_run, l_run, pp, pn, n0, n1, oacc);
+    land(Keep4{});
+    slot = s1;
+  };
+
+  copy_k(0, 0);
+  copy_k(min(1, nkt - 1) * AK, 1);
+  copy_k(min(2, nkt - 1) * AK, 2);
+  copy_v(0, 0);
+  land(Keep4{});
+  f32x16 a0, a1, b0, b1;
+  dma::qk(sm.k[0], lo, qf, a0, a1);
+  // iteration 0 copies K(3) into slot 0: every wave must be done reading K(0)
+  land(Keep4{});
+  bf16x8 pa[2][2] = {{zero8, zero8}, {zero8, zero8}}, pb[2][2];
+  int t = 0;
+  for (; t + 2 < nkt; t += 2) {
+    iter(t, a0, a1, b0, b1, pa, pb);
+    iter(t + 1, b0, b1, a0, a1, pb, pa);
+  }
+  if (t + 1 < nkt) {
+    iter(t, a0, a1, b0, b1, pa, pb);
+    a0 = b0;
+    a1 = b1;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) pa[kb][hf] = pb[kb][hf];
+    ++t;
+  }
+  {  // last tile t = nkt - 1 (possibly partial); V(t) was copied in iteration t-1
+    const int sprev = slot == 0 ? 2 : slot - 1;
+    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L, scale_log2)
+                                   : tile_max<false>(a0, a1, g, t * AK, L, scale_log2);
+    const float a_new = raise_max(mx, m_run, l_run);
+    rescale_o();
+    alpha = a_new;
+    tile_probs(a0, a1, scale_log2, m_run, l_run, pb);
+    dma::pv(sm.v[sprev], lo, pa, oacc);
+    rescale_o();
+    land(Keep0{});
+    dma::pv(sm.v[slot], lo, pb, oacc);
+  }
+  l_run += __shfl_xor(l_run, 32, kWave);
+  if (ql < L) {
+    const float inv = 1.0f / l_run;
+    bf16* orow = o + (int64_t)(seg0 + ql) * D + head * HD;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        bf16x4 ov;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ov[q] = (bf16)(oacc[db][rr * 4 + q] * inv);
+        *reinterpret_cast<bf16x4*>(orow + db * 32 + rr * 8 + g * 4) = ov;
+      }
+  }
+}
+
+__global__ __launch_bounds__(256, 2) void k_attn_bf16_dma(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D,
+                                                          int heads, float scale_log2, SegTable S) {
+  __shared__ __attribute__((aligned(1024))) dma::Smem sm;
+  attn_body_dma(qkv, o, D, heads, scale_log2, S, sm);
+}
+
 constexpr int kF32Max = 64;
 
 __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ qkv, float* __restrict__ o, int D, int d,
@@ -334,7 +732,10 @@ hipError_t launch_attention(sphinx_dtype dt, const void* qkv, void* o, int D, in
   if (dt == SPHINX_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
     const int grid = S.tile_prefix[S.nseg] * heads;
-    if (head_dim == 64)
+    // the copy kernel addresses K and V with 32-bit element offsets
+    if (head_dim == 64 && (int64_t)n * 3 * D < ((int64_t)1 << 31))
+      k_attn_bf16_dma<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
+    else if (head_dim == 64)
       k_attn_bf16<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
     else
       k_attn_bf16_d72<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
