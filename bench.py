@@ -290,7 +290,7 @@ def main():
     achieved = attn_flop / avg_s / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_entry("attention", args.config),
-                "kernel": "k_attn_bf16 (varlen flash attention, head_dim 64)",
+                "kernel": "k_attn_bf16_dma (varlen flash attention, head_dim 64)",
                 "algorithmic_flop_per_launch": attn_flop}
     step_flop = L * (attn_flop + sum(gemm_flop.values()))
     mfma_util = step_flop / (ms_per_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
