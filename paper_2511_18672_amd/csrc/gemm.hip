@@ -14,6 +14,10 @@
 // clamped to the last row and not stored.  The epilogue stages the fp32
 // tile in LDS and finishes it with 16-byte row-contiguous loads and stores.
 //
+// That register-staged kernel (k_gemm_bf16) is the fallback for operands beyond
+// 32-bit element offsets;
+// otherwise the bf16 path runs k_gemm_dma_* (described with its code).
+//
 // fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
 #include "kernels.hpp"
 
@@ -187,6 +191,227 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 GEMM with direct global->LDS copies (global_load_lds_dwordx4), used
+// whenever A and W are addressable with 32-bit element offsets.
+//  * Block tile 128x128x64, 4 waves in 2x2, each a 64x64 tile of 2x2
+//    v_mfma_f32_32x32x16_bf16; two workgroups per CU.
+//  * Operand tiles are unpadded 128-byte rows (A rows, then W rows, of one
+//    64-wide K step); chunk c of row r sits at c ^ ((r >> 1) & 7), which spreads
+//    the 16 rows of one ds_read_b128 pass (same chunk) over all 64 LDS banks.
+//    Each wave copies 8 rows per instruction: lane i of copy q writes slot i%8
+//    of row 8q + i/8 and reads the global chunk the permutation puts there, so
+//    the copy needs no registers, no LDS stores and no address VALU beyond one
+//    add per copy.
+//  * K steps live in a 2-slot ring.  The wait for the next step's copies and
+//    the workgroup barrier sit inside the last 16-deep k-step of the current
+//    one, so the next step's first fragments are read (and the following
+//    copies issued) while the last MFMAs of the current step run; inside a
+//    step each k-step's fragment reads are issued before the previous
+//    k-step's MFMAs.  Barriers carry no memory fence: each wave waits for its
+//    own copies (vmcnt) and LDS reads (lgkmcnt) first.
+//  * The accumulation order per output (k-steps of 16 in ascending k, then the
+//    same epilogue) equals k_gemm_bf16's, so the results are bit-identical.
+namespace dma {
+typedef __attribute__((address_space(3))) void lds_void;
+
+// s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
+// bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
+constexpr int wait_vm_lgkm0(int vm) { return 0x0070 | (vm & 15) | ((vm >> 4) << 14); }
+
+template <int BM, int BN, int NS>
+struct DmaCfg {
+  static constexpr int BK = 64;
+  static constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
+  static constexpr int STAGE = (BM + BN) * 128;     // bytes per K-step
+  static constexpr int COPIES = (BM + BN) / 32;     // copy instructions per wave per stage
+  static constexpr int CLD = BN + 4;                // epilogue staging row (fp32)
+  static constexpr int SMEM = NS * STAGE > BM * CLD * 4 ? NS * STAGE : BM * CLD * 4;
+};
+
+template <int EPI, int BM, int BN, int NS>
+__device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                              const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e,
+                                              unsigned char* smem) {
+  typedef DmaCfg<BM, BN, NS> C;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int g = lane >> 5, r32 = lane & 31;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+
+  // copy sources: instruction i of this wave fills rows 8q .. 8q+7 of the
+  // stage (q = wave * COPIES + i; rows < BM are A rows, the rest W rows)
+  const bf16* src[C::COPIES];
+  int soff[C::COPIES];
+#pragma unroll
+  for (int i = 0; i < C::COPIES; ++i) {
+    const int q = wave * C::COPIES + i;
+    const int row = 8 * q + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    if (8 * q < BM) {
+      src[i] = A;
+      soff[i] = min(m0 + row, M - 1) * K + c * 8;
+    } else {
+      src[i] = W;
+      soff[i] = (n0 + row - BM) * K + c * 8;
+    }
+  }
+  auto copy_stage = [&](int kt, int slot) {
+    unsigned char* base = smem + slot * C::STAGE;
+#pragma unroll
+    for (int i = 0; i < C::COPIES; ++i)
+      __builtin_amdgcn_global_load_lds(src[i] + soff[i] + kt * C::BK,
+                                       (lds_void*)(base + (wave * C::COPIES + i) * 1024), 16, 0, 0);
+  };
+  // fragment offsets inside a stage (k-step ks of 16)
+  int foff[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) foff[ks] = r32 * 128 + (((2 * ks + g) ^ ((r32 >> 1) & 7)) << 4);
+  const int a_row0 = wm * C::WM, b_row0 = BM + wn * C::WN;
+
+  f32x16 acc[C::TI][C::TJ];
+#pragma unroll
+  for (int i = 0; i < C::TI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TJ; ++j) acc[i][j] = f32x16{};
+
+  const int KT = K / C::BK;
+  static_assert(NS == 2 || NS == 3, "ring of 2 or 3 stages");
+  // Stage j lives in slot j % NS.  The wait for stage kt+1 and the barrier sit
+  // inside the last k-step of tile kt: after it every wave has read all of
+  // stage kt (so its slot can be refilled with stage kt+NS) and stage kt+1 has
+  // landed (so its first fragments can be read while the last MFMAs of tile
+  // kt run).  With 3 slots the copies of stage kt+2 may stay in flight.
+  auto sync_stage = [&](int next) {  // next = the stage that must have landed
+    if (NS == 3 && next + 1 < KT)
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(C::COPIES));
+    else
+      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < KT) copy_stage(s, s);
+  // the first min(NS, KT) stages are issued; stage 0 must land before the
+  // first reads, the later ones may stay in flight
+  if (NS == 3 && KT > 2)
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(2 * C::COPIES));
+  else if (KT > 1)
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(C::COPIES));
+  else
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+
+  bf16x8 fa[4][C::TI], fb[4][C::TJ];  // one register set per k-step
+  auto read = [&](const unsigned char* st, int ks, int buf) {
+#pragma unroll
+    for (int i = 0; i < C::TI; ++i)
+      fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + (a_row0 + 32 * i) * 128 + foff[ks]);
+#pragma unroll
+    for (int j = 0; j < C::TJ; ++j)
+      fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + (b_row0 + 32 * j) * 128 + foff[ks]);
+  };
+  int slot = 0;
+  read(smem, 0, 0);
+  for (int kt = 0; kt < KT; ++kt) {
+    const unsigned char* st = smem + slot * C::STAGE;
+    const int nslot = slot + 1 == NS ? 0 : slot + 1;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      if (ks < 3) {
+        read(st, ks + 1, ks + 1);
+      } else if (kt + 1 < KT) {
+        sync_stage(kt + 1);
+        if (kt + NS < KT) copy_stage(kt + NS, slot);
+        read(smem + nslot * C::STAGE, 0, 0);
+      }
+      // the next k-step's reads are issued before this k-step's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < C::TI; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    slot = nslot;
+  }
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+
+  // epilogue: fp32 tile staged in LDS, then 16-byte row-contiguous I/O
+  float* sC = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int i = 0; i < C::TI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sC[(a_row0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
+  __syncthreads();
+  constexpr int TPR = BN / 4;          // threads per row (one float4 each)
+  constexpr int RPP = 256 / TPR;       // rows per pass
+  const int c4 = (tid % TPR) * 4, rsub = tid / TPR;
+  const int n = n0 + c4;
+  float4 bv;
+  {
+    const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n);
+    bv = make_float4((float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]);
+  }
+#pragma unroll 4
+  for (int p = 0; p < BM / RPP; ++p) {
+    const int row = p * RPP + rsub;
+    const int m = m0 + row;
+    if (m >= M) continue;
+    float4 v = *reinterpret_cast<const float4*>(&sC[row * C::CLD + c4]);
+    v.x += bv.x;
+    v.y += bv.y;
+    v.z += bv.z;
+    v.w += bv.w;
+    if constexpr (EPI == EPI_GATED) {
+      float* hp = reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n;
+      const float4 gv = *reinterpret_cast<const float4*>(e.gate + (int64_t)e.crow[m] * e.ldg + n);
+      float4 h = *reinterpret_cast<const float4*>(hp);
+      h.x = fmaf(1.0f + gv.x, v.x, h.x);
+      h.y = fmaf(1.0f + gv.y, v.y, h.y);
+      h.z = fmaf(1.0f + gv.z, v.z, h.z);
+      h.w = fmaf(1.0f + gv.w, v.w, h.w);
+      *reinterpret_cast<float4*>(hp) = h;
+    } else {
+      if constexpr (EPI == EPI_GELU) {
+        v.x = gelu_tanh(v.x);
+        v.y = gelu_tanh(v.y);
+        v.z = gelu_tanh(v.z);
+        v.w = gelu_tanh(v.w);
+      }
+      bf16x4 o;
+      o[0] = (bf16)v.x;
+      o[1] = (bf16)v.y;
+      o[2] = (bf16)v.z;
+      o[3] = (bf16)v.w;
+      *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
+    }
+  }
+}
+#define SPHINX_GEMM_DMA_KERNEL(NAME, EPI)                                                                    \
+  __global__ __launch_bounds__(256, 2) void NAME(const bf16* __restrict__ A, const bf16* __restrict__ W,          \
+                                                 const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {  \
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, 2>::SMEM];                      \
+    gemm_dma_body<EPI, 128, 128, 2>(A, W, bias, M, N, K, e, smem);                                               \
+  }
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_bias, EPI_BIAS)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gelu, EPI_GELU)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gated, EPI_GATED)
+#undef SPHINX_GEMM_DMA_KERNEL
+}  // namespace dma
+
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, const float* __restrict__ W,
                                                   const float* __restrict__ bias, int M, int N, int K, GemmEpi e) {
@@ -236,9 +461,18 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
   if (dt == SPHINX_BF16) {
     const dim3 grid(N / BN, (M + BM - 1) / BM);
     const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
-    if (epi == EPI_BIAS) k_gemm_bf16<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
-    else if (epi == EPI_GELU) k_gemm_bf16<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
-    else k_gemm_bf16<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    const int64_t lim = (int64_t)1 << 31;  // the copy kernel uses 32-bit element offsets
+    if ((int64_t)M * K < lim && (int64_t)N * K < lim) {
+      if (epi == EPI_BIAS) dma::k_gemm_dma_bias<<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+      else if (epi == EPI_GELU) dma::k_gemm_dma_gelu<<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+      else dma::k_gemm_dma_gated<<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    } else if (epi == EPI_BIAS) {
+      k_gemm_bf16<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    } else if (epi == EPI_GELU) {
+      k_gemm_bf16<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    } else {
+      k_gemm_bf16<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+    }
   } else {
     const dim3 grid(N / 64, (M + 63) / 64);
     const float *a = (const float*)A, *w = (const float*)W, *b = (const float*)bias;
