@@ -199,12 +199,16 @@ sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const 
                                    int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, sphinx_layout in_layout,
                                    void* z_out, sphinx_dtype out_dtype, sphinx_layout out_layout, void* stream);
 
-/* Profiling aid (outside the method).  While enabled, every launch of a kernel
- * class is bracketed by two HIP events recorded on the stream of the launch;
- * sphinx_timing_read waits for the recorded events and returns the number of
- * launches and their summed GPU time since timing was last enabled.  Events are
- * created on first use and reused; nothing is allocated on the device.  The
- * timing state is process-wide and guarded by a mutex. */
+/* Profiling aid (outside the method).  sphinx_timing_enable(classes) takes a
+ * bit mask of kernel classes (bit k = class k; 0 turns timing off; bits at or
+ * above SPHINX_K_COUNT are SPHINX_E_INVALID).  While a class is enabled, every
+ * launch of it is bracketed by two HIP events recorded on the stream of the
+ * launch; sphinx_timing_read waits for the recorded events and returns the
+ * number of launches and their summed GPU time since timing was last enabled
+ * (a non-zero mask resets the sums).  Bracketing only the classes of interest
+ * keeps the events away from the other launches.  Events are created on first
+ * use and reused; nothing is allocated on the device.  The timing state is
+ * process-wide and guarded by a mutex. */
 typedef enum {
   SPHINX_K_SELECT = 0, /* mask + compaction (three kernels, one bracket) */
   SPHINX_K_GATHER,
@@ -221,7 +225,7 @@ typedef enum {
   SPHINX_K_COUNT
 } sphinx_kernel_class;
 
-sphinx_status sphinx_timing_enable(int32_t on);
+sphinx_status sphinx_timing_enable(int32_t classes);
 sphinx_status sphinx_timing_read(sphinx_kernel_class k, int64_t* launches, double* total_ms);
 
 #ifdef __cplusplus

@@ -207,9 +207,18 @@ def sphinx_scatter_blend(reqs, x_sel, idx, n_sel: int, z_in, in_dtype: int, in_l
         out_layout, _stream(stream)))
 
 
-def sphinx_timing_enable(on: bool = True):
-    """Bracket every kernel-class launch with HIP events on its stream (profiling aid)."""
-    _check("sphinx_timing_enable", lib().sphinx_timing_enable(1 if on else 0))
+def sphinx_timing_enable(on=True, classes: Optional[Sequence[str]] = None):
+    """Bracket the launches of the given kernel classes (all when None) with HIP
+    events on their stream (profiling aid); on=False turns timing off."""
+    if not on:
+        mask = 0
+    elif classes is None:
+        mask = (1 << len(KERNEL_CLASSES)) - 1
+    else:
+        mask = 0
+        for c in classes:
+            mask |= 1 << KERNEL_CLASSES.index(c)
+    _check("sphinx_timing_enable", lib().sphinx_timing_enable(mask))
 
 
 def sphinx_timing_read() -> Dict[str, tuple]:

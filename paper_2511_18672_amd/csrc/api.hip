@@ -173,7 +173,7 @@ std::vector<double> alpha_bar_table() {
 // ---- profiling aid: HIP-event brackets per kernel class ----------------------
 struct Timing {
   std::mutex mu;
-  bool on = false;
+  uint32_t mask = 0;  // bit k: bracket kernel class k
   struct Pending {
     int cls;
     hipEvent_t a, b;
@@ -207,7 +207,7 @@ class Bracket {
   Bracket(int cls, hipStream_t s) : cls_(cls), s_(s) {
     Timing& T = timing();
     std::lock_guard<std::mutex> g(T.mu);
-    if (!T.on) return;
+    if (((T.mask >> cls) & 1u) == 0) return;
     if (T.spare.empty()) {
       hipEvent_t a, b;
       if (hipEventCreate(&a) != hipSuccess) return;
@@ -553,15 +553,16 @@ sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const 
   return SPHINX_OK;
 }
 
-sphinx_status sphinx_timing_enable(int32_t on) {
+sphinx_status sphinx_timing_enable(int32_t classes) {
+  if (classes < 0 || classes >= (1 << SPHINX_K_COUNT)) return SPHINX_E_INVALID;
   Timing& T = timing();
   std::lock_guard<std::mutex> g(T.mu);
   T.resolve();
-  if (on) {
+  if (classes != 0) {
     std::fill(T.launches, T.launches + SPHINX_K_COUNT, 0);
     std::fill(T.ms, T.ms + SPHINX_K_COUNT, 0.0);
   }
-  T.on = on != 0;
+  T.mask = (uint32_t)classes;
   return SPHINX_OK;
 }
 

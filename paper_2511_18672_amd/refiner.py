@@ -90,9 +90,15 @@ class Refiner:
         self.u = torch.from_numpy(np.ascontiguousarray(u, np.float32)).to(dev)
         self.thr = torch.from_numpy(np.ascontiguousarray(thr, np.float32)).to(dev)
         self.z = torch.empty(16 * self.N, dtype=torch.float32, device=dev)  # state of record, in self.layout
-        self.mask = torch.empty(self.N, dtype=torch.uint8, device=dev)
-        self.idx = torch.empty(self.N, dtype=torch.int32, device=dev)
-        self.cu_sel = torch.empty(self.R + 1, dtype=torch.int32, device=dev)
+        # two selection slots: the selection of the next step is computed (and its
+        # cu_sel copied to pinned host memory) while the current step runs
+        self._mask = [torch.empty(self.N, dtype=torch.uint8, device=dev) for _ in range(2)]
+        self._idx = [torch.empty(self.N, dtype=torch.int32, device=dev) for _ in range(2)]
+        self._cu = [torch.empty(self.R + 1, dtype=torch.int32, device=dev) for _ in range(2)]
+        self._cu_pinned = [torch.empty(self.R + 1, dtype=torch.int32, pin_memory=True) for _ in range(2)]
+        self._cu_ready = [torch.cuda.Event() for _ in range(2)]
+        self._slot_key = [None, None]  # active-frame flags each slot was selected for
+        self.mask, self.idx, self.cu_sel = self._mask[0], self._idx[0], self._cu[0]
         self.max_sel = self.N if max_sel is None else int(max_sel)
         self.x_sel = torch.empty(16 * self.max_sel, dtype=torch.float32, device=dev)
         self.ws_sel = torch.empty(B.sphinx_select_workspace_bytes(self.N), dtype=torch.uint8, device=dev)
@@ -102,7 +108,7 @@ class Refiner:
         plans = [B.sphinx_plan_step(self.reqs, s_start, nsteps, i) for i in range(self.total_steps)]
         self.plan_host = {k: np.stack([p[k] for p in plans]) for k in plans[0]}
         self.plan = {k: torch.from_numpy(v).to(dev) for k, v in self.plan_host.items()}
-        self._active_key = None
+        self._pending = None  # (step index, slot) of a selection already enqueued
         self.n_sel = 0
         self.cu_host = None
 
@@ -110,24 +116,58 @@ class Refiner:
         """state <- fp32(z0) (a converting copy through scatter_blend with no tokens)."""
         B.sphinx_scatter_blend(self.reqs, None, None, 0, self.z0, self.dt, B.NCHW, self.z, B.F32, self.layout,
                                stream)
-        self._active_key = None
+        self._pending = None
+        self._slot_key = [None, None]
+
+    def _enqueue_select(self, k: int, slot: int, stream=None):
+        """Selection of schedule step k into `slot`; cu_sel reaches pinned host
+        memory asynchronously (no host synchronization)."""
+        B.sphinx_select_mask(self.reqs, self.u, self.thr, self.plan["active"][k], self._mask[slot], self._idx[slot],
+                             self._cu[slot], self.ws_sel, False, stream)
+        s = torch.cuda.current_stream() if stream is None else stream
+        with torch.cuda.stream(s):
+            self._cu_pinned[slot].copy_(self._cu[slot], non_blocking=True)
+            self._cu_ready[slot].record(s)
+        self._slot_key[slot] = self.plan_host["active"][k].copy()
 
     def select(self, k: int, stream=None) -> int:
-        self.cu_host = B.sphinx_select_mask(self.reqs, self.u, self.thr, self.plan["active"][k], self.mask,
-                                            self.idx, self.cu_sel, self.ws_sel, True, stream)
+        """Selection of schedule step k, waited for (it becomes the current one)."""
+        slot = 0 if self._pending is None else 1 - self._pending[1]
+        self._enqueue_select(k, slot, stream)
+        return self._use_slot(slot)
+
+    def _use_slot(self, slot: int) -> int:
+        self._cu_ready[slot].synchronize()
+        self.cu_host = self._cu_pinned[slot].numpy().copy()
         self.n_sel = int(self.cu_host[-1])
         if self.n_sel > self.max_sel:
             raise RuntimeError(f"{self.n_sel} selected tokens exceed the buffers sized for {self.max_sel}")
-        self._active_key = self.plan_host["active"][k].copy()
+        self.mask, self.idx, self.cu_sel = self._mask[slot], self._idx[slot], self._cu[slot]
+        self._cur_slot = slot
         return self.n_sel
 
     def step(self, i: int, force_select: bool = False, stream=None) -> int:
-        """One partial-denoising step (schedule index i modulo the schedule length)."""
+        """One partial-denoising step (schedule index i modulo the schedule length).
+
+        The selection (mask and compaction) runs whenever the set of active
+        frames changes, or every step with force_select.  The selection of step
+        i+1 is enqueued before this step's work, so its cu_sel read-back never
+        stalls the stream."""
         k = i % self.total_steps
-        if force_select or self._active_key is None or not np.array_equal(self.plan_host["active"][k],
-                                                                          self._active_key):
-            self.select(k, stream)
-        n = self.n_sel
+        if self._pending is not None and self._pending[0] == i:
+            slot = self._pending[1]
+        else:
+            slot = 0 if self._pending is None else 1 - self._pending[1]
+            self._enqueue_select(k, slot, stream)
+        # selection of the next step: a fresh one when asked or when the active
+        # frames change, otherwise the current one is reused
+        k1 = (i + 1) % self.total_steps
+        if force_select or not np.array_equal(self.plan_host["active"][k1], self._slot_key[slot]):
+            self._enqueue_select(k1, 1 - slot, stream)
+            self._pending = (i + 1, 1 - slot)
+        else:
+            self._pending = (i + 1, slot)
+        n = self._use_slot(slot)
         if n == 0:
             return 0
         P = self.plan

@@ -160,3 +160,13 @@ def test_plan_matches_oracle(L, name):
         for k in ("a", "b", "c1", "c2"):
             ref = getattr(p, k).astype(np.float32)
             assert np.array_equal(q[k], ref) or np.abs(q[k] - ref).max() <= 2 * np.spacing(np.abs(ref)).max(), (i, k)
+
+
+def test_timing_mask_validation(L):
+    assert L.sphinx_timing_enable(-1) == INVALID
+    assert L.sphinx_timing_enable(1 << len(S.KERNEL_CLASSES)) == INVALID
+    assert L.sphinx_timing_enable((1 << len(S.KERNEL_CLASSES)) - 1) == OK
+    assert L.sphinx_timing_enable(0) == OK
+    n, ms = ctypes.c_int64(), ctypes.c_double()
+    assert L.sphinx_timing_read(len(S.KERNEL_CLASSES), ctypes.byref(n), ctypes.byref(ms)) == INVALID
+    assert L.sphinx_timing_read(0, ctypes.byref(n), ctypes.byref(ms)) == OK and n.value == 0
