@@ -397,8 +397,6 @@ constexpr int kTileBytes = AK * 64 * 2;  // 8 KB
 
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
-typedef __attribute__((address_space(3))) void lds_void;
-
 constexpr int kRing = 3;  // tiles in flight per operand
 
 struct Smem {
@@ -568,14 +566,12 @@ __device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16
   auto copy_k = [&](int kbase, int buf) {
 #pragma unroll
     for (int n = 0; n < 2; ++n)
-      __builtin_amdgcn_global_load_lds(Kg + min(koff[n] + kbase * ld, klast[n]),
-                                       (dma::lds_void*)(sm.k[buf] + (2 * wave + n) * 1024), 16, 0, 0);
+      lds_dma16(Kg + min(koff[n] + kbase * ld, klast[n]), sm.k[buf] + (2 * wave + n) * 1024);
   };
   auto copy_v = [&](int kbase, int buf) {
 #pragma unroll
     for (int n = 0; n < 2; ++n)
-      __builtin_amdgcn_global_load_lds(Vg + min(voff[n] + kbase * ld, vlast[n]),
-                                       (dma::lds_void*)(sm.v[buf] + (2 * wave + n) * 1024), 16, 0, 0);
+      lds_dma16(Vg + min(voff[n] + kbase * ld, vlast[n]), sm.v[buf] + (2 * wave + n) * 1024);
   };
   // Barrier after this wave's LDS operations and all but its newest `keep`
   // copies (the copies issued in the current iteration stay in flight); no

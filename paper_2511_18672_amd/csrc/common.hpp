@@ -72,6 +72,32 @@ __device__ __forceinline__ TokPos decode_token(const ReqTable& T, int64_t t) {
   return p;
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin by linear id (x fastest).
+// Returns the tile that linear workgroup b of `total` should compute so that
+// each XCD gets one contiguous range of tiles: XCD x receives q + (x < r)
+// workgroups (q = total / 8, r = total % 8), and its k-th workgroup (b = 8k + x)
+// takes tile start(x) + k.  A bijection on [0, total) whatever the hardware
+// does; with the round-robin dealing, tiles that share operand rows stay in
+// one XCD's L2.
+__device__ __forceinline__ int xcd_tile(int b, int total) {
+  const int x = b & 7, k = b >> 3, q = total >> 3, r = total & 7;
+  return x * q + min(x, r) + k;
+}
+
+// Direct global->LDS copy, 16 bytes per lane (global_load_lds_dwordx4): lane
+// i's 16 bytes land at lds_dst + 16 i, where lds_dst must be wave-uniform.
+// Issued through inline asm rather than the builtin: with the builtin in a
+// loop the compiler's wait-count analysis treats every later LDS read as
+// possibly aliasing a pending copy and waits for all LDS reads (lgkmcnt(0))
+// before their first use.  Callers order the copies themselves: each wave
+// waits for its copies (s_waitcnt vmcnt) before the barrier that publishes
+// them.  The compiler's own vmcnt waits stay correct, since copies it does
+// not see only make them stricter.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, const void* lds_dst) {
+  const uint32_t m0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds_dst;
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gsrc), "s"(m0) : "memory", "m0");
+}
+
 __device__ __forceinline__ float bf2f(bf16 v) { return (float)v; }
 __device__ __forceinline__ bf16 f2bf(float v) { return (bf16)v; }  // round to nearest even
 

@@ -213,7 +213,6 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
 //  * The accumulation order per output (k-steps of 16 in ascending k, then the
 //    same epilogue) equals k_gemm_bf16's, so the results are bit-identical.
 namespace dma {
-typedef __attribute__((address_space(3))) void lds_void;
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
 // bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
@@ -238,7 +237,22 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int g = lane >> 5, r32 = lane & 31;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // One-dimensional grid; workgroups are dealt to the 8 XCDs round-robin.
+  // Wide N (more than 8 column tiles): tiles in plain N-fastest order, so XCD
+  // x always gets the column tiles n = x (mod 8) and keeps that eighth of W in
+  // its L2 for the whole kernel.  Narrow N: renumbered (xcd_tile) so that each
+  // XCD takes consecutive row blocks of A with all their column tiles, and A is
+  // fetched into one L2 instead of eight.
+  const int nt = N / BN;
+  int m0, n0;
+  if (nt > 8) {
+    m0 = ((int)blockIdx.x / nt) * BM;
+    n0 = ((int)blockIdx.x % nt) * BN;
+  } else {
+    const int tile = xcd_tile((int)blockIdx.x, (int)gridDim.x);
+    m0 = (tile / nt) * BM;
+    n0 = (tile % nt) * BN;
+  }
 
   // copy sources: instruction i of this wave fills rows 8q .. 8q+7 of the
   // stage (q = wave * COPIES + i; rows < BM are A rows, the rest W rows)
@@ -261,8 +275,7 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     unsigned char* base = smem + slot * C::STAGE;
 #pragma unroll
     for (int i = 0; i < C::COPIES; ++i)
-      __builtin_amdgcn_global_load_lds(src[i] + soff[i] + kt * C::BK,
-                                       (lds_void*)(base + (wave * C::COPIES + i) * 1024), 16, 0, 0);
+      lds_dma16(src[i] + soff[i] + kt * C::BK, base + (wave * C::COPIES + i) * 1024);
   };
   // fragment offsets inside a stage (k-step ks of 16)
   int foff[4];
@@ -463,9 +476,10 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
     const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
     const int64_t lim = (int64_t)1 << 31;  // the copy kernel uses 32-bit element offsets
     if ((int64_t)M * K < lim && (int64_t)N * K < lim) {
-      if (epi == EPI_BIAS) dma::k_gemm_dma_bias<<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
-      else if (epi == EPI_GELU) dma::k_gemm_dma_gelu<<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
-      else dma::k_gemm_dma_gated<<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
+      const int tiles = (int)(grid.x * grid.y);
+      if (epi == EPI_BIAS) dma::k_gemm_dma_bias<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+      else if (epi == EPI_GELU) dma::k_gemm_dma_gelu<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+      else dma::k_gemm_dma_gated<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
     } else if (epi == EPI_BIAS) {
       k_gemm_bf16<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
     } else if (epi == EPI_GELU) {
