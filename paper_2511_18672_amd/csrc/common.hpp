@@ -125,9 +125,15 @@ __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & (kWave - 1
 
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
+// GELU, tanh form: 0.5 z (1 + tanh(u)), u = sqrt(2/pi) (z + 0.044715 z^3).
+// Since 1 + tanh(u) = 2 / (1 + e^(-2u)), this is z / (1 + 2^(-2u log2 e)): one
+// hardware exp2 and one reciprocal (each within about an ulp of fp32), which
+// keeps the MLP epilogue cheap next to its MFMAs.  Large negative z gives
+// z / inf = -0, large positive z gives z.
 __device__ __forceinline__ float gelu_tanh(float z) {
-  const float k0 = 0.7978845608028654f, k1 = 0.044715f;
-  return 0.5f * z * (1.0f + tanhf(k0 * (z + k1 * z * z * z)));
+  const float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float u = z * fmaf(0.044715f * z, z, 1.0f);                     // z + 0.044715 z^3
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(c * u));
 }
 
 }  // namespace sphinx
