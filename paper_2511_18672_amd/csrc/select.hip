@@ -13,7 +13,8 @@
 //      of per-thread counts, stages their indices in LDS and stores them
 //      contiguously; it also writes cu_sel at request starts.
 // Thread order is token order, so idx comes out ascending without a sort and
-// the result is deterministic.
+// the result is deterministic.  (Non-temporal loads and stores measured slower
+// here than ordinary ones, unlike in gather/scatter.)
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -22,6 +23,7 @@ namespace {
 constexpr int kTPB = 256;
 constexpr int kPer = 16;              // consecutive tokens per thread
 constexpr int kChunk = kTPB * kPer;   // 4096 tokens per workgroup
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Global frame of token t and the first token of the next frame.
 __device__ __forceinline__ void frame_of(const ReqTable& T, int64_t t, int& g, int64_t& next) {
@@ -54,11 +56,11 @@ __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, co
     if (full) {
 #pragma unroll
       for (int q = 0; q < kPer / 4; ++q) {
-        const float4 f = reinterpret_cast<const float4*>(u + t0)[q];
-        v[4 * q] = f.x;
-        v[4 * q + 1] = f.y;
-        v[4 * q + 2] = f.z;
-        v[4 * q + 3] = f.w;
+        const f32x4 f = reinterpret_cast<const f32x4*>(u + t0)[q];
+        v[4 * q] = f[0];
+        v[4 * q + 1] = f[1];
+        v[4 * q + 2] = f[2];
+        v[4 * q + 3] = f[3];
       }
     } else {
 #pragma unroll
@@ -86,7 +88,7 @@ __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, co
       }
     }
     if (full) {
-      *reinterpret_cast<uint4*>(mask + t0) = make_uint4(w[0], w[1], w[2], w[3]);
+      *reinterpret_cast<u32x4*>(mask + t0) = u32x4{w[0], w[1], w[2], w[3]};
     } else {
       for (int e = 0; e < kPer; ++e)
         if (t0 + e < N) mask[t0 + e] = (uint8_t)((w[e >> 2] >> (8 * (e & 3))) & 1u);
@@ -142,11 +144,11 @@ __global__ __launch_bounds__(kTPB) void k_select_write(ReqTable T, int64_t N, co
   const int wave = threadIdx.x / kWave;
   uint32_t w[kPer / 4] = {0u, 0u, 0u, 0u};
   if (t0 + kPer <= N) {
-    const uint4 m4 = *reinterpret_cast<const uint4*>(mask + t0);
-    w[0] = m4.x;
-    w[1] = m4.y;
-    w[2] = m4.z;
-    w[3] = m4.w;
+    const u32x4 m4 = *reinterpret_cast<const u32x4*>(mask + t0);
+    w[0] = m4[0];
+    w[1] = m4[1];
+    w[2] = m4[2];
+    w[3] = m4[3];
   } else {
     for (int e = 0; e < kPer; ++e)
       if (t0 + e < N) w[e >> 2] |= (uint32_t)(mask[t0 + e] & 1u) << (8 * (e & 3));
