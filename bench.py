@@ -40,10 +40,13 @@ def parse():
     ap.add_argument("--config", default="headline", choices=["headline", "small", "frame_region", "batched"])
     ap.add_argument("--rho", type=float, default=None, help="selected fraction (headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", default="step", choices=["step", "copy", "sweep"],
+    ap.add_argument("--mode", default="step", choices=["step", "copy", "sweep", "peaks", "rho"],
                     help="step: the hot path; copy: a plain 1 GiB fp32 copy through scatter_blend (no tokens), "
                          "used to calibrate HBM byte counters and to measure achievable bandwidth; sweep: "
-                         "mask/compaction, gather and scatter at 2^20..2^26 tokens against the HBM roofline")
+                         "mask/compaction, gather and scatter at 2^20..2^26 tokens against the HBM roofline; "
+                         "peaks: achievable dense bf16 MFMA rate and copy bandwidth; rho: step time of the "
+                         "headline workload over the selected fraction")
+    ap.add_argument("--rhos", default="0.05,0.1,0.2,0.3,0.5,0.75,1.0", help="selected fractions of --mode rho")
     ap.add_argument("--layout", default="tokens", choices=["tokens", "nchw"],
                     help="layout of the fp32 state of record and the noise")
     ap.add_argument("--sweep-log2", default="20,22,24,26", help="token counts of the sweep (log2)")
@@ -132,6 +135,68 @@ def copy_mode(args):
     print(json.dumps({"mode": "copy", "bytes_per_launch": nbytes, "launches": cnt, "avg_us": round(avg_s * 1e6, 2),
                       "GB/s": round(nbytes / avg_s / 1e9, 1), "frac_of_8TBs": round(nbytes / avg_s / 8e12, 4)}),
           flush=True)
+
+
+def peaks_mode(args):
+    """Achievable rates to read the roofline fractions against: a bf16 MFMA loop
+    (four independent 32x32x16 chains per wave, 2048 workgroups of 4 waves) and
+    the 1 GiB fp32 copy."""
+    import torch
+
+    import paper_2511_18672_amd as S
+
+    out = torch.empty(S.PEAK_BLOCKS, dtype=torch.float32, device="cuda")
+    iters = 4096
+    flop = float(S.PEAK_BLOCKS) * 4 * iters * 4 * 32768
+    stream = torch.cuda.current_stream()
+    for _ in range(3):
+        S.sphinx_peak_mfma(iters, out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        S.sphinx_peak_mfma(iters, out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    avg_s = e0.elapsed_time(e1) / args.steps / 1e3
+    tf = flop / avg_s / 1e12
+    assert bool(torch.isfinite(out).all())
+    print(json.dumps({"mode": "peaks", "mfma_bf16_tflops": round(tf, 1),
+                      "frac_of_2500": round(tf / PEAK_BF16_TFLOPS, 4), "flop_per_launch": flop,
+                      "avg_us": round(avg_s * 1e6, 1)}), flush=True)
+    copy_mode(args)
+
+
+def rho_mode(args):
+    """Step time of the headline workload as the selected fraction grows; the
+    same uncertainty map with its threshold moved (select runs every step)."""
+    import torch
+
+    import paper_2511_18672_amd as S
+    import workloads as W
+
+    base = None
+    for rho in [float(x) for x in args.rhos.split(",")]:
+        wl = W.headline(rho=rho)
+        R = S.from_workload(wl, layout=S.TOKENS if args.layout == "tokens" else S.NCHW)
+        R.reset()
+        for i in range(args.warmup):
+            R.step(i, force_select=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        refined = 0
+        for i in range(args.warmup, args.warmup + args.steps):
+            refined += R.step(i, force_select=True)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = 1e3 * wall / args.steps
+        if base is None:
+            base = (rho, ms)
+        print(json.dumps({"mode": "rho", "rho": rho, "selected_tokens": int(R.n_sel), "tokens": int(wl.N),
+                          "ms_per_step": round(ms, 4), "refined_tokens_steps_per_s": round(refined / wall, 1),
+                          "ms_per_selected_ktoken": round(ms / (R.n_sel / 1e3), 4)}), flush=True)
+        del R, wl
+        torch.cuda.empty_cache()
 
 
 def sweep_mode(args):
@@ -230,6 +295,10 @@ def main():
         return sweep_mode(args)
     if args.mode == "copy" and args.gpus == 1:
         return copy_mode(args)
+    if args.mode == "peaks" and args.gpus == 1:
+        return peaks_mode(args)
+    if args.mode == "rho" and args.gpus == 1:
+        return rho_mode(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               f"(the selective-refinement step is built and measured on a single MI355X)", file=sys.stderr)

@@ -228,6 +228,16 @@ typedef enum {
 sphinx_status sphinx_timing_enable(int32_t classes);
 sphinx_status sphinx_timing_read(sphinx_kernel_class k, int64_t* launches, double* total_ms);
 
+/* Calibration aid (outside the method): the achievable dense bf16 MFMA rate.
+ * Enqueues SPHINX_PEAK_BLOCKS workgroups of 4 waves; each wave runs `iters`
+ * rounds of four independent v_mfma_f32_32x32x16_bf16 chains (4 * 32768 FLOP
+ * per round) and writes one checksum float per workgroup to `out` (dev float
+ * [SPHINX_PEAK_BLOCKS], caller-owned).  FLOPs per call:
+ * SPHINX_PEAK_BLOCKS * 4 * iters * 4 * 32768; the caller times the call on
+ * `stream`.  iters must lie in [1, 2^24]. */
+#define SPHINX_PEAK_BLOCKS 2048
+sphinx_status sphinx_peak_mfma(int32_t iters, float* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -8,12 +8,13 @@ from .binding import (BF16, F32, KERNEL_CLASSES, NCHW, TOKENS, EXPORTED, SphinxE
                       refine_step, scatter_blend, select_mask, sphinx_gather, sphinx_model_blob_bytes,
                       sphinx_model_param, sphinx_plan_step, sphinx_refine_step, sphinx_refine_workspace_bytes,
                       sphinx_scatter_blend, sphinx_select_mask, sphinx_select_workspace_bytes,
-                      sphinx_status_string, sphinx_timing_enable, sphinx_timing_read)
+                      sphinx_status_string, sphinx_timing_enable, sphinx_timing_read, sphinx_peak_mfma,
+                      PEAK_BLOCKS)
 from .refiner import Refiner, from_workload, pack_weights
 
 __all__ = ["BF16", "F32", "KERNEL_CLASSES", "NCHW", "TOKENS", "EXPORTED", "SphinxError", "Refiner", "from_workload", "pack_weights", "lib",
            "make_requests", "model_desc", "sphinx_gather", "sphinx_model_blob_bytes", "sphinx_model_param",
            "sphinx_plan_step", "sphinx_refine_step", "sphinx_refine_workspace_bytes", "sphinx_scatter_blend",
            "sphinx_select_mask", "sphinx_select_workspace_bytes", "sphinx_status_string", "sphinx_timing_enable",
-           "sphinx_timing_read", "select_mask",
+           "sphinx_timing_read", "sphinx_peak_mfma", "PEAK_BLOCKS", "select_mask",
            "gather", "refine_step", "scatter_blend", "plan_step"]

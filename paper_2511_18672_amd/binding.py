@@ -26,7 +26,9 @@ PARAMS = ["PE_W", "PE_B", "T1_W", "T1_B", "T2_W", "T2_B", "COND_W", "COND_B", "Q
 PARAM_ID = {n: i for i, n in enumerate(PARAMS)}
 EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_param", "sphinx_plan_step",
             "sphinx_select_workspace_bytes", "sphinx_select_mask", "sphinx_gather", "sphinx_refine_workspace_bytes",
-            "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read"]
+            "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
+            "sphinx_peak_mfma"]
+PEAK_BLOCKS = 2048
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
                   "gemm_mlp2", "final", "scatter"]
 
@@ -77,6 +79,7 @@ def lib() -> ctypes.CDLL:
                                            c_int32, P]),
         "sphinx_timing_enable": (c_int32, [c_int32]),
         "sphinx_timing_read": (c_int32, [c_int32, POINTER(c_int64), POINTER(ctypes.c_double)]),
+        "sphinx_peak_mfma": (c_int32, [c_int32, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -229,6 +232,11 @@ def sphinx_timing_read() -> Dict[str, tuple]:
         _check("sphinx_timing_read", lib().sphinx_timing_read(i, ctypes.byref(n), ctypes.byref(ms)))
         out[name] = (n.value, ms.value)
     return out
+
+
+def sphinx_peak_mfma(iters: int, out, stream=None):
+    """MFMA calibration loop (outside the method): SPHINX_PEAK_BLOCKS * 4 * iters * 4 * 32768 FLOP."""
+    _check("sphinx_peak_mfma", lib().sphinx_peak_mfma(iters, _ptr(out), _stream(stream)))
 
 
 select_mask = sphinx_select_mask

@@ -576,4 +576,9 @@ sphinx_status sphinx_timing_read(sphinx_kernel_class k, int64_t* launches, doubl
   return SPHINX_OK;
 }
 
+sphinx_status sphinx_peak_mfma(int32_t iters, float* out, void* stream) {
+  if (iters < 1 || iters > (1 << 24) || out == nullptr || !aligned(out, 16)) return SPHINX_E_INVALID;
+  return hip_status(launch_peak_mfma(iters, out, SPHINX_PEAK_BLOCKS, (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -467,6 +467,27 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, c
     }
   }
 }
+// Calibration loop: four independent 32x32x16 bf16 MFMA chains per wave.
+__global__ __launch_bounds__(256) void k_peak_mfma(int iters, float* __restrict__ out) {
+  bf16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (bf16)(1e-3f * (float)((threadIdx.x + i) & 15));
+    b[i] = (bf16)(1e-3f * (float)(i + 1));
+  }
+  f32x16 c0 = f32x16{}, c1 = f32x16{}, c2 = f32x16{}, c3 = f32x16{};
+  for (int it = 0; it < iters; ++it) {
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+  }
+  float sum = 0.0f;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) sum += c0[r] + c1[r] + c2[r] + c3[r];
+  sum = wave_sum(sum);
+  if (threadIdx.x == 0) out[blockIdx.x] = sum;
+}
 }  // namespace
 
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
@@ -494,6 +515,11 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
     else if (epi == EPI_GELU) k_gemm_f32<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
     else k_gemm_f32<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_peak_mfma(int iters, float* out, int blocks, hipStream_t s) {
+  k_peak_mfma<<<blocks, 256, 0, s>>>(iters, out);
   return hipGetLastError();
 }
 

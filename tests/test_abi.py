@@ -170,3 +170,14 @@ def test_timing_mask_validation(L):
     n, ms = ctypes.c_int64(), ctypes.c_double()
     assert L.sphinx_timing_read(len(S.KERNEL_CLASSES), ctypes.byref(n), ctypes.byref(ms)) == INVALID
     assert L.sphinx_timing_read(0, ctypes.byref(n), ctypes.byref(ms)) == OK and n.value == 0
+
+
+def test_peak_probe_validation(L):
+    """The MFMA calibration loop rejects an iteration count outside [1, 2^24]
+    and a missing or misaligned output before it touches a device."""
+    buf = (ctypes.c_float * 8)()
+    p = ctypes.addressof(buf)
+    assert L.sphinx_peak_mfma(0, ctypes.c_void_p(p), None) == INVALID
+    assert L.sphinx_peak_mfma((1 << 24) + 1, ctypes.c_void_p(p), None) == INVALID
+    assert L.sphinx_peak_mfma(16, None, None) == INVALID
+    assert L.sphinx_peak_mfma(16, ctypes.c_void_p(p + 4), None) == INVALID
