@@ -17,6 +17,12 @@ against the paper (Sphinx, arXiv 2511.18672):
 * Sec. 5.3 (spatially selective refinement): only positions inside the binary
   mask are forwarded to the diffusion model; confident regions bypass the
   partial denoising entirely and keep their values.
+* Sec. 5.2 (temporally consistent partial denoising) and Alg. 1's full_step /
+  store_temporal: with a cache period T, every T-th step forwards every token
+  and the keys and values of every block are cached; the steps in between
+  forward the masked tokens only and attend to the rest through the cache.
+  Tokens forwarded only as context enter as their clean latents noised to the
+  step's level (Alg. 1 resamples inactive content from the clean latents).
 * Sec. 3 (hybrid proposal): the regression output, with controlled noise
   injected, replaces Gaussian-noise initialisation and partial denoising
   removes the added noise.
@@ -135,9 +141,13 @@ class StepPlan:
     b: np.ndarray
     c1: np.ndarray
     c2: np.ndarray
+    full: Optional[np.ndarray] = None  # bool [R]: the request takes a full step (latent cache only)
+    a_ctx: Optional[np.ndarray] = None  # float64 [G]: add_noise(z0, tau_i) coefficients of context tokens
+    b_ctx: Optional[np.ndarray] = None
 
 
-def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Sequence[int]) -> List[StepPlan]:
+def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Sequence[int],
+               period: int = 0) -> List[StepPlan]:
     """Per-step, per-frame schedule (Alg. 1 loop with a per-frame start step).
 
     Each request walks its own grid from s_max = max of its frames' start
@@ -145,14 +155,25 @@ def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Seque
     own start); on its first active step it is newly active and receives
     add_noise at level tau_i.  A request takes part in global step i iff
     i < nsteps[r].
+
+    With a cache period T = ``period`` > 0 (Alg. 1: a full step when the step
+    counter is a multiple of T), a live request takes a full step at every i
+    with i mod T = 0, counted from its first step so that the first step
+    always fills the cache.  Every frame of a live request gets the context
+    coefficients (a_ctx, b_ctx) = (sqrt(abar(tau_i)), sqrt(1 - abar(tau_i))):
+    a token forwarded only as context enters as add_noise of its clean latent
+    at the step's level (Alg. 1 resamples inactive content from the clean
+    latents).
     """
     ab = alpha_bar()
     G = int(sum(frames_per_req))
     total = int(max(nsteps))
     out = []
+    R = len(frames_per_req)
     for i in range(total):
         p = StepPlan(np.zeros(G, bool), np.zeros(G, bool), np.full(G, -1, np.int64),
-                     np.ones(G), np.zeros(G), np.ones(G), np.zeros(G))
+                     np.ones(G), np.zeros(G), np.ones(G), np.zeros(G),
+                     np.zeros(R, bool), np.ones(G), np.zeros(G))
         g0 = 0
         for r, F in enumerate(frames_per_req):
             n = int(nsteps[r])
@@ -161,9 +182,11 @@ def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Seque
                 grid = timestep_grid(int(max(s)), n)
                 t, tn = grid[i], grid[i + 1]
                 c1, c2 = ddim_coeffs(t, tn, ab)
+                p.full[r] = period > 0 and i % period == 0
                 for f in range(F):
                     g = g0 + f
                     p.tau[g] = t
+                    p.a_ctx[g], p.b_ctx[g] = injection_coeffs(t, ab)
                     if t <= s[f]:
                         p.active[g] = True
                         p.newly[g] = (i == 0) or (grid[i - 1] > s[f])
@@ -288,20 +311,24 @@ def position_embedding(f, y, x, D: int) -> np.ndarray:
     return spatial + np.concatenate([np.sin(af), np.cos(af)], axis=1)
 
 
-def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048):
+def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048, kv_seg: Optional[np.ndarray] = None):
     """Non-causal softmax(q k^T / sqrt(d)) v per head, each query attending to
-    the keys of its own segment only (segments = contiguous row ranges seg[r]..seg[r+1])."""
+    the keys of its own segment only (segments = contiguous row ranges seg[r]..seg[r+1]).
+
+    With kv_seg, the queries of segment r attend to the key/value rows
+    kv_seg[r]..kv_seg[r+1] instead (k and v then have their own row count)."""
     n, D = q.shape
     d = D // heads
     scale = 1.0 / np.sqrt(d)
     out = np.zeros((n, D))
     for r in range(len(seg) - 1):
         s0, s1 = int(seg[r]), int(seg[r + 1])
+        k0, k1 = (s0, s1) if kv_seg is None else (int(kv_seg[r]), int(kv_seg[r + 1]))
         if s1 <= s0:
             continue
         for h in range(heads):
             cols = slice(h * d, (h + 1) * d)
-            kh, vh = k[s0:s1, cols], v[s0:s1, cols]
+            kh, vh = k[k0:k1, cols], v[k0:k1, cols]
             for c0 in range(s0, s1, chunk):
                 c1 = min(s1, c0 + chunk)
                 s = (q[c0:c1, cols] @ kh.T) * scale
@@ -334,11 +361,19 @@ def conditioning(model: Model, tau: np.ndarray) -> np.ndarray:
 
 
 def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.ndarray,
-            precision: str = "model") -> np.ndarray:
+            precision: str = "model", cache: Optional[list] = None, rows: Optional[np.ndarray] = None,
+            kv_seg: Optional[np.ndarray] = None) -> np.ndarray:
     """Noise prediction eps_hat [n][16] for packed tokens x [n][16].
 
     Tokens carry their in-request frame f, grid position (y, xx) and their
     frame's timestep tau_tok; attention runs inside each segment.
+
+    With a latent cache (Sec. 5.2), ``cache[l] = (K, V)`` holds block l's
+    keys and values of every token of the batch (global token order).  Each
+    block first stores the keys and values of the forwarded tokens at their
+    global positions ``rows``, then the queries of segment r attend to cache
+    rows kv_seg[r]..kv_seg[r+1] (all tokens of request r): fresh values for the
+    forwarded tokens, the stored ones for the rest.
     """
     w = model.weights
     D, H = model.D, model.heads
@@ -353,7 +388,12 @@ def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.
         a = rnd(layer_norm(h) * (1.0 + sc1) + sh1)
         qkv = linear(a, w[f"b{l}.qkv_w"], w[f"b{l}.qkv_b"])
         q, k, v = rnd(qkv[:, :D]), rnd(qkv[:, D:2 * D]), rnd(qkv[:, 2 * D:])
-        o = rnd(attention(q, k, v, H, seg))
+        if cache is None:
+            o = rnd(attention(q, k, v, H, seg))
+        else:
+            cache[l][0][rows] = k
+            cache[l][1][rows] = v
+            o = rnd(attention(q, cache[l][0], cache[l][1], H, seg, kv_seg=kv_seg))
         h = h + (1.0 + g1) * linear(o, w[f"b{l}.o_w"], w[f"b{l}.o_b"])
         a2 = rnd(layer_norm(h) * (1.0 + sc2) + sh2)
         m = rnd(gelu_tanh(linear(a2, w[f"b{l}.fc1_w"], w[f"b{l}.fc1_b"])))
@@ -376,6 +416,8 @@ class StepResult:
     eps_hat: np.ndarray
     x_out: np.ndarray  # after the DDIM update
     state: np.ndarray  # NCHW state after scatter
+    qidx: Optional[np.ndarray] = None  # forwarded tokens (latent cache: selected plus context)
+    cu_q: Optional[np.ndarray] = None  # forwarded tokens before each request start
 
 
 def per_token(values_per_frame: np.ndarray, info: TokenInfo) -> np.ndarray:
@@ -405,16 +447,71 @@ def step(wl, model: Model, state: np.ndarray, plan: StepPlan, precision: str = "
     return StepResult(mask, idx, cu, n, x, eps_hat, x_out, unpatchify(P, wl.requests))
 
 
-def refine(wl, precision: str = "model", denoiser=None, trace: bool = False, steps: Optional[int] = None):
+def step_cached(wl, model: Model, state: np.ndarray, plan: StepPlan, cache: list, precision: str = "model",
+                info: Optional[TokenInfo] = None) -> StepResult:
+    """One step of Alg. 1 with the latent cache (Sec. 5.2, Alg. 1 full_step /
+    store_temporal / partial_step with the cache).
+
+    The write set is the selection of ``step`` (mask within the active
+    frames).  A request taking a full step forwards every one of its tokens;
+    otherwise only the write set is forwarded.  Write-set tokens enter as in
+    ``step`` (the state, or add_noise on a frame's first active step); the
+    other forwarded tokens (context: unselected tokens and inactive frames)
+    enter as add_noise(z0, tau_i), their clean latent noised to the step's
+    level -- the state still holds z0 there, since only write-set tokens are
+    ever written.  The denoiser stores the keys and values of every forwarded
+    token in the cache and attends over the whole request through it, so a
+    partial step sees the context as it was at the last full step.  The DDIM
+    update is applied to the forwarded tokens and written back for the write
+    set only (unselected tokens keep their values, Sec. 5.3).
+    """
+    info = token_info(wl.requests) if info is None else info
+    tok_off = wl.tok_offset[:-1]
+    mask, idx, cu, n = select(wl.u, per_token(wl.thr, info), per_token(plan.active, info), tok_off)
+    forward = mask | plan.full[info.req]
+    qidx = np.flatnonzero(forward)
+    cu_q = np.array([np.count_nonzero(forward[:o]) for o in tok_off])
+    nq = int(qidx.size)
+    state = np.array(state, dtype=np.float64, copy=True)
+    if nq == 0:
+        z = np.zeros((0, TOKEN_DIM))
+        return StepResult(mask, idx, cu, n, z, z, z, state, qidx, cu_q)
+    P = patchify(state, wl.requests)
+    E = patchify(wl.eps, wl.requests)
+    g = info.gframe[qidx]
+    w = mask[qidx]
+    a = np.where(w, plan.a[g], plan.a_ctx[g])[:, None]
+    b = np.where(w, plan.b[g], plan.b_ctx[g])[:, None]
+    x = a * P[qidx] + b * E[qidx]
+    seg = np.concatenate([cu_q, [nq]])
+    eps_hat = denoise(model, x, info.f[qidx], info.y[qidx], info.x[qidx], plan.tau[g], seg, precision,
+                      cache=cache, rows=qidx, kv_seg=np.asarray(wl.tok_offset))
+    x_out = plan.c1[g][:, None] * x + plan.c2[g][:, None] * eps_hat
+    P[qidx[w]] = x_out[w]
+    return StepResult(mask, idx, cu, n, x, eps_hat, x_out, unpatchify(P, wl.requests), qidx, cu_q)
+
+
+def new_cache(model: Model, n_tokens: int) -> list:
+    """Per block, keys and values of every token (zeros until a full step writes them)."""
+    return [(np.zeros((n_tokens, model.D)), np.zeros((n_tokens, model.D))) for _ in range(model.L)]
+
+
+def refine(wl, precision: str = "model", denoiser=None, trace: bool = False, steps: Optional[int] = None,
+           period: int = 0):
     """Run the whole partial-denoising loop; returns the final NCHW state (float64)
-    and, with trace=True, the list of per-step results."""
+    and, with trace=True, the list of per-step results.  period > 0 turns on
+    the latent cache with a full step every ``period`` steps."""
     model = model_from_workload(wl)
-    plans = plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    plans = plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps, period)
     info = token_info(wl.requests)
     state = np.asarray(wl.z0, dtype=np.float64).copy()
+    cache = new_cache(model, wl.N) if period > 0 else None
     out = []
     for i, p in enumerate(plans[: steps if steps is not None else len(plans)]):
-        res = step(wl, model, state, p, precision, denoiser, info)
+        if cache is not None:
+            res = step_cached(wl, model, state, p, cache, precision, info)
+        else:
+            res = step(wl, model, state, p, precision, denoiser, info)
         state = res.state
         if trace:
             out.append(res)

@@ -422,8 +422,113 @@ def pin_packed_equals_separate(O):
         assert np.abs(sep - out[e0:e1]).max() < 1e-12, r
 
 
+# ----------------------------------------------------------------------------
+# latent cache (Sec. 5.2): full steps every T steps, partial steps through the cache
+# ----------------------------------------------------------------------------
+MICRO_F32_1BLOCK = W.ModelCfg(D=32, heads=2, head_dim=16, mlp=64, L=1, dtype="f32")
+
+
+def _abar_direct(t):
+    """alpha_bar(t) as the plain product of (1 - beta_i), beta linear 1e-4..2e-2 over 1000 steps."""
+    if t < 0:
+        return 1.0
+    i = np.arange(t + 1, dtype=np.float64)
+    return float(np.prod(1.0 - (1e-4 + (2e-2 - 1e-4) * i / 999.0)))
+
+
+def pin_cache_all_selected_dense(O):
+    """Every token selected: each step forwards (and re-stores) every token,
+    so the cache holds this step's keys and values and the loop equals dense
+    partial denoising whatever the period."""
+    wl = micro(model=MICRO_F32, requests=[W.Request(2, 8, 8), W.Request(1, 4, 8)], nsteps=[3, 2],
+               t_start=[0.5, 0.3])
+    wl.thr[:] = -np.inf
+    dense = O.refine_dense(wl, precision="fp64")
+    for period in (1, 2, 5):
+        got = O.refine(wl, precision="fp64", period=period)
+        assert np.abs(got - dense).max() < 1e-11, (period, np.abs(got - dense).max())
+
+
+def pin_cache_full_every_step(O):
+    """Period 1: every step is a full step.  Rebuilt here without a cache: all
+    tokens of the request go through the plain denoiser, selected ones from the
+    state (noised on the first step), the others as their clean latent noised
+    to the step's level, and only the selected tokens are written back."""
+    wl = micro(model=MICRO_F32, nsteps=[3], rho=[0.35])
+    got = O.refine(wl, precision="fp64", period=1)
+    model = O.model_from_workload(wl)
+    info = O.token_info(wl.requests)
+    s = int(wl.s_start[0])
+    n = int(wl.nsteps[0])
+    grid = [((n - i) * (s + 1)) // n - 1 for i in range(n + 1)]
+    Z0 = O.patchify(wl.z0, wl.requests)
+    E = O.patchify(wl.eps, wl.requests)
+    sel = np.asarray(wl.u) > np.repeat(wl.thr, wl.N // len(wl.thr))
+    P = Z0.astype(np.float64).copy()
+    for i in range(n):
+        t, tn = grid[i], grid[i + 1]
+        ab, abn = _abar_direct(t), _abar_direct(tn)
+        noised = math.sqrt(ab) * Z0 + math.sqrt(1 - ab) * E
+        x = np.where(sel[:, None], P if i > 0 else noised, noised)
+        eps_hat = O.denoise(model, x, info.f, info.y, info.x, np.full(wl.N, t), np.array([0, wl.N]), "fp64")
+        c1 = math.sqrt(abn / ab)
+        c2 = math.sqrt(1 - abn) - math.sqrt(abn * (1 - ab) / ab)
+        P[sel] = (c1 * x + c2 * eps_hat)[sel]
+    ref = O.unpatchify(P, wl.requests)
+    assert np.abs(got - ref).max() < 1e-11, np.abs(got - ref).max()
+    assert np.array_equal(O.patchify(got, wl.requests)[~sel], Z0[~sel].astype(np.float64))
+
+
+def pin_cache_partial_one_block(O):
+    """One block, period 2, two steps: step 0 is full, step 1 partial.  In a
+    one-block denoiser a token's key and value depend only on its own input and
+    timestep, so the partial step equals the plain denoiser over the selected
+    tokens at step 1 together with every other token as it entered step 0
+    (clean latent noised to tau_0, timestep tau_0)."""
+    wl = micro(model=MICRO_F32_1BLOCK, nsteps=[2], rho=[0.3])
+    got = O.refine(wl, precision="fp64", period=2)
+    model = O.model_from_workload(wl)
+    info = O.token_info(wl.requests)
+    s, n = int(wl.s_start[0]), 2
+    t0, t1, t2 = [((n - i) * (s + 1)) // n - 1 for i in range(n + 1)]
+    Z0 = O.patchify(wl.z0, wl.requests).astype(np.float64)
+    E = O.patchify(wl.eps, wl.requests)
+    sel = np.asarray(wl.u) > np.repeat(wl.thr, wl.N // len(wl.thr))
+    a0, a1, a2 = _abar_direct(t0), _abar_direct(t1), _abar_direct(t2)
+    ctx = math.sqrt(a0) * Z0 + math.sqrt(1 - a0) * E
+    # step 0 (full): every token at tau_0; the selected ones are updated
+    e0 = O.denoise(model, ctx, info.f, info.y, info.x, np.full(wl.N, t0), np.array([0, wl.N]), "fp64")
+    x1 = math.sqrt(a1 / a0) * ctx + (math.sqrt(1 - a1) - math.sqrt(a1 * (1 - a0) / a0)) * e0
+    # step 1 (partial): selected at tau_1 with their updated values, the rest frozen at step 0's input
+    x = np.where(sel[:, None], x1, ctx)
+    tau = np.where(sel, t1, t0)
+    e1 = O.denoise(model, x, info.f, info.y, info.x, tau, np.array([0, wl.N]), "fp64")
+    out = Z0.copy()
+    out[sel] = (math.sqrt(a2 / a1) * x + (math.sqrt(1 - a2) - math.sqrt(a2 * (1 - a1) / a1)) * e1)[sel]
+    ref = O.unpatchify(out, wl.requests)
+    assert np.abs(got - ref).max() < 1e-11, np.abs(got - ref).max()
+
+
+def pin_cache_context_matters(O):
+    """With the cache, unselected tokens reach the selected ones through
+    attention (without it they cannot): moving the clean latent of unselected
+    tokens moves the selected outputs, and only those."""
+    wl = micro(model=MICRO_F32, nsteps=[3])
+    base, tr = O.refine(wl, precision="fp64", trace=True, period=2)
+    sel = tr[0].mask
+    P = O.patchify(wl.z0, wl.requests)
+    P[~sel] += 1.0
+    wl.z0 = O.unpatchify(P, wl.requests).astype(np.float32)
+    moved = O.refine(wl, precision="fp64", period=2)
+    B, M = O.patchify(base, wl.requests), O.patchify(moved, wl.requests)
+    assert np.abs(B[sel] - M[sel]).max() > 1e-6
+    assert np.array_equal(M[~sel], P[~sel].astype(np.float32).astype(np.float64))
+
+
 ALL_PINS = [pin_alpha_bar_exact, pin_grid, pin_ddim_true_noise, pin_ddim_zero_noise, pin_alg1_active_counts,
             pin_patch_layout, pin_select_bruteforce, pin_select_threshold_count, pin_round_bf16,
             pin_layer_norm, pin_activations, pin_linear, pin_embeddings, pin_attention_bruteforce,
             pin_attention_sdpa, pin_attention_special, pin_denoiser_torch, pin_empty_mask_identity,
-            pin_all_selected_dense, pin_unselected_independence, pin_packed_equals_separate]
+            pin_all_selected_dense, pin_unselected_independence, pin_packed_equals_separate,
+            pin_cache_all_selected_dense, pin_cache_full_every_step, pin_cache_partial_one_block,
+            pin_cache_context_matters]

@@ -38,16 +38,19 @@ def _alpha_bar_off(*_):
     return np.cumprod(1.0 - (1e-4 + (2e-2 - 1e-4) * i / 1000))
 
 
-def _attention_no_scale(q, k, v, heads, seg, chunk=2048):
+def _attention_no_scale(q, k, v, heads, seg, chunk=2048, kv_seg=None):
     d = q.shape[1] // heads
-    return _orig["attention"](q * np.sqrt(d), k, v, heads, seg, chunk)
+    return _orig["attention"](q * np.sqrt(d), k, v, heads, seg, chunk, kv_seg)
 
 
-def _attention_no_segments(q, k, v, heads, seg, chunk=2048):
-    return _orig["attention"](q, k, v, heads, np.array([seg[0], seg[-1]]), chunk)
+def _attention_no_segments(q, k, v, heads, seg, chunk=2048, kv_seg=None):
+    kv = None if kv_seg is None else np.array([kv_seg[0], kv_seg[-1]])
+    return _orig["attention"](q, k, v, heads, np.array([seg[0], seg[-1]]), chunk, kv)
 
 
-def _attention_wrong_axis(q, k, v, heads, seg, chunk=2048):
+def _attention_wrong_axis(q, k, v, heads, seg, chunk=2048, kv_seg=None):
+    if kv_seg is not None:
+        raise NotImplementedError
     n, D = q.shape
     d = D // heads
     out = np.zeros((n, D))
@@ -107,7 +110,7 @@ def _pos_x_uses_y(f, y, x, D):
     return _orig["position_embedding"](f, y, y, D)
 
 
-def _denoise_raw_gate(model, x, f, y, xx, tau, seg, precision="model"):
+def _denoise_raw_gate(model, x, f, y, xx, tau, seg, precision="model", **kw):
     w = dict(model.weights)
     D = model.D
     for l in range(model.L):
@@ -116,11 +119,11 @@ def _denoise_raw_gate(model, x, f, y, xx, tau, seg, precision="model"):
         b[5 * D:6 * D] -= 1.0
         w[f"b{l}.ada_b"] = b
     m = O.Model(model.D, model.heads, model.mlp, model.L, model.dtype, w)
-    return _orig["denoise"](m, x, f, y, xx, tau, seg, precision)
+    return _orig["denoise"](m, x, f, y, xx, tau, seg, precision, **kw)
 
 
-def _plan_always_new(frames, s_start, nsteps):
-    plans = _orig["plan_steps"](frames, s_start, nsteps)
+def _plan_always_new(frames, s_start, nsteps, period=0):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
     ab = O.alpha_bar()
     for p in plans:
         for g in np.flatnonzero(p.active):
@@ -135,6 +138,62 @@ def _step_skips_update(wl, model, state, plan, precision="model", denoiser=None,
     P[res.idx] = res.x_in
     res.state = O.unpatchify(P, wl.requests)
     return res
+
+
+def _denoise_stale_entry(model, x, f, y, xx, tau, seg, precision="model", cache=None, rows=None, kv_seg=None):
+    """Attends over the cache as it was before the block stored the fresh rows."""
+    if cache is None:
+        return _orig["denoise"](model, x, f, y, xx, tau, seg, precision)
+    return _denoise_stale(model, x, f, y, xx, tau, seg, precision, cache, rows, kv_seg)
+
+
+def _denoise_stale(model, x, f, y, xx, tau, seg, precision, cache, rows, kv_seg):
+    before = [(k.copy(), v.copy()) for k, v in cache]
+    orig_attention = O.attention
+    calls = {"l": 0}
+
+    def attention_on_old(q, k, v, heads, seg_, chunk=2048, kv_seg=None):
+        l = calls["l"]
+        calls["l"] += 1
+        return orig_attention(q, before[l][0], before[l][1], heads, seg_, chunk, kv_seg)
+
+    O.attention = attention_on_old
+    try:
+        return _orig["denoise"](model, x, f, y, xx, tau, seg, precision, cache, rows, kv_seg)
+    finally:
+        O.attention = orig_attention
+
+
+def _plan_no_full_after_first(frames, s_start, nsteps, period=0):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+    for p in plans[1:]:
+        p.full[:] = False
+    return plans
+
+
+def _plan_context_unnoised(frames, s_start, nsteps, period=0):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+    for p in plans:
+        p.a_ctx[:] = 1.0
+        p.b_ctx[:] = 0.0
+    return plans
+
+
+def _step_cached_writes_context(wl, model, state, plan, cache, precision="model", info=None):
+    res = _orig["step_cached"](wl, model, state, plan, cache, precision, info)
+    if res.qidx.size:
+        P = O.patchify(res.state, wl.requests)
+        P[res.qidx] = res.x_out
+        res.state = O.unpatchify(P, wl.requests)
+    return res
+
+
+def _plan_full_at_odd_steps(frames, s_start, nsteps, period=0):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+    for i, p in enumerate(plans):
+        live = p.full | (p.tau[np.cumsum([0] + list(frames))[:-1]] >= 0)
+        p.full[:] = live & (period > 0) & ((i + 1) % max(period, 1) == 0)
+    return plans
 
 
 MUTANTS = {
@@ -159,6 +218,11 @@ MUTANTS = {
     "gate_without_one": ("denoise", _denoise_raw_gate),
     "reinject_every_step": ("plan_steps", _plan_always_new),
     "scatter_without_update": ("step", _step_skips_update),
+    "cache_read_before_store": ("denoise", _denoise_stale_entry),
+    "cache_never_refreshed": ("plan_steps", _plan_no_full_after_first),
+    "context_not_noised": ("plan_steps", _plan_context_unnoised),
+    "context_written_back": ("step_cached", _step_cached_writes_context),
+    "full_step_misplaced": ("plan_steps", _plan_full_at_odd_steps),
 }
 
 
