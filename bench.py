@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--layout", default="tokens", choices=["tokens", "nchw"],
                     help="layout of the fp32 state of record and the noise")
     ap.add_argument("--sweep-log2", default="20,22,24,26", help="token counts of the sweep (log2)")
+    ap.add_argument("--cache-period", type=int, default=0,
+                    help="latent cache with a full step every T steps (0: off, the default workload)")
     ap.add_argument("--select-every-step", type=int, default=1,
                     help="1: run mask+compaction in every step (default); 0: only when the active set changes")
     return ap.parse_args()
@@ -314,9 +316,12 @@ def main():
     else:
         wl = W.CONFIGS[args.config]()
     t_setup = time.perf_counter()
-    R = S.from_workload(wl, layout=S.TOKENS if args.layout == "tokens" else S.NCHW)
+    R = S.from_workload(wl, layout=S.TOKENS if args.layout == "tokens" else S.NCHW,
+                        cache_period=args.cache_period)
     R.reset()
     stream = torch.cuda.current_stream()
+    D, L, mlp = wl.model.D, wl.model.L, wl.model.mlp
+    req_tokens = np.diff(np.asarray(wl.tok_offset)).astype(np.float64)
     force = bool(args.select_every_step)
     for i in range(args.warmup):
         R.step(i, force_select=force)
@@ -328,8 +333,11 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     refined = 0
+    attn_flop_timed = 0.0  # latent cache: queries x all keys of the request, summed over the timed steps
     for i in range(args.warmup, args.warmup + args.steps):
         refined += R.step(i, force_select=force)
+        if args.cache_period > 0:
+            attn_flop_timed += 4.0 * D * float((np.diff(R.cu_fwd).astype(np.float64) * req_tokens).sum())
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     attn_timing = S.sphinx_timing_read()["attention"]
@@ -345,10 +353,11 @@ def main():
     ms_per_step = 1e3 * wall / args.steps
     value = refined / wall
     n = R.n_sel
-    D, L, mlp = wl.model.D, wl.model.L, wl.model.mlp
     cu = R.cu_host
     seg = np.diff(cu).astype(np.float64)
     attn_flop = 4.0 * D * float((seg ** 2).sum())
+    if args.cache_period > 0:  # launches differ between full and partial steps: average FLOPs per launch
+        attn_flop = attn_flop_timed * L / attn_timing[0]
     gemm_flop = {"gemm_qkv": 2.0 * n * D * 3 * D, "gemm_out": 2.0 * n * D * D, "gemm_mlp1": 2.0 * n * D * mlp,
                  "gemm_mlp2": 2.0 * n * mlp * D}
     kernels = {}
@@ -366,7 +375,7 @@ def main():
     avg_s = ms / cnt / 1e3
     achieved = attn_flop / avg_s / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_entry("attention", args.config),
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_entry("attention", args.config) if args.cache_period == 0 else None,
                 "kernel": "k_attn_bf16_dma (varlen flash attention, head_dim 64)",
                 "algorithmic_flop_per_launch": attn_flop}
     step_flop = L * (attn_flop + sum(gemm_flop.values()))
@@ -380,11 +389,13 @@ def main():
                                   f"D{D} H{wl.model.heads}x{wl.model.head_dim} L{L} MLP{mlp}, "
                                   f"{int(wl.max_steps)}-step DDIM schedule",
                       "selected_tokens": int(n), "tokens": int(wl.N), "select_every_step": force,
-                      "state_layout": args.layout},
+                      "state_layout": args.layout, "cache_period": args.cache_period},
            "mfma_util_step": round(mfma_util, 4),
            "roofline": roofline, "kernels": kernels,
            "kernels_note": f"per-class HIP-event averages from {n_breakdown} further untimed steps; "
-                           "only attention is bracketed inside the timed steps",
+                           "only attention is bracketed inside the timed steps"
+                           + ("; with the latent cache the GEMM rates assume the last step's write set and "
+                              "mix full and partial steps" if args.cache_period > 0 else ""),
            "setup_s": round(setup_s, 1)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)

@@ -199,6 +199,83 @@ sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const 
                                    int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, sphinx_layout in_layout,
                                    void* z_out, sphinx_dtype out_dtype, sphinx_layout out_layout, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Latent cache with periodic full steps (Sec. 5.2, temporally consistent
+ * partial denoising; Alg. 1 full_step every T steps with store_temporal, and
+ * partial_step that reads the cache).
+ *
+ * Every T-th step of a request (i mod T = 0, counting from its first step so
+ * that the first step fills the cache) is a full step: every token of the
+ * request is forwarded through the denoiser and every block's keys and values
+ * are stored in the cache.  In the steps between, only the selected tokens
+ * are forwarded; they store their fresh keys and values and attend over all
+ * tokens of their request through the cache, so unselected tokens and
+ * inactive frames take part as they were at the last full step.  The write
+ * set (tokens whose state is updated) is the selection of sphinx_select_mask
+ * in every step.  Tokens forwarded only as context enter as their clean
+ * latent noised to the step's level, add_noise(z0, tau_i) (Alg. 1 resamples
+ * inactive content from the clean latents); the state holds z0 there because
+ * only write-set tokens are ever written.  The cache rows of a token hold the
+ * keys and values last computed for it; when the selection only grows from
+ * step to step (fixed thresholds, a growing active set) this equals "the last
+ * full step" for every token not selected now.
+ *
+ * A step with the cache: sphinx_plan_step + sphinx_plan_cache (host);
+ * sphinx_select_mask for the write set and, on a full step, a second
+ * sphinx_select_mask with thr = -inf and active = forward_all for the
+ * forwarded set; sphinx_gather_ctx; sphinx_refine_step_cached;
+ * sphinx_scatter_masked.
+ * ------------------------------------------------------------------------ */
+
+/* Cache plan of step `step` for period T = `period` >= 1 (pure host code).
+ * full: host uint8 [R], 1 iff request r is live at this step (step <
+ * nsteps[r]) and step mod T = 0.  forward_all: host uint8 [G], full[r] of the
+ * frame's request.  a_ctx, b_ctx: host float [G], the context coefficients
+ * sqrt(abar(tau_i)), sqrt(1 - abar(tau_i)) of the request's current timestep
+ * (1, 0 for a finished request), in double precision rounded to float.
+ * s_start and nsteps as for sphinx_plan_step. */
+sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int32_t* s_start,
+                                const int32_t* nsteps, int32_t step, int32_t period, uint8_t* full,
+                                uint8_t* forward_all, float* a_ctx, float* b_ctx);
+
+/* Bytes of the latent cache: L blocks x N tokens x (key, value) x D elements
+ * of the model dtype, laid out [L][N][2][D] (token t of block l at element
+ * (l*N + t)*2D, its key first).  The caller owns and allocates it; rows that
+ * no call has stored are read as whatever they hold. */
+sphinx_status sphinx_kv_cache_bytes(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                    size_t* bytes);
+
+/* Gather of the forwarded tokens (Alg. 1 add_noise; context tokens resampled
+ * from the clean latents).  As sphinx_gather over idx[0..n), except that a
+ * token t with wmask[t] == 0 (not in the write set) uses a_ctx[g], b_ctx[g]
+ * instead of a[g], b[g].  wmask: dev uint8 [N] (the write-set mask of
+ * sphinx_select_mask); a, b, a_ctx, b_ctx: dev float [G]. */
+sphinx_status sphinx_gather_ctx(const sphinx_request* reqs, int32_t R, sphinx_layout layout, const void* state,
+                                sphinx_dtype state_dtype, const void* eps, sphinx_dtype eps_dtype, const int32_t* idx,
+                                int32_t n, const uint8_t* wmask, const float* a, const float* b, const float* a_ctx,
+                                const float* b_ctx, float* x, void* stream);
+
+/* sphinx_refine_step with the latent cache.  Rows x[0..n) are the forwarded
+ * tokens idx[0..n) (ascending within each request), segment r being rows
+ * [cu_host[r], cu_host[r+1]).  In every block the keys and values of the
+ * forwarded rows are first stored at their token rows of the block's cache
+ * slice, then each row attends over cache rows [tok_offset_r, tok_offset_r +
+ * tokens_r) of its request.  kv_cache: dev, sphinx_kv_cache_bytes bytes,
+ * 16-byte aligned, read and written.  Other arguments, workspace and errors as
+ * sphinx_refine_step (n up to N; size the workspace for the largest n). */
+sphinx_status sphinx_refine_step_cached(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                        const int32_t* idx, int32_t n, const int32_t* cu_host, const int32_t* tau,
+                                        const float* c1, const float* c2, float* x, void* kv_cache, void* ws,
+                                        size_t ws_bytes, void* stream);
+
+/* In-place scatter of the write set only (Sec. 5.3: unselected tokens keep
+ * their values): z token idx[j] <- x[j] for every j < n with wmask[idx[j]] =
+ * 1; forwarded context rows are dropped.  z: dev latents in `layout`/`dtype`
+ * (bf16 rounds to nearest even); wmask: dev uint8 [N]. */
+sphinx_status sphinx_scatter_masked(const sphinx_request* reqs, int32_t R, const float* x, const int32_t* idx,
+                                    int32_t n, const uint8_t* wmask, void* z, sphinx_dtype dtype,
+                                    sphinx_layout layout, void* stream);
+
 /* Profiling aid (outside the method).  sphinx_timing_enable(classes) takes a
  * bit mask of kernel classes (bit k = class k; 0 turns timing off; bits at or
  * above SPHINX_K_COUNT are SPHINX_E_INVALID).  While a class is enabled, every
@@ -222,6 +299,7 @@ typedef enum {
   SPHINX_K_GEMM_MLP2,
   SPHINX_K_FINAL,      /* final LayerNorm + projection + DDIM update */
   SPHINX_K_SCATTER,
+  SPHINX_K_KV_STORE,   /* latent cache store of the forwarded rows' keys and values */
   SPHINX_K_COUNT
 } sphinx_kernel_class;
 

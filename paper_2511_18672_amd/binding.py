@@ -27,10 +27,11 @@ PARAM_ID = {n: i for i, n in enumerate(PARAMS)}
 EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_param", "sphinx_plan_step",
             "sphinx_select_workspace_bytes", "sphinx_select_mask", "sphinx_gather", "sphinx_refine_workspace_bytes",
             "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
-            "sphinx_peak_mfma"]
+            "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_kv_cache_bytes", "sphinx_gather_ctx",
+            "sphinx_refine_step_cached", "sphinx_scatter_masked"]
 PEAK_BLOCKS = 2048
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
-                  "gemm_mlp2", "final", "scatter"]
+                  "gemm_mlp2", "final", "scatter", "kv_store"]
 
 
 class SphinxError(RuntimeError):
@@ -80,6 +81,13 @@ def lib() -> ctypes.CDLL:
         "sphinx_timing_enable": (c_int32, [c_int32]),
         "sphinx_timing_read": (c_int32, [c_int32, POINTER(c_int64), POINTER(ctypes.c_double)]),
         "sphinx_peak_mfma": (c_int32, [c_int32, P, P]),
+        "sphinx_plan_cache": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, c_int32, P, P, P, P]),
+        "sphinx_kv_cache_bytes": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, POINTER(c_size_t)]),
+        "sphinx_gather_ctx": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P,
+                                        P, P, P, P, P]),
+        "sphinx_refine_step_cached": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, P, c_int32, P, P, P,
+                                                P, P, P, P, c_size_t, P]),
+        "sphinx_scatter_masked": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, P, c_int32, c_int32, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -237,6 +245,45 @@ def sphinx_timing_read() -> Dict[str, tuple]:
 def sphinx_peak_mfma(iters: int, out, stream=None):
     """MFMA calibration loop (outside the method): SPHINX_PEAK_BLOCKS * 4 * iters * 4 * 32768 FLOP."""
     _check("sphinx_peak_mfma", lib().sphinx_peak_mfma(iters, _ptr(out), _stream(stream)))
+
+
+def sphinx_plan_cache(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int, period: int) -> Dict[str, np.ndarray]:
+    G = sum(r.frames for r in reqs)
+    s_start = np.ascontiguousarray(s_start, dtype=np.int32)
+    nsteps = np.ascontiguousarray(nsteps, dtype=np.int32)
+    out = {"full": np.zeros(len(reqs), np.uint8), "forward_all": np.zeros(G, np.uint8),
+           "a_ctx": np.zeros(G, np.float32), "b_ctx": np.zeros(G, np.float32)}
+    _check("sphinx_plan_cache", lib().sphinx_plan_cache(
+        reqs, len(reqs), _ptr(s_start), _ptr(nsteps), step, period, _ptr(out["full"]), _ptr(out["forward_all"]),
+        _ptr(out["a_ctx"]), _ptr(out["b_ctx"])))
+    return out
+
+
+def sphinx_kv_cache_bytes(desc: ModelDesc, reqs) -> int:
+    out = c_size_t()
+    _check("sphinx_kv_cache_bytes", lib().sphinx_kv_cache_bytes(ctypes.byref(desc), reqs, len(reqs),
+                                                                ctypes.byref(out)))
+    return out.value
+
+
+def sphinx_gather_ctx(reqs, layout: int, state, state_dtype: int, eps, eps_dtype: int, idx, n: int, wmask, a, b,
+                      a_ctx, b_ctx, x, stream=None):
+    _check("sphinx_gather_ctx", lib().sphinx_gather_ctx(
+        reqs, len(reqs), layout, _ptr(state), state_dtype, _ptr(eps), eps_dtype, _ptr(idx), n, _ptr(wmask), _ptr(a),
+        _ptr(b), _ptr(a_ctx), _ptr(b_ctx), _ptr(x), _stream(stream)))
+
+
+def sphinx_refine_step_cached(desc: ModelDesc, reqs, idx, n: int, cu_host: np.ndarray, tau, c1, c2, x, kv_cache, ws,
+                              stream=None):
+    cu = np.ascontiguousarray(cu_host, dtype=np.int32)
+    _check("sphinx_refine_step_cached", lib().sphinx_refine_step_cached(
+        ctypes.byref(desc), reqs, len(reqs), _ptr(idx), n, _ptr(cu), _ptr(tau), _ptr(c1), _ptr(c2), _ptr(x),
+        _ptr(kv_cache), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def sphinx_scatter_masked(reqs, x, idx, n: int, wmask, z, dtype: int, layout: int, stream=None):
+    _check("sphinx_scatter_masked", lib().sphinx_scatter_masked(
+        reqs, len(reqs), _ptr(x), _ptr(idx), n, _ptr(wmask), _ptr(z), dtype, layout, _stream(stream)))
 
 
 select_mask = sphinx_select_mask

@@ -334,6 +334,38 @@ sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int3
   return SPHINX_OK;
 }
 
+sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int32_t* s_start, const int32_t* nsteps,
+                                int32_t step, int32_t period, uint8_t* full, uint8_t* forward_all, float* a_ctx,
+                                float* b_ctx) {
+  ReqTable T;
+  int64_t N;
+  int32_t G;
+  sphinx_status st = build_table(reqs, R, &T, &N, &G);
+  if (st != SPHINX_OK) return st;
+  if (!s_start || !nsteps || !full || !forward_all || !a_ctx || !b_ctx || step < 0 || period < 1)
+    return SPHINX_E_INVALID;
+  for (int g = 0; g < G; ++g)
+    if (s_start[g] < 0 || s_start[g] >= SPHINX_TRAIN_STEPS) return SPHINX_E_INVALID;
+  for (int r = 0; r < R; ++r)
+    if (nsteps[r] < 1) return SPHINX_E_INVALID;
+  const std::vector<double> ab = alpha_bar_table();
+  for (int r = 0; r < R; ++r) {
+    const int F = T.frames[r], g0 = T.frame_off[r], n = nsteps[r];
+    int smax = 0;
+    for (int f = 0; f < F; ++f) smax = std::max(smax, s_start[g0 + f]);
+    const bool live = step < n;
+    const int t = live ? (int)(((int64_t)(n - step) * (smax + 1)) / n) - 1 : -1;
+    full[r] = (live && step % period == 0) ? 1 : 0;
+    for (int f = 0; f < F; ++f) {
+      const int g = g0 + f;
+      forward_all[g] = full[r];
+      a_ctx[g] = live ? (float)std::sqrt(alpha_bar_at(ab, t)) : 1.0f;
+      b_ctx[g] = live ? (float)std::sqrt(1.0 - alpha_bar_at(ab, t)) : 0.0f;
+    }
+  }
+  return SPHINX_OK;
+}
+
 sphinx_status sphinx_select_workspace_bytes(int64_t N, size_t* bytes) {
   if (bytes == nullptr || N < 1) return SPHINX_E_INVALID;
   if (N >= (int64_t)INT32_MAX) return SPHINX_E_UNSUPPORTED;
@@ -380,8 +412,28 @@ sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, sphinx_layout
   if (!aligned(state, 16) || (eps && !aligned(eps, 16)) || !aligned(idx, 16) || !aligned(x_sel, 16))
     return SPHINX_E_INVALID;
   Bracket br(SPHINX_K_GATHER, (hipStream_t)stream);
-  return hip_status(launch_gather(T, layout, state, state_dtype, eps, eps_dtype, idx, n_sel, a, b, x_sel,
-                                  (hipStream_t)stream));
+  return hip_status(launch_gather(T, layout, state, state_dtype, eps, eps_dtype, idx, n_sel, a, b,
+                                  GatherCtx{nullptr, nullptr, nullptr}, x_sel, (hipStream_t)stream));
+}
+
+sphinx_status sphinx_gather_ctx(const sphinx_request* reqs, int32_t R, sphinx_layout layout, const void* state,
+                                sphinx_dtype state_dtype, const void* eps, sphinx_dtype eps_dtype, const int32_t* idx,
+                                int32_t n, const uint8_t* wmask, const float* a, const float* b, const float* a_ctx,
+                                const float* b_ctx, float* x, void* stream) {
+  ReqTable T;
+  int64_t N;
+  int32_t G;
+  sphinx_status st = build_table(reqs, R, &T, &N, &G);
+  if (st != SPHINX_OK) return st;
+  if (n < 0 || n > N) return SPHINX_E_INVALID;
+  if (!valid_dtype(state_dtype) || !valid_dtype(eps_dtype) || !valid_layout(layout)) return SPHINX_E_UNSUPPORTED;
+  if (n == 0) return SPHINX_OK;
+  if (!state || !idx || !wmask || !a || !b || !a_ctx || !b_ctx || !x) return SPHINX_E_INVALID;
+  if (!aligned(state, 16) || (eps && !aligned(eps, 16)) || !aligned(idx, 16) || !aligned(x, 16))
+    return SPHINX_E_INVALID;
+  Bracket br(SPHINX_K_GATHER, (hipStream_t)stream);
+  return hip_status(launch_gather(T, layout, state, state_dtype, eps, eps_dtype, idx, n, a, b,
+                                  GatherCtx{wmask, a_ctx, b_ctx}, x, (hipStream_t)stream));
 }
 
 sphinx_status sphinx_refine_workspace_bytes(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
@@ -398,10 +450,27 @@ sphinx_status sphinx_refine_workspace_bytes(const sphinx_model_desc* m, const sp
   return SPHINX_OK;
 }
 
-sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
-                                 const int32_t* idx, int32_t n_sel, const int32_t* cu_sel_host,
-                                 const int32_t* tau, const float* c1, const float* c2, float* x_sel, void* ws,
-                                 size_t ws_bytes, void* stream) {
+sphinx_status sphinx_kv_cache_bytes(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                    size_t* bytes) {
+  sphinx_status st = check_model(m);
+  if (st != SPHINX_OK) return st;
+  ReqTable T;
+  int64_t N;
+  int32_t G;
+  st = build_table(reqs, R, &T, &N, &G);
+  if (st != SPHINX_OK) return st;
+  if (bytes == nullptr) return SPHINX_E_INVALID;
+  *bytes = (size_t)m->L * (size_t)N * 2 * (size_t)m->D * esize(m->dtype);
+  return SPHINX_OK;
+}
+
+namespace {
+// One denoiser pass plus the DDIM update over the n forwarded rows; with a
+// cache (kv_cache != NULL) every block stores the rows' keys and values and
+// attends over all tokens of each request through the cache.
+sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R, const int32_t* idx,
+                          int32_t n_sel, const int32_t* cu_sel_host, const int32_t* tau, const float* c1,
+                          const float* c2, float* x_sel, void* kv_cache, void* ws, size_t ws_bytes, void* stream) {
   sphinx_status st = check_model(m);
   if (st != SPHINX_OK) return st;
   ReqTable T;
@@ -419,29 +488,29 @@ sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_reques
   if (!idx || !tau || !c1 || !c2 || !x_sel || !ws || m->weights == nullptr) return SPHINX_E_INVALID;
   if (!aligned(idx, 16) || !aligned(x_sel, 16) || !aligned(ws, 256) || !aligned(m->weights, 256))
     return SPHINX_E_INVALID;
+  if (kv_cache != nullptr && !aligned(kv_cache, 16)) return SPHINX_E_INVALID;
   const RefineWs W = refine_layout(*m, T, G, n_sel);
   if (ws_bytes < W.total) return SPHINX_E_WORKSPACE;
+  const bool cached = kv_cache != nullptr;
 
-  // segments: requests with selected tokens, longest first for the attention schedule
+  // segments: requests with forwarded tokens, most keys first for the attention schedule
   SegTable S;
   std::memset(&S, 0, sizeof(S));
   std::vector<int> order;
   for (int r = 0; r < R; ++r)
-    if (cu_sel_host[r + 1] > cu_sel_host[r]) {
-      S.start_sorted[S.nseg_by_start] = cu_sel_host[r];
-      S.len_sorted[S.nseg_by_start] = cu_sel_host[r + 1] - cu_sel_host[r];
-      ++S.nseg_by_start;
-      order.push_back(r);
-    }
-  std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-    return cu_sel_host[x + 1] - cu_sel_host[x] > cu_sel_host[y + 1] - cu_sel_host[y];
-  });
+    if (cu_sel_host[r + 1] > cu_sel_host[r]) order.push_back(r);
+  auto keys = [&](int r) {
+    return cached ? (int64_t)(T.tok_off[r + 1] - T.tok_off[r]) : (int64_t)(cu_sel_host[r + 1] - cu_sel_host[r]);
+  };
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return keys(x) > keys(y); });
   S.nseg = (int)order.size();
   S.tile_prefix[0] = 0;
   for (int i = 0; i < S.nseg; ++i) {
     const int r = order[i];
     S.start[i] = cu_sel_host[r];
     S.len[i] = cu_sel_host[r + 1] - cu_sel_host[r];
+    S.kv_start[i] = cached ? (int)T.tok_off[r] : S.start[i];
+    S.kv_len[i] = (int)keys(r);
     S.tile_prefix[i + 1] = S.tile_prefix[i] + (S.len[i] + kAttnQueryTile - 1) / kAttnQueryTile;
   }
 
@@ -494,9 +563,19 @@ sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_reques
       GemmEpi e_qkv{qkv, 3 * D, nullptr, 0, nullptr};
       SPHINX_TRY(launch_gemm(EPI_BIAS, dt, abuf, P(SPHINX_P_QKV_W, l), P(SPHINX_P_QKV_B, l), n, 3 * D, D, e_qkv, s));
     }
+    AttnIO io{qkv, static_cast<const unsigned char*>(qkv) + (size_t)D * esize(dt),
+              static_cast<const unsigned char*>(qkv) + 2 * (size_t)D * esize(dt), obuf, 3 * D, 3 * D};
+    if (cached) {
+      unsigned char* cl = static_cast<unsigned char*>(kv_cache) + (size_t)l * (size_t)N * 2 * D * esize(dt);
+      Bracket br(SPHINX_K_KV_STORE, s);
+      SPHINX_TRY(launch_kv_store(dt, qkv, n, D, idx, cl, s));
+      io.k = cl;
+      io.v = cl + (size_t)D * esize(dt);
+      io.ldkv = 2 * D;
+    }
     {
       Bracket br(SPHINX_K_ATTENTION, s);
-      SPHINX_TRY(launch_attention(dt, qkv, obuf, D, m->heads, m->head_dim, n, S, s));
+      SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, S, s));
     }
     {
       Bracket br(SPHINX_K_GEMM_OUT, s);
@@ -525,6 +604,22 @@ sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_reques
                           P(SPHINX_P_OUT_B, 0), dt, c1, c2, x_sel, s));
   return SPHINX_OK;
 }
+}  // namespace
+
+sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                 const int32_t* idx, int32_t n_sel, const int32_t* cu_sel_host,
+                                 const int32_t* tau, const float* c1, const float* c2, float* x_sel, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  return refine_impl(m, reqs, R, idx, n_sel, cu_sel_host, tau, c1, c2, x_sel, nullptr, ws, ws_bytes, stream);
+}
+
+sphinx_status sphinx_refine_step_cached(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
+                                        const int32_t* idx, int32_t n, const int32_t* cu_host, const int32_t* tau,
+                                        const float* c1, const float* c2, float* x, void* kv_cache, void* ws,
+                                        size_t ws_bytes, void* stream) {
+  if (kv_cache == nullptr) return SPHINX_E_INVALID;
+  return refine_impl(m, reqs, R, idx, n, cu_host, tau, c1, c2, x, kv_cache, ws, ws_bytes, stream);
+}
 
 sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const float* x_sel, const int32_t* idx,
                                    int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, sphinx_layout in_layout,
@@ -549,8 +644,26 @@ sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const 
   hipStream_t s = (hipStream_t)stream;
   Bracket br(SPHINX_K_SCATTER, s);
   if (!in_place) SPHINX_TRY(launch_convert(T, z_in, in_dtype, in_layout, z_out, out_dtype, out_layout, s));
-  if (n_sel > 0) SPHINX_TRY(launch_scatter(T, x_sel, idx, n_sel, z_out, out_dtype, out_layout, s));
+  if (n_sel > 0) SPHINX_TRY(launch_scatter(T, x_sel, idx, n_sel, nullptr, z_out, out_dtype, out_layout, s));
   return SPHINX_OK;
+}
+
+sphinx_status sphinx_scatter_masked(const sphinx_request* reqs, int32_t R, const float* x, const int32_t* idx,
+                                    int32_t n, const uint8_t* wmask, void* z, sphinx_dtype dtype,
+                                    sphinx_layout layout, void* stream) {
+  ReqTable T;
+  int64_t N;
+  int32_t G;
+  sphinx_status st = build_table(reqs, R, &T, &N, &G);
+  if (st != SPHINX_OK) return st;
+  if (!valid_dtype(dtype) || !valid_layout(layout)) return SPHINX_E_UNSUPPORTED;
+  if (n < 0 || n > N) return SPHINX_E_INVALID;
+  if (n == 0) return SPHINX_OK;
+  if (!x || !idx || !wmask || !z || !aligned(x, 16) || !aligned(idx, 16) || !aligned(z, 16))
+    return SPHINX_E_INVALID;
+  hipStream_t s = (hipStream_t)stream;
+  Bracket br(SPHINX_K_SCATTER, s);
+  return hip_status(launch_scatter(T, x, idx, n, wmask, z, dtype, layout, s));
 }
 
 sphinx_status sphinx_timing_enable(int32_t classes) {

@@ -147,8 +147,8 @@ __device__ __forceinline__ void attn_tile(const bf16* __restrict__ sK, const bf1
 }
 
 template <int HD>
-__device__ __forceinline__ void attn_body(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D, int heads,
-                                          float scale_log2, const SegTable& S, AttnSmem<HD>& sm) {
+__device__ __forceinline__ void attn_body(const AttnIO& io, int D, int heads, float scale_log2, const SegTable& S,
+                                          AttnSmem<HD>& sm) {
   typedef AttnShape<HD> SH;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
@@ -163,11 +163,12 @@ __device__ __forceinline__ void attn_body(const bf16* __restrict__ qkv, bf16* __
   int s = 0;
   while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
   const int qt = tile - S.tile_prefix[s];
-  const int seg0 = S.start[s], L = S.len[s];
-  const int64_t ld = 3 * (int64_t)D;
-  const bf16* Qg = qkv + head * HD;
-  const bf16* Kg = qkv + D + head * HD;
-  const bf16* Vg = qkv + 2 * D + head * HD;
+  const int seg0 = S.start[s], Lq = S.len[s];
+  const int kv0 = S.kv_start[s], L = S.kv_len[s];  // L: keys of the segment
+  const int64_t ldq = io.ldq, ld = io.ldkv;
+  const bf16* Qg = static_cast<const bf16*>(io.q) + head * HD;
+  const bf16* Kg = static_cast<const bf16*>(io.k) + head * HD;
+  const bf16* Vg = static_cast<const bf16*>(io.v) + head * HD;
   const bf16x8 zero8 = {};
 
   // d columns past HD stay zero in both LDS buffers for the whole kernel
@@ -190,15 +191,15 @@ __device__ __forceinline__ void attn_body(const bf16* __restrict__ qkv, bf16* __
 #pragma unroll
   for (int ks = 0; ks < SH::KS; ++ks) {
     const int d0 = ks * 16 + g * 8;
-    qf[ks] = (ql < L && d0 < HD) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(seg0 + ql) * ld + d0) : zero8;
+    qf[ks] = (ql < Lq && d0 < HD) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(seg0 + ql) * ldq + d0) : zero8;
   }
 
   // Loaders: K as (key, 16-byte chunk) and V as (key pair, chunk) work items
   // spread over the 256 threads.  Rows past the segment end are clamped to its
   // last key: their scores are masked to -inf, so they get weight exactly 0 and
   // their (finite) values never contribute.
-  const bf16* kptr = Kg + (int64_t)seg0 * ld;
-  const bf16* vptr = Vg + (int64_t)seg0 * ld;
+  const bf16* kptr = Kg + (int64_t)kv0 * ld;
+  const bf16* vptr = Vg + (int64_t)kv0 * ld;
   bf16x8 rk[SH::KLOADS], rv[2 * SH::VLOADS];
   auto gload = [&](int kbase) {
 #pragma unroll
@@ -264,9 +265,9 @@ __device__ __forceinline__ void attn_body(const bf16* __restrict__ qkv, bf16* __
     __syncthreads();
   }
   l_run += __shfl_xor(l_run, 32, kWave);
-  if (ql < L) {
+  if (ql < Lq) {
     const float inv = 1.0f / l_run;
-    bf16* orow = o + (int64_t)(seg0 + ql) * D + head * HD;
+    bf16* orow = static_cast<bf16*>(io.o) + (int64_t)(seg0 + ql) * D + head * HD;
 #pragma unroll
     for (int db = 0; db < SH::DB; ++db)
 #pragma unroll
@@ -282,16 +283,15 @@ __device__ __forceinline__ void attn_body(const bf16* __restrict__ qkv, bf16* __
   }
 }
 
-__global__ __launch_bounds__(256, 2) void k_attn_bf16(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D,
-                                                      int heads, float scale_log2, SegTable S) {
+__global__ __launch_bounds__(256, 2) void k_attn_bf16(AttnIO io, int D, int heads, float scale_log2, SegTable S) {
   __shared__ __attribute__((aligned(16))) AttnSmem<64> sm;
-  attn_body<64>(qkv, o, D, heads, scale_log2, S, sm);
+  attn_body<64>(io, D, heads, scale_log2, S, sm);
 }
 
-__global__ __launch_bounds__(256, 2) void k_attn_bf16_d72(const bf16* __restrict__ qkv, bf16* __restrict__ o,
-                                                          int D, int heads, float scale_log2, SegTable S) {
+__global__ __launch_bounds__(256, 2) void k_attn_bf16_d72(AttnIO io, int D, int heads, float scale_log2,
+                                                          SegTable S) {
   __shared__ __attribute__((aligned(16))) AttnSmem<72> sm;
-  attn_body<72>(qkv, o, D, heads, scale_log2, S, sm);
+  attn_body<72>(io, D, heads, scale_log2, S, sm);
 }
 
 __device__ __forceinline__ float max_across_halves(float x) {
@@ -519,8 +519,8 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
 }
 }  // namespace dma
 
-__device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D, int heads,
-                                              float scale_log2, const SegTable& S, dma::Smem& sm) {
+__device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads, float scale_log2, const SegTable& S,
+                                              dma::Smem& sm) {
   constexpr int HD = 64;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -533,8 +533,9 @@ __device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16
   int s = 0;
   while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
   const int qt = tile - S.tile_prefix[s];
-  const int seg0 = S.start[s], L = S.len[s];
-  const int ld = 3 * D;
+  const int seg0 = S.start[s], Lq = S.len[s];
+  const int kv0 = S.kv_start[s], L = S.kv_len[s];  // L: keys of the segment
+  const int ldq = io.ldq, ld = io.ldkv;
   const bf16x8 zero8 = {};
 
   // V buffer 2 (that of "tile -1") starts all zero: the first iteration's PV
@@ -543,16 +544,16 @@ __device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16
 
   const int ql = qt * AQ + wave * 32 + r32;
   bf16x8 qf[4];
-  const bf16* Qg = qkv + (int64_t)seg0 * ld + head * HD;
+  const bf16* Qg = static_cast<const bf16*>(io.q) + (int64_t)seg0 * ldq + head * HD;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks)
-    qf[ks] = (ql < L) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)ql * ld + ks * 16 + g * 8) : zero8;
+    qf[ks] = (ql < Lq) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)ql * ldq + ks * 16 + g * 8) : zero8;
 
   // Copy sources: lane i of copy n (n = 0, 1) fills row 8(2 wave + n) + i/8,
   // slot i%8 of a tile.  Element offsets from the segment's first key, rows
   // clamped to the last key of the segment.
-  const bf16* Kg = qkv + (int64_t)seg0 * ld + D + head * HD;
-  const bf16* Vg = qkv + (int64_t)seg0 * ld + 2 * D + head * HD;
+  const bf16* Kg = static_cast<const bf16*>(io.k) + (int64_t)kv0 * ld + head * HD;
+  const bf16* Vg = static_cast<const bf16*>(io.v) + (int64_t)kv0 * ld + head * HD;
   int koff[2], voff[2], klast[2], vlast[2];
 #pragma unroll
   for (int n = 0; n < 2; ++n) {
@@ -661,9 +662,9 @@ __device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16
     dma::pv(sm.v[slot], lo, pb, oacc);
   }
   l_run += __shfl_xor(l_run, 32, kWave);
-  if (ql < L) {
+  if (ql < Lq) {
     const float inv = 1.0f / l_run;
-    bf16* orow = o + (int64_t)(seg0 + ql) * D + head * HD;
+    bf16* orow = static_cast<bf16*>(io.o) + (int64_t)(seg0 + ql) * D + head * HD;
 #pragma unroll
     for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -676,33 +677,36 @@ __device__ __forceinline__ void attn_body_dma(const bf16* __restrict__ qkv, bf16
   }
 }
 
-__global__ __launch_bounds__(256, 2) void k_attn_bf16_dma(const bf16* __restrict__ qkv, bf16* __restrict__ o, int D,
-                                                          int heads, float scale_log2, SegTable S) {
+__global__ __launch_bounds__(256, 2) void k_attn_bf16_dma(AttnIO io, int D, int heads, float scale_log2,
+                                                          SegTable S) {
   __shared__ __attribute__((aligned(1024))) dma::Smem sm;
-  attn_body_dma(qkv, o, D, heads, scale_log2, S, sm);
+  attn_body_dma(io, D, heads, scale_log2, S, sm);
 }
 
 constexpr int kF32Max = 64;
 
-__global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ qkv, float* __restrict__ o, int D, int d,
-                                                  int heads, int n, float scale, SegTable S) {
+__global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int heads, int n, float scale,
+                                                  SegTable S) {
   const int gid = blockIdx.x * 128 + threadIdx.x;
   if (gid >= n * heads) return;
   const int j = gid / heads, h = gid % heads;
   int s = 0;
-  while (s + 1 < S.nseg_by_start && S.start_sorted[s + 1] <= j) ++s;
-  const int seg0 = S.start_sorted[s], L = S.len_sorted[s];
-  const int64_t ld = 3 * (int64_t)D;
+  while (s + 1 < S.nseg && !(j >= S.start[s] && j < S.start[s] + S.len[s])) ++s;
+  const int kv0 = S.kv_start[s], L = S.kv_len[s];
+  const float* qp = static_cast<const float*>(io.q);
+  const float* kp = static_cast<const float*>(io.k);
+  const float* vp = static_cast<const float*>(io.v);
+  float* o = static_cast<float*>(io.o);
   float q[kF32Max], acc[kF32Max];
 #pragma unroll
   for (int c = 0; c < kF32Max; ++c) {
-    q[c] = (c < d) ? qkv[(int64_t)j * ld + h * d + c] : 0.0f;
+    q[c] = (c < d) ? qp[(int64_t)j * io.ldq + h * d + c] : 0.0f;
     acc[c] = 0.0f;
   }
   float m = -INFINITY, l = 0.0f;
-  for (int t = seg0; t < seg0 + L; ++t) {
-    const float* kr = qkv + (int64_t)t * ld + D + h * d;
-    const float* vr = qkv + (int64_t)t * ld + 2 * D + h * d;
+  for (int t = kv0; t < kv0 + L; ++t) {
+    const float* kr = kp + (int64_t)t * io.ldkv + h * d;
+    const float* vr = vp + (int64_t)t * io.ldkv + h * d;
     float sc = 0.0f;
 #pragma unroll
     for (int c = 0; c < kF32Max; ++c)
@@ -723,21 +727,23 @@ __global__ __launch_bounds__(128) void k_attn_f32(const float* __restrict__ qkv,
 }
 }  // namespace
 
-hipError_t launch_attention(sphinx_dtype dt, const void* qkv, void* o, int D, int heads, int head_dim, int n,
+hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,
                             const SegTable& S, hipStream_t s) {
   if (dt == SPHINX_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
     const int grid = S.tile_prefix[S.nseg] * heads;
-    // the copy kernel addresses K and V with 32-bit element offsets
-    if (head_dim == 64 && (int64_t)n * 3 * D < ((int64_t)1 << 31))
-      k_attn_bf16_dma<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
+    // the copy kernel addresses a segment's keys and values with 32-bit element offsets
+    int64_t kv_max = 0;
+    for (int i = 0; i < S.nseg; ++i) kv_max = std::max<int64_t>(kv_max, S.kv_len[i]);
+    if (head_dim == 64 && kv_max * io.ldkv < ((int64_t)1 << 31))
+      k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else if (head_dim == 64)
-      k_attn_bf16<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
+      k_attn_bf16<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else
-      k_attn_bf16_d72<<<grid, 256, 0, s>>>((const bf16*)qkv, (bf16*)o, D, heads, scale_log2, S);
+      k_attn_bf16_d72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
   } else {
     const float scale = 1.0f / sqrtf((float)head_dim);
-    k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>((const float*)qkv, (float*)o, D, head_dim, heads, n, scale, S);
+    k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>(io, D, head_dim, heads, n, scale, S);
   }
   return hipGetLastError();
 }

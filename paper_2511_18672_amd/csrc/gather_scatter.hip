@@ -83,13 +83,15 @@ template <typename ST, typename ET>
 __global__ __launch_bounds__(kTPB) void k_gather_nchw(ReqTable T, const ST* __restrict__ state,
                                                       const ET* __restrict__ eps, const int32_t* __restrict__ idx,
                                                       int n, const float* __restrict__ a,
-                                                      const float* __restrict__ b, float* __restrict__ x) {
+                                                      const float* __restrict__ b, GatherCtx C,
+                                                      float* __restrict__ x) {
   const int64_t j = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   if (j >= n) return;
   const int32_t t = idx[j];
   if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is read
   const TokPos tp = decode_token(T, t);
-  const float av = a[tp.g], bv = b[tp.g];
+  const bool ctx = C.wmask != nullptr && C.wmask[t] == 0;
+  const float av = ctx ? C.a[tp.g] : a[tp.g], bv = ctx ? C.b[tp.g] : b[tp.g];
   float v[16];
 #pragma unroll
   for (int p = 0; p < 8; ++p) {
@@ -115,7 +117,8 @@ template <typename ST, typename ET>
 __global__ __launch_bounds__(kTPB) void k_gather_tok(ReqTable T, const ST* __restrict__ state,
                                                      const ET* __restrict__ eps, const int32_t* __restrict__ idx,
                                                      int n, const float* __restrict__ a,
-                                                     const float* __restrict__ b, float* __restrict__ x) {
+                                                     const float* __restrict__ b, GatherCtx C,
+                                                     float* __restrict__ x) {
   const int64_t i = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   const int64_t j = i >> 2;
   if (j >= n) return;
@@ -123,7 +126,8 @@ __global__ __launch_bounds__(kTPB) void k_gather_tok(ReqTable T, const ST* __res
   const int32_t t = idx[j];
   if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is read
   const int g = frame_of_token(T, t);
-  const float av = a[g], bv = b[g];
+  const bool ctx = C.wmask != nullptr && C.wmask[t] == 0;
+  const float av = ctx ? C.a[g] : a[g], bv = ctx ? C.b[g] : b[g];
   const int64_t e = 16 * (int64_t)t + 4 * q;
   const float4 z = Vec<ST>::load4nt(state, e);
   float4 v = make_float4(av * z.x, av * z.y, av * z.z, av * z.w);
@@ -136,11 +140,13 @@ __global__ __launch_bounds__(kTPB) void k_gather_tok(ReqTable T, const ST* __res
 
 template <typename OT>
 __global__ __launch_bounds__(kTPB) void k_scatter_nchw(ReqTable T, const float* __restrict__ x,
-                                                       const int32_t* __restrict__ idx, int n, OT* __restrict__ out) {
+                                                       const int32_t* __restrict__ idx, int n,
+                                                       const uint8_t* __restrict__ wmask, OT* __restrict__ out) {
   const int64_t j = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   if (j >= n) return;
   const int32_t t = idx[j];
   if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is written
+  if (wmask != nullptr && wmask[t] == 0) return;  // context token: not written back
   const TokPos tp = decode_token(T, t);
   const float4* xr = reinterpret_cast<const float4*>(x + j * 16);
   float v[16];
@@ -158,13 +164,27 @@ __global__ __launch_bounds__(kTPB) void k_scatter_nchw(ReqTable T, const float* 
 
 template <typename OT>
 __global__ __launch_bounds__(kTPB) void k_scatter_tok(int64_t N, const float* __restrict__ x,
-                                                      const int32_t* __restrict__ idx, int n, OT* __restrict__ out) {
+                                                      const int32_t* __restrict__ idx, int n,
+                                                      const uint8_t* __restrict__ wmask, OT* __restrict__ out) {
   const int64_t i = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   const int64_t j = i >> 2;
   if (j >= n) return;
   const int32_t t = idx[j];
   if (t < 0 || t >= N) return;  // out-of-range index: nothing is written
+  if (wmask != nullptr && wmask[t] == 0) return;  // context token: not written back
   Vec<OT>::store4nt(out, 16 * (int64_t)t + 4 * (i & 3), Vec<float>::load4nt(x, 4 * i));
+}
+
+// Latent cache store: row j of qkv, columns [D, 3D) (key then value), to row
+// idx[j] of the cache, 16 bytes per thread.
+__global__ __launch_bounds__(kTPB) void k_kv_store(const uint4* __restrict__ qkv, int n, int row_chunks,
+                                                   const int32_t* __restrict__ idx, uint4* __restrict__ cache) {
+  // row_chunks = 16-byte chunks in D elements; a qkv row has 3, a cache row 2
+  const int64_t c = (int64_t)blockIdx.x * kTPB + threadIdx.x;
+  const int per = 2 * row_chunks;
+  if (c >= (int64_t)n * per) return;
+  const int j = (int)(c / per), k = (int)(c - (int64_t)j * per);
+  cache[(int64_t)idx[j] * per + k] = qkv[(int64_t)j * 3 * row_chunks + row_chunks + k];
 }
 
 // Same-layout f32 copy: four 16-byte non-temporal loads in flight per thread,
@@ -217,12 +237,12 @@ inline unsigned grid_for(int64_t threads) { return (unsigned)((threads + kTPB - 
 
 template <typename ST, typename ET>
 void gather_typed(const ReqTable& T, sphinx_layout lay, const void* state, const void* eps, const int32_t* idx,
-                  int n, const float* a, const float* b, float* x, hipStream_t s) {
+                  int n, const float* a, const float* b, const GatherCtx& C, float* x, hipStream_t s) {
   if (lay == SPHINX_LAYOUT_TOKENS)
     k_gather_tok<ST, ET><<<grid_for(4 * (int64_t)n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a,
-                                                                   b, x);
+                                                                   b, C, x);
   else
-    k_gather_nchw<ST, ET><<<grid_for(n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a, b, x);
+    k_gather_nchw<ST, ET><<<grid_for(n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a, b, C, x);
 }
 
 template <typename IT, typename OT>
@@ -245,35 +265,43 @@ void convert_typed(const ReqTable& T, int64_t N, const void* in, sphinx_layout i
 }  // namespace
 
 hipError_t launch_gather(const ReqTable& T, sphinx_layout lay, const void* state, sphinx_dtype sdt, const void* eps,
-                         sphinx_dtype edt, const int32_t* idx, int n, const float* a, const float* b, float* x,
-                         hipStream_t s) {
+                         sphinx_dtype edt, const int32_t* idx, int n, const float* a, const float* b,
+                         const GatherCtx& C, float* x, hipStream_t s) {
   if (sdt == SPHINX_F32 && edt == SPHINX_F32)
-    gather_typed<float, float>(T, lay, state, eps, idx, n, a, b, x, s);
+    gather_typed<float, float>(T, lay, state, eps, idx, n, a, b, C, x, s);
   else if (sdt == SPHINX_F32 && edt == SPHINX_BF16)
-    gather_typed<float, bf16>(T, lay, state, eps, idx, n, a, b, x, s);
+    gather_typed<float, bf16>(T, lay, state, eps, idx, n, a, b, C, x, s);
   else if (sdt == SPHINX_BF16 && edt == SPHINX_F32)
-    gather_typed<bf16, float>(T, lay, state, eps, idx, n, a, b, x, s);
+    gather_typed<bf16, float>(T, lay, state, eps, idx, n, a, b, C, x, s);
   else
-    gather_typed<bf16, bf16>(T, lay, state, eps, idx, n, a, b, x, s);
+    gather_typed<bf16, bf16>(T, lay, state, eps, idx, n, a, b, C, x, s);
   return hipGetLastError();
 }
 
-hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, void* out, sphinx_dtype odt,
-                          sphinx_layout lay, hipStream_t s) {
+hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, const uint8_t* wmask,
+                          void* out, sphinx_dtype odt, sphinx_layout lay, hipStream_t s) {
   const int64_t N = T.tok_off[T.R];
   if (lay == SPHINX_LAYOUT_TOKENS) {
     const unsigned g = grid_for(4 * (int64_t)n);
     if (odt == SPHINX_F32)
-      k_scatter_tok<float><<<g, kTPB, 0, s>>>(N, x, idx, n, (float*)out);
+      k_scatter_tok<float><<<g, kTPB, 0, s>>>(N, x, idx, n, wmask, (float*)out);
     else
-      k_scatter_tok<bf16><<<g, kTPB, 0, s>>>(N, x, idx, n, (bf16*)out);
+      k_scatter_tok<bf16><<<g, kTPB, 0, s>>>(N, x, idx, n, wmask, (bf16*)out);
   } else {
     const unsigned g = grid_for(n);
     if (odt == SPHINX_F32)
-      k_scatter_nchw<float><<<g, kTPB, 0, s>>>(T, x, idx, n, (float*)out);
+      k_scatter_nchw<float><<<g, kTPB, 0, s>>>(T, x, idx, n, wmask, (float*)out);
     else
-      k_scatter_nchw<bf16><<<g, kTPB, 0, s>>>(T, x, idx, n, (bf16*)out);
+      k_scatter_nchw<bf16><<<g, kTPB, 0, s>>>(T, x, idx, n, wmask, (bf16*)out);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const int32_t* idx, void* cache,
+                           hipStream_t s) {
+  const int row_chunks = D * (dt == SPHINX_BF16 ? 2 : 4) / 16;
+  k_kv_store<<<grid_for((int64_t)n * 2 * row_chunks), kTPB, 0, s>>>((const uint4*)qkv, n, row_chunks, idx,
+                                                                     (uint4*)cache);
   return hipGetLastError();
 }
 

@@ -17,15 +17,36 @@ struct GemmEpi {
   const int32_t* crow;   // EPI_GATED: conditioning row of each token
 };
 
-// Attention segments (one per request with selected tokens).
+// Attention segments (one per request with forwarded tokens): the queries of
+// segment i are rows [start, start+len) of q, its keys and values rows
+// [kv_start, kv_start+kv_len) of k and v (the same rows without a latent
+// cache; all tokens of the request with one).
 struct SegTable {
-  int nseg;                                  // non-empty segments, longest first
+  int nseg;                                  // non-empty segments, most keys first
   int start[SPHINX_MAX_REQUESTS];
   int len[SPHINX_MAX_REQUESTS];
+  int kv_start[SPHINX_MAX_REQUESTS];
+  int kv_len[SPHINX_MAX_REQUESTS];
   int tile_prefix[SPHINX_MAX_REQUESTS + 1];  // prefix sums of 128-query tiles
-  int nseg_by_start;                         // non-empty segments in row order
-  int start_sorted[SPHINX_MAX_REQUESTS];
-  int len_sorted[SPHINX_MAX_REQUESTS];
+};
+
+// Attention operands: q rows with stride ldq, k and v rows with stride ldkv
+// (elements), output rows with stride D.
+struct AttnIO {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  int ldq;
+  int ldkv;
+};
+
+// Context tokens of a gather with a latent cache: tokens t with wmask[t] == 0
+// take the coefficients a[g], b[g] of this struct instead of the write-set ones.
+struct GatherCtx {
+  const uint8_t* wmask;  // NULL: every token uses the write-set coefficients
+  const float* a;
+  const float* b;
 };
 
 constexpr int kAttnQueryTile = 128;
@@ -37,10 +58,14 @@ hipError_t launch_select(const ReqTable& T, int64_t N, const float* u, const flo
 
 // gather_scatter.hip
 hipError_t launch_gather(const ReqTable& T, sphinx_layout lay, const void* state, sphinx_dtype sdt, const void* eps,
-                         sphinx_dtype edt, const int32_t* idx, int n, const float* a, const float* b, float* x,
-                         hipStream_t s);
-hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, void* out, sphinx_dtype odt,
-                          sphinx_layout lay, hipStream_t s);
+                         sphinx_dtype edt, const int32_t* idx, int n, const float* a, const float* b,
+                         const GatherCtx& ctx, float* x, hipStream_t s);
+hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx, int n, const uint8_t* wmask,
+                          void* out, sphinx_dtype odt, sphinx_layout lay, hipStream_t s);
+// Latent cache store: cache row idx[j] (2D elements: key then value) <- qkv row j
+// columns [D, 3D).
+hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const int32_t* idx, void* cache,
+                           hipStream_t s);
 hipError_t launch_convert(const ReqTable& T, const void* in, sphinx_dtype idt, sphinx_layout il, void* out,
                           sphinx_dtype odt, sphinx_layout ol, hipStream_t s);
 
@@ -69,7 +94,7 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
 hipError_t launch_peak_mfma(int iters, float* out, int blocks, hipStream_t s);
 
 // attention.hip
-hipError_t launch_attention(sphinx_dtype dt, const void* qkv, void* o, int D, int heads, int head_dim, int n,
+hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,
                             const SegTable& S, hipStream_t s);
 
 }  // namespace sphinx

@@ -8,6 +8,12 @@ and ``sphinx_scatter_blend``.  Python only sequences the calls; every value is
 computed by libsphinx.so.  The per-step schedule comes from
 ``sphinx_plan_step`` (library host code) and is uploaded once.
 
+With ``cache_period`` T > 0 the latent cache of Sec. 5.2 is on: every T-th
+step is a full step that forwards every token of the live requests (a second
+``sphinx_select_mask`` with threshold -inf over the frames of full requests),
+and every step runs ``sphinx_gather_ctx``, ``sphinx_refine_step_cached`` and
+``sphinx_scatter_masked`` so that only the write set (the mask) is updated.
+
 The fp32 state of record and the noise live token-major by default (token t's
 16 values contiguous at 16*t), so each gathered or scattered token is one
 contiguous row; the NCHW latents are converted once at ``reset`` and back in
@@ -63,7 +69,7 @@ class Refiner:
 
     def __init__(self, requests: Sequence, cfg, blob: torch.Tensor, s_start: np.ndarray, nsteps: np.ndarray,
                  u: np.ndarray, thr: np.ndarray, z0: np.ndarray, eps: np.ndarray, device="cuda",
-                 max_sel: Optional[int] = None, layout: int = B.TOKENS):
+                 max_sel: Optional[int] = None, layout: int = B.TOKENS, cache_period: int = 0):
         if not torch.cuda.is_available():
             raise RuntimeError("Refiner needs a GPU: the selective-refinement step has no CPU path")
         B.lib()
@@ -110,7 +116,23 @@ class Refiner:
         self.plan = {k: torch.from_numpy(v).to(dev) for k, v in self.plan_host.items()}
         self._pending = None  # (step index, slot) of a selection already enqueued
         self.n_sel = 0
+        self.n_fwd = 0
+        self.cu_fwd = None
         self.cu_host = None
+        self.cache_period = int(cache_period)
+        self.kv_cache = None
+        if self.cache_period > 0:
+            if self.max_sel != self.N:
+                raise ValueError("the latent cache forwards every token on full steps: max_sel must be N")
+            self.kv_cache = torch.zeros(B.sphinx_kv_cache_bytes(self.desc, self.reqs), dtype=torch.uint8, device=dev)
+            cplans = [B.sphinx_plan_cache(self.reqs, s_start, nsteps, i, self.cache_period)
+                      for i in range(self.total_steps)]
+            self.cache_host = {k: np.stack([p[k] for p in cplans]) for k in cplans[0]}
+            self.cache_plan = {k: torch.from_numpy(v).to(dev) for k, v in self.cache_host.items()}
+            self.thr_all = torch.full((self.G,), -float("inf"), dtype=torch.float32, device=dev)
+            self._fmask = torch.empty(self.N, dtype=torch.uint8, device=dev)
+            self._fidx = torch.empty(self.N, dtype=torch.int32, device=dev)
+            self._fcu = torch.empty(self.R + 1, dtype=torch.int32, device=dev)
 
     def reset(self, stream=None):
         """state <- fp32(z0) (a converting copy through scatter_blend with no tokens)."""
@@ -168,6 +190,8 @@ class Refiner:
         else:
             self._pending = (i + 1, slot)
         n = self._use_slot(slot)
+        if self.kv_cache is not None:
+            return self._step_cached(k, n, stream)
         if n == 0:
             return 0
         P = self.plan
@@ -177,6 +201,26 @@ class Refiner:
                              P["c2"][k], self.x_sel, self.ws, stream)
         B.sphinx_scatter_blend(self.reqs, self.x_sel, self.idx, n, self.z, B.F32, self.layout, self.z, B.F32,
                                self.layout, stream)
+        return n
+
+    def _step_cached(self, k: int, n: int, stream=None) -> int:
+        """Step k with the latent cache; the write-set selection is current."""
+        P, C = self.plan, self.cache_plan
+        if self.cache_host["full"][k].any():
+            cu_f = B.sphinx_select_mask(self.reqs, self.u, self.thr_all, C["forward_all"][k], self._fmask,
+                                        self._fidx, self._fcu, self.ws_sel, True, stream)
+            idx_f, n_f = self._fidx, int(cu_f[-1])
+        else:
+            cu_f, idx_f, n_f = self.cu_host, self.idx, n
+        self.n_fwd = n_f
+        self.cu_fwd = np.asarray(cu_f).copy()
+        if n_f == 0:
+            return 0
+        B.sphinx_gather_ctx(self.reqs, self.layout, self.z, B.F32, self.eps, self.dt, idx_f, n_f, self.mask,
+                            P["a"][k], P["b"][k], C["a_ctx"][k], C["b_ctx"][k], self.x_sel, stream)
+        B.sphinx_refine_step_cached(self.desc, self.reqs, idx_f, n_f, cu_f, P["tau"][k], P["c1"][k], P["c2"][k],
+                                    self.x_sel, self.kv_cache, self.ws, stream)
+        B.sphinx_scatter_masked(self.reqs, self.x_sel, idx_f, n_f, self.mask, self.z, B.F32, self.layout, stream)
         return n
 
     def run(self, stream=None) -> torch.Tensor:
