@@ -326,3 +326,62 @@ def custom(name: str, model: ModelCfg, requests: Sequence[Request], rho: Sequenc
 
 CONFIGS = {"tiny": tiny, "small": small, "headline": headline,
            "frame_region": frame_region, "batched": batched}
+
+
+# ----------------------------------------------------------------------------
+# image-space inputs of the mask front-end (regression output frames and opacity)
+# ----------------------------------------------------------------------------
+SEED_IMAGES = 5
+IMAGE_SCALE = 8  # image pixels per latent pixel (8x VAE)
+
+
+def _box_blur(img: np.ndarray, r: int) -> np.ndarray:
+    """(2r+1)^2 box mean of an [H][W][C] float image with clamped borders (input synthesis only)."""
+    H, W = img.shape[:2]
+    p = np.pad(img, ((r, r), (r, r), (0, 0)), mode="edge")
+    c = np.cumsum(np.cumsum(p, axis=0), axis=1)
+    c = np.pad(c, ((1, 0), (1, 0), (0, 0)))
+    k = 2 * r + 1
+    s = c[k:k + H, k:k + W] - c[0:H, k:k + W] - c[k:k + H, 0:W] + c[0:H, 0:W]
+    return s / (k * k)
+
+
+def frontend_frame(rng, H: int, W: int, blur_discs: int = 5, holes: int = 6):
+    """One synthetic regression output: a textured RGB frame (uint8 [H][W][3])
+    with `blur_discs` box-blurred discs standing in for motion blur, and an
+    opacity map (float32 [H][W]) near 1 with `holes` low-opacity Gaussian
+    holes standing in for disoccluded regions."""
+    yy, xx = np.mgrid[0:H, 0:W].astype(np.float64)
+    base = np.zeros((H, W, 3))
+    for c in range(3):
+        for _ in range(3):
+            fy, fx, ph = rng.random(3) * np.array([6.0, 6.0, 6.28])
+            base[..., c] += 40.0 * np.sin(2 * np.pi * (fy * yy / H + fx * xx / W) + ph)
+    sharp = np.clip(128.0 + base + rng.uniform(-48.0, 48.0, size=(H, W, 3)), 0, 255)
+    blurred = _box_blur(sharp, 3)
+    inside = np.zeros((H, W), bool)
+    for _ in range(blur_discs):
+        cy, cx = rng.random() * H, rng.random() * W
+        rad = (0.05 + 0.1 * rng.random()) * min(H, W)
+        inside |= (yy - cy) ** 2 + (xx - cx) ** 2 < rad * rad
+    img = np.where(inside[..., None], blurred, sharp)
+    rgb = np.rint(img).astype(np.uint8)
+    opac = np.ones((H, W))
+    for _ in range(holes):
+        cy, cx = rng.random() * H, rng.random() * W
+        sig = (0.02 + 0.04 * rng.random()) * min(H, W)
+        opac -= 0.95 * np.exp(-((yy - cy) ** 2 + (xx - cx) ** 2) / (2 * sig * sig))
+    opac = np.clip(opac + 0.02 * rng.standard_normal((H, W)), 0.0, 1.0).astype(np.float32)
+    return rgb, opac
+
+
+def frontend_inputs(requests: Sequence[Request], seed: int = SEED_IMAGES):
+    """Per request: RGB frames uint8 [F][8h][8w][3] and opacity float32 [F][8h][8w]."""
+    rng = np.random.default_rng(seed)
+    rgb, opac = [], []
+    for q in requests:
+        H, W = IMAGE_SCALE * q.h, IMAGE_SCALE * q.w
+        frames = [frontend_frame(rng, H, W) for _ in range(q.frames)]
+        rgb.append(np.stack([f[0] for f in frames]))
+        opac.append(np.stack([f[1] for f in frames]))
+    return rgb, opac
