@@ -40,12 +40,13 @@ def parse():
     ap.add_argument("--config", default="headline", choices=["headline", "small", "frame_region", "batched"])
     ap.add_argument("--rho", type=float, default=None, help="selected fraction (headline only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", default="step", choices=["step", "copy", "sweep", "peaks", "rho"],
+    ap.add_argument("--mode", default="step", choices=["step", "copy", "sweep", "peaks", "rho", "frontend"],
                     help="step: the hot path; copy: a plain 1 GiB fp32 copy through scatter_blend (no tokens), "
                          "used to calibrate HBM byte counters and to measure achievable bandwidth; sweep: "
                          "mask/compaction, gather and scatter at 2^20..2^26 tokens against the HBM roofline; "
                          "peaks: achievable dense bf16 MFMA rate and copy bandwidth; rho: step time of the "
-                         "headline workload over the selected fraction")
+                         "headline workload over the selected fraction; frontend: the mask front-end on the "
+                         "headline views (14 x 576 x 1024) against the HBM roofline")
     ap.add_argument("--rhos", default="0.05,0.1,0.2,0.3,0.5,0.75,1.0", help="selected fractions of --mode rho")
     ap.add_argument("--layout", default="tokens", choices=["tokens", "nchw"],
                     help="layout of the fp32 state of record and the noise")
@@ -201,6 +202,45 @@ def rho_mode(args):
         torch.cuda.empty_cache()
 
 
+def frontend_mode(args):
+    """The mask front-end (luma, Laplacian variance, smoothing, per-frame Otsu,
+    opacity, 16x16 pooling) over the 14 headline views of 576 x 1024.
+    Algorithmic bytes: 3 (RGB) + 4 (opacity) per pixel read, 1 + 4 per token
+    written (mask and uncertainty)."""
+    import torch
+
+    import paper_2511_18672_amd as S
+    import workloads as W
+
+    reqs_py = [W.Request(14, 72, 128)]
+    rgb, opac = W.frontend_inputs(reqs_py)
+    reqs = S.make_requests(reqs_py)
+    N, G = reqs_py[0].tokens, reqs_py[0].frames
+    d_rgb = torch.from_numpy(rgb[0].ravel()).cuda()
+    d_op = torch.from_numpy(opac[0].ravel()).cuda()
+    mask = torch.empty(N, dtype=torch.uint8, device="cuda")
+    u = torch.empty(N, dtype=torch.float32, device="cuda")
+    thr = torch.empty(G, dtype=torch.int32, device="cuda")
+    ws = torch.empty(S.sphinx_mask_frontend_workspace_bytes(reqs), dtype=torch.uint8, device="cuda")
+    for _ in range(max(args.warmup, 1)):
+        S.sphinx_mask_frontend(reqs, d_rgb, d_op, 0.5, mask, u, thr, ws)
+    torch.cuda.synchronize()
+    S.sphinx_timing_enable(True, classes=["frontend"])
+    for _ in range(args.steps):
+        S.sphinx_mask_frontend(reqs, d_rgb, d_op, 0.5, mask, u, thr, ws)
+    torch.cuda.synchronize()
+    cnt, ms = S.sphinx_timing_read()["frontend"]
+    S.sphinx_timing_enable(False)
+    pixels = 256 * N
+    nbytes = 7 * pixels + 5 * N
+    avg_s = ms / cnt / 1e3
+    print(json.dumps({"mode": "frontend", "frames": G, "image": "576x1024", "pixels": pixels, "tokens": N,
+                      "masked_tokens": int(mask.sum().item()), "avg_us": round(avg_s * 1e6, 2),
+                      "Mpix_per_s": round(pixels / avg_s / 1e6, 1), "algorithmic_bytes": nbytes,
+                      "GB/s": round(nbytes / avg_s / 1e9, 1), "frac_of_8TBs": round(nbytes / avg_s / 8e12, 4)}),
+          flush=True)
+
+
 def sweep_mode(args):
     """HBM roofline of the memory-bound kernels at large token counts.
 
@@ -301,6 +341,8 @@ def main():
         return peaks_mode(args)
     if args.mode == "rho" and args.gpus == 1:
         return rho_mode(args)
+    if args.mode == "frontend" and args.gpus == 1:
+        return frontend_mode(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
               f"(the selective-refinement step is built and measured on a single MI355X)", file=sys.stderr)

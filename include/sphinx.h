@@ -276,6 +276,42 @@ sphinx_status sphinx_scatter_masked(const sphinx_request* reqs, int32_t R, const
                                     int32_t n, const uint8_t* wmask, void* z, sphinx_dtype dtype,
                                     sphinx_layout layout, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Mask front-end (Sec. 5.3 spatially selective refinement; Alg. 1
+ * laplacian_var, otsu(norm(.)), the opacity mask 1[O < tau_o] and their
+ * union): the token mask of every request from the regression output frames
+ * and their opacity, integer-exact.
+ *
+ *   luma   Y = (77 R + 150 G + 29 B + 128) >> 8
+ *   blur   L = 4-neighbour Laplacian of Y; V = 81 * sum(L^2) - (sum L)^2 over
+ *          the 9 x 9 window (81^2 times the local variance of L); Wm = sum of
+ *          V over the 5 x 5 box; per frame q = floor(255 (Wm - min) / (max -
+ *          min)) (0 for a constant frame) and inv = 255 - q; Otsu's threshold
+ *          t of inv over the frame (the t in 0..254 maximising the
+ *          between-class variance, exact, smallest t on ties); blurry = inv > t.
+ *          Every stencil reads its input with replicated borders.
+ *   mask   pixel = (opacity < tau_o) | blurry; token (f, y, x) = OR over
+ *          image pixels [16y, 16y+16) x [16x, 16x+16) of frame f (a latent
+ *          pixel is 8 x 8 image pixels, a token 2 x 2 latent pixels).
+ * ------------------------------------------------------------------------ */
+
+/* Workspace bytes of sphinx_mask_frontend (about one byte per image pixel). */
+sphinx_status sphinx_mask_frontend_workspace_bytes(const sphinx_request* reqs, int32_t R, size_t* bytes);
+
+/* rgb: dev uint8, per request [frames][8h][8w][3] (interleaved RGB, rows of
+ * the image), requests concatenated (request r starts at byte 768 *
+ * tok_offset_r).  opacity: dev float, per request [frames][8h][8w], request r
+ * at element 256 * tok_offset_r.  tau_o: opacity threshold (strict; 0.5 in
+ * the paper; NaN selects nothing by opacity).  token_mask: dev uint8 [N] out
+ * (0/1).  uncert: dev float [N] out or NULL; 1.0 where the token is masked,
+ * else 0.0, so that sphinx_select_mask with thr = 0.5 selects exactly the
+ * mask.  otsu_t: dev int32 [G] out or NULL (each frame's threshold).  Images
+ * are limited to 2^26 pixels per frame (h * w <= 2^20).  Bit-exact and
+ * deterministic. */
+sphinx_status sphinx_mask_frontend(const sphinx_request* reqs, int32_t R, const uint8_t* rgb, const float* opacity,
+                                   float tau_o, uint8_t* token_mask, float* uncert, int32_t* otsu_t, void* ws,
+                                   size_t ws_bytes, void* stream);
+
 /* Profiling aid (outside the method).  sphinx_timing_enable(classes) takes a
  * bit mask of kernel classes (bit k = class k; 0 turns timing off; bits at or
  * above SPHINX_K_COUNT are SPHINX_E_INVALID).  While a class is enabled, every
@@ -300,6 +336,7 @@ typedef enum {
   SPHINX_K_FINAL,      /* final LayerNorm + projection + DDIM update */
   SPHINX_K_SCATTER,
   SPHINX_K_KV_STORE,   /* latent cache store of the forwarded rows' keys and values */
+  SPHINX_K_FRONTEND,   /* mask front-end (five kernels, one bracket) */
   SPHINX_K_COUNT
 } sphinx_kernel_class;
 

@@ -6,7 +6,8 @@ step driver; it has no CPU fallback and raises if the library is missing.
 """
 from .binding import (BF16, F32, KERNEL_CLASSES, NCHW, PEAK_BLOCKS, TOKENS, EXPORTED, SphinxError, gather, lib,
                       make_requests, model_desc, plan_step, refine_step, scatter_blend, select_mask, sphinx_gather,
-                      sphinx_gather_ctx, sphinx_kv_cache_bytes, sphinx_model_blob_bytes, sphinx_model_param,
+                      sphinx_gather_ctx, sphinx_kv_cache_bytes, sphinx_mask_frontend,
+                      sphinx_mask_frontend_workspace_bytes, sphinx_model_blob_bytes, sphinx_model_param,
                       sphinx_peak_mfma, sphinx_plan_cache, sphinx_plan_step, sphinx_refine_step,
                       sphinx_refine_step_cached, sphinx_refine_workspace_bytes, sphinx_scatter_blend,
                       sphinx_scatter_masked, sphinx_select_mask, sphinx_select_workspace_bytes,
@@ -15,7 +16,8 @@ from .refiner import Refiner, from_workload, pack_weights
 
 __all__ = ["BF16", "F32", "KERNEL_CLASSES", "NCHW", "PEAK_BLOCKS", "TOKENS", "EXPORTED", "SphinxError", "Refiner",
            "from_workload", "pack_weights", "lib", "make_requests", "model_desc", "sphinx_gather",
-           "sphinx_gather_ctx", "sphinx_kv_cache_bytes", "sphinx_model_blob_bytes", "sphinx_model_param",
+           "sphinx_gather_ctx", "sphinx_kv_cache_bytes", "sphinx_mask_frontend",
+           "sphinx_mask_frontend_workspace_bytes", "sphinx_model_blob_bytes", "sphinx_model_param",
            "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_plan_step", "sphinx_refine_step",
            "sphinx_refine_step_cached", "sphinx_refine_workspace_bytes", "sphinx_scatter_blend",
            "sphinx_scatter_masked", "sphinx_select_mask", "sphinx_select_workspace_bytes", "sphinx_status_string",

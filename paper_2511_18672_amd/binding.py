@@ -28,10 +28,11 @@ EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_par
             "sphinx_select_workspace_bytes", "sphinx_select_mask", "sphinx_gather", "sphinx_refine_workspace_bytes",
             "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
             "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_kv_cache_bytes", "sphinx_gather_ctx",
-            "sphinx_refine_step_cached", "sphinx_scatter_masked"]
+            "sphinx_refine_step_cached", "sphinx_scatter_masked", "sphinx_mask_frontend_workspace_bytes",
+            "sphinx_mask_frontend"]
 PEAK_BLOCKS = 2048
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
-                  "gemm_mlp2", "final", "scatter", "kv_store"]
+                  "gemm_mlp2", "final", "scatter", "kv_store", "frontend"]
 
 
 class SphinxError(RuntimeError):
@@ -88,6 +89,9 @@ def lib() -> ctypes.CDLL:
         "sphinx_refine_step_cached": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, P, c_int32, P, P, P,
                                                 P, P, P, P, c_size_t, P]),
         "sphinx_scatter_masked": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, P, c_int32, c_int32, P]),
+        "sphinx_mask_frontend_workspace_bytes": (c_int32, [POINTER(Request), c_int32, POINTER(c_size_t)]),
+        "sphinx_mask_frontend": (c_int32, [POINTER(Request), c_int32, P, P, ctypes.c_float, P, P, P, P, c_size_t,
+                                           P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -284,6 +288,19 @@ def sphinx_refine_step_cached(desc: ModelDesc, reqs, idx, n: int, cu_host: np.nd
 def sphinx_scatter_masked(reqs, x, idx, n: int, wmask, z, dtype: int, layout: int, stream=None):
     _check("sphinx_scatter_masked", lib().sphinx_scatter_masked(
         reqs, len(reqs), _ptr(x), _ptr(idx), n, _ptr(wmask), _ptr(z), dtype, layout, _stream(stream)))
+
+
+def sphinx_mask_frontend_workspace_bytes(reqs) -> int:
+    out = c_size_t()
+    _check("sphinx_mask_frontend_workspace_bytes", lib().sphinx_mask_frontend_workspace_bytes(
+        reqs, len(reqs), ctypes.byref(out)))
+    return out.value
+
+
+def sphinx_mask_frontend(reqs, rgb, opacity, tau_o: float, token_mask, uncert, otsu_t, ws, stream=None):
+    _check("sphinx_mask_frontend", lib().sphinx_mask_frontend(
+        reqs, len(reqs), _ptr(rgb), _ptr(opacity), tau_o, _ptr(token_mask), _ptr(uncert), _ptr(otsu_t), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
 
 
 select_mask = sphinx_select_mask

@@ -666,6 +666,44 @@ sphinx_status sphinx_scatter_masked(const sphinx_request* reqs, int32_t R, const
   return hip_status(launch_scatter(T, x, idx, n, wmask, z, dtype, layout, s));
 }
 
+namespace {
+sphinx_status front_check(const sphinx_request* reqs, int32_t R, ReqTable* T, int32_t* G) {
+  int64_t N;
+  sphinx_status st = build_table(reqs, R, T, &N, G);
+  if (st != SPHINX_OK) return st;
+  for (int r = 0; r < R; ++r)
+    if ((int64_t)T->h[r] * T->w[r] > ((int64_t)1 << 20)) return SPHINX_E_UNSUPPORTED;
+  return SPHINX_OK;
+}
+}  // namespace
+
+sphinx_status sphinx_mask_frontend_workspace_bytes(const sphinx_request* reqs, int32_t R, size_t* bytes) {
+  ReqTable T;
+  int32_t G;
+  sphinx_status st = front_check(reqs, R, &T, &G);
+  if (st != SPHINX_OK) return st;
+  if (bytes == nullptr) return SPHINX_E_INVALID;
+  *bytes = front_ws_bytes(T, G);
+  return SPHINX_OK;
+}
+
+sphinx_status sphinx_mask_frontend(const sphinx_request* reqs, int32_t R, const uint8_t* rgb, const float* opacity,
+                                   float tau_o, uint8_t* token_mask, float* uncert, int32_t* otsu_t, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  ReqTable T;
+  int32_t G;
+  sphinx_status st = front_check(reqs, R, &T, &G);
+  if (st != SPHINX_OK) return st;
+  if (!rgb || !opacity || !token_mask || !ws) return SPHINX_E_INVALID;
+  if (!aligned(rgb, 16) || !aligned(opacity, 16) || !aligned(token_mask, 16) || !aligned(ws, 256) ||
+      (uncert && !aligned(uncert, 16)) || (otsu_t && !aligned(otsu_t, 16)))
+    return SPHINX_E_INVALID;
+  if (ws_bytes < front_ws_bytes(T, G)) return SPHINX_E_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  Bracket br(SPHINX_K_FRONTEND, s);
+  return hip_status(launch_front(T, G, rgb, opacity, tau_o, token_mask, uncert, otsu_t, ws, s));
+}
+
 sphinx_status sphinx_timing_enable(int32_t classes) {
   if (classes < 0 || classes >= (1 << SPHINX_K_COUNT)) return SPHINX_E_INVALID;
   Timing& T = timing();

@@ -69,6 +69,15 @@ hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const
 hipError_t launch_convert(const ReqTable& T, const void* in, sphinx_dtype idt, sphinx_layout il, void* out,
                           sphinx_dtype odt, sphinx_layout ol, hipStream_t s);
 
+// frontend.hip: tiles of the mask front-end, per request
+struct FrontTiles {
+  int tile_off[SPHINX_MAX_REQUESTS + 1];
+};
+int front_tiles(const ReqTable& T, FrontTiles* F);
+size_t front_ws_bytes(const ReqTable& T, int G);
+hipError_t launch_front(const ReqTable& T, int G, const uint8_t* rgb, const float* opacity, float tau,
+                        uint8_t* mask, float* u, int32_t* thr_out, void* ws, hipStream_t s);
+
 // cond.hip
 hipError_t launch_cond_rows(const int32_t* tau, int G, int32_t* fmap, int32_t* utau, int32_t* U, hipStream_t s);
 hipError_t launch_temb(const int32_t* utau, const int32_t* U, int Gmax, float* temb, hipStream_t s);

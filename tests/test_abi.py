@@ -181,3 +181,21 @@ def test_peak_probe_validation(L):
     assert L.sphinx_peak_mfma((1 << 24) + 1, ctypes.c_void_p(p), None) == INVALID
     assert L.sphinx_peak_mfma(16, None, None) == INVALID
     assert L.sphinx_peak_mfma(16, ctypes.c_void_p(p + 4), None) == INVALID
+
+
+def test_frontend_validation(L):
+    P = ctypes.c_void_p
+    reqs = _reqs([(2, 8, 8)])
+    need = ctypes.c_size_t()
+    assert L.sphinx_mask_frontend_workspace_bytes(reqs, 1, ctypes.byref(need)) == OK and need.value > 0
+    assert L.sphinx_mask_frontend_workspace_bytes(reqs, 1, None) == INVALID
+    big = _reqs([(1, 2048, 1024)])  # 2^21 latent pixels: 2^27 image pixels per frame
+    assert L.sphinx_mask_frontend_workspace_bytes(big, 1, ctypes.byref(need)) == UNSUPPORTED
+    args = lambda rgb, op, m, ws, nbytes: (reqs, 1, rgb, op, ctypes.c_float(0.5), m, None, None, ws, nbytes, None)
+    ok = need.value
+    L.sphinx_mask_frontend_workspace_bytes(reqs, 1, ctypes.byref(need))
+    assert L.sphinx_mask_frontend(*args(None, P(256), P(256), P(256), need.value)) == INVALID
+    assert L.sphinx_mask_frontend(*args(P(256), P(260), P(256), P(256), need.value)) == INVALID
+    assert L.sphinx_mask_frontend(*args(P(256), P(256), P(256), P(272), need.value)) == INVALID
+    assert L.sphinx_mask_frontend(*args(P(256), P(256), P(256), P(256), need.value - 1)) == WORKSPACE
+    assert ok == need.value
