@@ -141,6 +141,35 @@ sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int3
                                const int32_t* nsteps /*host[R]*/, int32_t step, uint8_t* active,
                                uint8_t* newly, int32_t* tau, float* a, float* b, float* c1, float* c2);
 
+/* Adaptive start steps (Sec. 5.1, Eq. 2 and the k-decision logic; Alg. 1
+ * k <- K_c(r), k_min <- min(k)).  Pure host code, double precision.
+ *   Frame f of request r (F frames) is target f+1 of F, at t = (f+1)/(F+1).
+ *   Reference quality (Eq. 2): Q* = c0 + (c1 - c0) * (t^gamma if c1 >= c0,
+ *   else 1 - (1-t)^gamma), with c0 = q_in[2r], c1 = q_in[2r+1] the quality
+ *   scores of the request's two input views.
+ *   Ratio r_f = q_reg[g] / Q*; start step k_f = table.k[i] with i the number
+ *   of breakpoints table.ratio[] <= r_f, using table tables[cluster[r]].
+ *   Outputs: k[g], the start index s[g] = round(1000 (S - k)/S) - 1 (half up;
+ *   the t_start = 1 - k/S of the plan), nsteps[r] = S - min over the request's
+ *   frames of k (the loop from k_min to S-1), and optionally ratio[g].
+ * With s_start = s and these nsteps, sphinx_plan_step activates frame f at
+ * loop step u = k_f (Alg. 1 A_u = 1[k <= u]) when 1000 is a multiple of S.
+ * Requirements: gamma in (0, 1]; 1 <= S <= 1000; every table has 0..15
+ * strictly increasing finite breakpoints and n+1 non-decreasing k in
+ * [0, S-1]; cluster[r] in [0, n_tables); c0, c1 > 0 and q_reg >= 0 finite. */
+#define SPHINX_KLOGIC_MAX 15
+typedef struct {
+  int32_t n;                          /* number of breakpoints */
+  float ratio[SPHINX_KLOGIC_MAX];     /* breakpoints of the quality ratio */
+  int32_t k[SPHINX_KLOGIC_MAX + 1];   /* start step below ratio[0], ..., at or above ratio[n-1] */
+} sphinx_klogic;
+
+sphinx_status sphinx_adaptive_start(const sphinx_request* reqs, int32_t R, const float* q_in /*host[2R]*/,
+                                    const float* q_reg /*host[G]*/, float gamma, const sphinx_klogic* tables,
+                                    int32_t n_tables, const int32_t* cluster /*host[R]*/, int32_t S,
+                                    int32_t* k /*host[G]*/, int32_t* s_start /*host[G]*/,
+                                    int32_t* nsteps /*host[R]*/, double* ratio /*host[G] or NULL*/);
+
 /* Workspace bytes needed by sphinx_select_mask for N tokens. */
 sphinx_status sphinx_select_workspace_bytes(int64_t N, size_t* bytes);
 

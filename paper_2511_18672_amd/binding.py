@@ -29,7 +29,7 @@ EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_par
             "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
             "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_kv_cache_bytes", "sphinx_gather_ctx",
             "sphinx_refine_step_cached", "sphinx_scatter_masked", "sphinx_mask_frontend_workspace_bytes",
-            "sphinx_mask_frontend"]
+            "sphinx_mask_frontend", "sphinx_adaptive_start"]
 PEAK_BLOCKS = 2048
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
                   "gemm_mlp2", "final", "scatter", "kv_store", "frontend"]
@@ -44,6 +44,21 @@ class SphinxError(RuntimeError):
 class Request(ctypes.Structure):
     _fields_ = [("frames", c_int32), ("h", c_int32), ("w", c_int32), ("frame_offset", c_int32),
                 ("tok_offset", c_int64)]
+
+
+class KLogic(ctypes.Structure):
+    _fields_ = [("n", c_int32), ("ratio", ctypes.c_float * 15), ("k", c_int32 * 16)]
+
+
+def make_klogic(ratio: Sequence[float], k: Sequence[int]) -> KLogic:
+    """C k-decision table: len(ratio) breakpoints, len(ratio)+1 start steps."""
+    t = KLogic()
+    t.n = len(ratio)
+    for i, v in enumerate(ratio):
+        t.ratio[i] = v
+    for i, v in enumerate(k):
+        t.k[i] = v
+    return t
 
 
 class ModelDesc(ctypes.Structure):
@@ -90,6 +105,8 @@ def lib() -> ctypes.CDLL:
                                                 P, P, P, P, c_size_t, P]),
         "sphinx_scatter_masked": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, P, c_int32, c_int32, P]),
         "sphinx_mask_frontend_workspace_bytes": (c_int32, [POINTER(Request), c_int32, POINTER(c_size_t)]),
+        "sphinx_adaptive_start": (c_int32, [POINTER(Request), c_int32, P, P, ctypes.c_float, POINTER(KLogic), c_int32,
+                                            P, c_int32, P, P, P, P]),
         "sphinx_mask_frontend": (c_int32, [POINTER(Request), c_int32, P, P, ctypes.c_float, P, P, P, P, c_size_t,
                                            P]),
     }
@@ -301,6 +318,22 @@ def sphinx_mask_frontend(reqs, rgb, opacity, tau_o: float, token_mask, uncert, o
     _check("sphinx_mask_frontend", lib().sphinx_mask_frontend(
         reqs, len(reqs), _ptr(rgb), _ptr(opacity), tau_o, _ptr(token_mask), _ptr(uncert), _ptr(otsu_t), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def sphinx_adaptive_start(reqs, q_in: np.ndarray, q_reg: np.ndarray, gamma: float, tables: Sequence[KLogic],
+                          cluster: np.ndarray, S: int = 50) -> Dict[str, np.ndarray]:
+    """Per-frame start steps k and start indices, per-request step counts, ratios."""
+    G = sum(r.frames for r in reqs)
+    q_in = np.ascontiguousarray(q_in, dtype=np.float32).ravel()
+    q_reg = np.ascontiguousarray(q_reg, dtype=np.float32)
+    cluster = np.ascontiguousarray(cluster, dtype=np.int32)
+    arr = (KLogic * len(tables))(*tables)
+    out = {"k": np.zeros(G, np.int32), "s_start": np.zeros(G, np.int32), "nsteps": np.zeros(len(reqs), np.int32),
+           "ratio": np.zeros(G, np.float64)}
+    _check("sphinx_adaptive_start", lib().sphinx_adaptive_start(
+        reqs, len(reqs), _ptr(q_in), _ptr(q_reg), gamma, arr, len(tables), _ptr(cluster), S, _ptr(out["k"]),
+        _ptr(out["s_start"]), _ptr(out["nsteps"]), _ptr(out["ratio"])))
+    return out
 
 
 select_mask = sphinx_select_mask

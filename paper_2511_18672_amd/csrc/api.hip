@@ -366,6 +366,58 @@ sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int
   return SPHINX_OK;
 }
 
+sphinx_status sphinx_adaptive_start(const sphinx_request* reqs, int32_t R, const float* q_in, const float* q_reg,
+                                    float gamma, const sphinx_klogic* tables, int32_t n_tables,
+                                    const int32_t* cluster, int32_t S, int32_t* k, int32_t* s_start,
+                                    int32_t* nsteps, double* ratio) {
+  ReqTable T;
+  int64_t N;
+  int32_t G;
+  sphinx_status st = build_table(reqs, R, &T, &N, &G);
+  if (st != SPHINX_OK) return st;
+  if (!q_in || !q_reg || !tables || !cluster || !k || !s_start || !nsteps) return SPHINX_E_INVALID;
+  if (!(gamma > 0.0f && gamma <= 1.0f) || S < 1 || S > 1000 || n_tables < 1) return SPHINX_E_INVALID;
+  for (int c = 0; c < n_tables; ++c) {
+    const sphinx_klogic& t = tables[c];
+    if (t.n < 0 || t.n > SPHINX_KLOGIC_MAX) return SPHINX_E_INVALID;
+    for (int i = 0; i < t.n; ++i)
+      if (!std::isfinite(t.ratio[i]) || (i > 0 && !(t.ratio[i] > t.ratio[i - 1]))) return SPHINX_E_INVALID;
+    for (int i = 0; i <= t.n; ++i)
+      if (t.k[i] < 0 || t.k[i] >= S || (i > 0 && t.k[i] < t.k[i - 1])) return SPHINX_E_INVALID;
+  }
+  for (int r = 0; r < R; ++r) {
+    if (cluster[r] < 0 || cluster[r] >= n_tables) return SPHINX_E_INVALID;
+    if (!(q_in[2 * r] > 0.0f) || !(q_in[2 * r + 1] > 0.0f) || !std::isfinite(q_in[2 * r]) ||
+        !std::isfinite(q_in[2 * r + 1]))
+      return SPHINX_E_INVALID;
+  }
+  for (int g = 0; g < G; ++g)
+    if (!(q_reg[g] >= 0.0f) || !std::isfinite(q_reg[g])) return SPHINX_E_INVALID;
+  for (int r = 0; r < R; ++r) {
+    const int F = T.frames[r], g0 = T.frame_off[r];
+    const double c0 = q_in[2 * r], c1 = q_in[2 * r + 1];
+    const sphinx_klogic& tab = tables[cluster[r]];
+    int kmin = S;
+    for (int f = 0; f < F; ++f) {
+      const int g = g0 + f;
+      const double t = (double)(f + 1) / (double)(F + 1);
+      const double ft = c1 >= c0 ? std::pow(t, (double)gamma) : 1.0 - std::pow(1.0 - t, (double)gamma);
+      const double q_ref = c0 + (c1 - c0) * ft;
+      const double rat = (double)q_reg[g] / q_ref;
+      int i = 0;
+      while (i < tab.n && rat >= (double)tab.ratio[i]) ++i;
+      k[g] = tab.k[i];
+      // round(1000 (S - k) / S) half up, minus 1
+      const int64_t num = 1000 * (int64_t)(S - k[g]);
+      s_start[g] = (int32_t)((2 * num + S) / (2 * (int64_t)S)) - 1;
+      if (ratio != nullptr) ratio[g] = rat;
+      kmin = std::min(kmin, k[g]);
+    }
+    nsteps[r] = S - kmin;
+  }
+  return SPHINX_OK;
+}
+
 sphinx_status sphinx_select_workspace_bytes(int64_t N, size_t* bytes) {
   if (bytes == nullptr || N < 1) return SPHINX_E_INVALID;
   if (N >= (int64_t)INT32_MAX) return SPHINX_E_UNSUPPORTED;

@@ -92,3 +92,38 @@ def test_frontend_headline_shape():
     cu_h = S.sphinx_select_mask(r, torch.from_numpy(u).cuda(), thr, None, m2, idx, cu, ws)
     assert np.array_equal(m2.cpu().numpy(), mask)
     assert int(cu_h[-1]) == int(mask.sum())
+
+
+def test_pipeline_frontend_adaptive_refine():
+    """Alg. 1 from the regression output on: the front-end mask (as the 0/1
+    uncertainty map at thr 0.5), adaptive per-frame start steps from synthetic
+    quality scores, then the partial-denoising loop, against the oracle's
+    composition of the same three parts."""
+    import oracle as O
+    import oracle.adaptive_start as A
+
+    model = W.ModelCfg(D=128, heads=2, head_dim=64, mlp=512, L=2, dtype="bf16")
+    reqs_py = [W.Request(3, 16, 16), W.Request(2, 8, 24)]
+    rgb, opac = W.frontend_inputs(reqs_py, seed=21)
+    _, u_gpu, _ = run_frontend(reqs_py, rgb, opac)
+    ref_mask, _ = M.request_masks(reqs_py, rgb, opac)
+    assert np.array_equal(u_gpu, ref_mask.astype(np.float32))
+    q_in, q_reg = W.quality_scores(reqs_py, seed=22)
+    table = ([0.8, 0.9, 1.0], [40, 43, 45, 47])
+    got = S.sphinx_adaptive_start(S.make_requests(reqs_py), q_in, q_reg, 0.5, [S.make_klogic(*table)],
+                                  np.zeros(2, np.int32), 50)
+    ks, ss, ns, _ = A.adaptive_start([q.frames for q in reqs_py], q_in.astype(np.float64), q_reg.astype(np.float64),
+                                     0.5, [A.KLogic([float(np.float32(x)) for x in table[0]], table[1])], [0, 0], 50)
+    assert np.array_equal(got["s_start"], ss) and np.array_equal(got["nsteps"], ns)
+    wl = W.custom("pipeline", model, reqs_py, [0.5, 0.5], [0.5, 0.5], [3, 3])
+    wl.u = u_gpu
+    wl.thr = np.full(wl.G, 0.5, np.float32)
+    wl.s_start = got["s_start"].astype(np.int32)
+    wl.nsteps = got["nsteps"].astype(np.int32)
+    R = S.from_workload(wl)
+    out = R.run().cpu().numpy().astype(np.float64)
+    ref = O.refine(wl, precision="model")
+    err = np.abs(out - ref).max()
+    print(f"[pipeline] k = {list(ks)}, steps = {list(ns)}, masked = {int(ref_mask.sum())}/{wl.N}, "
+          f"max_abs = {err:.3e}")
+    assert err <= 2e-2

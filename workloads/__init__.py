@@ -385,3 +385,16 @@ def frontend_inputs(requests: Sequence[Request], seed: int = SEED_IMAGES):
         rgb.append(np.stack([f[0] for f in frames]))
         opac.append(np.stack([f[1] for f in frames]))
     return rgb, opac
+
+
+SEED_QUALITY = 6
+
+
+def quality_scores(requests: Sequence[Request], seed: int = SEED_QUALITY):
+    """Synthetic perceptual quality scores standing in for MUSIQ (Sec. 5.1):
+    per request the two input views' scores U[40, 75) (float32 [R][2]) and per
+    frame a regression output score U[0.7, 1.05) times the mean of the two."""
+    rng = np.random.default_rng(seed)
+    q_in = rng.uniform(40.0, 75.0, size=(len(requests), 2)).astype(np.float32)
+    q_reg = np.concatenate([rng.uniform(0.7, 1.05, q.frames) * q_in[r].mean() for r, q in enumerate(requests)])
+    return q_in, q_reg.astype(np.float32)
