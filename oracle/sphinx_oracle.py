@@ -147,7 +147,7 @@ class StepPlan:
 
 
 def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Sequence[int],
-               period: int = 0) -> List[StepPlan]:
+               period: int = 0, per_frame_grid: bool = False) -> List[StepPlan]:
     """Per-step, per-frame schedule (Alg. 1 loop with a per-frame start step).
 
     Each request walks its own grid from s_max = max of its frames' start
@@ -164,6 +164,10 @@ def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Seque
     a token forwarded only as context enters as add_noise of its clean latent
     at the step's level (Alg. 1 resamples inactive content from the clean
     latents).
+
+    per_frame_grid=True is the other reading of Alg. 1's per-frame start:
+    every frame walks its own n-step grid from its own s_f, so all frames are
+    active from the first step (newly active there) at their own timesteps.
     """
     ab = alpha_bar()
     G = int(sum(frames_per_req))
@@ -185,6 +189,16 @@ def plan_steps(frames_per_req: Sequence[int], s_start: np.ndarray, nsteps: Seque
                 p.full[r] = period > 0 and i % period == 0
                 for f in range(F):
                     g = g0 + f
+                    if per_frame_grid:
+                        own = timestep_grid(int(s[f]), n)
+                        p.tau[g] = own[i]
+                        p.active[g] = True
+                        p.newly[g] = i == 0
+                        p.c1[g], p.c2[g] = ddim_coeffs(own[i], own[i + 1], ab)
+                        p.a_ctx[g], p.b_ctx[g] = injection_coeffs(own[i], ab)
+                        if i == 0:
+                            p.a[g], p.b[g] = injection_coeffs(own[0], ab)
+                        continue
                     p.tau[g] = t
                     p.a_ctx[g], p.b_ctx[g] = injection_coeffs(t, ab)
                     if t <= s[f]:
@@ -339,6 +353,42 @@ def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048, kv_seg: O
     return out
 
 
+def attention_groups(q, k, v, heads: int, gq: np.ndarray, gk: np.ndarray):
+    """Non-causal softmax(q k^T / sqrt(d)) v per head where query row i attends
+    to the key rows j with gk[j] == gq[i] (groups need not be contiguous)."""
+    n, D = q.shape
+    d = D // heads
+    scale = 1.0 / np.sqrt(d)
+    out = np.zeros((n, D))
+    for g in np.unique(gq):
+        qi = np.flatnonzero(gq == g)
+        kj = np.flatnonzero(gk == g)
+        for h in range(heads):
+            cols = slice(h * d, (h + 1) * d)
+            s = (q[qi, cols] @ k[kj, cols].T) * scale
+            s -= s.max(axis=1, keepdims=True)
+            p = np.exp(s)
+            p /= p.sum(axis=1, keepdims=True)
+            out[qi, cols] = p @ v[kj, cols]
+    return out
+
+
+def block_attention(attn: str, l: int) -> str:
+    """Attention of block l: 'joint' over the request, or for a factorised
+    denoiser (the spatial / temporal split of the paper's denoisers, Sec. 4 and
+    Sec. 5.2) 'spatial' (same frame) in even blocks and 'temporal' (same
+    (y, x) position across the request's frames) in odd blocks."""
+    if attn == "joint":
+        return "joint"
+    return "spatial" if l % 2 == 0 else "temporal"
+
+
+def attention_group_ids(kind: str, req, f, y, x) -> np.ndarray:
+    """Group of every token for a spatial or temporal block."""
+    key = np.stack([req, f] if kind == "spatial" else [req, y, x], axis=1)
+    return np.unique(key, axis=0, return_inverse=True)[1].ravel()
+
+
 @dataclass
 class Model:
     D: int
@@ -347,11 +397,12 @@ class Model:
     L: int
     dtype: str
     weights: Dict[str, np.ndarray]
+    attention: str = "joint"
 
 
 def model_from_workload(wl) -> Model:
     m = wl.model
-    return Model(m.D, m.heads, m.mlp, m.L, m.dtype, wl.weights)
+    return Model(m.D, m.heads, m.mlp, m.L, m.dtype, wl.weights, getattr(m, "attention", "joint"))
 
 
 def conditioning(model: Model, tau: np.ndarray) -> np.ndarray:
@@ -362,7 +413,7 @@ def conditioning(model: Model, tau: np.ndarray) -> np.ndarray:
 
 def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.ndarray,
             precision: str = "model", cache: Optional[list] = None, rows: Optional[np.ndarray] = None,
-            kv_seg: Optional[np.ndarray] = None) -> np.ndarray:
+            kv_seg: Optional[np.ndarray] = None, kv_pos: Optional[tuple] = None) -> np.ndarray:
     """Noise prediction eps_hat [n][16] for packed tokens x [n][16].
 
     Tokens carry their in-request frame f, grid position (y, xx) and their
@@ -374,6 +425,11 @@ def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.
     global positions ``rows``, then the queries of segment r attend to cache
     rows kv_seg[r]..kv_seg[r+1] (all tokens of request r): fresh values for the
     forwarded tokens, the stored ones for the rest.
+
+    A factorised denoiser (model.attention == "factorised") restricts block
+    l's attention to the segment's tokens of the same frame (even l) or of the
+    same (y, x) position (odd l); with the cache, kv_pos = (f, y, x) of every
+    cached token gives the key groups.
     """
     w = model.weights
     D, H = model.D, model.heads
@@ -388,12 +444,27 @@ def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.
         a = rnd(layer_norm(h) * (1.0 + sc1) + sh1)
         qkv = linear(a, w[f"b{l}.qkv_w"], w[f"b{l}.qkv_b"])
         q, k, v = rnd(qkv[:, :D]), rnd(qkv[:, D:2 * D]), rnd(qkv[:, 2 * D:])
+        kind = block_attention(model.attention, l)
         if cache is None:
-            o = rnd(attention(q, k, v, H, seg))
+            if kind == "joint":
+                o = rnd(attention(q, k, v, H, seg))
+            else:
+                req = np.searchsorted(seg, np.arange(x.shape[0]), side="right") - 1
+                grp = attention_group_ids(kind, req, f, y, xx)
+                o = rnd(attention_groups(q, k, v, H, grp, grp))
         else:
             cache[l][0][rows] = k
             cache[l][1][rows] = v
-            o = rnd(attention(q, cache[l][0], cache[l][1], H, seg, kv_seg=kv_seg))
+            if kind == "joint":
+                o = rnd(attention(q, cache[l][0], cache[l][1], H, seg, kv_seg=kv_seg))
+            else:
+                n_all = cache[l][0].shape[0]
+                req_q = np.searchsorted(seg, np.arange(x.shape[0]), side="right") - 1
+                req_k = np.searchsorted(kv_seg, np.arange(n_all), side="right") - 1
+                both = attention_group_ids(kind, np.concatenate([req_q, req_k]), np.concatenate([f, kv_pos[0]]),
+                                           np.concatenate([y, kv_pos[1]]), np.concatenate([xx, kv_pos[2]]))
+                gq, gk = both[:x.shape[0]], both[x.shape[0]:]
+                o = rnd(attention_groups(q, cache[l][0], cache[l][1], H, gq, gk))
         h = h + (1.0 + g1) * linear(o, w[f"b{l}.o_w"], w[f"b{l}.o_b"])
         a2 = rnd(layer_norm(h) * (1.0 + sc2) + sh2)
         m = rnd(gelu_tanh(linear(a2, w[f"b{l}.fc1_w"], w[f"b{l}.fc1_b"])))
@@ -485,7 +556,7 @@ def step_cached(wl, model: Model, state: np.ndarray, plan: StepPlan, cache: list
     x = a * P[qidx] + b * E[qidx]
     seg = np.concatenate([cu_q, [nq]])
     eps_hat = denoise(model, x, info.f[qidx], info.y[qidx], info.x[qidx], plan.tau[g], seg, precision,
-                      cache=cache, rows=qidx, kv_seg=np.asarray(wl.tok_offset))
+                      cache=cache, rows=qidx, kv_seg=np.asarray(wl.tok_offset), kv_pos=(info.f, info.y, info.x))
     x_out = plan.c1[g][:, None] * x + plan.c2[g][:, None] * eps_hat
     P[qidx[w]] = x_out[w]
     return StepResult(mask, idx, cu, n, x, eps_hat, x_out, unpatchify(P, wl.requests), qidx, cu_q)
@@ -497,12 +568,12 @@ def new_cache(model: Model, n_tokens: int) -> list:
 
 
 def refine(wl, precision: str = "model", denoiser=None, trace: bool = False, steps: Optional[int] = None,
-           period: int = 0):
+           period: int = 0, per_frame_grid: bool = False):
     """Run the whole partial-denoising loop; returns the final NCHW state (float64)
     and, with trace=True, the list of per-step results.  period > 0 turns on
     the latent cache with a full step every ``period`` steps."""
     model = model_from_workload(wl)
-    plans = plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps, period)
+    plans = plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps, period, per_frame_grid)
     info = token_info(wl.requests)
     state = np.asarray(wl.z0, dtype=np.float64).copy()
     cache = new_cache(model, wl.N) if period > 0 else None

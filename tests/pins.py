@@ -26,6 +26,7 @@ import workloads as W
 
 MICRO_F32 = W.ModelCfg(D=32, heads=2, head_dim=16, mlp=64, L=2, dtype="f32")
 MICRO_BF16 = W.ModelCfg(D=32, heads=2, head_dim=16, mlp=64, L=2, dtype="bf16")
+MICRO_FACT = W.ModelCfg(D=32, heads=2, head_dim=16, mlp=64, L=3, dtype="f32", attention="factorised")
 
 
 def micro(model=MICRO_F32, requests=None, rho=None, t_start=None, nsteps=None, name="micro"):
@@ -324,7 +325,7 @@ def pin_attention_special(O):
 # ----------------------------------------------------------------------------
 # the denoiser against a torch functional rebuild
 # ----------------------------------------------------------------------------
-def torch_denoiser(O, model, x, f, y, xx, tau, seg, precision):
+def torch_denoiser(O, model, x, f, y, xx, tau, seg, precision, attention="joint"):
     import torch
     import torch.nn.functional as F
 
@@ -341,12 +342,16 @@ def torch_denoiser(O, model, x, f, y, xx, tau, seg, precision):
     allowed = torch.zeros((n, n), dtype=torch.bool)
     for r in range(len(seg) - 1):
         allowed[seg[r]:seg[r + 1], seg[r]:seg[r + 1]] = True
+    f_, y_, x_ = (torch.as_tensor(np.asarray(a)) for a in (f, y, xx))
+    same_frame = allowed & (f_[:, None] == f_[None, :])
+    same_column = allowed & (y_[:, None] == y_[None, :]) & (x_[:, None] == x_[None, :])
     for l in range(model.L):
+        mask = allowed if attention == "joint" else (same_frame if l % 2 == 0 else same_column)
         mod = F.linear(c, wt[f"b{l}.ada_w"], wt[f"b{l}.ada_b"]).chunk(6, dim=1)
         a = rnd(ln(h) * (1 + mod[1]) + mod[0])
         q, k, v = (rnd(z) for z in F.linear(a, wt[f"b{l}.qkv_w"], wt[f"b{l}.qkv_b"]).chunk(3, dim=1))
         heads = lambda z: z.reshape(n, H, d).transpose(0, 1)
-        o = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), attn_mask=allowed)
+        o = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), attn_mask=mask)
         o = rnd(o.transpose(0, 1).reshape(n, D))
         h = h + (1 + mod[2]) * F.linear(o, wt[f"b{l}.o_w"], wt[f"b{l}.o_b"])
         a2 = rnd(ln(h) * (1 + mod[4]) + mod[3])
@@ -454,7 +459,11 @@ def pin_cache_full_every_step(O):
     tokens of the request go through the plain denoiser, selected ones from the
     state (noised on the first step), the others as their clean latent noised
     to the step's level, and only the selected tokens are written back."""
-    wl = micro(model=MICRO_F32, nsteps=[3], rho=[0.35])
+    for cfg in (MICRO_F32, MICRO_FACT):
+        _cache_full_every_step(O, micro(model=cfg, nsteps=[3], rho=[0.35]))
+
+
+def _cache_full_every_step(O, wl):
     got = O.refine(wl, precision="fp64", period=1)
     model = O.model_from_workload(wl)
     info = O.token_info(wl.requests)
@@ -525,10 +534,91 @@ def pin_cache_context_matters(O):
     assert np.array_equal(M[~sel], P[~sel].astype(np.float32).astype(np.float64))
 
 
+# ----------------------------------------------------------------------------
+# factorised spatial / temporal attention and the per-frame grid reading
+# ----------------------------------------------------------------------------
+def pin_attention_groups_bruteforce(O):
+    rng = np.random.default_rng(14)
+    n, H, d = 13, 2, 3
+    q, k, v = (rng.standard_normal((n, H * d)) for _ in range(3))
+    g = rng.integers(0, 4, n)
+    got = O.attention_groups(q, k, v, H, g, g)
+    for i in range(n):
+        js = [j for j in range(n) if g[j] == g[i]]
+        for h in range(H):
+            c = slice(h * d, (h + 1) * d)
+            s = [float(q[i, c] @ k[j, c]) / math.sqrt(d) for j in js]
+            e = [math.exp(a - max(s)) for a in s]
+            ref = sum(w * v[j, c] for w, j in zip(e, js)) / sum(e)
+            assert np.abs(got[i, c] - ref).max() < 1e-12
+
+
+def pin_factorised_torch(O):
+    """A factorised denoiser (even blocks: same frame; odd blocks: same (y, x))
+    against the torch rebuild with explicit boolean masks."""
+    wl = micro(model=MICRO_FACT, requests=[W.Request(3, 8, 8), W.Request(2, 4, 8)], rho=[0.5, 0.6])
+    model = O.model_from_workload(wl)
+    assert model.attention == "factorised"
+    info = O.token_info(wl.requests)
+    rng = np.random.default_rng(5)
+    idx = np.sort(rng.choice(wl.N, 40, replace=False))
+    n0 = int((idx < wl.tok_offset[1]).sum())
+    seg = np.array([0, n0, 40])
+    x = O.patchify(wl.z0, wl.requests)[idx]
+    tau = np.where(info.req[idx] == 0, 479, 139)
+    got = O.denoise(model, x, info.f[idx], info.y[idx], info.x[idx], tau, seg, "fp64")
+    ref = torch_denoiser(O, model, x, info.f[idx], info.y[idx], info.x[idx], tau, seg, "fp64", "factorised")
+    assert np.abs(got - ref).max() < 1e-11, np.abs(got - ref).max()
+
+
+def pin_factorised_special(O):
+    """One frame: a spatial block is the joint block; a temporal block is a
+    one-token segment per position, which returns the token's own value."""
+    one_block = W.ModelCfg(D=32, heads=2, head_dim=16, mlp=64, L=1, dtype="f32", attention="factorised")
+    joint = W.ModelCfg(D=32, heads=2, head_dim=16, mlp=64, L=1, dtype="f32")
+    wl = micro(model=one_block, requests=[W.Request(1, 8, 8)])
+    wj = micro(model=joint, requests=[W.Request(1, 8, 8)])
+    info = O.token_info(wl.requests)
+    x = O.patchify(wl.z0, wl.requests)
+    tau = np.full(wl.N, 300)
+    seg = np.array([0, wl.N])
+    a = O.denoise(O.model_from_workload(wl), x, info.f, info.y, info.x, tau, seg, "fp64")
+    b = O.denoise(O.model_from_workload(wj), x, info.f, info.y, info.x, tau, seg, "fp64")
+    assert np.abs(a - b).max() < 1e-13
+    rng = np.random.default_rng(15)
+    q, k, v = (rng.standard_normal((wl.N, 32)) for _ in range(3))
+    grp = O.attention_group_ids("temporal", np.zeros(wl.N, int), info.f, info.y, info.x)
+    assert len(np.unique(grp)) == wl.N
+    assert np.abs(O.attention_groups(q, k, v, 2, grp, grp) - v).max() < 1e-14
+
+
+def pin_per_frame_grid(O):
+    """The per-frame-grid reading: every frame walks its own grid from its own
+    start, is injected once at its start, and with the true injected noise
+    returns z0."""
+    wl = micro(requests=[W.Request(4, 4, 4)], t_start=[("uniform", 0.2, 0.8)], nsteps=[5], rho=[0.6])
+    plans = O.plan_steps([4], wl.s_start, wl.nsteps, per_frame_grid=True)
+    for f in range(4):
+        own = [((5 - i) * (int(wl.s_start[f]) + 1)) // 5 - 1 for i in range(6)]
+        assert [int(p.tau[f]) for p in plans] == own[:5]
+        assert all(p.active[f] for p in plans) and [bool(p.newly[f]) for p in plans] == [True] + [False] * 4
+        assert abs(plans[0].a[f] - math.sqrt(_abar_direct(own[0]))) < 1e-15
+    den = _true_noise_denoiser(O, wl)
+    final = O.refine(wl, precision="fp64", denoiser=den, per_frame_grid=True)
+    assert np.abs(final - wl.z0).max() < 1e-9
+    same = micro(requests=[W.Request(3, 4, 4)], nsteps=[4])
+    a = O.plan_steps([3], same.s_start, same.nsteps, per_frame_grid=True)
+    b = O.plan_steps([3], same.s_start, same.nsteps)
+    for pa, pb in zip(a, b):  # one start for all frames: the two readings agree
+        for fld in ("active", "newly", "tau", "a", "b", "c1", "c2"):
+            assert np.array_equal(getattr(pa, fld), getattr(pb, fld)), fld
+
+
 ALL_PINS = [pin_alpha_bar_exact, pin_grid, pin_ddim_true_noise, pin_ddim_zero_noise, pin_alg1_active_counts,
             pin_patch_layout, pin_select_bruteforce, pin_select_threshold_count, pin_round_bf16,
             pin_layer_norm, pin_activations, pin_linear, pin_embeddings, pin_attention_bruteforce,
             pin_attention_sdpa, pin_attention_special, pin_denoiser_torch, pin_empty_mask_identity,
             pin_all_selected_dense, pin_unselected_independence, pin_packed_equals_separate,
             pin_cache_all_selected_dense, pin_cache_full_every_step, pin_cache_partial_one_block,
-            pin_cache_context_matters]
+            pin_cache_context_matters, pin_attention_groups_bruteforce, pin_factorised_torch,
+            pin_factorised_special, pin_per_frame_grid]

@@ -122,8 +122,8 @@ def _denoise_raw_gate(model, x, f, y, xx, tau, seg, precision="model", **kw):
     return _orig["denoise"](m, x, f, y, xx, tau, seg, precision, **kw)
 
 
-def _plan_always_new(frames, s_start, nsteps, period=0):
-    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+def _plan_always_new(frames, s_start, nsteps, period=0, per_frame_grid=False):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period, per_frame_grid)
     ab = O.alpha_bar()
     for p in plans:
         for g in np.flatnonzero(p.active):
@@ -164,15 +164,15 @@ def _denoise_stale(model, x, f, y, xx, tau, seg, precision, cache, rows, kv_seg)
         O.attention = orig_attention
 
 
-def _plan_no_full_after_first(frames, s_start, nsteps, period=0):
-    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+def _plan_no_full_after_first(frames, s_start, nsteps, period=0, per_frame_grid=False):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period, per_frame_grid)
     for p in plans[1:]:
         p.full[:] = False
     return plans
 
 
-def _plan_context_unnoised(frames, s_start, nsteps, period=0):
-    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+def _plan_context_unnoised(frames, s_start, nsteps, period=0, per_frame_grid=False):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period, per_frame_grid)
     for p in plans:
         p.a_ctx[:] = 1.0
         p.b_ctx[:] = 0.0
@@ -188,12 +188,31 @@ def _step_cached_writes_context(wl, model, state, plan, cache, precision="model"
     return res
 
 
-def _plan_full_at_odd_steps(frames, s_start, nsteps, period=0):
-    plans = _orig["plan_steps"](frames, s_start, nsteps, period)
+def _plan_full_at_odd_steps(frames, s_start, nsteps, period=0, per_frame_grid=False):
+    plans = _orig["plan_steps"](frames, s_start, nsteps, period, per_frame_grid)
     for i, p in enumerate(plans):
         live = p.full | (p.tau[np.cumsum([0] + list(frames))[:-1]] >= 0)
         p.full[:] = live & (period > 0) & ((i + 1) % max(period, 1) == 0)
     return plans
+
+
+def _groups_temporal_by_frame(kind, req, f, y, x):
+    return _orig["attention_group_ids"]("spatial", req, f, y, x)
+
+
+def _groups_spatial_no_request(kind, req, f, y, x):
+    if kind == "spatial":
+        return _orig["attention_group_ids"](kind, np.zeros_like(req), f, y, x)
+    return _orig["attention_group_ids"](kind, req, f, y, x)
+
+
+def _block_order_swapped(attn, l):
+    kind = _orig["block_attention"](attn, l)
+    return {"spatial": "temporal", "temporal": "spatial"}.get(kind, kind)
+
+
+def _plan_grid_shared(frames, s_start, nsteps, period=0, per_frame_grid=False):
+    return _orig["plan_steps"](frames, s_start, nsteps, period, False)
 
 
 MUTANTS = {
@@ -223,6 +242,10 @@ MUTANTS = {
     "context_not_noised": ("plan_steps", _plan_context_unnoised),
     "context_written_back": ("step_cached", _step_cached_writes_context),
     "full_step_misplaced": ("plan_steps", _plan_full_at_odd_steps),
+    "temporal_groups_by_frame": ("attention_group_ids", _groups_temporal_by_frame),
+    "spatial_groups_ignore_request": ("attention_group_ids", _groups_spatial_no_request),
+    "factorised_order_swapped": ("block_attention", _block_order_swapped),
+    "per_frame_grid_ignored": ("plan_steps", _plan_grid_shared),
 }
 
 

@@ -64,10 +64,12 @@ class ModelCfg:
     mlp: int
     L: int
     dtype: str  # "f32" or "bf16": storage/operand type of weights, latents
+    attention: str = "joint"  # "joint" or "factorised" (even blocks spatial, odd blocks temporal)
 
     def __post_init__(self):
         assert self.D == self.heads * self.head_dim
         assert self.dtype in ("f32", "bf16")
+        assert self.attention in ("joint", "factorised")
 
 
 @dataclass
