@@ -66,6 +66,20 @@ typedef enum { SPHINX_F32 = 0, SPHINX_BF16 = 1 } sphinx_dtype;
 
 typedef enum { SPHINX_LAYOUT_NCHW = 0, SPHINX_LAYOUT_TOKENS = 1 } sphinx_layout;
 
+/* Attention of the denoiser blocks.  JOINT: every block attends over the
+ * request's tokens.  FACTORISED (the spatial / temporal split of the paper's
+ * video denoisers, Sec. 4 and Sec. 5.2): even blocks attend within a frame,
+ * odd blocks across the request's frames at the same (y, x) position.  A
+ * factorised model supports at most SPHINX_MAX_REQUESTS frames in a call and
+ * 64 frames per request. */
+typedef enum { SPHINX_ATTN_JOINT = 0, SPHINX_ATTN_FACTORISED = 1 } sphinx_attention;
+
+/* Timestep grids of frames with different start indices (Alg. 1 per-frame
+ * start): SHARED walks one grid per request from the largest start and lets a
+ * frame join when the grid reaches its start; PER_FRAME walks every frame's
+ * own n-step grid from its own start, all frames active from the first step. */
+typedef enum { SPHINX_GRID_SHARED = 0, SPHINX_GRID_PER_FRAME = 1 } sphinx_grid;
+
 typedef struct {
   int32_t frames;       /* F >= 1 */
   int32_t h, w;         /* latent height and width, even, h/2 and w/2 <= 1024 */
@@ -82,6 +96,7 @@ typedef struct {
   int32_t mlp;      /* MLP hidden size */
   int32_t L;        /* number of blocks */
   sphinx_dtype dtype; /* storage and GEMM-operand type of weights/activations */
+  sphinx_attention attention; /* block attention pattern */
   const void* weights; /* dev */
 } sphinx_model_desc;
 
@@ -140,6 +155,15 @@ sphinx_status sphinx_model_param(const sphinx_model_desc* m, sphinx_param p, int
 sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int32_t* s_start /*host[G]*/,
                                const int32_t* nsteps /*host[R]*/, int32_t step, uint8_t* active,
                                uint8_t* newly, int32_t* tau, float* a, float* b, float* c1, float* c2);
+
+/* sphinx_plan_step with a choice of grid.  SPHINX_GRID_SHARED is
+ * sphinx_plan_step.  SPHINX_GRID_PER_FRAME: frame f of a live request walks
+ * tau_i = floor((n-i)(s_f+1)/n) - 1 from its own start s_f; it is active at
+ * every step i < n, newly active at i = 0 (a = sqrt(abar(s_f)), b =
+ * sqrt(1 - abar(s_f))), and its DDIM coefficients use its own tau_i, tau_{i+1}. */
+sphinx_status sphinx_plan_step_grid(const sphinx_request* reqs, int32_t R, const int32_t* s_start,
+                                    const int32_t* nsteps, int32_t step, sphinx_grid grid, uint8_t* active,
+                                    uint8_t* newly, int32_t* tau, float* a, float* b, float* c1, float* c2);
 
 /* Adaptive start steps (Sec. 5.1, Eq. 2 and the k-decision logic; Alg. 1
  * k <- K_c(r), k_min <- min(k)).  Pure host code, double precision.
@@ -261,11 +285,12 @@ sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const 
  * nsteps[r]) and step mod T = 0.  forward_all: host uint8 [G], full[r] of the
  * frame's request.  a_ctx, b_ctx: host float [G], the context coefficients
  * sqrt(abar(tau_i)), sqrt(1 - abar(tau_i)) of the request's current timestep
- * (1, 0 for a finished request), in double precision rounded to float.
- * s_start and nsteps as for sphinx_plan_step. */
+ * (1, 0 for a finished request), in double precision rounded to float;
+ * with SPHINX_GRID_PER_FRAME the frame's own tau_i.  s_start and nsteps as for
+ * sphinx_plan_step. */
 sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int32_t* s_start,
-                                const int32_t* nsteps, int32_t step, int32_t period, uint8_t* full,
-                                uint8_t* forward_all, float* a_ctx, float* b_ctx);
+                                const int32_t* nsteps, int32_t step, int32_t period, sphinx_grid grid,
+                                uint8_t* full, uint8_t* forward_all, float* a_ctx, float* b_ctx);
 
 /* Bytes of the latent cache: L blocks x N tokens x (key, value) x D elements
  * of the model dtype, laid out [L][N][2][D] (token t of block l at element

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsphinx.s
 
 F32, BF16 = 0, 1
 NCHW, TOKENS = 0, 1  # sphinx_layout
+ATTN_JOINT, ATTN_FACTORISED = 0, 1  # sphinx_attention
+GRID_SHARED, GRID_PER_FRAME = 0, 1  # sphinx_grid
 MAX_REQUESTS = 64
 STATUS_NAMES = {0: "SPHINX_OK", 1: "SPHINX_E_INVALID", 2: "SPHINX_E_UNSUPPORTED", 3: "SPHINX_E_WORKSPACE",
                 4: "SPHINX_E_HIP"}
@@ -25,6 +27,7 @@ PARAMS = ["PE_W", "PE_B", "T1_W", "T1_B", "T2_W", "T2_B", "COND_W", "COND_B", "Q
           "FC1_W", "FC1_B", "FC2_W", "FC2_B", "OUT_W", "OUT_B"]
 PARAM_ID = {n: i for i, n in enumerate(PARAMS)}
 EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_param", "sphinx_plan_step",
+            "sphinx_plan_step_grid",
             "sphinx_select_workspace_bytes", "sphinx_select_mask", "sphinx_gather", "sphinx_refine_workspace_bytes",
             "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
             "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_kv_cache_bytes", "sphinx_gather_ctx",
@@ -63,7 +66,7 @@ def make_klogic(ratio: Sequence[float], k: Sequence[int]) -> KLogic:
 
 class ModelDesc(ctypes.Structure):
     _fields_ = [("D", c_int32), ("heads", c_int32), ("head_dim", c_int32), ("mlp", c_int32), ("L", c_int32),
-                ("dtype", c_int32), ("weights", c_void_p)]
+                ("dtype", c_int32), ("attention", c_int32), ("weights", c_void_p)]
 
 
 _lib = None
@@ -84,6 +87,7 @@ def lib() -> ctypes.CDLL:
         "sphinx_model_param": (c_int32, [POINTER(ModelDesc), c_int32, c_int32, POINTER(c_size_t),
                                          POINTER(c_size_t)]),
         "sphinx_plan_step": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, P, P, P, P, P, P, P]),
+        "sphinx_plan_step_grid": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, c_int32, P, P, P, P, P, P, P]),
         "sphinx_select_workspace_bytes": (c_int32, [c_int64, POINTER(c_size_t)]),
         "sphinx_select_mask": (c_int32, [POINTER(Request), c_int32, P, P, P, P, P, P, P, P, c_size_t, P]),
         "sphinx_gather": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P, P,
@@ -97,7 +101,7 @@ def lib() -> ctypes.CDLL:
         "sphinx_timing_enable": (c_int32, [c_int32]),
         "sphinx_timing_read": (c_int32, [c_int32, POINTER(c_int64), POINTER(ctypes.c_double)]),
         "sphinx_peak_mfma": (c_int32, [c_int32, P, P]),
-        "sphinx_plan_cache": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, c_int32, P, P, P, P]),
+        "sphinx_plan_cache": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, c_int32, c_int32, P, P, P, P]),
         "sphinx_kv_cache_bytes": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, POINTER(c_size_t)]),
         "sphinx_gather_ctx": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P,
                                         P, P, P, P, P]),
@@ -158,7 +162,8 @@ def dtype_code(name: str) -> int:
 
 
 def model_desc(cfg, weights_ptr: Optional[int] = None) -> ModelDesc:
-    return ModelDesc(cfg.D, cfg.heads, cfg.head_dim, cfg.mlp, cfg.L, dtype_code(cfg.dtype), weights_ptr)
+    attn = ATTN_FACTORISED if getattr(cfg, "attention", "joint") == "factorised" else ATTN_JOINT
+    return ModelDesc(cfg.D, cfg.heads, cfg.head_dim, cfg.mlp, cfg.L, dtype_code(cfg.dtype), attn, weights_ptr)
 
 
 # ----------------------------------------------------------------------------
@@ -181,17 +186,28 @@ def sphinx_model_param(desc: ModelDesc, param: str, block: int = 0):
     return off.value, cnt.value
 
 
-def sphinx_plan_step(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int) -> Dict[str, np.ndarray]:
+def sphinx_plan_step(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int, grid: int = GRID_SHARED
+                     ) -> Dict[str, np.ndarray]:
+    """Step schedule of all frames (sphinx_plan_step_grid; the shared grid is sphinx_plan_step)."""
     G = sum(r.frames for r in reqs)
     s_start = np.ascontiguousarray(s_start, dtype=np.int32)
     nsteps = np.ascontiguousarray(nsteps, dtype=np.int32)
     out = {"active": np.zeros(G, np.uint8), "newly": np.zeros(G, np.uint8), "tau": np.zeros(G, np.int32),
            "a": np.zeros(G, np.float32), "b": np.zeros(G, np.float32), "c1": np.zeros(G, np.float32),
            "c2": np.zeros(G, np.float32)}
-    _check("sphinx_plan_step", lib().sphinx_plan_step(
-        reqs, len(reqs), _ptr(s_start), _ptr(nsteps), step, _ptr(out["active"]), _ptr(out["newly"]),
-        _ptr(out["tau"]), _ptr(out["a"]), _ptr(out["b"]), _ptr(out["c1"]), _ptr(out["c2"])))
+    if grid == GRID_SHARED:
+        _check("sphinx_plan_step", lib().sphinx_plan_step(
+            reqs, len(reqs), _ptr(s_start), _ptr(nsteps), step, _ptr(out["active"]), _ptr(out["newly"]),
+            _ptr(out["tau"]), _ptr(out["a"]), _ptr(out["b"]), _ptr(out["c1"]), _ptr(out["c2"])))
+    else:
+        _check("sphinx_plan_step_grid", lib().sphinx_plan_step_grid(
+            reqs, len(reqs), _ptr(s_start), _ptr(nsteps), step, grid, _ptr(out["active"]), _ptr(out["newly"]),
+            _ptr(out["tau"]), _ptr(out["a"]), _ptr(out["b"]), _ptr(out["c1"]), _ptr(out["c2"])))
     return out
+
+
+def sphinx_plan_step_grid(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int, grid: int) -> Dict[str, np.ndarray]:
+    return sphinx_plan_step(reqs, s_start, nsteps, step, grid)
 
 
 def sphinx_select_workspace_bytes(N: int) -> int:
@@ -268,14 +284,15 @@ def sphinx_peak_mfma(iters: int, out, stream=None):
     _check("sphinx_peak_mfma", lib().sphinx_peak_mfma(iters, _ptr(out), _stream(stream)))
 
 
-def sphinx_plan_cache(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int, period: int) -> Dict[str, np.ndarray]:
+def sphinx_plan_cache(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int, period: int,
+                      grid: int = GRID_SHARED) -> Dict[str, np.ndarray]:
     G = sum(r.frames for r in reqs)
     s_start = np.ascontiguousarray(s_start, dtype=np.int32)
     nsteps = np.ascontiguousarray(nsteps, dtype=np.int32)
     out = {"full": np.zeros(len(reqs), np.uint8), "forward_all": np.zeros(G, np.uint8),
            "a_ctx": np.zeros(G, np.float32), "b_ctx": np.zeros(G, np.float32)}
     _check("sphinx_plan_cache", lib().sphinx_plan_cache(
-        reqs, len(reqs), _ptr(s_start), _ptr(nsteps), step, period, _ptr(out["full"]), _ptr(out["forward_all"]),
+        reqs, len(reqs), _ptr(s_start), _ptr(nsteps), step, period, grid, _ptr(out["full"]), _ptr(out["forward_all"]),
         _ptr(out["a_ctx"]), _ptr(out["b_ctx"])))
     return out
 

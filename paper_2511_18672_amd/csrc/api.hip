@@ -53,6 +53,7 @@ sphinx_status check_model(const sphinx_model_desc* m) {
   if (m->D <= 0 || m->heads <= 0 || m->head_dim <= 0 || m->mlp <= 0 || m->L <= 0) return SPHINX_E_INVALID;
   if ((int64_t)m->heads * m->head_dim != m->D) return SPHINX_E_INVALID;
   if (!valid_dtype(m->dtype)) return SPHINX_E_UNSUPPORTED;
+  if (m->attention != SPHINX_ATTN_JOINT && m->attention != SPHINX_ATTN_FACTORISED) return SPHINX_E_UNSUPPORTED;
   if (m->dtype == SPHINX_BF16) {
     if ((m->head_dim != 64 && m->head_dim != 72) || m->D % 128 != 0 || m->mlp % 128 != 0 || m->D > 2048)
       return SPHINX_E_UNSUPPORTED;
@@ -117,7 +118,7 @@ Blob blob_layout(const sphinx_model_desc& m) {
 }
 
 struct RefineWs {
-  size_t fmap, utau, U, temb, cbuf, sc, mod, Ty, Tx, Tf, gframe, crow, posc, h, a, big, total;
+  size_t fmap, utau, U, temb, cbuf, sc, mod, Ty, Tx, Tf, gframe, crow, posc, fcnt, pos, h, a, big, total;
   int maxHp, maxWp, maxF;
 };
 
@@ -150,6 +151,8 @@ RefineWs refine_layout(const sphinx_model_desc& m, const ReqTable& T, int G, int
   w.gframe = take((size_t)n * 4);
   w.crow = take((size_t)n * 4);
   w.posc = take((size_t)n * 4);
+  w.fcnt = take((size_t)G * 4);           // factorised: forwarded rows per frame
+  w.pos = take((size_t)T.tok_off[T.R] * 4);  // factorised: token -> forwarded row
   w.h = take((size_t)n * D * 4);
   w.a = take((size_t)n * D * act);
   w.big = take((size_t)n * std::max<size_t>(4 * D, (size_t)m.mlp) * act);
@@ -291,33 +294,53 @@ sphinx_status sphinx_model_param(const sphinx_model_desc* m, sphinx_param p, int
   return SPHINX_E_INVALID;
 }
 
-sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int32_t* s_start, const int32_t* nsteps,
-                               int32_t step, uint8_t* active, uint8_t* newly, int32_t* tau, float* a, float* b,
-                               float* c1, float* c2) {
+sphinx_status sphinx_plan_step_grid(const sphinx_request* reqs, int32_t R, const int32_t* s_start,
+                                    const int32_t* nsteps, int32_t step, sphinx_grid grid_kind, uint8_t* active,
+                                    uint8_t* newly, int32_t* tau, float* a, float* b, float* c1, float* c2) {
   ReqTable T;
   int64_t N;
   int32_t G;
   sphinx_status st = build_table(reqs, R, &T, &N, &G);
   if (st != SPHINX_OK) return st;
   if (!s_start || !nsteps || !active || !newly || !tau || !a || !b || !c1 || !c2 || step < 0) return SPHINX_E_INVALID;
+  if (grid_kind != SPHINX_GRID_SHARED && grid_kind != SPHINX_GRID_PER_FRAME) return SPHINX_E_INVALID;
   for (int g = 0; g < G; ++g)
     if (s_start[g] < 0 || s_start[g] >= SPHINX_TRAIN_STEPS) return SPHINX_E_INVALID;
   for (int r = 0; r < R; ++r)
     if (nsteps[r] < 1) return SPHINX_E_INVALID;
   const std::vector<double> ab = alpha_bar_table();
+  auto ddim = [&](int t, int tn, double* o1, double* o2) {
+    const double ac = alpha_bar_at(ab, t), an = alpha_bar_at(ab, tn);
+    *o1 = std::sqrt(an / ac);
+    *o2 = std::sqrt(1.0 - an) - std::sqrt(an * (1.0 - ac) / ac);
+  };
   for (int r = 0; r < R; ++r) {
     const int F = T.frames[r], g0 = T.frame_off[r], n = nsteps[r];
+    const bool live = step < n;
+    if (grid_kind == SPHINX_GRID_PER_FRAME) {
+      for (int f = 0; f < F; ++f) {
+        const int g = g0 + f, s = s_start[g];
+        auto grid = [&](int i) { return (int)(((int64_t)(n - i) * (s + 1)) / n) - 1; };
+        const int t = live ? grid(step) : -1;
+        double cc1 = 1.0, cc2 = 0.0;
+        if (live) ddim(t, grid(step + 1), &cc1, &cc2);
+        const bool nw = live && step == 0;
+        active[g] = live ? 1 : 0;
+        newly[g] = nw ? 1 : 0;
+        tau[g] = t;
+        a[g] = nw ? (float)std::sqrt(alpha_bar_at(ab, t)) : 1.0f;
+        b[g] = nw ? (float)std::sqrt(1.0 - alpha_bar_at(ab, t)) : 0.0f;
+        c1[g] = (float)cc1;
+        c2[g] = (float)cc2;
+      }
+      continue;
+    }
     int smax = 0;
     for (int f = 0; f < F; ++f) smax = std::max(smax, s_start[g0 + f]);
     auto grid = [&](int i) { return (int)(((int64_t)(n - i) * (smax + 1)) / n) - 1; };
-    const bool live = step < n;
     const int t = live ? grid(step) : -1;
     double cc1 = 1.0, cc2 = 0.0;
-    if (live) {
-      const double ac = alpha_bar_at(ab, t), an = alpha_bar_at(ab, grid(step + 1));
-      cc1 = std::sqrt(an / ac);
-      cc2 = std::sqrt(1.0 - an) - std::sqrt(an * (1.0 - ac) / ac);
-    }
+    if (live) ddim(t, grid(step + 1), &cc1, &cc2);
     for (int f = 0; f < F; ++f) {
       const int g = g0 + f;
       const bool act = live && t <= s_start[g];
@@ -334,9 +357,16 @@ sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int3
   return SPHINX_OK;
 }
 
+sphinx_status sphinx_plan_step(const sphinx_request* reqs, int32_t R, const int32_t* s_start, const int32_t* nsteps,
+                               int32_t step, uint8_t* active, uint8_t* newly, int32_t* tau, float* a, float* b,
+                               float* c1, float* c2) {
+  return sphinx_plan_step_grid(reqs, R, s_start, nsteps, step, SPHINX_GRID_SHARED, active, newly, tau, a, b, c1,
+                               c2);
+}
+
 sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int32_t* s_start, const int32_t* nsteps,
-                                int32_t step, int32_t period, uint8_t* full, uint8_t* forward_all, float* a_ctx,
-                                float* b_ctx) {
+                                int32_t step, int32_t period, sphinx_grid grid_kind, uint8_t* full,
+                                uint8_t* forward_all, float* a_ctx, float* b_ctx) {
   ReqTable T;
   int64_t N;
   int32_t G;
@@ -344,6 +374,7 @@ sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int
   if (st != SPHINX_OK) return st;
   if (!s_start || !nsteps || !full || !forward_all || !a_ctx || !b_ctx || step < 0 || period < 1)
     return SPHINX_E_INVALID;
+  if (grid_kind != SPHINX_GRID_SHARED && grid_kind != SPHINX_GRID_PER_FRAME) return SPHINX_E_INVALID;
   for (int g = 0; g < G; ++g)
     if (s_start[g] < 0 || s_start[g] >= SPHINX_TRAIN_STEPS) return SPHINX_E_INVALID;
   for (int r = 0; r < R; ++r)
@@ -358,9 +389,13 @@ sphinx_status sphinx_plan_cache(const sphinx_request* reqs, int32_t R, const int
     full[r] = (live && step % period == 0) ? 1 : 0;
     for (int f = 0; f < F; ++f) {
       const int g = g0 + f;
+      // the frame's own timestep on a per-frame grid
+      const int tf = (grid_kind == SPHINX_GRID_PER_FRAME && live)
+                         ? (int)(((int64_t)(n - step) * (s_start[g] + 1)) / n) - 1
+                         : t;
       forward_all[g] = full[r];
-      a_ctx[g] = live ? (float)std::sqrt(alpha_bar_at(ab, t)) : 1.0f;
-      b_ctx[g] = live ? (float)std::sqrt(1.0 - alpha_bar_at(ab, t)) : 0.0f;
+      a_ctx[g] = live ? (float)std::sqrt(alpha_bar_at(ab, tf)) : 1.0f;
+      b_ctx[g] = live ? (float)std::sqrt(1.0 - alpha_bar_at(ab, tf)) : 0.0f;
     }
   }
   return SPHINX_OK;
@@ -541,6 +576,12 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
   if (!aligned(idx, 16) || !aligned(x_sel, 16) || !aligned(ws, 256) || !aligned(m->weights, 256))
     return SPHINX_E_INVALID;
   if (kv_cache != nullptr && !aligned(kv_cache, 16)) return SPHINX_E_INVALID;
+  const bool factorised = m->attention == SPHINX_ATTN_FACTORISED;
+  if (factorised) {
+    if (G > SPHINX_MAX_REQUESTS) return SPHINX_E_UNSUPPORTED;
+    for (int r = 0; r < R; ++r)
+      if (T.frames[r] > 64) return SPHINX_E_UNSUPPORTED;
+  }
   const RefineWs W = refine_layout(*m, T, G, n_sel);
   if (ws_bytes < W.total) return SPHINX_E_WORKSPACE;
   const bool cached = kv_cache != nullptr;
@@ -585,6 +626,45 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
   void* obuf = base + W.big + (size_t)n * 3 * D * esize(dt);
   void* mbuf = base + W.big;
 
+  // factorised: frame segments (host copy of the per-frame counts: one stream
+  // synchronisation) and the token -> row map of the temporal blocks
+  SegTable Sf;
+  std::memset(&Sf, 0, sizeof(Sf));
+  if (factorised) {
+    std::vector<int32_t> cnt(G);
+    SPHINX_TRY(launch_frame_counts(T, idx, n, G, I32(W.fcnt), s));
+    SPHINX_TRY(hipMemcpyAsync(cnt.data(), I32(W.fcnt), (size_t)G * 4, hipMemcpyDeviceToHost, s));
+    SPHINX_TRY(hipStreamSynchronize(s));
+    SPHINX_TRY(launch_pos_map(N, idx, n, I32(W.pos), s));
+    std::vector<int> frames;
+    std::vector<int> fstart(G);
+    int run = 0;
+    for (int g = 0; g < G; ++g) {
+      fstart[g] = run;
+      run += cnt[g];
+      if (cnt[g] > 0) frames.push_back(g);
+    }
+    if (run != n) return SPHINX_E_INVALID;  // an idx outside [0, N): rejected before any further launch
+    auto frame_keys = [&](int g) {
+      int r = 0;
+      while (r + 1 < R && T.frame_off[r + 1] <= g) ++r;
+      return cached ? (T.h[r] / 2) * (T.w[r] / 2) : cnt[g];
+    };
+    std::stable_sort(frames.begin(), frames.end(), [&](int x, int y) { return frame_keys(x) > frame_keys(y); });
+    Sf.nseg = (int)frames.size();
+    for (int i = 0; i < Sf.nseg; ++i) {
+      const int g = frames[i];
+      int r = 0;
+      while (r + 1 < R && T.frame_off[r + 1] <= g) ++r;
+      const int tpf = (T.h[r] / 2) * (T.w[r] / 2);
+      Sf.start[i] = fstart[g];
+      Sf.len[i] = cnt[g];
+      Sf.kv_start[i] = cached ? (int)(T.tok_off[r] + (int64_t)(g - T.frame_off[r]) * tpf) : fstart[g];
+      Sf.kv_len[i] = cached ? tpf : cnt[g];
+      Sf.tile_prefix[i + 1] = Sf.tile_prefix[i] + (Sf.len[i] + kAttnQueryTile - 1) / kAttnQueryTile;
+    }
+  }
+
   // conditioning: one row per run of frames with equal timestep
   {
   Bracket br(SPHINX_K_COND, s);
@@ -620,14 +700,19 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
     if (cached) {
       unsigned char* cl = static_cast<unsigned char*>(kv_cache) + (size_t)l * (size_t)N * 2 * D * esize(dt);
       Bracket br(SPHINX_K_KV_STORE, s);
-      SPHINX_TRY(launch_kv_store(dt, qkv, n, D, idx, cl, s));
+      SPHINX_TRY(launch_kv_store(dt, qkv, n, D, idx, N, cl, s));
       io.k = cl;
       io.v = cl + (size_t)D * esize(dt);
       io.ldkv = 2 * D;
     }
     {
       Bracket br(SPHINX_K_ATTENTION, s);
-      SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, S, s));
+      if (!factorised)
+        SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, S, s));
+      else if (l % 2 == 0)  // spatial: within the frame
+        SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, Sf, s));
+      else  // temporal: across the request's frames at the same position
+        SPHINX_TRY(launch_attn_temporal(dt, T, io, D, m->heads, m->head_dim, I32(W.pos), cached, s));
     }
     {
       Bracket br(SPHINX_K_GEMM_OUT, s);

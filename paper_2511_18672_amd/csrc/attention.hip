@@ -749,3 +749,106 @@ hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads,
 }
 
 }  // namespace sphinx
+
+// ---------------------------------------------------------------------------
+// Temporal attention of a factorised denoiser: the forwarded tokens at one
+// (y, x) position of a request attend to each other across frames (to all of
+// the request's frames at that position through the latent cache).  A column
+// holds at most 64 tokens, so this is a few dot products per query: one
+// workgroup per column, one wave per head, one lane per query, fp32 math with
+// an online softmax.  The keys and values of a column are read once per head
+// (every lane reads the same row).
+// ---------------------------------------------------------------------------
+namespace sphinx {
+namespace {
+constexpr int kTempMaxD = 72;
+
+template <typename T>
+__device__ __forceinline__ float ld_el(const T* p) {
+  return (float)*p;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, int D, int d, int heads, float scale,
+                                                       const int32_t* __restrict__ pos, int cached) {
+  __shared__ int rows[64];   // forwarded row of each query member
+  __shared__ int krows[64];  // key rows (qkv rows, or cache token rows)
+  __shared__ int nq_s, nk_s;
+  // column -> request and in-frame position
+  int c = (int)blockIdx.x, r = 0;
+  for (;; ++r) {
+    const int cols = (RT.h[r] >> 1) * (RT.w[r] >> 1);
+    if (c < cols || r + 1 == RT.R) break;
+    c -= cols;
+  }
+  const int F = RT.frames[r];
+  const int64_t tpf = (int64_t)(RT.h[r] >> 1) * (RT.w[r] >> 1);
+  if (threadIdx.x == 0) {
+    int nq = 0, nk = 0;
+    for (int f = 0; f < F; ++f) {
+      const int64_t t = RT.tok_off[r] + f * tpf + c;
+      const int p = pos[t];
+      if (p >= 0) rows[nq++] = p;
+      if (cached)
+        krows[nk++] = (int)t;
+      else if (p >= 0)
+        krows[nk++] = p;
+    }
+    nq_s = nq;
+    nk_s = nk;
+  }
+  __syncthreads();
+  const int nq = nq_s, nk = nk_s;
+  if (nq == 0) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const T* Q = static_cast<const T*>(io.q);
+  const T* K = static_cast<const T*>(io.k);
+  const T* V = static_cast<const T*>(io.v);
+  T* O = static_cast<T*>(io.o);
+  for (int h = wave; h < heads; h += 4) {
+    if (lane >= nq) continue;
+    const int qr = rows[lane];
+    float q[kTempMaxD], acc[kTempMaxD];
+#pragma unroll
+    for (int e = 0; e < kTempMaxD; ++e) {
+      q[e] = e < d ? ld_el(Q + (int64_t)qr * io.ldq + h * d + e) * scale : 0.0f;
+      acc[e] = 0.0f;
+    }
+    float m = -INFINITY, l = 0.0f;
+    for (int j = 0; j < nk; ++j) {
+      const T* kr = K + (int64_t)krows[j] * io.ldkv + h * d;
+      const T* vr = V + (int64_t)krows[j] * io.ldkv + h * d;
+      float sc = 0.0f;
+#pragma unroll
+      for (int e = 0; e < kTempMaxD; ++e)
+        if (e < d) sc = fmaf(q[e], ld_el(kr + e), sc);
+      const float mn = fmaxf(m, sc);
+      const float corr = __expf(m - mn), p = __expf(sc - mn);
+      l = fmaf(l, corr, p);
+#pragma unroll
+      for (int e = 0; e < kTempMaxD; ++e)
+        if (e < d) acc[e] = fmaf(acc[e], corr, p * ld_el(vr + e));
+      m = mn;
+    }
+    const float inv = 1.0f / l;
+    T* orow = O + (int64_t)qr * D + h * d;
+#pragma unroll
+    for (int e = 0; e < kTempMaxD; ++e)
+      if (e < d) orow[e] = (T)(acc[e] * inv);
+  }
+}
+}  // namespace
+
+hipError_t launch_attn_temporal(sphinx_dtype dt, const ReqTable& T, const AttnIO& io, int D, int heads,
+                                int head_dim, const int32_t* pos, bool cached, hipStream_t s) {
+  int64_t cols = 0;
+  for (int r = 0; r < T.R; ++r) cols += (int64_t)(T.h[r] >> 1) * (T.w[r] >> 1);
+  const float scale = 1.0f / sqrtf((float)head_dim);
+  if (dt == SPHINX_BF16)
+    k_attn_temporal<bf16><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cached ? 1 : 0);
+  else
+    k_attn_temporal<float><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cached ? 1 : 0);
+  return hipGetLastError();
+}
+
+}  // namespace sphinx

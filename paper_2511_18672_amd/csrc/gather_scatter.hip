@@ -178,13 +178,16 @@ __global__ __launch_bounds__(kTPB) void k_scatter_tok(int64_t N, const float* __
 // Latent cache store: row j of qkv, columns [D, 3D) (key then value), to row
 // idx[j] of the cache, 16 bytes per thread.
 __global__ __launch_bounds__(kTPB) void k_kv_store(const uint4* __restrict__ qkv, int n, int row_chunks,
-                                                   const int32_t* __restrict__ idx, uint4* __restrict__ cache) {
+                                                   const int32_t* __restrict__ idx, int64_t N,
+                                                   uint4* __restrict__ cache) {
   // row_chunks = 16-byte chunks in D elements; a qkv row has 3, a cache row 2
   const int64_t c = (int64_t)blockIdx.x * kTPB + threadIdx.x;
   const int per = 2 * row_chunks;
   if (c >= (int64_t)n * per) return;
   const int j = (int)(c / per), k = (int)(c - (int64_t)j * per);
-  cache[(int64_t)idx[j] * per + k] = qkv[(int64_t)j * 3 * row_chunks + row_chunks + k];
+  const int32_t t = idx[j];
+  if (t < 0 || t >= N) return;  // out-of-range index: nothing is stored
+  cache[(int64_t)t * per + k] = qkv[(int64_t)j * 3 * row_chunks + row_chunks + k];
 }
 
 // Same-layout f32 copy: four 16-byte non-temporal loads in flight per thread,
@@ -297,10 +300,10 @@ hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx,
   return hipGetLastError();
 }
 
-hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const int32_t* idx, void* cache,
-                           hipStream_t s) {
+hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const int32_t* idx, int64_t N,
+                           void* cache, hipStream_t s) {
   const int row_chunks = D * (dt == SPHINX_BF16 ? 2 : 4) / 16;
-  k_kv_store<<<grid_for((int64_t)n * 2 * row_chunks), kTPB, 0, s>>>((const uint4*)qkv, n, row_chunks, idx,
+  k_kv_store<<<grid_for((int64_t)n * 2 * row_chunks), kTPB, 0, s>>>((const uint4*)qkv, n, row_chunks, idx, N,
                                                                      (uint4*)cache);
   return hipGetLastError();
 }

@@ -64,8 +64,8 @@ hipError_t launch_scatter(const ReqTable& T, const float* x, const int32_t* idx,
                           void* out, sphinx_dtype odt, sphinx_layout lay, hipStream_t s);
 // Latent cache store: cache row idx[j] (2D elements: key then value) <- qkv row j
 // columns [D, 3D).
-hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const int32_t* idx, void* cache,
-                           hipStream_t s);
+hipError_t launch_kv_store(sphinx_dtype dt, const void* qkv, int n, int D, const int32_t* idx, int64_t N,
+                           void* cache, hipStream_t s);
 hipError_t launch_convert(const ReqTable& T, const void* in, sphinx_dtype idt, sphinx_layout il, void* out,
                           sphinx_dtype odt, sphinx_layout ol, hipStream_t s);
 
@@ -105,5 +105,13 @@ hipError_t launch_peak_mfma(int iters, float* out, int blocks, hipStream_t s);
 // attention.hip
 hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,
                             const SegTable& S, hipStream_t s);
+// Temporal attention of a factorised denoiser: pos[t] = forwarded row of token t
+// or -1; keys are the forwarded tokens of the column (or all of its frames from
+// the cache when `cached`).  Frames per request <= 64.
+hipError_t launch_attn_temporal(sphinx_dtype dt, const ReqTable& T, const AttnIO& io, int D, int heads,
+                                int head_dim, const int32_t* pos, bool cached, hipStream_t s);
+// Per-frame counts of the forwarded rows and the token -> row map (rowwise.hip).
+hipError_t launch_frame_counts(const ReqTable& T, const int32_t* idx, int n, int G, int32_t* cnt, hipStream_t s);
+hipError_t launch_pos_map(int64_t N, const int32_t* idx, int n, int32_t* pos, hipStream_t s);
 
 }  // namespace sphinx

@@ -259,4 +259,41 @@ hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm,
   return hipGetLastError();
 }
 
+// Forwarded rows per frame (the spatial segments of a factorised denoiser):
+// cnt[g] = number of rows j with frame(idx[j]) = g.  Integer atomics, so the
+// counts are exact whatever the order.
+__global__ __launch_bounds__(256) void k_zero_i32(int32_t* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+__global__ __launch_bounds__(256) void k_frame_counts(ReqTable T, const int32_t* __restrict__ idx, int n,
+                                                      int32_t* __restrict__ cnt) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= n) return;
+  const int32_t t = idx[j];
+  if (t >= 0 && t < T.tok_off[T.R]) atomicAdd(&cnt[frame_of_token(T, t)], 1);  // others are not counted
+}
+// Token -> forwarded row map: pos[t] = j for t = idx[j], -1 elsewhere.
+__global__ __launch_bounds__(256) void k_fill_neg(int32_t* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = -1;
+}
+__global__ __launch_bounds__(256) void k_pos_scatter(const int32_t* __restrict__ idx, int n, int64_t N,
+                                                     int32_t* __restrict__ pos) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < n && idx[j] >= 0 && idx[j] < N) pos[idx[j]] = j;
+}
+
+hipError_t launch_frame_counts(const ReqTable& T, const int32_t* idx, int n, int G, int32_t* cnt, hipStream_t s) {
+  k_zero_i32<<<(unsigned)((G + 255) / 256), 256, 0, s>>>(cnt, G);
+  k_frame_counts<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(T, idx, n, cnt);
+  return hipGetLastError();
+}
+
+hipError_t launch_pos_map(int64_t N, const int32_t* idx, int n, int32_t* pos, hipStream_t s) {
+  k_fill_neg<<<(unsigned)((N + 255) / 256), 256, 0, s>>>(pos, N);
+  k_pos_scatter<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(idx, n, N, pos);
+  return hipGetLastError();
+}
+
 }  // namespace sphinx

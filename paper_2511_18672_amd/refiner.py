@@ -69,7 +69,8 @@ class Refiner:
 
     def __init__(self, requests: Sequence, cfg, blob: torch.Tensor, s_start: np.ndarray, nsteps: np.ndarray,
                  u: np.ndarray, thr: np.ndarray, z0: np.ndarray, eps: np.ndarray, device="cuda",
-                 max_sel: Optional[int] = None, layout: int = B.TOKENS, cache_period: int = 0):
+                 max_sel: Optional[int] = None, layout: int = B.TOKENS, cache_period: int = 0,
+                 per_frame_grid: bool = False):
         if not torch.cuda.is_available():
             raise RuntimeError("Refiner needs a GPU: the selective-refinement step has no CPU path")
         B.lib()
@@ -111,7 +112,8 @@ class Refiner:
         self.ws = torch.empty(B.sphinx_refine_workspace_bytes(self.desc, self.reqs, self.max_sel),
                               dtype=torch.uint8, device=dev)
         self.total_steps = int(np.max(nsteps))
-        plans = [B.sphinx_plan_step(self.reqs, s_start, nsteps, i) for i in range(self.total_steps)]
+        self.grid = B.GRID_PER_FRAME if per_frame_grid else B.GRID_SHARED
+        plans = [B.sphinx_plan_step(self.reqs, s_start, nsteps, i, self.grid) for i in range(self.total_steps)]
         self.plan_host = {k: np.stack([p[k] for p in plans]) for k in plans[0]}
         self.plan = {k: torch.from_numpy(v).to(dev) for k, v in self.plan_host.items()}
         self._pending = None  # (step index, slot) of a selection already enqueued
@@ -125,7 +127,7 @@ class Refiner:
             if self.max_sel != self.N:
                 raise ValueError("the latent cache forwards every token on full steps: max_sel must be N")
             self.kv_cache = torch.zeros(B.sphinx_kv_cache_bytes(self.desc, self.reqs), dtype=torch.uint8, device=dev)
-            cplans = [B.sphinx_plan_cache(self.reqs, s_start, nsteps, i, self.cache_period)
+            cplans = [B.sphinx_plan_cache(self.reqs, s_start, nsteps, i, self.cache_period, self.grid)
                       for i in range(self.total_steps)]
             self.cache_host = {k: np.stack([p[k] for p in cplans]) for k in cplans[0]}
             self.cache_plan = {k: torch.from_numpy(v).to(dev) for k, v in self.cache_host.items()}

@@ -145,6 +145,44 @@ def test_blob_layout(L, cfg):
     assert sum((b - a) // esz for a, b in spans) == expect
 
 
+@pytest.mark.parametrize("name", ["frame_region", "batched"])
+def test_plan_per_frame_grid_matches_oracle(L, name):
+    """The per-frame-grid reading of per-frame starts (every frame on its own grid)."""
+    import oracle as O
+
+    wl = W.CONFIGS[name](with_weights=False)
+    reqs = S.make_requests(wl.requests)
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps, per_frame_grid=True)
+    for i, p in enumerate(plans):
+        q = S.sphinx_plan_step_grid(reqs, wl.s_start, wl.nsteps, i, S.GRID_PER_FRAME)
+        assert np.array_equal(q["active"].astype(bool), p.active), i
+        assert np.array_equal(q["newly"].astype(bool), p.newly), i
+        assert np.array_equal(q["tau"], p.tau), i
+        for k in ("a", "b", "c1", "c2"):
+            ref = getattr(p, k).astype(np.float32)
+            assert np.array_equal(q[k], ref) or np.abs(q[k] - ref).max() <= 2 * np.spacing(np.abs(ref)).max(), (i, k)
+        c = S.sphinx_plan_cache(reqs, wl.s_start, wl.nsteps, i, 3, S.GRID_PER_FRAME)
+        assert np.array_equal(c["full"].astype(bool), np.array([i % 3 == 0 and i < n for n in wl.nsteps]))
+        for k in ("a_ctx", "b_ctx"):
+            ref = getattr(p, k).astype(np.float32)
+            assert np.abs(c[k] - ref).max() <= 2 * np.spacing(np.abs(ref)).max() + 0.0, (i, k)
+
+
+def test_attention_mode_validation(L):
+    out = ctypes.c_size_t()
+    d = S.model_desc(W.SMALL_MODEL, 256)
+    d.attention = 2
+    assert L.sphinx_model_blob_bytes(ctypes.byref(d), ctypes.byref(out)) == UNSUPPORTED
+    d.attention = 1
+    assert L.sphinx_model_blob_bytes(ctypes.byref(d), ctypes.byref(out)) == OK
+    # a factorised model takes at most 64 frames per call and 64 frames per request
+    P = ctypes.c_void_p
+    many = _reqs([(65, 4, 4)])
+    cu = (ctypes.c_int32 * 2)(0, 3)
+    assert L.sphinx_refine_step(ctypes.byref(d), many, 1, P(256), 3, cu, P(256), P(256), P(256), P(256), P(256),
+                                1 << 30, None) == UNSUPPORTED
+
+
 @pytest.mark.parametrize("name", ["tiny", "small", "headline", "frame_region", "batched"])
 def test_plan_matches_oracle(L, name):
     import oracle as O
