@@ -51,6 +51,10 @@ def parse():
     ap.add_argument("--layout", default="tokens", choices=["tokens", "nchw"],
                     help="layout of the fp32 state of record and the noise")
     ap.add_argument("--sweep-log2", default="20,22,24,26", help="token counts of the sweep (log2)")
+    ap.add_argument("--attention", default="joint", choices=["joint", "factorised"],
+                    help="denoiser attention: joint over the request, or spatial/temporal in alternating blocks")
+    ap.add_argument("--per-frame-grid", action="store_true",
+                    help="every frame on its own timestep grid from its own start (other reading of per-frame starts)")
     ap.add_argument("--cache-period", type=int, default=0,
                     help="latent cache with a full step every T steps (0: off, the default workload)")
     ap.add_argument("--select-every-step", type=int, default=1,
@@ -353,13 +357,19 @@ def main():
     import workloads as W
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    import dataclasses
+
+    kw = {}
+    if args.attention != "joint":
+        base = W.XL_MODEL if args.config == "frame_region" else W.HEADLINE_MODEL
+        kw["model"] = dataclasses.replace(base, attention=args.attention)
     if args.config == "headline":
-        wl = W.headline(rho=args.rho) if args.rho is not None else W.headline()
+        wl = W.headline(rho=args.rho, **kw) if args.rho is not None else W.headline(**kw)
     else:
-        wl = W.CONFIGS[args.config]()
+        wl = W.CONFIGS[args.config](**kw)
     t_setup = time.perf_counter()
     R = S.from_workload(wl, layout=S.TOKENS if args.layout == "tokens" else S.NCHW,
-                        cache_period=args.cache_period)
+                        cache_period=args.cache_period, per_frame_grid=args.per_frame_grid)
     R.reset()
     stream = torch.cuda.current_stream()
     D, L, mlp = wl.model.D, wl.model.L, wl.model.mlp
@@ -398,6 +408,15 @@ def main():
     cu = R.cu_host
     seg = np.diff(cu).astype(np.float64)
     attn_flop = 4.0 * D * float((seg ** 2).sum())
+    if args.attention == "factorised":  # spatial (per frame) and temporal (per position) launches alternate
+        idx = R.idx[:n].cpu().numpy().astype(np.int64)
+        toff = np.asarray(wl.tok_offset)
+        r_of = np.searchsorted(toff, idx, side="right") - 1
+        tpf = np.array([q.hp * q.wp for q in wl.requests])[r_of]
+        loc = idx - toff[r_of]
+        frame_cnt = np.unique(np.stack([r_of, loc // tpf], 1), axis=0, return_counts=True)[1].astype(np.float64)
+        col_cnt = np.unique(np.stack([r_of, loc % tpf], 1), axis=0, return_counts=True)[1].astype(np.float64)
+        attn_flop = 4.0 * D * float((frame_cnt ** 2).sum() + (col_cnt ** 2).sum()) / 2.0
     if args.cache_period > 0:  # launches differ between full and partial steps: average FLOPs per launch
         attn_flop = attn_flop_timed * L / attn_timing[0]
     gemm_flop = {"gemm_qkv": 2.0 * n * D * 3 * D, "gemm_out": 2.0 * n * D * D, "gemm_mlp1": 2.0 * n * D * mlp,
@@ -418,7 +437,8 @@ def main():
     achieved = attn_flop / avg_s / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_entry("attention", args.config) if args.cache_period == 0 else None,
-                "kernel": "k_attn_bf16_dma (varlen flash attention, head_dim 64)",
+                "kernel": "k_attn_bf16_dma (varlen flash attention, head_dim 64)" if args.attention == "joint"
+                else "attention class: k_attn_bf16_dma per frame and k_attn_temporal per position, alternating",
                 "algorithmic_flop_per_launch": attn_flop}
     step_flop = L * (attn_flop + sum(gemm_flop.values()))
     mfma_util = step_flop / (ms_per_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12)
@@ -431,7 +451,8 @@ def main():
                                   f"D{D} H{wl.model.heads}x{wl.model.head_dim} L{L} MLP{mlp}, "
                                   f"{int(wl.max_steps)}-step DDIM schedule",
                       "selected_tokens": int(n), "tokens": int(wl.N), "select_every_step": force,
-                      "state_layout": args.layout, "cache_period": args.cache_period},
+                      "state_layout": args.layout, "cache_period": args.cache_period,
+                      "attention": args.attention, "per_frame_grid": args.per_frame_grid},
            "mfma_util_step": round(mfma_util, 4),
            "roofline": roofline, "kernels": kernels,
            "kernels_note": f"per-class HIP-event averages from {n_breakdown} further untimed steps; "

@@ -71,7 +71,10 @@ typedef enum { SPHINX_LAYOUT_NCHW = 0, SPHINX_LAYOUT_TOKENS = 1 } sphinx_layout;
  * video denoisers, Sec. 4 and Sec. 5.2): even blocks attend within a frame,
  * odd blocks across the request's frames at the same (y, x) position.  A
  * factorised model supports at most SPHINX_MAX_REQUESTS frames in a call and
- * 64 frames per request. */
+ * 64 frames per request (fp32 models: head_dim a multiple of 4).  Its spatial
+ * blocks need the forwarded rows per frame on the host: a refine call on a
+ * factorised model synchronizes its stream once to read them, and requires
+ * idx in ascending order (as sphinx_select_mask produces). */
 typedef enum { SPHINX_ATTN_JOINT = 0, SPHINX_ATTN_FACTORISED = 1 } sphinx_attention;
 
 /* Timestep grids of frames with different start indices (Alg. 1 per-frame

@@ -579,6 +579,7 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
   const bool factorised = m->attention == SPHINX_ATTN_FACTORISED;
   if (factorised) {
     if (G > SPHINX_MAX_REQUESTS) return SPHINX_E_UNSUPPORTED;
+    if (m->dtype == SPHINX_F32 && m->head_dim % 4 != 0) return SPHINX_E_UNSUPPORTED;  // 16-byte head rows
     for (int r = 0; r < R; ++r)
       if (T.frames[r] > 64) return SPHINX_E_UNSUPPORTED;
   }

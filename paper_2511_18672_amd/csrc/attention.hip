@@ -755,26 +755,49 @@ hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads,
 // (y, x) position of a request attend to each other across frames (to all of
 // the request's frames at that position through the latent cache).  A column
 // holds at most 64 tokens, so this is a few dot products per query: one
-// workgroup per column, one wave per head, one lane per query, fp32 math with
-// an online softmax.  The keys and values of a column are read once per head
-// (every lane reads the same row).
+// workgroup per column (members found with one ballot), one wave per head,
+// one lane per query.  Each wave stages its head's key and value rows in LDS
+// in chunks with 16-byte loads; the lanes then read them as broadcasts.  fp32
+// math with an online softmax.
 // ---------------------------------------------------------------------------
 namespace sphinx {
 namespace {
-constexpr int kTempMaxD = 72;
 
 template <typename T>
-__device__ __forceinline__ float ld_el(const T* p) {
-  return (float)*p;
-}
+struct TempVec;  // 16 bytes of a row as floats
+template <>
+struct TempVec<bf16> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void get(const bf16* p, float* o) {
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = (float)v[i];
+  }
+};
+template <>
+struct TempVec<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void get(const float* p, float* o) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = v[i];
+  }
+};
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, int D, int d, int heads, float scale,
-                                                       const int32_t* __restrict__ pos, int cached) {
-  __shared__ int rows[64];   // forwarded row of each query member
-  __shared__ int krows[64];  // key rows (qkv rows, or cache token rows)
+// HD: the head dimension when EXACT, else an upper bound with the runtime d
+// (fp32 models); a multiple of the 16-byte vector.
+template <typename T, int HD, bool EXACT>
+__global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, int D, int d_rt, int heads,
+                                                       float scale, const int32_t* __restrict__ pos, int cached) {
+  constexpr int VN = TempVec<T>::N;             // elements per 16-byte vector
+  constexpr int NV = HD / VN;                   // vectors per head row (upper bound)
+  constexpr int KC = sizeof(T) == 2 ? 32 : 16;  // keys per staged chunk
+  const int d = EXACT ? HD : d_rt;
+  const int vpr = EXACT ? NV : d_rt / VN;
+  __shared__ int rows[64];                    // forwarded row of each query member
+  __shared__ int krows[64];                   // key rows (qkv rows, or cache token rows)
   __shared__ int nq_s, nk_s;
-  // column -> request and in-frame position
+  __shared__ __attribute__((aligned(16))) T stage[4][2][KC * HD];
   int c = (int)blockIdx.x, r = 0;
   for (;; ++r) {
     const int cols = (RT.h[r] >> 1) * (RT.w[r] >> 1);
@@ -783,71 +806,116 @@ __global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, i
   }
   const int F = RT.frames[r];
   const int64_t tpf = (int64_t)(RT.h[r] >> 1) * (RT.w[r] >> 1);
-  if (threadIdx.x == 0) {
-    int nq = 0, nk = 0;
-    for (int f = 0; f < F; ++f) {
-      const int64_t t = RT.tok_off[r] + f * tpf + c;
-      const int p = pos[t];
-      if (p >= 0) rows[nq++] = p;
-      if (cached)
-        krows[nk++] = (int)t;
-      else if (p >= 0)
-        krows[nk++] = p;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (wave == 0) {  // members of the column in frame order
+    int p = -1;
+    int64_t t = 0;
+    if (lane < F) {
+      t = RT.tok_off[r] + lane * tpf + c;
+      p = pos[t];
     }
-    nq_s = nq;
-    nk_s = nk;
+    const uint64_t bq = __ballot(p >= 0);
+    const int iq = __popcll(bq & ((1ull << lane) - 1ull));
+    if (p >= 0) rows[iq] = p;
+    if (cached) {
+      if (lane < F) krows[lane] = (int)t;
+    } else if (p >= 0) {
+      krows[iq] = p;
+    }
+    if (lane == 0) {
+      nq_s = __popcll(bq);
+      nk_s = cached ? F : __popcll(bq);
+    }
   }
   __syncthreads();
   const int nq = nq_s, nk = nk_s;
   if (nq == 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const T* Q = static_cast<const T*>(io.q);
   const T* K = static_cast<const T*>(io.k);
   const T* V = static_cast<const T*>(io.v);
   T* O = static_cast<T*>(io.o);
+  T* sk = stage[wave][0];
+  T* sv = stage[wave][1];
   for (int h = wave; h < heads; h += 4) {
-    if (lane >= nq) continue;
-    const int qr = rows[lane];
-    float q[kTempMaxD], acc[kTempMaxD];
+    float q[HD], acc[HD];
+    const bool mine = lane < nq;
+    const int qr = mine ? rows[lane] : rows[0];
 #pragma unroll
-    for (int e = 0; e < kTempMaxD; ++e) {
-      q[e] = e < d ? ld_el(Q + (int64_t)qr * io.ldq + h * d + e) * scale : 0.0f;
+    for (int v = 0; v < NV; ++v) {
+      if (EXACT || v < vpr) TempVec<T>::get(Q + (int64_t)qr * io.ldq + h * d + v * VN, q + v * VN);
+      else
+#pragma unroll
+        for (int i = 0; i < VN; ++i) q[v * VN + i] = 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < HD; ++e) {
+      q[e] *= scale;
       acc[e] = 0.0f;
     }
     float m = -INFINITY, l = 0.0f;
-    for (int j = 0; j < nk; ++j) {
-      const T* kr = K + (int64_t)krows[j] * io.ldkv + h * d;
-      const T* vr = V + (int64_t)krows[j] * io.ldkv + h * d;
-      float sc = 0.0f;
+    for (int k0 = 0; k0 < nk; k0 += KC) {
+      const int cnt = min(KC, nk - k0);
+      // this wave's chunk of key and value rows into LDS (16-byte copies)
+      for (int i = lane; i < cnt * vpr; i += kWave) {
+        const int row = i / vpr, v = i - row * vpr;
+        const int64_t src = (int64_t)krows[k0 + row] * io.ldkv + h * d + v * VN;
+        *reinterpret_cast<uint4*>(sk + row * HD + v * VN) = *reinterpret_cast<const uint4*>(K + src);
+        *reinterpret_cast<uint4*>(sv + row * HD + v * VN) = *reinterpret_cast<const uint4*>(V + src);
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // the wave's own LDS writes are complete (lockstep wave)
+      asm volatile("" ::: "memory");
+      if (mine) {
+        for (int j = 0; j < cnt; ++j) {
+          float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // independent partial dot products
 #pragma unroll
-      for (int e = 0; e < kTempMaxD; ++e)
-        if (e < d) sc = fmaf(q[e], ld_el(kr + e), sc);
-      const float mn = fmaxf(m, sc);
-      const float corr = __expf(m - mn), p = __expf(sc - mn);
-      l = fmaf(l, corr, p);
+          for (int v = 0; v < NV; ++v) {
+            if (EXACT || v < vpr) {
+              float kv[VN];
+              TempVec<T>::get(sk + j * HD + v * VN, kv);
 #pragma unroll
-      for (int e = 0; e < kTempMaxD; ++e)
-        if (e < d) acc[e] = fmaf(acc[e], corr, p * ld_el(vr + e));
-      m = mn;
+              for (int i = 0; i < VN; ++i) part[i & 3] = fmaf(q[v * VN + i], kv[i], part[i & 3]);
+            }
+          }
+          const float sc = (part[0] + part[1]) + (part[2] + part[3]);
+          const float mn = fmaxf(m, sc);
+          const float corr = __expf(m - mn), p = __expf(sc - mn);
+          l = fmaf(l, corr, p);
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            if (EXACT || v < vpr) {
+              float vv[VN];
+              TempVec<T>::get(sv + j * HD + v * VN, vv);
+#pragma unroll
+              for (int i = 0; i < VN; ++i) acc[v * VN + i] = fmaf(acc[v * VN + i], corr, p * vv[i]);
+            }
+          }
+          m = mn;
+        }
+      }
+      asm volatile("" ::: "memory");
     }
-    const float inv = 1.0f / l;
-    T* orow = O + (int64_t)qr * D + h * d;
+    if (mine) {
+      const float inv = 1.0f / l;
+      T* orow = O + (int64_t)qr * D + h * d;
 #pragma unroll
-    for (int e = 0; e < kTempMaxD; ++e)
-      if (e < d) orow[e] = (T)(acc[e] * inv);
+      for (int e = 0; e < HD; ++e)
+        if (EXACT || e < d) orow[e] = (T)(acc[e] * inv);
+    }
   }
 }
 }  // namespace
-
 hipError_t launch_attn_temporal(sphinx_dtype dt, const ReqTable& T, const AttnIO& io, int D, int heads,
                                 int head_dim, const int32_t* pos, bool cached, hipStream_t s) {
   int64_t cols = 0;
   for (int r = 0; r < T.R; ++r) cols += (int64_t)(T.h[r] >> 1) * (T.w[r] >> 1);
   const float scale = 1.0f / sqrtf((float)head_dim);
-  if (dt == SPHINX_BF16)
-    k_attn_temporal<bf16><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cached ? 1 : 0);
+  const int cf = cached ? 1 : 0;
+  if (dt == SPHINX_BF16 && head_dim == 64)
+    k_attn_temporal<bf16, 64, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cf);
+  else if (dt == SPHINX_BF16)
+    k_attn_temporal<bf16, 72, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cf);
   else
-    k_attn_temporal<float><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cached ? 1 : 0);
+    k_attn_temporal<float, 64, false><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cf);
   return hipGetLastError();
 }
 
