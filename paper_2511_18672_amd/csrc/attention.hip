@@ -464,10 +464,13 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16
 }
 
 // One iteration's MFMA work interleaved by hand with the softmax of the
-// previous tile: all fragment reads first, then 16 steps of one MFMA
-// (QK(t+1) for steps 0..7, PV(t-1) for steps 8..15) and one pair of
-// probabilities (two exponentials, one bf16 pack, one row-sum dot product),
-// each step fenced so the compiler keeps the order.
+// previous tile: all fragment reads first, then 16 steps of one MFMA (QK(t+1)
+// for steps 0..7, PV(t-1) for steps 8..15) and softmax work on three
+// consecutive probability pairs, software-pipelined so that no instruction of
+// a step waits on another of the same step: the scaled and shifted scores of
+// pair st+2, the exponentials of pair st+1, and the bf16 pack and row-sum
+// dot product of pair st.  Each step is fenced so the compiler keeps the
+// order.  The arithmetic per probability is unchanged.
 __device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff& lo, const bf16x8 (&qf)[4],
                                        const f32x16& c0, const f32x16& c1, float scale_log2, float m_run,
                                        float& l_run, const bf16x8 (&pp)[2][2], bf16x8 (&pn)[2][2], f32x16& n0,
@@ -488,6 +491,19 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
         const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
         vf[kb][hf][db] = tr_pair(p, p + 8 * 128);
       }
+  // pair st: score block w = st & 1 (s0 or s1), rows r, r+1 with r = 8 (st >> 3) + 2 ((st >> 1) & 3)
+  auto score = [&](int st, int e) -> float {
+    const int r = (st >> 3) * 8 + 2 * ((st >> 1) & 3) + e;
+    return (st & 1) ? c1[r] : c0[r];
+  };
+  float x[16][2], ex[16][2];
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    x[0][e] = fmaf(score(0, e), scale_log2, -m_run);
+    x[1][e] = fmaf(score(1, e), scale_log2, -m_run);
+  }
+#pragma unroll
+  for (int e = 0; e < 2; ++e) ex[0][e] = fast_exp2(x[0][e]);
   __builtin_amdgcn_sched_barrier(0);
   const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
@@ -505,16 +521,21 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
       const int kb = (st - 8) >> 2, hf = ((st - 8) >> 1) & 1, db = (st - 8) & 1;
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kb][hf][db], pp[kb][hf], oacc[db], 0, 0, 0);
     }
-    // probability pair st: half hf, pair i, score block w (s0 or s1)
-    const int hf = st >> 3, i = (st >> 1) & 3, w = st & 1;
-    const int r = hf * 8 + 2 * i;
-    const f32x16& sc = w ? c1 : c0;
-    bf16x2 pr;
-    pr[0] = (bf16)fast_exp2(fmaf(sc[r], scale_log2, -m_run));
-    pr[1] = (bf16)fast_exp2(fmaf(sc[r + 1], scale_log2, -m_run));
-    psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, psum, false);
-    pn[w][hf][2 * i] = pr[0];
-    pn[w][hf][2 * i + 1] = pr[1];
+    if (st + 2 < 16)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) x[st + 2][e] = fmaf(score(st + 2, e), scale_log2, -m_run);
+    if (st + 1 < 16)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) ex[st + 1][e] = fast_exp2(x[st + 1][e]);
+    {
+      const int hf = st >> 3, i = (st >> 1) & 3, w = st & 1;
+      bf16x2 pr;
+      pr[0] = (bf16)ex[st][0];
+      pr[1] = (bf16)ex[st][1];
+      psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, psum, false);
+      pn[w][hf][2 * i] = pr[0];
+      pn[w][hf][2 * i + 1] = pr[1];
+    }
     __builtin_amdgcn_sched_barrier(0);
   }
   l_run += psum;

@@ -6,7 +6,8 @@
 //  * k_temb        sinusoidal timestep embedding, 256 wide, in fp64.
 //  * k_rowgemm     out[u][n] = act(sum_k X[u][k] W[n][k] + b[n]) for the U rows:
 //                  the timestep MLP and the adaLN projections of all blocks in
-//                  one pass over the weights (weight-read bound; fp32 math).
+//                  one pass over the weights (weight-read bound; one wave per
+//                  output column, fp32 math).
 //  * k_pos_tables  fp64 sinusoid tables for patch rows, columns and frames.
 //  * k_token_meta  per selected row: global frame, conditioning row, packed
 //                  (frame, y, x) position.
@@ -45,49 +46,77 @@ __global__ __launch_bounds__(kTPB) void k_temb(const int32_t* __restrict__ utau,
   temb[(int64_t)u * SPHINX_TEMB_DIM + c] = (float)(c < 128 ? cos(arg) : sin(arg));
 }
 
-// 64 output columns per workgroup, conditioning rows processed 16 at a time.
+// out[u][n] = act(sum_k X[u][k] W[n][k] + b[n]) for the U conditioning rows.
+// One wave per output column: the lanes stream the column's weight row with
+// 16-byte loads (8 bf16 or 4 fp32 per vector, vectors lane, lane+64, ...), so
+// the launch reads every weight exactly once with full-line accesses; the U
+// rows of X are small and come from L1/L2.  Partial dot products are reduced
+// across the wave.
+template <typename WT>
+struct WVec;
+template <>
+struct WVec<bf16> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void get(const bf16* p, float* w) {
+    const bf16x8 v = *reinterpret_cast<const bf16x8*>(p);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = (float)v[i];
+  }
+};
+template <>
+struct WVec<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void get(const float* p, float* w) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) w[i] = v[i];
+  }
+};
+
+constexpr int kGemvMaxVec = 4;  // K <= 4 * 64 * (elements per vector)
 template <typename WT, bool SILU_OUT>
 __global__ __launch_bounds__(kTPB) void k_rowgemm(const float* __restrict__ X, int ldx, const int32_t* __restrict__ Up,
-                                                  int K, const WT* __restrict__ W, const WT* __restrict__ bias,
+                                                  int K, int N, const WT* __restrict__ W, const WT* __restrict__ bias,
                                                   float* __restrict__ out, int ldo) {
-  __shared__ float s_w[64][65];
-  __shared__ float s_x[16][64];
+  constexpr int VN = WVec<WT>::N;
+  const int n = blockIdx.x * (kTPB / kWave) + (int)(threadIdx.x / kWave);
+  if (n >= N) return;
+  const int lane = lane_id();
   const int U = *Up;
-  const int n0 = blockIdx.x * 64;
-  const int tn = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  for (int r0 = 0; r0 < U; r0 += 16) {
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int k0 = 0; k0 < K; k0 += 64) {
-      {  // weight tile: 64 columns x 64 k, stored [k][n]
-        const int row = threadIdx.x >> 2, kc = (threadIdx.x & 3) * 16;
-        const WT* src = W + (int64_t)(n0 + row) * K + k0 + kc;
+  const int nvec = K / VN;
+  float w[kGemvMaxVec][VN];
+  const WT* wr = W + (int64_t)n * K;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) s_w[kc + i][row] = load_as_f32(src, i);
-      }
-      {  // input tile: 16 rows x 64 k
-        const int row = threadIdx.x >> 4, kc = (threadIdx.x & 15) * 4;
+  for (int i = 0; i < kGemvMaxVec; ++i) {
+    const int v = lane + kWave * i;
+    if (v < nvec)
+      WVec<WT>::get(wr + v * VN, w[i]);
+    else
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          s_x[row][kc + i] = (r0 + row < U) ? X[(int64_t)(r0 + row) * ldx + k0 + kc + i] : 0.0f;
-      }
-      __syncthreads();
-#pragma unroll 8
-      for (int k = 0; k < 64; ++k) {
-        const float w = s_w[k][tn];
+      for (int e = 0; e < VN; ++e) w[i][e] = 0.0f;
+  }
+  const float bv = load_as_f32(bias, n);
+  for (int u = 0; u < U; ++u) {
+    const float* xr = X + (int64_t)u * ldx;
+    float acc = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[i] = fmaf(s_x[rg + 4 * i][k], w, acc[i]);
-      }
-      __syncthreads();
+    for (int i = 0; i < kGemvMaxVec; ++i) {
+      const int v = lane + kWave * i;
+      if (v < nvec)
+#pragma unroll
+        for (int e = 0; e < VN; e += 4) {
+          const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + v * VN + e);
+          acc = fmaf(w[i][e], xv[0], acc);
+          acc = fmaf(w[i][e + 1], xv[1], acc);
+          acc = fmaf(w[i][e + 2], xv[2], acc);
+          acc = fmaf(w[i][e + 3], xv[3], acc);
+        }
     }
-    const float bv = load_as_f32(bias, n0 + tn);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = r0 + rg + 4 * i;
-      if (r < U) {
-        float v = acc[i] + bv;
-        if (SILU_OUT) v = silu(v);
-        out[(int64_t)r * ldo + n0 + tn] = v;
-      }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      float v = acc + bv;
+      if (SILU_OUT) v = silu(v);
+      out[(int64_t)u * ldo + n] = v;
     }
   }
 }
@@ -146,17 +175,17 @@ hipError_t launch_temb(const int32_t* utau, const int32_t* U, int Gmax, float* t
 
 hipError_t launch_rowgemm(const float* X, int ldx, const int32_t* U, int K, const void* W, const void* b,
                           sphinx_dtype wdt, int N, bool silu_out, float* out, int ldo, hipStream_t s) {
-  const int g = N / 64;
+  const int g = (N + kTPB / kWave - 1) / (kTPB / kWave);
   if (wdt == SPHINX_BF16) {
     if (silu_out)
-      k_rowgemm<bf16, true><<<g, kTPB, 0, s>>>(X, ldx, U, K, (const bf16*)W, (const bf16*)b, out, ldo);
+      k_rowgemm<bf16, true><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const bf16*)W, (const bf16*)b, out, ldo);
     else
-      k_rowgemm<bf16, false><<<g, kTPB, 0, s>>>(X, ldx, U, K, (const bf16*)W, (const bf16*)b, out, ldo);
+      k_rowgemm<bf16, false><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const bf16*)W, (const bf16*)b, out, ldo);
   } else {
     if (silu_out)
-      k_rowgemm<float, true><<<g, kTPB, 0, s>>>(X, ldx, U, K, (const float*)W, (const float*)b, out, ldo);
+      k_rowgemm<float, true><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const float*)W, (const float*)b, out, ldo);
     else
-      k_rowgemm<float, false><<<g, kTPB, 0, s>>>(X, ldx, U, K, (const float*)W, (const float*)b, out, ldo);
+      k_rowgemm<float, false><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const float*)W, (const float*)b, out, ldo);
   }
   return hipGetLastError();
 }

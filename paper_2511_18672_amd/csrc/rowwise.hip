@@ -15,24 +15,68 @@ constexpr int kTPB = 256;
 constexpr int kRowsPerBlock = kTPB / kWave;
 constexpr int kMaxPer = 32;  // D <= 2048
 
+// 16 weights of one output column as floats (a [..][16] row of WT).
+template <typename WT>
+__device__ __forceinline__ void load16(const WT* p, float (&w)[16]);
+template <>
+__device__ __forceinline__ void load16<bf16>(const bf16* p, float (&w)[16]) {
+  const bf16x8 a = reinterpret_cast<const bf16x8*>(p)[0], b = reinterpret_cast<const bf16x8*>(p)[1];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    w[k] = (float)a[k];
+    w[8 + k] = (float)b[k];
+  }
+}
+template <>
+__device__ __forceinline__ void load16<float>(const float* p, float (&w)[16]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 v = reinterpret_cast<const f32x4*>(p)[q];
+    w[4 * q] = v[0];
+    w[4 * q + 1] = v[1];
+    w[4 * q + 2] = v[2];
+    w[4 * q + 3] = v[3];
+  }
+}
+
+// One thread per (row, four consecutive columns), grid (column blocks, rows):
+// 16-byte loads of x, the four weight rows and the position tables, one
+// 16-byte store of h.
 template <typename WT>
 __global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int n, int D, const WT* __restrict__ pe_w,
                                                 const WT* __restrict__ pe_b, const float* __restrict__ Ty,
                                                 const float* __restrict__ Tx, const float* __restrict__ Tf,
                                                 const int32_t* __restrict__ posc, float* __restrict__ h) {
-  const int64_t gid = (int64_t)blockIdx.x * kTPB + threadIdx.x;
-  if (gid >= (int64_t)n * D) return;
-  const int j = (int)(gid / D), c = (int)(gid % D);
+  const int quads = D >> 2;
+  const int j = (int)blockIdx.y, qd = (int)blockIdx.x * kTPB + (int)threadIdx.x;
+  if (qd >= quads) return;
+  const int c0 = 4 * qd;
   const int pc = posc[j];
   const int f = pc >> 20, y = (pc >> 10) & 1023, xx = pc & 1023;
-  const float* xr = x + (int64_t)j * 16;
-  float v = load_as_f32(pe_b, c);
+  float xr[16];
 #pragma unroll
-  for (int k = 0; k < 16; ++k) v = fmaf(xr[k], load_as_f32(pe_w, (int64_t)c * 16 + k), v);
+  for (int q = 0; q < 4; ++q) {
+    const f32x4 v = reinterpret_cast<const f32x4*>(x + (int64_t)j * 16)[q];
+    xr[4 * q] = v[0];
+    xr[4 * q + 1] = v[1];
+    xr[4 * q + 2] = v[2];
+    xr[4 * q + 3] = v[3];
+  }
   const int half = D / 2;
-  v += (c < half) ? Ty[(int64_t)y * half + c] : Tx[(int64_t)xx * half + (c - half)];
-  v += Tf[(int64_t)f * D + c];
-  h[gid] = v;
+  const f32x4 pos = (c0 < half) ? *reinterpret_cast<const f32x4*>(Ty + (int64_t)y * half + c0)
+                                : *reinterpret_cast<const f32x4*>(Tx + (int64_t)xx * half + (c0 - half));
+  const f32x4 tf = *reinterpret_cast<const f32x4*>(Tf + (int64_t)f * D + c0);
+  f32x4 out;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    float w[16];
+    load16<WT>(pe_w + (int64_t)(c0 + e) * 16, w);
+    float v = load_as_f32(pe_b, c0 + e);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v = fmaf(xr[k], w[k], v);
+    out[e] = v + pos[e] + tf[e];
+  }
+  *reinterpret_cast<f32x4*>(h + (int64_t)j * D + c0) = out;
 }
 
 // Loads the row into registers and returns (mean, rstd).
@@ -156,6 +200,10 @@ __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, in
     }
 }
 
+// One wave per row; lane owns the column quads lane + 64 i.  The output
+// weights sit transposed in LDS ([D][16]: a column's 16 weights contiguous),
+// so a column costs two (bf16) or four (fp32) 16-byte LDS reads.
+constexpr int kMaxQuads = 8;  // D <= 2048
 template <typename WT>
 __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int n, int D,
                                                 const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
@@ -163,29 +211,55 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
                                                 const WT* __restrict__ out_w, const WT* __restrict__ out_b,
                                                 const float* __restrict__ c1, const float* __restrict__ c2,
                                                 float* __restrict__ x) {
-  extern __shared__ unsigned char s_raw[];
-  WT* s_w = reinterpret_cast<WT*>(s_raw);  // [16][D]
-  for (int i = threadIdx.x; i < 16 * D; i += kTPB) s_w[i] = out_w[i];
+  extern __shared__ __attribute__((aligned(16))) unsigned char s_raw[];
+  WT* s_wt = reinterpret_cast<WT*>(s_raw);  // [D][16]
+  for (int k = 0; k < 16; ++k)
+    for (int c = threadIdx.x; c < D; c += kTPB) s_wt[c * 16 + k] = out_w[(int64_t)k * D + c];
   __syncthreads();
   const int lane = lane_id();
-  const int per = D / kWave;
+  const int quads = D >> 2;
   for (int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave); row < n;
        row += gridDim.x * kRowsPerBlock) {
-    float v[kMaxPer];
-    float mu, rstd;
-    row_stats(h + (int64_t)row * D, D, lane, v, mu, rstd);
+    const float* hr = h + (int64_t)row * D;
+    f32x4 v[kMaxQuads];
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxQuads; ++i) {
+      const int q = lane + kWave * i;
+      v[i] = (q < quads) ? reinterpret_cast<const f32x4*>(hr)[q] : f32x4{0.f, 0.f, 0.f, 0.f};
+      s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+    }
+    const float mu = wave_sum(s) / (float)D;
+    float s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxQuads; ++i)
+      if (lane + kWave * i < quads)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float d = v[i][e] - mu;
+          s2 = fmaf(d, d, s2);
+        }
+    const float rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
     const float* m = mod + (int64_t)crow[row] * ldm;
     float acc[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) acc[k] = 0.f;
 #pragma unroll
-    for (int i = 0; i < kMaxPer; ++i)
-      if (i < per) {
-        const int c = i * kWave + lane;
-        const float a = fmaf((v[i] - mu) * rstd, 1.0f + m[sc_off + c], m[sh_off + c]);
+    for (int i = 0; i < kMaxQuads; ++i) {
+      const int q = lane + kWave * i;
+      if (q < quads) {
+        const f32x4 sc = *reinterpret_cast<const f32x4*>(m + sc_off + 4 * q);
+        const f32x4 sh = *reinterpret_cast<const f32x4*>(m + sh_off + 4 * q);
 #pragma unroll
-        for (int k = 0; k < 16; ++k) acc[k] = fmaf(a, load_as_f32(s_w, (int64_t)k * D + c), acc[k]);
+        for (int e = 0; e < 4; ++e) {
+          const float a = fmaf((v[i][e] - mu) * rstd, 1.0f + sc[e], sh[e]);
+          float w[16];
+          load16<WT>(s_wt + (4 * q + e) * 16, w);
+#pragma unroll
+          for (int k = 0; k < 16; ++k) acc[k] = fmaf(a, w[k], acc[k]);
+        }
       }
+    }
     // butterfly reduce-scatter: after the four halving steps lane holds output
     // k = 8*b5 + 4*b4 + 2*b3 + b2 (b = lane bits), summed over lanes that differ
     // in those bits; the last two steps sum over lane bits 1 and 0.
@@ -219,7 +293,7 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
 hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const void* pe_b, sphinx_dtype wdt,
                         const float* Ty, const float* Tx, const float* Tf, const int32_t* posc, float* h,
                         hipStream_t s) {
-  const int g = (int)(((int64_t)n * D + kTPB - 1) / kTPB);
+  const dim3 g((unsigned)((D / 4 + kTPB - 1) / kTPB), (unsigned)n);
   if (wdt == SPHINX_BF16)
     k_embed<bf16><<<g, kTPB, 0, s>>>(x, n, D, (const bf16*)pe_w, (const bf16*)pe_b, Ty, Tx, Tf, posc, h);
   else
