@@ -464,33 +464,32 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16
 }
 
 // One iteration's MFMA work interleaved by hand with the softmax of the
-// previous tile: all fragment reads first, then 16 steps of one MFMA (QK(t+1)
-// for steps 0..7, PV(t-1) for steps 8..15) and softmax work on three
-// consecutive probability pairs, software-pipelined so that no instruction of
-// a step waits on another of the same step: the scaled and shifted scores of
-// pair st+2, the exponentials of pair st+1, and the bf16 pack and row-sum
-// dot product of pair st.  Each step is fenced so the compiler keeps the
-// order.  The arithmetic per probability is unchanged.
+// previous tile: 16 steps of one MFMA (QK(t+1) for steps 0..7, PV(t-1) for
+// steps 8..15) and softmax work on three consecutive probability pairs,
+// software-pipelined so that no instruction of a step waits on another of the
+// same step: the scaled and shifted scores of pair st+2, the exponentials of
+// pair st+1, and the bf16 pack and row-sum dot product of pair st.  The
+// operand fragment of step st is read from LDS two steps ahead (a ring of
+// three), which keeps the register footprint low enough for three waves per
+// SIMD.  Each step is fenced so the compiler keeps the order.  The arithmetic
+// per probability is unchanged.
+__device__ __forceinline__ bf16x8 step_frag(const char* sK, const char* sV, const LaneOff& lo, int st) {
+  if (st < 8) {
+    const int ks = st >> 1;
+    return *reinterpret_cast<const bf16x8*>(sK + lo.k[ks] + ((st & 1) ? 4096 : 0));
+  }
+  const int kb = (st - 8) >> 2, hf = ((st - 8) >> 1) & 1, db = (st - 8) & 1;
+  const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
+  return tr_pair(p, p + 8 * 128);
+}
+
 __device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff& lo, const bf16x8 (&qf)[4],
                                        const f32x16& c0, const f32x16& c1, float scale_log2, float m_run,
                                        float& l_run, const bf16x8 (&pp)[2][2], bf16x8 (&pn)[2][2], f32x16& n0,
                                        f32x16& n1, f32x16 (&oacc)[2]) {
-  bf16x8 kf[4][2];
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    kf[ks][0] = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks]);
-    kf[ks][1] = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks] + 4096);
-  }
-  bf16x8 vf[2][2][2];
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-      for (int db = 0; db < 2; ++db) {
-        const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
-        vf[kb][hf][db] = tr_pair(p, p + 8 * 128);
-      }
+  bf16x8 fr[3];
+  fr[0] = step_frag(sK, sV, lo, 0);
+  fr[1] = step_frag(sK, sV, lo, 1);
   // pair st: score block w = st & 1 (s0 or s1), rows r, r+1 with r = 8 (st >> 3) + 2 ((st >> 1) & 3)
   auto score = [&](int st, int e) -> float {
     const int r = (st >> 3) * 8 + 2 * ((st >> 1) & 3) + e;
@@ -511,15 +510,17 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
   n1 = f32x16{};
 #pragma unroll
   for (int st = 0; st < 16; ++st) {
+    if (st + 2 < 16) fr[(st + 2) % 3] = step_frag(sK, sV, lo, st + 2);
+    const bf16x8 f = fr[st % 3];
     if (st < 8) {
       const int ks = st >> 1;
       if (st & 1)
-        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][1], qf[ks], n1, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, qf[ks], n1, 0, 0, 0);
       else
-        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[ks][0], qf[ks], n0, 0, 0, 0);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, qf[ks], n0, 0, 0, 0);
     } else {
       const int kb = (st - 8) >> 2, hf = ((st - 8) >> 1) & 1, db = (st - 8) & 1;
-      oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[kb][hf][db], pp[kb][hf], oacc[db], 0, 0, 0);
+      oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, pp[kb][hf], oacc[db], 0, 0, 0);
     }
     if (st + 2 < 16)
 #pragma unroll
@@ -735,7 +736,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
 }
 
-__global__ __launch_bounds__(256, 2) void k_attn_bf16_dma(AttnIO io, int D, int heads, float scale_log2,
+__global__ __launch_bounds__(256, 3) void k_attn_bf16_dma(AttnIO io, int D, int heads, float scale_log2,
                                                           SegTable S, AttnSplit sp) {
   __shared__ __attribute__((aligned(1024))) dma::Smem sm;
   attn_body_dma(io, D, heads, scale_log2, S, sp, sm);
@@ -838,19 +839,25 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int h
 // work.  Needs U (units) divisible by 8; sp <= 8, tail * sp <= kMaxPartsPerXcd.
 AttnSplit plan_split(const SegTable& S, int heads, float* part, size_t part_floats) {
   AttnSplit p{1, 0, 0, 0, part};
-  static int cus = 0;
+  static int cus = 0, per_cu = 0;
   if (cus == 0) {
-    int dev = 0, v = 0;
+    int dev = 0, v = 0, b = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
       cus = v;
     else
       cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, reinterpret_cast<const void*>(k_attn_bf16_dma), 256, 0) ==
+            hipSuccess &&
+        b > 0)
+      per_cu = b;
+    else
+      per_cu = 2;
   }
   const int ntiles = S.tile_prefix[S.nseg];
   const int U = ntiles * heads;
   if (part == nullptr || U % 8 != 0 || cus % 8 != 0) return p;
-  const int q = U / 8, slots = 2 * (cus / 8);  // two workgroups per CU
+  const int q = U / 8, slots = per_cu * (cus / 8);  // resident workgroups per XCD
   const int k0 = (q / slots) * slots, tail = q - k0;
   if (k0 == 0 || tail == 0) return p;
   // fewest key tiles among the tail units
