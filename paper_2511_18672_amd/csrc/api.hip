@@ -118,8 +118,7 @@ Blob blob_layout(const sphinx_model_desc& m) {
 }
 
 struct RefineWs {
-  size_t fmap, utau, U, temb, cbuf, sc, mod, Ty, Tx, Tf, gframe, crow, posc, fcnt, pos, h, a, big, part, part_bytes,
-      total;
+  size_t fmap, utau, U, temb, cbuf, sc, mod, Ty, Tx, Tf, gframe, crow, posc, fcnt, pos, h, a, big, total;
   int maxHp, maxWp, maxF;
 };
 
@@ -157,11 +156,6 @@ RefineWs refine_layout(const sphinx_model_desc& m, const ReqTable& T, int G, int
   w.h = take((size_t)n * D * 4);
   w.a = take((size_t)n * D * act);
   w.big = take((size_t)n * std::max<size_t>(4 * D, (size_t)m.mlp) * act);
-  // attention key-range partials (bf16 head_dim-64 models with enough query tiles to fill a round)
-  w.part_bytes = 0;
-  if (m.dtype == SPHINX_BF16 && m.head_dim == 64 && (n + 127) / 128 * (int64_t)m.heads >= 512)
-    w.part_bytes = kAttnPartBytes;
-  w.part = take(w.part_bytes);
   w.total = off;
   return w;
 }
@@ -715,11 +709,9 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
     {
       Bracket br(SPHINX_K_ATTENTION, s);
       if (!factorised)
-        SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, S, W.part_bytes ? F32(W.part) : nullptr,
-                                    W.part_bytes / 4, s));
+        SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, S, s));
       else if (l % 2 == 0)  // spatial: within the frame
-        SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, Sf, W.part_bytes ? F32(W.part) : nullptr,
-                                    W.part_bytes / 4, s));
+        SPHINX_TRY(launch_attention(dt, io, D, m->heads, m->head_dim, n, Sf, s));
       else  // temporal: across the request's frames at the same position
         SPHINX_TRY(launch_attn_temporal(dt, T, io, D, m->heads, m->head_dim, I32(W.pos), cached, s));
     }

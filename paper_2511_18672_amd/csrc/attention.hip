@@ -40,8 +40,6 @@ namespace sphinx {
 
 namespace {
 constexpr int AQ = 128;  // queries per workgroup
-// floats of one key-range partial of a split unit: O [128][64], m [128], l [128]
-constexpr int kPartFloats = AQ * 64 + 2 * AQ;
 constexpr int AK = 64;   // keys per LDS tile
 constexpr int VLD = AK + 8;
 constexpr float kRescaleLog2 = 8.0f;  // rescale only when the running max grows by > 2^8
@@ -544,32 +542,18 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
 }  // namespace dma
 
 __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads, float scale_log2, const SegTable& S,
-                                              const AttnSplit& sp, dma::Smem& sm) {
+                                              dma::Smem& sm) {
   constexpr int HD = 64;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, r32 = lane & 31;
   const int ntiles = S.tile_prefix[S.nseg];
   const int work = ntiles * heads;
-  // Unit of this workgroup.  Workgroups are dealt to the 8 XCDs round-robin;
-  // XCD x runs the contiguous units [x q, (x+1) q) (whole heads stay in its
-  // L2).  With a split plan, the last `tail` units of each XCD (the partly
-  // filled final round) are cut into sp parts along the keys.
-  int lid = (int)blockIdx.x, part = 0, nparts = 1, split_idx = 0;
-  if (sp.sp > 1) {
-    const int x = lid & 7, k = lid >> 3;
-    int local = k;
-    if (k >= sp.k0) {
-      const int kk = k - sp.k0;
-      local = sp.k0 + kk / sp.sp;
-      part = kk - (kk / sp.sp) * sp.sp;
-      nparts = sp.sp;
-      split_idx = (x * sp.tail + (local - sp.k0)) * sp.sp + part;
-    }
-    lid = x * sp.q + local;
-  } else if (work % 8 == 0) {
-    lid = (lid & 7) * (work >> 3) + (lid >> 3);
-  }
+  // Workgroups are dealt to the 8 XCDs round-robin by linear id; renumbered so
+  // that XCD x runs the contiguous units [x q, (x+1) q), i.e. whole heads, and
+  // keeps a head's K and V in its L2.
+  int lid = (int)blockIdx.x;
+  if (work % 8 == 0) lid = (lid & 7) * (work >> 3) + (lid >> 3);
   const int head = lid / ntiles, tile = lid - head * ntiles;
   int s = 0;
   while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
@@ -635,10 +619,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   const dma::LaneOff lo = dma::lane_offsets(lane);
   f32x16 oacc[2] = {f32x16{}, f32x16{}};
   float m_run = -INFINITY, l_run = 0.0f;
-  const int nkt_all = (L + AK - 1) / AK;
-  const int kt0 = part * nkt_all / nparts;                  // first key tile of this part
-  const int nkt = (part + 1) * nkt_all / nparts - kt0;      // key tiles of this part (>= 1)
-  const bool has_last = kt0 + nkt == nkt_all;               // holds the segment's (partial) last tile
+  const int nkt = (L + AK - 1) / AK;
 
   // Tile j of K and of V lives in ring slot j % 3.  Iteration t: softmax of
   // tile t, QK(t+1), PV(t-1); copies K(t+3) (clamped to the last tile: a
@@ -657,9 +638,9 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   auto iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, bf16x8 (&pp)[2][2],
                   bf16x8 (&pn)[2][2]) {
     const int s1 = slot == 2 ? 0 : slot + 1, s2 = slot == 0 ? 2 : slot - 1;  // (t+1) % 3, (t-1) % 3
-    copy_k((kt0 + min(t + 3, nkt - 1)) * AK, slot);
-    copy_v((kt0 + t + 1) * AK, s1);
-    const float a_new = raise_max(tile_max<false>(c0, c1, g, (kt0 + t) * AK, L, scale_log2), m_run, l_run);
+    copy_k(min(t + 3, nkt - 1) * AK, slot);
+    copy_v((t + 1) * AK, s1);
+    const float a_new = raise_max(tile_max<false>(c0, c1, g, t * AK, L, scale_log2), m_run, l_run);
     rescale_o();
     alpha = a_new;
     dma::region(sm.k[s1], sm.v[s2], lo, qf, c0, c1, scale_log2, m_run, l_run, pp, pn, n0, n1, oacc);
@@ -667,10 +648,10 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     slot = s1;
   };
 
-  copy_k(kt0 * AK, 0);
-  copy_k((kt0 + min(1, nkt - 1)) * AK, 1);
-  copy_k((kt0 + min(2, nkt - 1)) * AK, 2);
-  copy_v(kt0 * AK, 0);
+  copy_k(0, 0);
+  copy_k(min(1, nkt - 1) * AK, 1);
+  copy_k(min(2, nkt - 1) * AK, 2);
+  copy_v(0, 0);
   land(Keep4{});
   f32x16 a0, a1, b0, b1;
   dma::qk(sm.k[0], lo, qf, a0, a1);
@@ -694,8 +675,8 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
   {  // last tile t = nkt - 1 (possibly partial); V(t) was copied in iteration t-1
     const int sprev = slot == 0 ? 2 : slot - 1;
-    const float mx = (has_last && L % AK != 0) ? tile_max<true>(a0, a1, g, (kt0 + t) * AK, L, scale_log2)
-                                               : tile_max<false>(a0, a1, g, (kt0 + t) * AK, L, scale_log2);
+    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L, scale_log2)
+                                   : tile_max<false>(a0, a1, g, t * AK, L, scale_log2);
     const float a_new = raise_max(mx, m_run, l_run);
     rescale_o();
     alpha = a_new;
@@ -706,21 +687,6 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     dma::pv(sm.v[slot], lo, pb, oacc);
   }
   l_run += __shfl_xor(l_run, 32, kWave);
-  if (nparts > 1) {  // unnormalised partial O, row max and sum of this key range
-    float* po = sp.part + (size_t)split_idx * kPartFloats;
-    const int lq = wave * 32 + r32;
-#pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr)
-        *reinterpret_cast<f32x4*>(po + lq * HD + db * 32 + rr * 8 + g * 4) =
-            f32x4{oacc[db][rr * 4], oacc[db][rr * 4 + 1], oacc[db][rr * 4 + 2], oacc[db][rr * 4 + 3]};
-    if (g == 0) {
-      po[AQ * HD + lq] = m_run;
-      po[AQ * HD + AQ + lq] = l_run;
-    }
-    return;
-  }
   if (ql < Lq) {
     const float inv = 1.0f / l_run;
     bf16* orow = static_cast<bf16*>(io.o) + (int64_t)(seg0 + ql) * D + head * HD;
@@ -737,57 +703,9 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
 }
 
 __global__ __launch_bounds__(256, 3) void k_attn_bf16_dma(AttnIO io, int D, int heads, float scale_log2,
-                                                          SegTable S, AttnSplit sp) {
+                                                          SegTable S) {
   __shared__ __attribute__((aligned(1024))) dma::Smem sm;
-  attn_body_dma(io, D, heads, scale_log2, S, sp, sm);
-}
-
-// Merge of the key-range parts of the split units: per query, the parts'
-// (O, m, l) combine as O = sum_p 2^(m_p - M) O_p / sum_p 2^(m_p - M) l_p with
-// M = max_p m_p (base-2 softmax, as in the attention kernel).
-__global__ __launch_bounds__(256) void k_attn_merge(AttnIO io, int D, int heads, SegTable S, AttnSplit sp) {
-  constexpr int HD = 64;
-  const int i = blockIdx.x;  // split unit: XCD x, its (i % tail)-th tail unit
-  const int x = i / sp.tail, j = i - x * sp.tail;
-  const int lid = x * sp.q + sp.k0 + j;
-  const int ntiles = S.tile_prefix[S.nseg];
-  const int head = lid / ntiles, tile = lid - head * ntiles;
-  int s = 0;
-  while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
-  const int qt = tile - S.tile_prefix[s];
-  const int lq = threadIdx.x >> 1, half = threadIdx.x & 1;  // 128 queries x two 32-dim halves
-  const int ql = qt * AQ + lq;
-  if (ql >= S.len[s]) return;
-  const float* base = sp.part + (size_t)i * sp.sp * kPartFloats;
-  float M = -INFINITY;
-  for (int p = 0; p < sp.sp; ++p) M = fmaxf(M, base[(size_t)p * kPartFloats + AQ * HD + lq]);
-  float den = 0.0f, o[32];
-#pragma unroll
-  for (int e = 0; e < 32; ++e) o[e] = 0.0f;
-  for (int p = 0; p < sp.sp; ++p) {
-    const float* po = base + (size_t)p * kPartFloats;
-    const float w = exp2f(po[AQ * HD + lq] - M);
-    den = fmaf(w, po[AQ * HD + AQ + lq], den);
-#pragma unroll
-    for (int e = 0; e < 32; e += 4) {
-      const f32x4 v = *reinterpret_cast<const f32x4*>(po + lq * HD + half * 32 + e);
-      o[e] = fmaf(w, v[0], o[e]);
-      o[e + 1] = fmaf(w, v[1], o[e + 1]);
-      o[e + 2] = fmaf(w, v[2], o[e + 2]);
-      o[e + 3] = fmaf(w, v[3], o[e + 3]);
-    }
-  }
-  const float inv = 1.0f / den;
-  bf16* orow = static_cast<bf16*>(io.o) + (int64_t)(S.start[s] + ql) * D + head * HD + half * 32;
-#pragma unroll
-  for (int e = 0; e < 32; e += 4) {
-    bf16x4 ov;
-    ov[0] = (bf16)(o[e] * inv);
-    ov[1] = (bf16)(o[e + 1] * inv);
-    ov[2] = (bf16)(o[e + 2] * inv);
-    ov[3] = (bf16)(o[e + 3] * inv);
-    *reinterpret_cast<bf16x4*>(orow + e) = ov;
-  }
+  attn_body_dma(io, D, heads, scale_log2, S, sm);
 }
 
 constexpr int kF32Max = 64;
@@ -834,77 +752,16 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int h
 }
 }  // namespace
 
-// Split plan of the DMA kernel: the units of each XCD's partly filled final
-// round are cut along the keys so that the final round is filled with shorter
-// work.  Needs U (units) divisible by 8; sp <= 8, tail * sp <= kMaxPartsPerXcd.
-AttnSplit plan_split(const SegTable& S, int heads, float* part, size_t part_floats) {
-  AttnSplit p{1, 0, 0, 0, part};
-  static int cus = 0, per_cu = 0;
-  if (cus == 0) {
-    int dev = 0, v = 0, b = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-      cus = v;
-    else
-      cus = 256;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, reinterpret_cast<const void*>(k_attn_bf16_dma), 256, 0) ==
-            hipSuccess &&
-        b > 0)
-      per_cu = b;
-    else
-      per_cu = 2;
-  }
-  const int ntiles = S.tile_prefix[S.nseg];
-  const int U = ntiles * heads;
-  if (part == nullptr || U % 8 != 0 || cus % 8 != 0) return p;
-  const int q = U / 8, slots = per_cu * (cus / 8);  // resident workgroups per XCD
-  const int k0 = (q / slots) * slots, tail = q - k0;
-  if (k0 == 0 || tail == 0) return p;
-  // fewest key tiles among the tail units
-  int min_kt = 1 << 30;
-  for (int x = 0; x < 8; ++x)
-    for (int j = 0; j < tail; ++j) {
-      const int lid = x * q + k0 + j, tile = lid % ntiles;
-      int sg = 0;
-      while (sg + 1 < S.nseg && S.tile_prefix[sg + 1] <= tile) ++sg;
-      min_kt = std::min(min_kt, (S.kv_len[sg] + AK - 1) / AK);
-    }
-  double best = 1.0;  // the unsplit tail costs one full unit
-  int best_sp = 1;
-  for (int c = 2; c <= 8; ++c) {
-    if (c > min_kt || tail * c > kMaxPartsPerXcd || (size_t)8 * tail * c * kPartFloats > part_floats) break;
-    const double cost = (double)((tail * c + slots - 1) / slots) / c + 0.03 * c;  // + merge and prologue overhead
-    if (cost < best - 1e-9) {
-      best = cost;
-      best_sp = c;
-    }
-  }
-  if (best_sp == 1) return p;
-  p.sp = best_sp;
-  p.k0 = k0;
-  p.tail = tail;
-  p.q = q;
-  return p;
-}
-
 hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,
-                            const SegTable& S, float* part, size_t part_floats, hipStream_t s) {
+                            const SegTable& S, hipStream_t s) {
   if (dt == SPHINX_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
     const int grid = S.tile_prefix[S.nseg] * heads;
     // the copy kernel addresses a segment's keys and values with 32-bit element offsets
     int64_t kv_max = 0;
     for (int i = 0; i < S.nseg; ++i) kv_max = std::max<int64_t>(kv_max, S.kv_len[i]);
-    if (head_dim == 64 && kv_max * io.ldkv < ((int64_t)1 << 31)) {
-      const AttnSplit sp = plan_split(S, heads, part, part_floats);
-      if (sp.sp > 1) {
-        const int blocks = 8 * (sp.k0 + sp.tail * sp.sp);
-        k_attn_bf16_dma<<<blocks, 256, 0, s>>>(io, D, heads, scale_log2, S, sp);
-        k_attn_merge<<<8 * sp.tail, 256, 0, s>>>(io, D, heads, S, sp);
-      } else {
-        k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S, sp);
-      }
-    }
+    if (head_dim == 64 && kv_max * io.ldkv < ((int64_t)1 << 31))
+      k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else if (head_dim == 64)
       k_attn_bf16<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else

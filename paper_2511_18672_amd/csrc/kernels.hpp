@@ -103,21 +103,8 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
 hipError_t launch_peak_mfma(int iters, float* out, int blocks, hipStream_t s);
 
 // attention.hip
-// Key-range split of the attention's final partly filled round: the last
-// `tail` of the q units of each XCD are cut into sp parts whose fp32 partials
-// (kAttnPartFloats each) go to `part` and are merged by a second kernel.
-struct AttnSplit {
-  int sp;  // parts per tail unit (1: no split)
-  int k0;  // whole units per XCD
-  int tail;
-  int q;   // units per XCD
-  float* part;
-};
-constexpr int kMaxPartsPerXcd = 256;
-constexpr size_t kAttnPartFloats = 128 * 64 + 2 * 128;
-constexpr size_t kAttnPartBytes = 8 * kMaxPartsPerXcd * kAttnPartFloats * sizeof(float);
 hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,
-                            const SegTable& S, float* part, size_t part_floats, hipStream_t s);
+                            const SegTable& S, hipStream_t s);
 // Temporal attention of a factorised denoiser: pos[t] = forwarded row of token t
 // or -1; keys are the forwarded tokens of the column (or all of its frames from
 // the cache when `cached`).  Frames per request <= 64.

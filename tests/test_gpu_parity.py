@@ -306,10 +306,8 @@ def _packed_vs_separate(wl):
 
 def test_batched_packed_equals_separate():
     """Four requests packed varlen into one launch give the same result as each
-    request alone (segment isolation).  Bit for bit up to GEMM tiling where no
-    attention unit is split along its keys (fewer than 512 query-tile units);
-    at the full batched shape the packed launch splits the last round's units
-    (a different summation order), so there it agrees to the parity bound."""
+    request alone (segment isolation), for a small batch and at the full
+    batched shape: every row's arithmetic is independent of the packing."""
     small = W.custom("batched_small", W.HEADLINE_MODEL, [W.Request(6, 32, 32), W.Request(4, 24, 32),
                                                          W.Request(2, 16, 16)], [0.1, 0.6, 1.0], [0.3, 0.5, 0.7],
                      [10, 25, 25])
@@ -317,7 +315,7 @@ def test_batched_packed_equals_separate():
     full = _packed_vs_separate(W.batched())
     print(f"[batched] packed vs separate max_abs: small batch {exact:.3e}, full batched shape {full:.3e}")
     assert exact <= 1e-5
-    assert full <= 2e-2
+    assert full <= 1e-5
 
 
 XL1 = W.ModelCfg(D=1152, heads=16, head_dim=72, mlp=4608, L=1, dtype="bf16")
