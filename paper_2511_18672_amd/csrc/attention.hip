@@ -412,24 +412,24 @@ __device__ __forceinline__ bf16x8 tr_pair(const char* p0, const char* p1) {
 }
 
 // Per-lane byte offsets inside a tile (loop invariant).
+// The swizzled chunk index only flips bits 5-6 of the K offset with the k-step
+// and bit 6 of the V offset with the block, so one offset of each suffices.
 struct LaneOff {
-  int k[4];   // QK A fragment, k-step ks, key rows 0..31 (rows 32..63: +4096)
-  int v[2];   // PV A fragment, block db, first transpose read (second: +1024)
+  int k0;  // QK A fragment of k-step 0, key rows 0..31 (rows 32..63: +4096)
+  int v0;  // PV A fragment of block 0, first transpose read (second: +1024)
+  __device__ int k(int ks) const { return k0 ^ (ks << 5); }
+  __device__ int v(int db) const { return v0 ^ (db << 6); }
 };
 
 __device__ __forceinline__ LaneOff lane_offsets(int lane) {
   LaneOff o;
   const int r32 = lane & 31, g = lane >> 5;
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) o.k[ks] = r32 * 128 + (((2 * ks + g) ^ ((r32 >> 1) & 7)) << 4);
+  o.k0 = r32 * 128 + ((g ^ ((r32 >> 1) & 7)) << 4);  // chunk 2 ks + g, XOR-swizzled by row pair
   const int j = lane & 15, b = lane >> 4;
   const int row = 4 * g + (j >> 2);
-#pragma unroll
-  for (int db = 0; db < 2; ++db) {
-    const int byte = 64 * db + 32 * (b & 1) + 8 * (j & 3);
-    const int chunk = (byte >> 4) ^ (2 * (row & 3));
-    o.v[db] = row * 128 + (chunk << 4) + (byte & 8);
-  }
+  const int byte = 32 * (b & 1) + 8 * (j & 3);
+  const int chunk = (byte >> 4) ^ (2 * (row & 3));
+  o.v0 = row * 128 + (chunk << 4) + (byte & 8);
   return o;
 }
 
@@ -439,8 +439,8 @@ __device__ __forceinline__ void qk(const char* sK, const LaneOff& lo, const bf16
   s1 = f32x16{};
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
-    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks]);
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(sK + lo.k[ks] + 4096);
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(sK + lo.k(ks));
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(sK + lo.k(ks) + 4096);
     s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
   }
@@ -455,89 +455,133 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16
     for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
       for (int db = 0; db < 2; ++db) {
-        const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
+        const char* p = sV + lo.v(db) + (32 * kb + 16 * hf) * 128;
         const bf16x8 vf = tr_pair(p, p + 8 * 128);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
       }
 }
 
 // One iteration's MFMA work interleaved by hand with the softmax of the
-// previous tile: 16 steps of one MFMA (QK(t+1) for steps 0..7, PV(t-1) for
-// steps 8..15) and softmax work on three consecutive probability pairs,
-// software-pipelined so that no instruction of a step waits on another of the
-// same step: the scaled and shifted scores of pair st+2, the exponentials of
-// pair st+1, and the bf16 pack and row-sum dot product of pair st.  The
-// operand fragment of step st is read from LDS two steps ahead (a ring of
-// three), which keeps the register footprint low enough for three waves per
-// SIMD.  Each step is fenced so the compiler keeps the order.  The arithmetic
-// per probability is unchanged.
+// previous tile: 18 steps of one MFMA (PV(t-1) for the first eight; QK(t+1),
+// four head-dim k-steps for each of the two 32-key blocks; then for each block
+// one k-step that adds -max through a column of ones, so that the scores
+// arrive scaled and shifted) and softmax work on two consecutive probability
+// pairs, software-pipelined so that no instruction of a step waits on another
+// of the same step: the exponentials of pair st+1 and the bf16 pack and
+// row-sum dot product of pair st.  PV first lets the previous probabilities
+// die while the new ones are made, and the QK accumulators only come alive in
+// the second half, which keeps the register footprint low enough for three
+// waves per SIMD; so does reading the operand fragment of a step from LDS two
+// steps ahead (a ring of three).  Each step is fenced so the compiler keeps
+// the order.
 __device__ __forceinline__ bf16x8 step_frag(const char* sK, const char* sV, const LaneOff& lo, int st) {
   if (st < 8) {
-    const int ks = st >> 1;
-    return *reinterpret_cast<const bf16x8*>(sK + lo.k[ks] + ((st & 1) ? 4096 : 0));
+    const int kb = st >> 2, hf = (st >> 1) & 1, db = st & 1;
+    const char* p = sV + lo.v(db) + (32 * kb + 16 * hf) * 128;
+    return tr_pair(p, p + 8 * 128);
   }
-  const int kb = (st - 8) >> 2, hf = ((st - 8) >> 1) & 1, db = (st - 8) & 1;
-  const char* p = sV + lo.v[db] + (32 * kb + 16 * hf) * 128;
-  return tr_pair(p, p + 8 * 128);
+  const int ks = (st - 8) >> 1;
+  return *reinterpret_cast<const bf16x8*>(sK + lo.k(ks) + ((st & 1) ? 4096 : 0));
 }
 
 __device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff& lo, const bf16x8 (&qf)[4],
-                                       const f32x16& c0, const f32x16& c1, float scale_log2, float m_run,
-                                       float& l_run, const bf16x8 (&pp)[2][2], bf16x8 (&pn)[2][2], f32x16& n0,
-                                       f32x16& n1, f32x16 (&oacc)[2]) {
+                                       float m_run, const f32x16& c0, const f32x16& c1, float& l_run,
+                                       const bf16x8 (&pp)[2][2], bf16x8 (&pn)[2][2], f32x16& n0, f32x16& n1,
+                                       f32x16 (&oacc)[2]) {
   bf16x8 fr[3];
   fr[0] = step_frag(sK, sV, lo, 0);
   fr[1] = step_frag(sK, sV, lo, 1);
-  // pair st: score block w = st & 1 (s0 or s1), rows r, r+1 with r = 8 (st >> 3) + 2 ((st >> 1) & 3)
+  // pair st: score block w = st & 1 (c0 or c1), rows r, r+1 with r = 8 (st >> 3) + 2 ((st >> 1) & 3)
   auto score = [&](int st, int e) -> float {
     const int r = (st >> 3) * 8 + 2 * ((st >> 1) & 3) + e;
     return (st & 1) ? c1[r] : c0[r];
   };
-  float x[16][2], ex[16][2];
+  float ex[16][2];
 #pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    x[0][e] = fmaf(score(0, e), scale_log2, -m_run);
-    x[1][e] = fmaf(score(1, e), scale_log2, -m_run);
-  }
-#pragma unroll
-  for (int e = 0; e < 2; ++e) ex[0][e] = fast_exp2(x[0][e]);
+  for (int e = 0; e < 2; ++e) ex[0][e] = fast_exp2(score(0, e));
   __builtin_amdgcn_sched_barrier(0);
-  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+  const bf16x2 ones2 = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
-  n0 = f32x16{};
-  n1 = f32x16{};
 #pragma unroll
-  for (int st = 0; st < 16; ++st) {
+  for (int st = 0; st < 18; ++st) {
     if (st + 2 < 16) fr[(st + 2) % 3] = step_frag(sK, sV, lo, st + 2);
-    const bf16x8 f = fr[st % 3];
     if (st < 8) {
-      const int ks = st >> 1;
+      const int kb = st >> 2, hf = (st >> 1) & 1, db = st & 1;
+      oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], pp[kb][hf], oacc[db], 0, 0, 0);
+    } else if (st < 16) {
+      const int ks = (st - 8) >> 1;
       if (st & 1)
-        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, qf[ks], n1, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? f32x16{} : n1, 0, 0, 0);
       else
-        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, qf[ks], n0, 0, 0, 0);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? f32x16{} : n0, 0, 0, 0);
     } else {
-      const int kb = (st - 8) >> 2, hf = ((st - 8) >> 1) & 1, db = (st - 8) & 1;
-      oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, pp[kb][hf], oacc[db], 0, 0, 0);
+      // one k = 8 step: k = 0 and k = 4 of A are one for every key, k = 0
+      // and k = 4 of B (the lanes of both halves) hold -max/2 of the query
+      // (bf16-exact, as max is), the other k are zero: the step adds -max
+      const float half_neg_m = -0.5f * m_run;
+      v4s ones{}, qaug{};
+      ones[0] = (short)0x3f80;  // bf16 1.0
+      qaug[0] = (short)(__builtin_bit_cast(unsigned, half_neg_m) >> 16);
+      if (st == 16)
+        n0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(ones, qaug, n0, 0, 0, 0);
+      else
+        n1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(ones, qaug, n1, 0, 0, 0);
     }
-    if (st + 2 < 16)
-#pragma unroll
-      for (int e = 0; e < 2; ++e) x[st + 2][e] = fmaf(score(st + 2, e), scale_log2, -m_run);
     if (st + 1 < 16)
 #pragma unroll
-      for (int e = 0; e < 2; ++e) ex[st + 1][e] = fast_exp2(x[st + 1][e]);
-    {
+      for (int e = 0; e < 2; ++e) ex[st + 1][e] = fast_exp2(score(st + 1, e));
+    if (st < 16) {
       const int hf = st >> 3, i = (st >> 1) & 3, w = st & 1;
       bf16x2 pr;
       pr[0] = (bf16)ex[st][0];
       pr[1] = (bf16)ex[st][1];
-      psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, psum, false);
+      psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones2, psum, false);
       pn[w][hf][2 * i] = pr[0];
       pn[w][hf][2 * i + 1] = pr[1];
     }
     __builtin_amdgcn_sched_barrier(0);
   }
   l_run += psum;
+}
+
+// Probabilities exp2(s - delta) of the last tile's shifted scores, rounded to
+// bf16 in P^T operand order; their row sum is added to l_run.
+__device__ __forceinline__ void last_probs(const f32x16& s0, const f32x16& s1, float delta, float& l_run,
+                                           bf16x8 (&pf)[2][2]) {
+  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+  float psum = 0.0f;
+#pragma unroll
+  for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = hf * 8 + 2 * i;
+      bf16x2 a, b;
+      a[0] = (bf16)fast_exp2(s0[r] - delta);
+      a[1] = (bf16)fast_exp2(s0[r + 1] - delta);
+      b[0] = (bf16)fast_exp2(s1[r] - delta);
+      b[1] = (bf16)fast_exp2(s1[r + 1] - delta);
+      psum = __builtin_amdgcn_fdot2_f32_bf16(a, ones, psum, false);
+      psum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, psum, false);
+      pf[0][hf][2 * i] = a[0];
+      pf[0][hf][2 * i + 1] = a[1];
+      pf[1][hf][2 * i] = b[0];
+      pf[1][hf][2 * i + 1] = b[1];
+    }
+  l_run += psum;
+}
+
+// Running max for scores that arrive shifted by it: mx is the tile max
+// relative to m_run.  The max moves, to m_run + mx rounded to bf16 (so that
+// -max/2 is exact as a bf16 operand), only where mx exceeds 2^kRescaleLog2;
+// returns the factor for O (exactly 1 elsewhere) and, in delta, by how much
+// the max moved, i.e. the shift the tile's scores still need.
+__device__ __forceinline__ float raise_max_shifted(float mx, float& m_run, float& l_run, float& delta) {
+  const float m_new = (mx > kRescaleLog2) ? (float)(bf16)(m_run + mx) : m_run;
+  delta = m_new - m_run;
+  const float alpha = fast_exp2(-delta);
+  l_run *= alpha;
+  m_run = m_new;
+  return alpha;
 }
 }  // namespace dma
 
@@ -571,33 +615,54 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   bf16x8 qf[4];
   const bf16* Qg = static_cast<const bf16*>(io.q) + (int64_t)seg0 * ldq + head * HD;
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks)
+  for (int ks = 0; ks < 4; ++ks) {
     qf[ks] = (ql < Lq) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)ql * ldq + ks * 16 + g * 8) : zero8;
+    // scores come out of the MFMAs already scaled: q * log2(e) / sqrt(d), rounded to bf16
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qf[ks][e] = (bf16)((float)qf[ks][e] * scale_log2);
+  }
+
 
   // Copy sources: lane i of copy n (n = 0, 1) fills row 8(2 wave + n) + i/8,
-  // slot i%8 of a tile.  Element offsets from the segment's first key, rows
-  // clamped to the last key of the segment.
+  // slot i%8 of a tile.  The tile's first key row is a wave-uniform base
+  // address; each lane keeps its byte offset from it.  In a tile that runs
+  // past the segment's last key the rows past it repeat that key.
   const bf16* Kg = static_cast<const bf16*>(io.k) + (int64_t)kv0 * ld + head * HD;
   const bf16* Vg = static_cast<const bf16*>(io.v) + (int64_t)kv0 * ld + head * HD;
-  int koff[2], voff[2], klast[2], vlast[2];
+  auto copy_row = [&](int n) { return 8 * (2 * wave + n) + (lane >> 3); };
+  auto k_chunk = [&](int row) { return (lane & 7) ^ ((row >> 1) & 7); };
+  auto v_chunk = [&](int row) { return (lane & 7) ^ (2 * (row & 3)); };
+  uint32_t koff[2];
 #pragma unroll
-  for (int n = 0; n < 2; ++n) {
-    const int row = 8 * (2 * wave + n) + (lane >> 3);
-    const int kc = (lane & 7) ^ ((row >> 1) & 7), vc = (lane & 7) ^ (2 * (row & 3));
-    koff[n] = row * ld + kc * 8;
-    voff[n] = row * ld + vc * 8;
-    klast[n] = (L - 1) * ld + kc * 8;
-    vlast[n] = (L - 1) * ld + vc * 8;
-  }
+  for (int n = 0; n < 2; ++n) koff[n] = 2u * (uint32_t)(copy_row(n) * ld + k_chunk(copy_row(n)) * 8);
+  const uint32_t voff = 2u * (uint32_t)(copy_row(0) * ld + v_chunk(copy_row(0)) * 8);  // copy 1: 8 rows on
   auto copy_k = [&](int kbase, int buf) {
+    const bf16* base = Kg + (int64_t)kbase * ld;
+    if (kbase + AK <= L) {
 #pragma unroll
-    for (int n = 0; n < 2; ++n)
-      lds_dma16(Kg + min(koff[n] + kbase * ld, klast[n]), sm.k[buf] + (2 * wave + n) * 1024);
+      for (int n = 0; n < 2; ++n) lds_dma16_at(base, koff[n], sm.k[buf] + (2 * wave + n) * 1024);
+    } else {
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int row = copy_row(n);
+        const uint32_t off = 2u * (uint32_t)(min(row, L - 1 - kbase) * ld + k_chunk(row) * 8);
+        lds_dma16_at(base, off, sm.k[buf] + (2 * wave + n) * 1024);
+      }
+    }
   };
   auto copy_v = [&](int kbase, int buf) {
+    const bf16* base = Vg + (int64_t)kbase * ld;
+    if (kbase + AK <= L) {
 #pragma unroll
-    for (int n = 0; n < 2; ++n)
-      lds_dma16(Vg + min(voff[n] + kbase * ld, vlast[n]), sm.v[buf] + (2 * wave + n) * 1024);
+      for (int n = 0; n < 2; ++n) lds_dma16_at(base + n * 8 * ld, voff, sm.v[buf] + (2 * wave + n) * 1024);
+    } else {
+#pragma unroll
+      for (int n = 0; n < 2; ++n) {
+        const int row = copy_row(n);
+        const uint32_t off = 2u * (uint32_t)(min(row, L - 1 - kbase) * ld + v_chunk(row) * 8);
+        lds_dma16_at(base, off, sm.v[buf] + (2 * wave + n) * 1024);
+      }
+    }
   };
   // Barrier after this wave's LDS operations and all but its newest `keep`
   // copies (the copies issued in the current iteration stay in flight); no
@@ -618,7 +683,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
 
   const dma::LaneOff lo = dma::lane_offsets(lane);
   f32x16 oacc[2] = {f32x16{}, f32x16{}};
-  float m_run = -INFINITY, l_run = 0.0f;
+  float m_run, l_run = 0.0f;
   const int nkt = (L + AK - 1) / AK;
 
   // Tile j of K and of V lives in ring slot j % 3.  Iteration t: softmax of
@@ -635,15 +700,26 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     }
   };
   int slot = 0;  // t % 3
+  // The scores of every tile arrive shifted by the running max as it stood
+  // when their QK was issued (tile 0: shifted here by its own max).  Unless
+  // the max moved since, the probabilities are exp2 of the MFMA output with
+  // no further arithmetic.
   auto iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, bf16x8 (&pp)[2][2],
                   bf16x8 (&pn)[2][2]) {
     const int s1 = slot == 2 ? 0 : slot + 1, s2 = slot == 0 ? 2 : slot - 1;  // (t+1) % 3, (t-1) % 3
     copy_k(min(t + 3, nkt - 1) * AK, slot);
     copy_v((t + 1) * AK, s1);
-    const float a_new = raise_max(tile_max<false>(c0, c1, g, t * AK, L, scale_log2), m_run, l_run);
+    float delta;
+    const float a_new = dma::raise_max_shifted(tile_max<false>(c0, c1, g, t * AK, L, 1.0f), m_run, l_run, delta);
     rescale_o();
     alpha = a_new;
-    dma::region(sm.k[s1], sm.v[s2], lo, qf, c0, c1, scale_log2, m_run, l_run, pp, pn, n0, n1, oacc);
+    if (__ballot(delta != 0.0f) != 0)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        c0[r] -= delta;
+        c1[r] -= delta;
+      }
+    dma::region(sm.k[s1], sm.v[s2], lo, qf, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
     land(Keep4{});
     slot = s1;
   };
@@ -655,6 +731,14 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   land(Keep4{});
   f32x16 a0, a1, b0, b1;
   dma::qk(sm.k[0], lo, qf, a0, a1);
+  {  // the running max starts at tile 0's (keys past L masked), rounded to bf16
+    m_run = (float)(bf16)tile_max<true>(a0, a1, g, 0, L, 1.0f);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      a0[r] -= m_run;
+      a1[r] -= m_run;
+    }
+  }
   // iteration 0 copies K(3) into slot 0: every wave must be done reading K(0)
   land(Keep4{});
   bf16x8 pa[2][2] = {{zero8, zero8}, {zero8, zero8}}, pb[2][2];
@@ -675,12 +759,13 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
   {  // last tile t = nkt - 1 (possibly partial); V(t) was copied in iteration t-1
     const int sprev = slot == 0 ? 2 : slot - 1;
-    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L, scale_log2)
-                                   : tile_max<false>(a0, a1, g, t * AK, L, scale_log2);
-    const float a_new = raise_max(mx, m_run, l_run);
+    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L, 1.0f)
+                                   : tile_max<false>(a0, a1, g, t * AK, L, 1.0f);
+    float delta;
+    const float a_new = dma::raise_max_shifted(mx, m_run, l_run, delta);
     rescale_o();
     alpha = a_new;
-    tile_probs(a0, a1, scale_log2, m_run, l_run, pb);
+    dma::last_probs(a0, a1, delta, l_run, pb);
     dma::pv(sm.v[sprev], lo, pa, oacc);
     rescale_o();
     land(Keep0{});

@@ -98,6 +98,15 @@ __device__ __forceinline__ void lds_dma16(const void* gsrc, const void* lds_dst)
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gsrc), "s"(m0) : "memory", "m0");
 }
 
+// The same copy from a wave-uniform base address (an SGPR pair) plus a
+// per-lane 32-bit byte offset, so that moving the source costs scalar
+// arithmetic only.
+__device__ __forceinline__ void lds_dma16_at(const void* sbase, uint32_t voff, const void* lds_dst) {
+  const uint32_t m0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)lds_dst;
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(m0)
+               : "memory", "m0");
+}
+
 __device__ __forceinline__ float bf2f(bf16 v) { return (float)v; }
 __device__ __forceinline__ bf16 f2bf(float v) { return (bf16)v; }  // round to nearest even
 
