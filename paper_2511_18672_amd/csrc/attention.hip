@@ -294,16 +294,26 @@ __global__ __launch_bounds__(256, 2) void k_attn_bf16_d72(AttnIO io, int D, int 
   attn_body<72>(io, D, heads, scale_log2, S, sm);
 }
 
-__device__ __forceinline__ float max_across_halves(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+// Three-way max as one instruction.  Written out because the compiler
+// otherwise first quiets each MFMA result that enters a two-operand max (an
+// extra instruction per value); scores are never signalling NaNs.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
 }
 
-// Row max of one 64-key tile in log2 units (scores s0: keys 0..31, s1: keys
-// 32..63 of the tile, slot r = key 8*(r/4) + 4*g + r%4; lanes l and l^32 hold
-// the two halves of the same query's keys).
+__device__ __forceinline__ float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return max3(__uint_as_float(r[0]), __uint_as_float(r[1]), __uint_as_float(r[1]));
+}
+
+// Row max of one 64-key tile (scores s0: keys 0..31, s1: keys 32..63 of the
+// tile, slot r = key 8*(r/4) + 4*g + r%4; lanes l and l^32 hold the two
+// halves of the same query's keys).  With MASK, keys past L are set to -inf
+// first.
 template <bool MASK>
-__device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kbase, int L, float scale_log2) {
+__device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kbase, int L) {
   if (MASK) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -312,51 +322,17 @@ __device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kba
       if (key + 32 >= L) s1[r] = -INFINITY;
     }
   }
+  // four independent chains of four max3 over the 32 values, then one max3 and a max
   float m4[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    float t = fmaxf(fmaxf(s0[4 * q], s0[4 * q + 1]), s0[4 * q + 2]);
-    t = fmaxf(fmaxf(t, s0[4 * q + 3]), s1[4 * q]);
-    t = fmaxf(fmaxf(t, s1[4 * q + 1]), s1[4 * q + 2]);
-    m4[q] = fmaxf(t, s1[4 * q + 3]);
+    float t = max3(s0[4 * q], s0[4 * q + 1], s0[4 * q + 2]);
+    t = max3(t, s0[4 * q + 3], s1[4 * q]);
+    t = max3(t, s1[4 * q + 1], s1[4 * q + 2]);
+    m4[q] = t;
   }
-  return max_across_halves(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * scale_log2;
-}
-
-// Probabilities exp2(s * scale - m) of one tile, rounded to bf16 in P^T
-// operand order; their row sum (of the rounded values) is added to l_run.
-__device__ __forceinline__ void tile_probs(const f32x16& s0, const f32x16& s1, float scale_log2, float m_run,
-                                           float& l_run, bf16x8 (&pf)[2][2]) {
-  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
-  float psum = 0.0f;
-#pragma unroll
-  for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = hf * 8 + 2 * i;
-      bf16x2 a, b;
-      a[0] = (bf16)fast_exp2(fmaf(s0[r], scale_log2, -m_run));
-      a[1] = (bf16)fast_exp2(fmaf(s0[r + 1], scale_log2, -m_run));
-      b[0] = (bf16)fast_exp2(fmaf(s1[r], scale_log2, -m_run));
-      b[1] = (bf16)fast_exp2(fmaf(s1[r + 1], scale_log2, -m_run));
-      psum = __builtin_amdgcn_fdot2_f32_bf16(a, ones, psum, false);
-      psum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, psum, false);
-      pf[0][hf][2 * i] = a[0];
-      pf[0][hf][2 * i + 1] = a[1];
-      pf[1][hf][2 * i] = b[0];
-      pf[1][hf][2 * i + 1] = b[1];
-    }
-  l_run += psum;
-}
-
-// Moves the running max to mx where it grew by more than 2^kRescaleLog2 and
-// returns the factor for O (exactly 1, exp2(0), on lanes that keep theirs).
-__device__ __forceinline__ float raise_max(float mx, float& m_run, float& l_run) {
-  const float m_new = (mx > m_run + kRescaleLog2) ? mx : m_run;
-  const float alpha = fast_exp2(m_run - m_new);
-  l_run *= alpha;
-  m_run = m_new;
-  return alpha;
+  const float m = max3(max3(m4[0], m4[1], s1[3]), max3(m4[2], m4[3], s1[7]), max3(s1[11], s1[15], s1[15]));
+  return max_across_halves(m);
 }
 
 // ---------------------------------------------------------------------------
@@ -542,6 +518,14 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
     __builtin_amdgcn_sched_barrier(0);
   }
   l_run += psum;
+  // Pin the probabilities here: otherwise the compiler sinks their whole
+  // computation past the next iteration's branches, next to their use,
+  // undoing the interleaving with this iteration's MFMAs.
+#pragma unroll
+  for (int w = 0; w < 2; ++w)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) asm volatile("" : "+v"(pn[w][hf]));
+  asm volatile("" : "+v"(l_run));
 }
 
 // Probabilities exp2(s - delta) of the last tile's shifted scores, rounded to
@@ -710,7 +694,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     copy_k(min(t + 3, nkt - 1) * AK, slot);
     copy_v((t + 1) * AK, s1);
     float delta;
-    const float a_new = dma::raise_max_shifted(tile_max<false>(c0, c1, g, t * AK, L, 1.0f), m_run, l_run, delta);
+    const float a_new = dma::raise_max_shifted(tile_max<false>(c0, c1, g, t * AK, L), m_run, l_run, delta);
     rescale_o();
     alpha = a_new;
     if (__ballot(delta != 0.0f) != 0)
@@ -732,7 +716,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   f32x16 a0, a1, b0, b1;
   dma::qk(sm.k[0], lo, qf, a0, a1);
   {  // the running max starts at tile 0's (keys past L masked), rounded to bf16
-    m_run = (float)(bf16)tile_max<true>(a0, a1, g, 0, L, 1.0f);
+    m_run = (float)(bf16)tile_max<true>(a0, a1, g, 0, L);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       a0[r] -= m_run;
@@ -759,8 +743,8 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
   {  // last tile t = nkt - 1 (possibly partial); V(t) was copied in iteration t-1
     const int sprev = slot == 0 ? 2 : slot - 1;
-    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L, 1.0f)
-                                   : tile_max<false>(a0, a1, g, t * AK, L, 1.0f);
+    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L)
+                                   : tile_max<false>(a0, a1, g, t * AK, L);
     float delta;
     const float a_new = dma::raise_max_shifted(mx, m_run, l_run, delta);
     rescale_o();
