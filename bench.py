@@ -146,8 +146,9 @@ def copy_mode(args):
 
 def peaks_mode(args):
     """Achievable rates to read the roofline fractions against: a bf16 MFMA loop
-    (four independent 32x32x16 chains per wave, 2048 workgroups of 4 waves) and
-    the 1 GiB fp32 copy."""
+    (four independent 32x32x16 chains per wave, 2048 workgroups of 4 waves) on
+    constant and on random operands (the sustained rate depends on the data),
+    and the 1 GiB fp32 copy."""
     import torch
 
     import paper_2511_18672_amd as S
@@ -156,21 +157,24 @@ def peaks_mode(args):
     iters = 4096
     flop = float(S.PEAK_BLOCKS) * 4 * iters * 4 * 32768
     stream = torch.cuda.current_stream()
-    for _ in range(3):
-        S.sphinx_peak_mfma(iters, out)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        S.sphinx_peak_mfma(iters, out)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    avg_s = e0.elapsed_time(e1) / args.steps / 1e3
-    tf = flop / avg_s / 1e12
-    assert bool(torch.isfinite(out).all())
-    print(json.dumps({"mode": "peaks", "mfma_bf16_tflops": round(tf, 1),
-                      "frac_of_2500": round(tf / PEAK_BF16_TFLOPS, 4), "flop_per_launch": flop,
-                      "avg_us": round(avg_s * 1e6, 1)}), flush=True)
+    rec = {"mode": "peaks", "flop_per_launch": flop}
+    for name, kind in (("constant", S.PEAK_CONSTANT), ("random", S.PEAK_RANDOM)):
+        for _ in range(3):
+            S.sphinx_peak_mfma(iters, out, kind)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            S.sphinx_peak_mfma(iters, out, kind)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        avg_s = e0.elapsed_time(e1) / args.steps / 1e3
+        tf = flop / avg_s / 1e12
+        assert bool(torch.isfinite(out).all())
+        rec[f"mfma_bf16_tflops_{name}"] = round(tf, 1)
+        rec[f"frac_of_2500_{name}"] = round(tf / PEAK_BF16_TFLOPS, 4)
+        rec[f"avg_us_{name}"] = round(avg_s * 1e6, 1)
+    print(json.dumps(rec), flush=True)
     copy_mode(args)
 
 

@@ -406,9 +406,17 @@ sphinx_status sphinx_timing_read(sphinx_kernel_class k, int64_t* launches, doubl
  * per round) and writes one checksum float per workgroup to `out` (dev float
  * [SPHINX_PEAK_BLOCKS], caller-owned).  FLOPs per call:
  * SPHINX_PEAK_BLOCKS * 4 * iters * 4 * 32768; the caller times the call on
- * `stream`.  iters must lie in [1, 2^24]. */
+ * `stream`.  iters must lie in [1, 2^24].  operands selects the data the
+ * MFMAs multiply, since the sustained rate depends on it (the chip lowers its
+ * clock as the operand bits toggle more):
+ *   SPHINX_PEAK_CONSTANT: small constants, the same every round (best case);
+ *   SPHINX_PEAK_RANDOM:   hashed random bf16 in [-2, 2), eight operand pairs
+ *                         in rotation (closer to real activations).
+ * Any other value: SPHINX_E_INVALID. */
 #define SPHINX_PEAK_BLOCKS 2048
-sphinx_status sphinx_peak_mfma(int32_t iters, float* out, void* stream);
+#define SPHINX_PEAK_CONSTANT 0
+#define SPHINX_PEAK_RANDOM 1
+sphinx_status sphinx_peak_mfma(int32_t iters, int32_t operands, float* out, void* stream);
 
 #ifdef __cplusplus
 }

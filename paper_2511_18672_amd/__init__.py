@@ -4,7 +4,7 @@ The compute path is ``libsphinx.so`` (hand-written HIP for gfx950 behind the C
 ABI of include/sphinx.h).  This package is its thin Python binding plus the
 step driver; it has no CPU fallback and raises if the library is missing.
 """
-from .binding import (ATTN_FACTORISED, ATTN_JOINT, GRID_PER_FRAME, GRID_SHARED, sphinx_plan_step_grid, BF16, F32, KLogic, make_klogic, sphinx_adaptive_start, KERNEL_CLASSES, NCHW, PEAK_BLOCKS, TOKENS, EXPORTED, SphinxError, gather, lib,
+from .binding import (ATTN_FACTORISED, ATTN_JOINT, GRID_PER_FRAME, GRID_SHARED, sphinx_plan_step_grid, BF16, F32, KLogic, make_klogic, sphinx_adaptive_start, KERNEL_CLASSES, NCHW, PEAK_BLOCKS, PEAK_CONSTANT, PEAK_RANDOM, TOKENS, EXPORTED, SphinxError, gather, lib,
                       make_requests, model_desc, plan_step, refine_step, scatter_blend, select_mask, sphinx_gather,
                       sphinx_gather_ctx, sphinx_kv_cache_bytes, sphinx_mask_frontend,
                       sphinx_mask_frontend_workspace_bytes, sphinx_model_blob_bytes, sphinx_model_param,
@@ -14,7 +14,7 @@ from .binding import (ATTN_FACTORISED, ATTN_JOINT, GRID_PER_FRAME, GRID_SHARED, 
                       sphinx_status_string, sphinx_timing_enable, sphinx_timing_read)
 from .refiner import Refiner, from_workload, pack_weights
 
-__all__ = ["ATTN_FACTORISED", "ATTN_JOINT", "GRID_PER_FRAME", "GRID_SHARED", "sphinx_plan_step_grid", "BF16", "F32", "KLogic", "make_klogic", "sphinx_adaptive_start", "KERNEL_CLASSES", "NCHW", "PEAK_BLOCKS", "TOKENS", "EXPORTED", "SphinxError", "Refiner",
+__all__ = ["ATTN_FACTORISED", "ATTN_JOINT", "GRID_PER_FRAME", "GRID_SHARED", "sphinx_plan_step_grid", "BF16", "F32", "KLogic", "make_klogic", "sphinx_adaptive_start", "KERNEL_CLASSES", "NCHW", "PEAK_BLOCKS", "PEAK_CONSTANT", "PEAK_RANDOM", "TOKENS", "EXPORTED", "SphinxError", "Refiner",
            "from_workload", "pack_weights", "lib", "make_requests", "model_desc", "sphinx_gather",
            "sphinx_gather_ctx", "sphinx_kv_cache_bytes", "sphinx_mask_frontend",
            "sphinx_mask_frontend_workspace_bytes", "sphinx_model_blob_bytes", "sphinx_model_param",

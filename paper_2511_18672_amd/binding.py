@@ -34,6 +34,7 @@ EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_par
             "sphinx_refine_step_cached", "sphinx_scatter_masked", "sphinx_mask_frontend_workspace_bytes",
             "sphinx_mask_frontend", "sphinx_adaptive_start"]
 PEAK_BLOCKS = 2048
+PEAK_CONSTANT, PEAK_RANDOM = 0, 1
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
                   "gemm_mlp2", "final", "scatter", "kv_store", "frontend"]
 
@@ -100,7 +101,7 @@ def lib() -> ctypes.CDLL:
                                            c_int32, P]),
         "sphinx_timing_enable": (c_int32, [c_int32]),
         "sphinx_timing_read": (c_int32, [c_int32, POINTER(c_int64), POINTER(ctypes.c_double)]),
-        "sphinx_peak_mfma": (c_int32, [c_int32, P, P]),
+        "sphinx_peak_mfma": (c_int32, [c_int32, c_int32, P, P]),
         "sphinx_plan_cache": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, c_int32, c_int32, P, P, P, P]),
         "sphinx_kv_cache_bytes": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, POINTER(c_size_t)]),
         "sphinx_gather_ctx": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P,
@@ -279,9 +280,10 @@ def sphinx_timing_read() -> Dict[str, tuple]:
     return out
 
 
-def sphinx_peak_mfma(iters: int, out, stream=None):
-    """MFMA calibration loop (outside the method): SPHINX_PEAK_BLOCKS * 4 * iters * 4 * 32768 FLOP."""
-    _check("sphinx_peak_mfma", lib().sphinx_peak_mfma(iters, _ptr(out), _stream(stream)))
+def sphinx_peak_mfma(iters: int, out, operands: int = PEAK_CONSTANT, stream=None):
+    """MFMA calibration loop (outside the method): SPHINX_PEAK_BLOCKS * 4 * iters * 4 * 32768 FLOP
+    on constant (PEAK_CONSTANT) or random (PEAK_RANDOM) bf16 operands."""
+    _check("sphinx_peak_mfma", lib().sphinx_peak_mfma(iters, operands, _ptr(out), _stream(stream)))
 
 
 def sphinx_plan_cache(reqs, s_start: np.ndarray, nsteps: np.ndarray, step: int, period: int,

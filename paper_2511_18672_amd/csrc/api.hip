@@ -865,9 +865,11 @@ sphinx_status sphinx_timing_read(sphinx_kernel_class k, int64_t* launches, doubl
   return SPHINX_OK;
 }
 
-sphinx_status sphinx_peak_mfma(int32_t iters, float* out, void* stream) {
+sphinx_status sphinx_peak_mfma(int32_t iters, int32_t operands, float* out, void* stream) {
   if (iters < 1 || iters > (1 << 24) || out == nullptr || !aligned(out, 16)) return SPHINX_E_INVALID;
-  return hip_status(launch_peak_mfma(iters, out, SPHINX_PEAK_BLOCKS, (hipStream_t)stream));
+  if (operands != SPHINX_PEAK_CONSTANT && operands != SPHINX_PEAK_RANDOM) return SPHINX_E_INVALID;
+  return hip_status(launch_peak_mfma(iters, operands == SPHINX_PEAK_RANDOM, out, SPHINX_PEAK_BLOCKS,
+                                     (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -19,6 +19,8 @@
 // otherwise the bf16 path runs k_gemm_dma_* (described with its code).
 //
 // fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -468,20 +470,44 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ A, c
   }
 }
 // Calibration loop: four independent 32x32x16 bf16 MFMA chains per wave.
+// MFMA calibration loop; RANDOM: operands are hashed random bf16 in [-2, 2),
+// eight (A, B) pairs used in rotation.
+__device__ __forceinline__ float peak_rand(unsigned x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return (float)(x & 0xffffu) * (4.0f / 65536.0f) - 2.0f;
+}
+
+template <bool RANDOM>
 __global__ __launch_bounds__(256) void k_peak_mfma(int iters, float* __restrict__ out) {
-  bf16x8 a, b;
+  constexpr int NS = RANDOM ? 8 : 1;
+  const unsigned t = blockIdx.x * 256u + threadIdx.x;
+  bf16x8 a[NS], b[NS];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    a[i] = (bf16)(1e-3f * (float)((threadIdx.x + i) & 15));
-    b[i] = (bf16)(1e-3f * (float)(i + 1));
-  }
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      a[s][i] = RANDOM ? (bf16)peak_rand(t * 64u + s * 8u + i) : (bf16)(1e-3f * (float)((threadIdx.x + i) & 15));
+      b[s][i] = RANDOM ? (bf16)peak_rand(0x9e3779b9u ^ (t * 64u + s * 8u + i)) : (bf16)(1e-3f * (float)(i + 1));
+    }
   f32x16 c0 = f32x16{}, c1 = f32x16{}, c2 = f32x16{}, c3 = f32x16{};
-  for (int it = 0; it < iters; ++it) {
-    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
-    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
-    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+  // one round: four MFMAs on operand pairs s..s+3 (static register indices)
+  auto round = [&](auto sc) {
+    constexpr int s = decltype(sc)::value;
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s % NS], b[(s + 1) % NS], c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(s + 1) % NS], b[(s + 2) % NS], c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(s + 2) % NS], b[(s + 3) % NS], c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(s + 3) % NS], b[s % NS], c3, 0, 0, 0);
+  };
+  int it = 0;
+  for (; it + 1 < iters; it += 2) {
+    round(std::integral_constant<int, 0>{});
+    round(std::integral_constant<int, 4>{});
   }
+  if (it < iters) round(std::integral_constant<int, 0>{});
   float sum = 0.0f;
 #pragma unroll
   for (int r = 0; r < 16; ++r) sum += c0[r] + c1[r] + c2[r] + c3[r];
@@ -518,8 +544,11 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
   return hipGetLastError();
 }
 
-hipError_t launch_peak_mfma(int iters, float* out, int blocks, hipStream_t s) {
-  k_peak_mfma<<<blocks, 256, 0, s>>>(iters, out);
+hipError_t launch_peak_mfma(int iters, bool random, float* out, int blocks, hipStream_t s) {
+  if (random)
+    k_peak_mfma<true><<<blocks, 256, 0, s>>>(iters, out);
+  else
+    k_peak_mfma<false><<<blocks, 256, 0, s>>>(iters, out);
   return hipGetLastError();
 }
 

@@ -100,7 +100,7 @@ hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm,
 // gemm.hip
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
                        const GemmEpi& e, hipStream_t s);
-hipError_t launch_peak_mfma(int iters, float* out, int blocks, hipStream_t s);
+hipError_t launch_peak_mfma(int iters, bool random, float* out, int blocks, hipStream_t s);
 
 // attention.hip
 hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,

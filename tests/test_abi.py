@@ -211,14 +211,17 @@ def test_timing_mask_validation(L):
 
 
 def test_peak_probe_validation(L):
-    """The MFMA calibration loop rejects an iteration count outside [1, 2^24]
-    and a missing or misaligned output before it touches a device."""
+    """The MFMA calibration loop rejects an iteration count outside [1, 2^24],
+    an unknown operand kind and a missing or misaligned output before it
+    touches a device."""
     buf = (ctypes.c_float * 8)()
     p = ctypes.addressof(buf)
-    assert L.sphinx_peak_mfma(0, ctypes.c_void_p(p), None) == INVALID
-    assert L.sphinx_peak_mfma((1 << 24) + 1, ctypes.c_void_p(p), None) == INVALID
-    assert L.sphinx_peak_mfma(16, None, None) == INVALID
-    assert L.sphinx_peak_mfma(16, ctypes.c_void_p(p + 4), None) == INVALID
+    assert L.sphinx_peak_mfma(0, 0, ctypes.c_void_p(p), None) == INVALID
+    assert L.sphinx_peak_mfma((1 << 24) + 1, 0, ctypes.c_void_p(p), None) == INVALID
+    assert L.sphinx_peak_mfma(16, 0, None, None) == INVALID
+    assert L.sphinx_peak_mfma(16, 0, ctypes.c_void_p(p + 4), None) == INVALID
+    assert L.sphinx_peak_mfma(16, 2, ctypes.c_void_p(p), None) == INVALID
+    assert L.sphinx_peak_mfma(16, -1, ctypes.c_void_p(p), None) == INVALID
 
 
 def test_frontend_validation(L):
