@@ -19,6 +19,7 @@
 // otherwise the bf16 path runs k_gemm_dma_* (described with its code).
 //
 // fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
+#include <atomic>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -214,27 +215,34 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
 //    own copies (vmcnt) and LDS reads (lgkmcnt) first.
 //  * The accumulation order per output (k-steps of 16 in ascending k, then the
 //    same epilogue) equals k_gemm_bf16's, so the results are bit-identical.
+//  * A 192-row variant (wave tiles 96x64, 80 KB of LDS, epilogue staged one
+//    wave row at a time) is launched where its smaller tile count packs into
+//    fewer rounds of two workgroups per CU; same results.
 namespace dma {
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
 // bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8)
 constexpr int wait_vm_lgkm0(int vm) { return 0x0070 | (vm & 15) | ((vm >> 4) << 14); }
 
-template <int BM, int BN, int NS>
+// EH: the fp32 epilogue tile is staged in EH row halves (EH = 2 when the
+// whole tile would need more LDS than the operand ring).
+template <int BM, int BN, int NS, int EH = 1>
 struct DmaCfg {
   static constexpr int BK = 64;
   static constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
   static constexpr int STAGE = (BM + BN) * 128;     // bytes per K-step
   static constexpr int COPIES = (BM + BN) / 32;     // copy instructions per wave per stage
   static constexpr int CLD = BN + 4;                // epilogue staging row (fp32)
-  static constexpr int SMEM = NS * STAGE > BM * CLD * 4 ? NS * STAGE : BM * CLD * 4;
+  static constexpr int EROWS = BM / EH;             // tile rows staged at once
+  static constexpr int SMEM = NS * STAGE > EROWS * CLD * 4 ? NS * STAGE : EROWS * CLD * 4;
+  static_assert(EH == 1 || EH == 2, "whole tile or two halves (one per wave row)");
 };
 
-template <int EPI, int BM, int BN, int NS>
+template <int EPI, int BM, int BN, int NS, int EH = 1>
 __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                               const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e,
                                               unsigned char* smem) {
-  typedef DmaCfg<BM, BN, NS> C;
+  typedef DmaCfg<BM, BN, NS, EH> C;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -361,16 +369,9 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 
-  // epilogue: fp32 tile staged in LDS, then 16-byte row-contiguous I/O
+  // epilogue: fp32 tile staged in LDS (whole, or one wave row's half at a
+  // time), then 16-byte row-contiguous I/O
   float* sC = reinterpret_cast<float*>(smem);
-#pragma unroll
-  for (int i = 0; i < C::TI; ++i)
-#pragma unroll
-    for (int j = 0; j < C::TJ; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        sC[(a_row0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
-  __syncthreads();
   constexpr int TPR = BN / 4;          // threads per row (one float4 each)
   constexpr int RPP = 256 / TPR;       // rows per pass
   const int c4 = (tid % TPR) * 4, rsub = tid / TPR;
@@ -380,50 +381,71 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n);
     bv = make_float4((float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]);
   }
-#pragma unroll 4
-  for (int p = 0; p < BM / RPP; ++p) {
-    const int row = p * RPP + rsub;
-    const int m = m0 + row;
-    if (m >= M) continue;
-    float4 v = *reinterpret_cast<const float4*>(&sC[row * C::CLD + c4]);
-    v.x += bv.x;
-    v.y += bv.y;
-    v.z += bv.z;
-    v.w += bv.w;
-    if constexpr (EPI == EPI_GATED) {
-      float* hp = reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n;
-      const float4 gv = *reinterpret_cast<const float4*>(e.gate + (int64_t)e.crow[m] * e.ldg + n);
-      float4 h = *reinterpret_cast<const float4*>(hp);
-      h.x = fmaf(1.0f + gv.x, v.x, h.x);
-      h.y = fmaf(1.0f + gv.y, v.y, h.y);
-      h.z = fmaf(1.0f + gv.z, v.z, h.z);
-      h.w = fmaf(1.0f + gv.w, v.w, h.w);
-      *reinterpret_cast<float4*>(hp) = h;
-    } else {
-      if constexpr (EPI == EPI_GELU) {
-        v.x = gelu_tanh(v.x);
-        v.y = gelu_tanh(v.y);
-        v.z = gelu_tanh(v.z);
-        v.w = gelu_tanh(v.w);
-      }
-      bf16x4 o;
-      o[0] = (bf16)v.x;
-      o[1] = (bf16)v.y;
-      o[2] = (bf16)v.z;
-      o[3] = (bf16)v.w;
-      *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
+#pragma unroll
+  for (int h = 0; h < EH; ++h) {
+    if (EH == 1 || wm == h) {
+      const int r0 = a_row0 - h * C::EROWS;
+#pragma unroll
+      for (int i = 0; i < C::TI; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            sC[(r0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
     }
+    __syncthreads();
+#pragma unroll 4
+    for (int p = 0; p < C::EROWS / RPP; ++p) {
+      const int row = p * RPP + rsub;
+      const int m = m0 + h * C::EROWS + row;
+      if (m >= M) continue;
+      float4 v = *reinterpret_cast<const float4*>(&sC[row * C::CLD + c4]);
+      v.x += bv.x;
+      v.y += bv.y;
+      v.z += bv.z;
+      v.w += bv.w;
+      if constexpr (EPI == EPI_GATED) {
+        float* hp = reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n;
+        const float4 gv = *reinterpret_cast<const float4*>(e.gate + (int64_t)e.crow[m] * e.ldg + n);
+        float4 hv = *reinterpret_cast<const float4*>(hp);
+        hv.x = fmaf(1.0f + gv.x, v.x, hv.x);
+        hv.y = fmaf(1.0f + gv.y, v.y, hv.y);
+        hv.z = fmaf(1.0f + gv.z, v.z, hv.z);
+        hv.w = fmaf(1.0f + gv.w, v.w, hv.w);
+        *reinterpret_cast<float4*>(hp) = hv;
+      } else {
+        if constexpr (EPI == EPI_GELU) {
+          v.x = gelu_tanh(v.x);
+          v.y = gelu_tanh(v.y);
+          v.z = gelu_tanh(v.z);
+          v.w = gelu_tanh(v.w);
+        }
+        bf16x4 o;
+        o[0] = (bf16)v.x;
+        o[1] = (bf16)v.y;
+        o[2] = (bf16)v.z;
+        o[3] = (bf16)v.w;
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
+      }
+    }
+    if (h + 1 < EH) __syncthreads();  // the next half reuses the staging rows
   }
 }
-#define SPHINX_GEMM_DMA_KERNEL(NAME, EPI)                                                                    \
+#define SPHINX_GEMM_DMA_KERNEL(NAME, EPI, BM, EH)                                                            \
   __global__ __launch_bounds__(256, 2) void NAME(const bf16* __restrict__ A, const bf16* __restrict__ W,          \
                                                  const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {  \
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, 2>::SMEM];                      \
-    gemm_dma_body<EPI, 128, 128, 2>(A, W, bias, M, N, K, e, smem);                                               \
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<BM, 128, 2, EH>::SMEM];                   \
+    gemm_dma_body<EPI, BM, 128, 2, EH>(A, W, bias, M, N, K, e, smem);                                            \
   }
-SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_bias, EPI_BIAS)
-SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gelu, EPI_GELU)
-SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gated, EPI_GATED)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_bias, EPI_BIAS, 128, 1)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gelu, EPI_GELU, 128, 1)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gated, EPI_GATED, 128, 1)
+// 192-row tiles (wave tiles 96x64, epilogue in two halves; 80 KB of LDS, so
+// still two workgroups per CU): fewer tiles for the same M, and 5/6 of the
+// LDS reads per MFMA of the 128-row tile
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_bias, EPI_BIAS, 192, 2)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
+SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
 }  // namespace dma
 
@@ -516,6 +538,31 @@ __global__ __launch_bounds__(256) void k_peak_mfma(int iters, float* __restrict_
 }
 }  // namespace
 
+namespace {
+// Compute units of the current device (cached per device; 256 if unknown).
+int cu_count() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int c = cache[dev].load(std::memory_order_relaxed);
+  if (c <= 0) {
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || c <= 0) c = 256;
+    cache[dev].store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+
+// Relative time of `tiles` workgroups at two per CU: whole rounds, plus half a
+// round for a last round that leaves every CU at most one tile (a lone tile
+// runs about twice as fast), else a whole one; `w` is the tile's cost in
+// 128-row-tile rounds.  Measured on the block GEMMs at M from 4.9k to 19.4k,
+// this picks the faster of the 128- and 192-row tiles or one within 1 %.
+double tile_rounds(int64_t tiles, int64_t slots, double w) {
+  const int64_t full = tiles / slots, rem = tiles % slots;
+  return w * ((double)full + (rem == 0 ? 0.0 : rem * 2 <= slots ? 0.5 : 1.0));
+}
+}  // namespace
+
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
                        const GemmEpi& e, hipStream_t s) {
   if (dt == SPHINX_BF16) {
@@ -523,10 +570,20 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
     const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
     const int64_t lim = (int64_t)1 << 31;  // the copy kernel uses 32-bit element offsets
     if ((int64_t)M * K < lim && (int64_t)N * K < lim) {
-      const int tiles = (int)(grid.x * grid.y);
-      if (epi == EPI_BIAS) dma::k_gemm_dma_bias<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
-      else if (epi == EPI_GELU) dma::k_gemm_dma_gelu<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
-      else dma::k_gemm_dma_gated<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+      const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
+      const int64_t t128 = nt * ((M + 127) / 128), t192 = nt * ((M + 191) / 192);
+      // a 192-row tile does 1.5x the work of a 128-row one in 1.41x the time
+      if (tile_rounds(t192, slots, 1.41) < tile_rounds(t128, slots, 1.0)) {
+        const int tiles = (int)t192;
+        if (epi == EPI_BIAS) dma::k_gemm_dma192_bias<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+        else if (epi == EPI_GELU) dma::k_gemm_dma192_gelu<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+        else dma::k_gemm_dma192_gated<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+      } else {
+        const int tiles = (int)t128;
+        if (epi == EPI_BIAS) dma::k_gemm_dma_bias<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+        else if (epi == EPI_GELU) dma::k_gemm_dma_gelu<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+        else dma::k_gemm_dma_gated<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+      }
     } else if (epi == EPI_BIAS) {
       k_gemm_bf16<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
     } else if (epi == EPI_GELU) {
