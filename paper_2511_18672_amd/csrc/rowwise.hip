@@ -39,44 +39,56 @@ __device__ __forceinline__ void load16<float>(const float* p, float (&w)[16]) {
   }
 }
 
-// One thread per (row, four consecutive columns), grid (column blocks, rows):
-// 16-byte loads of x, the four weight rows and the position tables, one
-// 16-byte store of h.
+// One thread per four consecutive columns and a block of kEmbedRows rows,
+// grid (column blocks, row blocks): the thread's 4 x 16 weights stay in
+// registers across the rows (the weight matrix is read once per row block,
+// not once per row); per row 16-byte loads of the position tables and one
+// 16-byte store of h (x and the packed position are wave-uniform).
+constexpr int kEmbedRows = 8;
+
 template <typename WT>
 __global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int n, int D, const WT* __restrict__ pe_w,
                                                 const WT* __restrict__ pe_b, const float* __restrict__ Ty,
                                                 const float* __restrict__ Tx, const float* __restrict__ Tf,
                                                 const int32_t* __restrict__ posc, float* __restrict__ h) {
   const int quads = D >> 2;
-  const int j = (int)blockIdx.y, qd = (int)blockIdx.x * kTPB + (int)threadIdx.x;
+  const int qd = (int)blockIdx.x * kTPB + (int)threadIdx.x;
   if (qd >= quads) return;
   const int c0 = 4 * qd;
-  const int pc = posc[j];
-  const int f = pc >> 20, y = (pc >> 10) & 1023, xx = pc & 1023;
-  float xr[16];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const f32x4 v = reinterpret_cast<const f32x4*>(x + (int64_t)j * 16)[q];
-    xr[4 * q] = v[0];
-    xr[4 * q + 1] = v[1];
-    xr[4 * q + 2] = v[2];
-    xr[4 * q + 3] = v[3];
-  }
-  const int half = D / 2;
-  const f32x4 pos = (c0 < half) ? *reinterpret_cast<const f32x4*>(Ty + (int64_t)y * half + c0)
-                                : *reinterpret_cast<const f32x4*>(Tx + (int64_t)xx * half + (c0 - half));
-  const f32x4 tf = *reinterpret_cast<const f32x4*>(Tf + (int64_t)f * D + c0);
-  f32x4 out;
+  float w[4][16], b[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    float w[16];
-    load16<WT>(pe_w + (int64_t)(c0 + e) * 16, w);
-    float v = load_as_f32(pe_b, c0 + e);
-#pragma unroll
-    for (int k = 0; k < 16; ++k) v = fmaf(xr[k], w[k], v);
-    out[e] = v + pos[e] + tf[e];
+    load16<WT>(pe_w + (int64_t)(c0 + e) * 16, w[e]);
+    b[e] = load_as_f32(pe_b, c0 + e);
   }
-  *reinterpret_cast<f32x4*>(h + (int64_t)j * D + c0) = out;
+  const int half = D / 2;
+  const int j0 = (int)blockIdx.y * kEmbedRows, j1 = min(j0 + kEmbedRows, n);
+#pragma unroll 2
+  for (int j = j0; j < j1; ++j) {
+    const int pc = posc[j];
+    const int f = pc >> 20, y = (pc >> 10) & 1023, xx = pc & 1023;
+    float xr[16];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4 v = reinterpret_cast<const f32x4*>(x + (int64_t)j * 16)[q];
+      xr[4 * q] = v[0];
+      xr[4 * q + 1] = v[1];
+      xr[4 * q + 2] = v[2];
+      xr[4 * q + 3] = v[3];
+    }
+    const f32x4 pos = (c0 < half) ? *reinterpret_cast<const f32x4*>(Ty + (int64_t)y * half + c0)
+                                  : *reinterpret_cast<const f32x4*>(Tx + (int64_t)xx * half + (c0 - half));
+    const f32x4 tf = *reinterpret_cast<const f32x4*>(Tf + (int64_t)f * D + c0);
+    f32x4 out;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float v = b[e];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) v = fmaf(xr[k], w[e][k], v);
+      out[e] = v + pos[e] + tf[e];
+    }
+    *reinterpret_cast<f32x4*>(h + (int64_t)j * D + c0) = out;
+  }
 }
 
 // Loads the row into registers and returns (mean, rstd).
@@ -213,8 +225,24 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
                                                 float* __restrict__ x) {
   extern __shared__ __attribute__((aligned(16))) unsigned char s_raw[];
   WT* s_wt = reinterpret_cast<WT*>(s_raw);  // [D][16]
-  for (int k = 0; k < 16; ++k)
-    for (int c = threadIdx.x; c < D; c += kTPB) s_wt[c * 16 + k] = out_w[(int64_t)k * D + c];
+  {  // transposed fill, [16][D] -> [D][16]: sixteen independent 16-byte loads per thread
+    constexpr int VE = 16 / (int)sizeof(WT);
+    typedef WT vec_t __attribute__((ext_vector_type(16 / sizeof(WT))));
+    for (int c0 = (int)threadIdx.x * VE; c0 < D; c0 += kTPB * VE) {
+      vec_t wk[16];
+#pragma unroll
+      for (int k = 0; k < 16; ++k) wk[k] = *reinterpret_cast<const vec_t*>(out_w + (int64_t)k * D + c0);
+#pragma unroll
+      for (int i = 0; i < VE; ++i)
+#pragma unroll
+        for (int q = 0; q < 16 / VE; ++q) {
+          vec_t col;
+#pragma unroll
+          for (int u = 0; u < VE; ++u) col[u] = wk[q * VE + u][i];
+          *reinterpret_cast<vec_t*>(s_wt + (c0 + i) * 16 + q * VE) = col;
+        }
+    }
+  }
   __syncthreads();
   const int lane = lane_id();
   const int quads = D >> 2;
@@ -293,7 +321,7 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
 hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const void* pe_b, sphinx_dtype wdt,
                         const float* Ty, const float* Tx, const float* Tf, const int32_t* posc, float* h,
                         hipStream_t s) {
-  const dim3 g((unsigned)((D / 4 + kTPB - 1) / kTPB), (unsigned)n);
+  const dim3 g((unsigned)((D / 4 + kTPB - 1) / kTPB), (unsigned)((n + kEmbedRows - 1) / kEmbedRows));
   if (wdt == SPHINX_BF16)
     k_embed<bf16><<<g, kTPB, 0, s>>>(x, n, D, (const bf16*)pe_w, (const bf16*)pe_b, Ty, Tx, Tf, posc, h);
   else
