@@ -438,10 +438,10 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16
 }
 
 // One iteration's MFMA work interleaved by hand with the softmax of the
-// previous tile: 18 steps of one MFMA (PV(t-1) for the first eight; QK(t+1),
-// four head-dim k-steps for each of the two 32-key blocks; then for each block
-// one k-step that adds -max through a column of ones, so that the scores
-// arrive scaled and shifted) and softmax work on two consecutive probability
+// previous tile: 16 steps of one MFMA (PV(t-1) for the first eight; QK(t+1),
+// four head-dim k-steps for each of the two 32-key blocks, the first of them
+// accumulating onto -max, so that the scores arrive scaled and shifted) and
+// softmax work on two consecutive probability
 // pairs, software-pipelined so that no instruction of a step waits on another
 // of the same step: the exponentials of pair st+1 and the bf16 pack and
 // row-sum dot product of pair st.  PV first lets the previous probabilities
@@ -478,35 +478,29 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
   __builtin_amdgcn_sched_barrier(0);
   const bf16x2 ones2 = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
+  f32x16 negm;  // -m_run in every element, built just before the first QK step
 #pragma unroll
-  for (int st = 0; st < 18; ++st) {
+  for (int st = 0; st < 16; ++st) {
     if (st + 2 < 16) fr[(st + 2) % 3] = step_frag(sK, sV, lo, st + 2);
     if (st < 8) {
       const int kb = st >> 2, hf = (st >> 1) & 1, db = st & 1;
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], pp[kb][hf], oacc[db], 0, 0, 0);
-    } else if (st < 16) {
+      if (st == 7)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) negm[r] = -m_run;
+    } else {
+      // the first k-step accumulates onto -max (every element of a lane
+      // belongs to its query), so the scores arrive shifted
       const int ks = (st - 8) >> 1;
       if (st & 1)
-        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? f32x16{} : n1, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? negm : n1, 0, 0, 0);
       else
-        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? f32x16{} : n0, 0, 0, 0);
-    } else {
-      // one k = 8 step: k = 0 and k = 4 of A are one for every key, k = 0
-      // and k = 4 of B (the lanes of both halves) hold -max/2 of the query
-      // (bf16-exact, as max is), the other k are zero: the step adds -max
-      const float half_neg_m = -0.5f * m_run;
-      v4s ones{}, qaug{};
-      ones[0] = (short)0x3f80;  // bf16 1.0
-      qaug[0] = (short)(__builtin_bit_cast(unsigned, half_neg_m) >> 16);
-      if (st == 16)
-        n0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(ones, qaug, n0, 0, 0, 0);
-      else
-        n1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(ones, qaug, n1, 0, 0, 0);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? negm : n0, 0, 0, 0);
     }
     if (st + 1 < 16)
 #pragma unroll
       for (int e = 0; e < 2; ++e) ex[st + 1][e] = fast_exp2(score(st + 1, e));
-    if (st < 16) {
+    {
       const int hf = st >> 3, i = (st >> 1) & 3, w = st & 1;
       bf16x2 pr;
       pr[0] = (bf16)ex[st][0];
@@ -555,12 +549,12 @@ __device__ __forceinline__ void last_probs(const f32x16& s0, const f32x16& s1, f
 }
 
 // Running max for scores that arrive shifted by it: mx is the tile max
-// relative to m_run.  The max moves, to m_run + mx rounded to bf16 (so that
-// -max/2 is exact as a bf16 operand), only where mx exceeds 2^kRescaleLog2;
-// returns the factor for O (exactly 1 elsewhere) and, in delta, by how much
-// the max moved, i.e. the shift the tile's scores still need.
+// relative to m_run.  The max moves, to m_run + mx, only where mx exceeds
+// 2^kRescaleLog2; returns the factor for O (exactly 1 elsewhere) and, in
+// delta, by how much the max moved, i.e. the shift the tile's scores still
+// need.
 __device__ __forceinline__ float raise_max_shifted(float mx, float& m_run, float& l_run, float& delta) {
-  const float m_new = (mx > kRescaleLog2) ? (float)(bf16)(m_run + mx) : m_run;
+  const float m_new = (mx > kRescaleLog2) ? m_run + mx : m_run;
   delta = m_new - m_run;
   const float alpha = fast_exp2(-delta);
   l_run *= alpha;
@@ -715,8 +709,8 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   land(Keep4{});
   f32x16 a0, a1, b0, b1;
   dma::qk(sm.k[0], lo, qf, a0, a1);
-  {  // the running max starts at tile 0's (keys past L masked), rounded to bf16
-    m_run = (float)(bf16)tile_max<true>(a0, a1, g, 0, L);
+  {  // the running max starts at tile 0's (keys past L masked)
+    m_run = tile_max<true>(a0, a1, g, 0, L);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       a0[r] -= m_run;
