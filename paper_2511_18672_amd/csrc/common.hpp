@@ -118,10 +118,26 @@ template <typename T> __device__ __forceinline__ T store_from_f32(float v);
 template <> __device__ __forceinline__ float store_from_f32<float>(float v) { return v; }
 template <> __device__ __forceinline__ bf16 store_from_f32<bf16>(float v) { return (bf16)v; }
 
+// Lane v of the same row (16 lanes) selected by a DPP control word.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over the 64 lanes of a fully active wave, in every lane (bit-identical
+// in all lanes: each step adds two values in both orders' common result).
+// Within a row of 16 lanes: quad permutations (lane ^ 1, lane ^ 2), then the
+// half-row and row mirrors; across rows: the gfx950 row-pair and half swaps.
+// No LDS round trips, unlike a shuffle butterfly.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
-  return v;
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror: the other quad of the 8-lane half
+  v += dpp_f<0x140>(v);  // row_mirror: the other half of the row
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
 }
 
 __device__ __forceinline__ float wave_max(float v) {

@@ -164,31 +164,35 @@ template <> struct VecStore<bf16, 4> {
 
 // One wave per row; lane handles V consecutive values per 64*V-wide chunk, so
 // every load and store of a wave is one contiguous 256*V- (fp32) or 128*V-byte run.
-template <typename OT, int V>
+// CH: chunks of 64 V columns per row when known at compile time (then all
+// row loads issue back to back), 0 for any D.
+template <typename OT, int V, int CH>
 __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, int n, int D,
                                                  const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
                                                  const int32_t* __restrict__ crow, OT* __restrict__ out) {
   typedef typename VecF<V>::T VT;
-  constexpr int kMaxChunks = kMaxPer / V;
+  constexpr int kMaxChunks = CH > 0 ? CH : kMaxPer / V;
   const int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
   if (row >= n) return;
   const int lane = lane_id();
-  const int chunks = D / (kWave * V);
+  const int chunks = CH > 0 ? CH : D / (kWave * V);
   const float* hr = h + (int64_t)row * D;
+  const float* m = mod + (int64_t)crow[row] * ldm;
   VT v[kMaxChunks];
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < kMaxChunks; ++i)
-    if (i < chunks) {
-      v[i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+    if (CH > 0 || i < chunks) v[i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+#pragma unroll
+  for (int i = 0; i < kMaxChunks; ++i)
+    if (CH > 0 || i < chunks)
 #pragma unroll
       for (int e = 0; e < V; ++e) s += VecF<V>::get(v[i], e);
-    }
   const float mu = wave_sum(s) / (float)D;
   float s2 = 0.f;
 #pragma unroll
   for (int i = 0; i < kMaxChunks; ++i)
-    if (i < chunks) {
+    if (CH > 0 || i < chunks) {
 #pragma unroll
       for (int e = 0; e < V; ++e) {
         const float d = VecF<V>::get(v[i], e) - mu;
@@ -196,11 +200,10 @@ __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, in
       }
     }
   const float rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
-  const float* m = mod + (int64_t)crow[row] * ldm;
   OT* o = out + (int64_t)row * D;
 #pragma unroll
   for (int i = 0; i < kMaxChunks; ++i)
-    if (i < chunks) {
+    if (CH > 0 || i < chunks) {
       const int c = (i * kWave + lane) * V;
       const VT sh = *reinterpret_cast<const VT*>(m + sh_off + c);
       const VT sc = *reinterpret_cast<const VT*>(m + sc_off + c);
@@ -335,14 +338,23 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
   // 16-byte vectors need every row and every modulation chunk on a 16-byte boundary
   const bool v4 = (D % (kWave * 4) == 0) && (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
   const bool v2 = (D % (kWave * 2) == 0) && (ldm % 2 == 0) && (sh_off % 2 == 0) && (sc_off % 2 == 0);
+  const int ch4 = v4 ? D / (kWave * 4) : 0;
   if (odt == SPHINX_BF16) {
-    if (v4) k_ln_mod<bf16, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
-    else if (v2) k_ln_mod<bf16, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
-    else k_ln_mod<bf16, 1><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (bf16*)out);
+    bf16* o = (bf16*)out;
+    if (ch4 == 4) k_ln_mod<bf16, 4, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch4 == 2) k_ln_mod<bf16, 4, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch4 == 8) k_ln_mod<bf16, 4, 8><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (v4) k_ln_mod<bf16, 4, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (v2) k_ln_mod<bf16, 2, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else k_ln_mod<bf16, 1, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
   } else {
-    if (v4) k_ln_mod<float, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
-    else if (v2) k_ln_mod<float, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
-    else k_ln_mod<float, 1><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, (float*)out);
+    float* o = (float*)out;
+    if (ch4 == 4) k_ln_mod<float, 4, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch4 == 2) k_ln_mod<float, 4, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch4 == 8) k_ln_mod<float, 4, 8><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (v4) k_ln_mod<float, 4, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (v2) k_ln_mod<float, 2, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else k_ln_mod<float, 1, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
   }
   return hipGetLastError();
 }
