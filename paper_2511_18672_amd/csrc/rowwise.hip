@@ -39,6 +39,42 @@ __device__ __forceinline__ void load16<float>(const float* p, float (&w)[16]) {
   }
 }
 
+// Output-weight table of k_final in LDS: column c's 16 weights are 32 (bf16)
+// or 64 (fp32) bytes, i.e. CPC 16-byte chunks.  Chunk q of column c sits at
+// chunk (CPC c + q) ^ x(c), x(c) < 4 CPC flipping only the chunk's place
+// among the 4 columns sharing c >> 2, with x(c) = (c >> 3) & 7 for bf16 and
+// (c >> 2) & 15 for fp32: the 16 lanes of one read pass, which take columns
+// 4 (l + 64 i) + e, then hit 16 different 16-byte bank groups.
+template <typename WT>
+__device__ __forceinline__ int wt_chunk(int c, int q) {
+  constexpr int CPC = 16 * (int)sizeof(WT) / 16;
+  const int x = sizeof(WT) == 2 ? (c >> 3) & 7 : (c >> 2) & 15;
+  return (CPC * c + q) ^ x;
+}
+
+// The reader's form of wt_chunk for column c = 4 (l + 64 i) + e of lane l:
+// x(c) depends on the lane only, so chunk = 4 CPC (l + 64 i) + ((CPC e + q)
+// ^ x_l), and the i term is an immediate offset.
+template <typename WT>
+__device__ __forceinline__ int wt_lane_off(int lane, int e, int q) {
+  constexpr int CPC = 16 * (int)sizeof(WT) / 16;
+  const int xl = sizeof(WT) == 2 ? (lane >> 1) & 7 : lane & 15;
+  return 16 * (4 * CPC * lane + ((CPC * e + q) ^ xl));
+}
+
+template <typename WT>
+__device__ __forceinline__ void load16_at(const unsigned char* tab, const int (&off)[16 * (int)sizeof(WT) / 16],
+                                          int i, float (&w)[16]) {
+  constexpr int VE = 16 / (int)sizeof(WT), CPC = 16 / VE;
+  typedef WT vec_t __attribute__((ext_vector_type(16 / sizeof(WT))));
+#pragma unroll
+  for (int q = 0; q < CPC; ++q) {
+    const vec_t v = *reinterpret_cast<const vec_t*>(tab + off[q] + 4096 * CPC * i);
+#pragma unroll
+    for (int u = 0; u < VE; ++u) w[q * VE + u] = (float)v[u];
+  }
+}
+
 // One thread per four consecutive columns and a block of kEmbedRows rows,
 // grid (column blocks, row blocks): the thread's 4 x 16 weights stay in
 // registers across the rows (the weight matrix is read once per row block,
@@ -216,8 +252,9 @@ __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, in
 }
 
 // One wave per row; lane owns the column quads lane + 64 i.  The output
-// weights sit transposed in LDS ([D][16]: a column's 16 weights contiguous),
-// so a column costs two (bf16) or four (fp32) 16-byte LDS reads.
+// weights sit transposed in LDS (a column's 16 weights in two (bf16) or four
+// (fp32) 16-byte chunks, swizzled as wt_chunk describes), so a column costs
+// two or four conflict-free 16-byte LDS reads.
 constexpr int kMaxQuads = 8;  // D <= 2048
 template <typename WT>
 __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int n, int D,
@@ -242,15 +279,30 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
           vec_t col;
 #pragma unroll
           for (int u = 0; u < VE; ++u) col[u] = wk[q * VE + u][i];
-          *reinterpret_cast<vec_t*>(s_wt + (c0 + i) * 16 + q * VE) = col;
+          reinterpret_cast<vec_t*>(s_wt)[wt_chunk<WT>(c0 + i, q)] = col;
         }
     }
   }
   __syncthreads();
   const int lane = lane_id();
   const int quads = D >> 2;
+  constexpr int CPC = 16 * (int)sizeof(WT) / 16;
+  int woff[4][CPC];  // byte offsets of this lane's weight chunks (column quad 0)
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+#pragma unroll
+    for (int q = 0; q < CPC; ++q) woff[e][q] = wt_lane_off<WT>(lane, e, q);
+  // this lane's output after the reduce-scatter below
+  const int kout = ((lane >> 5) & 1) * 8 + ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1);
+  const float bout = load_as_f32(out_b, kout);
   for (int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave); row < n;
        row += gridDim.x * kRowsPerBlock) {
+    // the row's conditioning index, frame, DDIM coefficients and state are
+    // loaded up front, beside the row itself, so that only the modulation
+    // loads wait for the statistics
+    const int cr = crow[row], gf = gframe[row];
+    float* xp = x + (int64_t)row * 16 + kout;
+    const float c1g = c1[gf], c2g = c2[gf], xold = *xp;
     const float* hr = h + (int64_t)row * D;
     f32x4 v[kMaxQuads];
     float s = 0.f;
@@ -271,7 +323,7 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
           s2 = fmaf(d, d, s2);
         }
     const float rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
-    const float* m = mod + (int64_t)crow[row] * ldm;
+    const float* m = mod + (int64_t)cr * ldm;
     float acc[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) acc[k] = 0.f;
@@ -285,7 +337,7 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
         for (int e = 0; e < 4; ++e) {
           const float a = fmaf((v[i][e] - mu) * rstd, 1.0f + sc[e], sh[e]);
           float w[16];
-          load16<WT>(s_wt + (4 * q + e) * 16, w);
+          load16_at<WT>(s_raw, woff[e], i, w);
 #pragma unroll
           for (int k = 0; k < 16; ++k) acc[k] = fmaf(a, w[k], acc[k]);
         }
@@ -310,13 +362,7 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
     float e = acc[0];
     e += __shfl_xor(e, 2, kWave);
     e += __shfl_xor(e, 1, kWave);
-    if ((lane & 3) == 0) {
-      const int k = ((lane >> 5) & 1) * 8 + ((lane >> 4) & 1) * 4 + ((lane >> 3) & 1) * 2 + ((lane >> 2) & 1);
-      const float eps_hat = e + load_as_f32(out_b, k);
-      const int g = gframe[row];
-      float* xp = x + (int64_t)row * 16 + k;
-      *xp = fmaf(c2[g], eps_hat, c1[g] * *xp);
-    }
+    if ((lane & 3) == 0) *xp = fmaf(c2g, e + bout, c1g * xold);
   }
 }
 }  // namespace
