@@ -487,7 +487,14 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], pp[kb][hf], oacc[db], 0, 0, 0);
       if (st == 7)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) negm[r] = -m_run;
+        for (int r = 0; r < 16; r += 2) {  // eight 64-bit moves of the (-m, -m) pair
+          const unsigned u = __float_as_uint(-m_run);
+          const uint64_t pair = ((uint64_t)u << 32) | u;
+          uint64_t d;
+          asm volatile("v_mov_b64 %0, %1" : "=v"(d) : "v"(pair));
+          negm[r] = __uint_as_float((unsigned)d);
+          negm[r + 1] = __uint_as_float((unsigned)(d >> 32));
+        }
     } else {
       // the first k-step accumulates onto -max (every element of a lane
       // belongs to its query), so the scores arrive shifted
