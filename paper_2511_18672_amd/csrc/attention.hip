@@ -369,15 +369,34 @@ __device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kba
 //    end of iteration t+1 (a per-wave vmcnt wait that leaves the newest copies
 //    in flight, then the workgroup barrier; no memory fence).
 namespace dma {
-constexpr int kTileBytes = AK * 64 * 2;  // 8 KB
-
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
 constexpr int kRing = 3;  // tiles in flight per operand
 
+// Tile geometry per head dimension.  head_dim 64: 128-byte rows, PV in two
+// 32-row blocks of O^T, QK in four 16-deep k-steps.  head_dim 72: 144-byte
+// rows (nine 16-byte chunks; nine is odd, so the 16 rows of a read pass fall
+// on 16 different bank groups without a swizzle), PV in three blocks (rows
+// 72..95 of the third are computed and dropped), QK in four 16-deep k-steps
+// and one 8-deep k-step (dims 64..71, v_mfma_f32_32x32x8_bf16).
+template <int HD>
+struct Geo;
+template <>
+struct Geo<64> {
+  static constexpr int RB = 128, DB = 2, KS = 4, NPV = 8, NQK = 8, TILE = AK * RB, PAD = 0, COPIES = 2;
+};
+template <>
+struct Geo<72> {
+  // PAD: a third-block V^T read of the last key row runs up to 40 bytes past
+  // its tile (into dims that are dropped); the pad keeps it inside the ring.
+  static constexpr int RB = 144, DB = 3, KS = 5, NPV = 12, NQK = 10, TILE = AK * RB, PAD = 64, COPIES = 3;
+};
+
+template <int HD>
 struct Smem {
-  char k[kRing][kTileBytes];
-  char v[kRing][kTileBytes];
+  char k[kRing][Geo<HD>::TILE];
+  char v[kRing][Geo<HD>::TILE];
+  char pad[Geo<HD>::PAD + 16];
 };
 
 __device__ __forceinline__ bf16x8 tr_pair(const char* p0, const char* p1) {
@@ -388,60 +407,84 @@ __device__ __forceinline__ bf16x8 tr_pair(const char* p0, const char* p1) {
 }
 
 // Per-lane byte offsets inside a tile (loop invariant).
-// The swizzled chunk index only flips bits 5-6 of the K offset with the k-step
-// and bit 6 of the V offset with the block, so one offset of each suffices.
+// head_dim 64: the swizzled chunk index only flips bits 5-6 of the K offset
+// with the k-step and bit 6 of the V offset with the block, so one offset of
+// each suffices.  head_dim 72: unswizzled, the k-step and the block add
+// constants.
+template <int HD>
 struct LaneOff {
-  int k0;  // QK A fragment of k-step 0, key rows 0..31 (rows 32..63: +4096)
-  int v0;  // PV A fragment of block 0, first transpose read (second: +1024)
-  __device__ int k(int ks) const { return k0 ^ (ks << 5); }
-  __device__ int v(int db) const { return v0 ^ (db << 6); }
+  int k0;  // QK A fragment of k-step 0, key rows 0..31 (rows 32..63: + 32 RB)
+  int v0;  // PV A fragment of block 0, first transpose read (second: + 8 RB)
+  __device__ int k(int ks) const { return HD == 64 ? k0 ^ (ks << 5) : k0 + 32 * ks; }
+  __device__ int v(int db) const { return HD == 64 ? v0 ^ (db << 6) : v0 + 64 * db; }
+  int k4o;  // head_dim 72, k-step 4 (8 deep): dims 64 + 4 g .. + 3 of key row r32
+  __device__ int k4() const { return k4o; }
 };
 
-__device__ __forceinline__ LaneOff lane_offsets(int lane) {
-  LaneOff o;
+template <int HD>
+__device__ __forceinline__ LaneOff<HD> lane_offsets(int lane) {
+  LaneOff<HD> o;
   const int r32 = lane & 31, g = lane >> 5;
-  o.k0 = r32 * 128 + ((g ^ ((r32 >> 1) & 7)) << 4);  // chunk 2 ks + g, XOR-swizzled by row pair
   const int j = lane & 15, b = lane >> 4;
   const int row = 4 * g + (j >> 2);
   const int byte = 32 * (b & 1) + 8 * (j & 3);
-  const int chunk = (byte >> 4) ^ (2 * (row & 3));
-  o.v0 = row * 128 + (chunk << 4) + (byte & 8);
+  if constexpr (HD == 64) {
+    o.k0 = r32 * 128 + ((g ^ ((r32 >> 1) & 7)) << 4);  // chunk 2 ks + g, XOR-swizzled by row pair
+    const int chunk = (byte >> 4) ^ (2 * (row & 3));
+    o.v0 = row * 128 + (chunk << 4) + (byte & 8);
+    o.k4o = 0;
+  } else {
+    o.k0 = r32 * 144 + 16 * g;  // chunk 2 ks + g
+    o.v0 = row * 144 + byte;
+    o.k4o = r32 * 144 + 128 + 8 * g;
+  }
   return o;
 }
 
-__device__ __forceinline__ void qk(const char* sK, const LaneOff& lo, const bf16x8 (&qf)[4], f32x16& s0,
-                                   f32x16& s1) {
+template <int HD>
+__device__ __forceinline__ void qk(const char* sK, const LaneOff<HD>& lo, const bf16x8 (&qf)[4], const v4s& q4,
+                                   f32x16& s0, f32x16& s1) {
+  constexpr int RB = Geo<HD>::RB;
   s0 = f32x16{};
   s1 = f32x16{};
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
     const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(sK + lo.k(ks));
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(sK + lo.k(ks) + 4096);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(sK + lo.k(ks) + 32 * RB);
     s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
+  }
+  if constexpr (HD == 72) {
+    const v4s k0 = *reinterpret_cast<const v4s*>(sK + lo.k4());
+    const v4s k1 = *reinterpret_cast<const v4s*>(sK + lo.k4() + 32 * RB);
+    s0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(k0, q4, s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(k1, q4, s1, 0, 0, 0);
   }
 }
 
 // O^T += V^T P^T; P^T k-slot (g, j) of (kb, hf) is key 32 kb + 16 hf + 8 (j/4) + 4 g + j%4.
-__device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16x8 (&pf)[2][2],
-                                   f32x16 (&oacc)[2]) {
+template <int HD>
+__device__ __forceinline__ void pv(const char* sV, const LaneOff<HD>& lo, const bf16x8 (&pf)[2][2],
+                                   f32x16 (&oacc)[Geo<HD>::DB]) {
+  constexpr int RB = Geo<HD>::RB;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-      for (int db = 0; db < 2; ++db) {
-        const char* p = sV + lo.v(db) + (32 * kb + 16 * hf) * 128;
-        const bf16x8 vf = tr_pair(p, p + 8 * 128);
+      for (int db = 0; db < Geo<HD>::DB; ++db) {
+        const char* p = sV + lo.v(db) + (32 * kb + 16 * hf) * RB;
+        const bf16x8 vf = tr_pair(p, p + 8 * RB);
         oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
       }
 }
 
 // One iteration's MFMA work interleaved by hand with the softmax of the
-// previous tile: 16 steps of one MFMA (PV(t-1) for the first eight; QK(t+1),
-// four head-dim k-steps for each of the two 32-key blocks, the first of them
-// accumulating onto -max, so that the scores arrive scaled and shifted) and
-// softmax work on two consecutive probability
+// previous tile: one MFMA per step (PV(t-1) first: 8 steps at head_dim 64,
+// 12 at 72; then QK(t+1), the head-dim k-steps of the two 32-key blocks
+// alternately, the first of them accumulating onto -max, so that the scores
+// arrive scaled and shifted) and, in the first 16 steps, softmax work on two
+// consecutive probability
 // pairs, software-pipelined so that no instruction of a step waits on another
 // of the same step: the exponentials of pair st+1 and the bf16 pack and
 // row-sum dot product of pair st.  PV first lets the previous probabilities
@@ -450,23 +493,49 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff& lo, const bf16
 // waves per SIMD; so does reading the operand fragment of a step from LDS two
 // steps ahead (a ring of three).  Each step is fenced so the compiler keeps
 // the order.
-__device__ __forceinline__ bf16x8 step_frag(const char* sK, const char* sV, const LaneOff& lo, int st) {
-  if (st < 8) {
-    const int kb = st >> 2, hf = (st >> 1) & 1, db = st & 1;
-    const char* p = sV + lo.v(db) + (32 * kb + 16 * hf) * 128;
-    return tr_pair(p, p + 8 * 128);
+// PV step st: probability block (kb, hf) and O^T block db.
+template <int HD>
+__device__ __forceinline__ void pv_step(int st, int& kb, int& hf, int& db) {
+  if constexpr (HD == 64) {
+    kb = st >> 2;
+    hf = (st >> 1) & 1;
+    db = st & 1;
+  } else {
+    kb = st / 6;
+    hf = (st / 3) & 1;
+    db = st % 3;
   }
-  const int ks = (st - 8) >> 1;
-  return *reinterpret_cast<const bf16x8*>(sK + lo.k(ks) + ((st & 1) ? 4096 : 0));
 }
 
-__device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff& lo, const bf16x8 (&qf)[4],
-                                       float m_run, const f32x16& c0, const f32x16& c1, float& l_run,
-                                       const bf16x8 (&pp)[2][2], bf16x8 (&pn)[2][2], f32x16& n0, f32x16& n1,
-                                       f32x16 (&oacc)[2]) {
+template <int HD>
+__device__ __forceinline__ bf16x8 step_frag(const char* sK, const char* sV, const LaneOff<HD>& lo, int st) {
+  constexpr int RB = Geo<HD>::RB, NPV = Geo<HD>::NPV;
+  if (st < NPV) {
+    int kb, hf, db;
+    pv_step<HD>(st, kb, hf, db);
+    const char* p = sV + lo.v(db) + (32 * kb + 16 * hf) * RB;
+    return tr_pair(p, p + 8 * RB);
+  }
+  const int ks = (st - NPV) >> 1;
+  const int wofs = ((st - NPV) & 1) ? 32 * RB : 0;
+  if (HD == 72 && ks == 4) {  // 8 deep: the low half carries the operand
+    const v4s k = *reinterpret_cast<const v4s*>(sK + lo.k4() + wofs);
+    const v4s r[2] = {k, k};
+    return *reinterpret_cast<const bf16x8*>(r);
+  }
+  return *reinterpret_cast<const bf16x8*>(sK + lo.k(ks) + wofs);
+}
+
+template <int HD>
+__device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff<HD>& lo,
+                                       const bf16x8 (&qf)[4], const v4s& q4, float m_run, const f32x16& c0,
+                                       const f32x16& c1, float& l_run, const bf16x8 (&pp)[2][2],
+                                       bf16x8 (&pn)[2][2], f32x16& n0, f32x16& n1,
+                                       f32x16 (&oacc)[Geo<HD>::DB]) {
+  constexpr int NPV = Geo<HD>::NPV, NSTEP = NPV + Geo<HD>::NQK;
   bf16x8 fr[3];
-  fr[0] = step_frag(sK, sV, lo, 0);
-  fr[1] = step_frag(sK, sV, lo, 1);
+  fr[0] = step_frag<HD>(sK, sV, lo, 0);
+  fr[1] = step_frag<HD>(sK, sV, lo, 1);
   // pair st: score block w = st & 1 (c0 or c1), rows r, r+1 with r = 8 (st >> 3) + 2 ((st >> 1) & 3)
   auto score = [&](int st, int e) -> float {
     const int r = (st >> 3) * 8 + 2 * ((st >> 1) & 3) + e;
@@ -480,12 +549,13 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
   float psum = 0.0f;
   f32x16 negm;  // -m_run in every element, built just before the first QK step
 #pragma unroll
-  for (int st = 0; st < 16; ++st) {
-    if (st + 2 < 16) fr[(st + 2) % 3] = step_frag(sK, sV, lo, st + 2);
-    if (st < 8) {
-      const int kb = st >> 2, hf = (st >> 1) & 1, db = st & 1;
+  for (int st = 0; st < NSTEP; ++st) {
+    if (st + 2 < NSTEP) fr[(st + 2) % 3] = step_frag<HD>(sK, sV, lo, st + 2);
+    if (st < NPV) {
+      int kb, hf, db;
+      pv_step<HD>(st, kb, hf, db);
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], pp[kb][hf], oacc[db], 0, 0, 0);
-      if (st == 7)
+      if (st == NPV - 1)
 #pragma unroll
         for (int r = 0; r < 16; r += 2) {  // eight 64-bit moves of the (-m, -m) pair
           const unsigned u = __float_as_uint(-m_run);
@@ -498,16 +568,23 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
     } else {
       // the first k-step accumulates onto -max (every element of a lane
       // belongs to its query), so the scores arrive shifted
-      const int ks = (st - 8) >> 1;
-      if (st & 1)
+      const int ks = (st - NPV) >> 1;
+      if (HD == 72 && ks == 4) {
+        const v4s a = *reinterpret_cast<const v4s*>(&fr[st % 3]);
+        if ((st - NPV) & 1)
+          n1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, q4, n1, 0, 0, 0);
+        else
+          n0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, q4, n0, 0, 0, 0);
+      } else if ((st - NPV) & 1) {
         n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? negm : n1, 0, 0, 0);
-      else
+      } else {
         n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? negm : n0, 0, 0, 0);
+      }
     }
     if (st + 1 < 16)
 #pragma unroll
       for (int e = 0; e < 2; ++e) ex[st + 1][e] = fast_exp2(score(st + 1, e));
-    {
+    if (st < 16) {
       const int hf = st >> 3, i = (st >> 1) & 3, w = st & 1;
       bf16x2 pr;
       pr[0] = (bf16)ex[st][0];
@@ -570,9 +647,10 @@ __device__ __forceinline__ float raise_max_shifted(float mx, float& m_run, float
 }
 }  // namespace dma
 
+template <int HD>
 __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads, float scale_log2, const SegTable& S,
-                                              dma::Smem& sm) {
-  constexpr int HD = 64;
+                                              dma::Smem<HD>& sm) {
+  typedef dma::Geo<HD> G;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, r32 = lane & 31;
@@ -593,11 +671,14 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   const bf16x8 zero8 = {};
 
   // V buffer 2 (that of "tile -1") starts all zero: the first iteration's PV
-  // multiplies it by zero probabilities.
-  for (int i = tid; i < dma::kTileBytes / 16; i += 256) reinterpret_cast<bf16x8*>(sm.v[2])[i] = zero8;
+  // multiplies it by zero probabilities.  (So does the pad behind it, which
+  // third-block reads of head_dim 72 run into.)
+  for (int i = tid; i < G::TILE / 16; i += 256) reinterpret_cast<bf16x8*>(sm.v[2])[i] = zero8;
+  if (G::PAD > 0 && tid < (G::PAD + 16) / 16) reinterpret_cast<bf16x8*>(sm.pad)[tid] = zero8;
 
   const int ql = qt * AQ + wave * 32 + r32;
   bf16x8 qf[4];
+  dma::v4s q4 = {};  // head_dim 72: dims 64 + 4 g .. + 3
   const bf16* Qg = static_cast<const bf16*>(io.q) + (int64_t)seg0 * ldq + head * HD;
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -606,32 +687,54 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
 #pragma unroll
     for (int e = 0; e < 8; ++e) qf[ks][e] = (bf16)((float)qf[ks][e] * scale_log2);
   }
+  if constexpr (HD == 72) {
+    bf16x4 v = {};
+    if (ql < Lq) v = *reinterpret_cast<const bf16x4*>(Qg + (int64_t)ql * ldq + 64 + g * 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = (bf16)((float)v[e] * scale_log2);
+    q4 = __builtin_bit_cast(dma::v4s, v);
+  }
 
 
-  // Copy sources: lane i of copy n (n = 0, 1) fills row 8(2 wave + n) + i/8,
-  // slot i%8 of a tile.  The tile's first key row is a wave-uniform base
-  // address; each lane keeps its byte offset from it.  In a tile that runs
-  // past the segment's last key the rows past it repeat that key.
+  // Copy sources.  head_dim 64: lane i of copy n (n = 0, 1) fills row
+  // 8(2 wave + n) + i/8, slot i%8 of a tile.  head_dim 72: a wave fills rows
+  // 16 wave .. +15, 144 chunks, chunk t = 64 n + i by copy n (n = 0, 1, 2; the
+  // third copy with 16 lanes), at row t/9, slot t%9.  The tile's first key row
+  // is a wave-uniform base address; each lane keeps its byte offset from it.
+  // In a tile that runs past the segment's last key the rows past it repeat
+  // that key.
   const bf16* Kg = static_cast<const bf16*>(io.k) + (int64_t)kv0 * ld + head * HD;
   const bf16* Vg = static_cast<const bf16*>(io.v) + (int64_t)kv0 * ld + head * HD;
-  auto copy_row = [&](int n) { return 8 * (2 * wave + n) + (lane >> 3); };
+  auto copy_row = [&](int n) {
+    return HD == 64 ? 8 * (2 * wave + n) + (lane >> 3) : 16 * wave + (64 * n + lane) / 9;
+  };
   auto k_chunk = [&](int row) { return (lane & 7) ^ ((row >> 1) & 7); };
   auto v_chunk = [&](int row) { return (lane & 7) ^ (2 * (row & 3)); };
-  uint32_t koff[2];
+  auto chunk72 = [&](int n) { return (64 * n + lane) % 9; };
+  auto active = [&](int n) { return HD == 64 || n < 2 || lane < 16; };
+  auto dst = [&](char* tile, int n) {
+    return HD == 64 ? tile + (2 * wave + n) * 1024 : tile + wave * 2304 + n * 1024;
+  };
+  uint32_t koff[G::COPIES], voff;
 #pragma unroll
-  for (int n = 0; n < 2; ++n) koff[n] = 2u * (uint32_t)(copy_row(n) * ld + k_chunk(copy_row(n)) * 8);
-  const uint32_t voff = 2u * (uint32_t)(copy_row(0) * ld + v_chunk(copy_row(0)) * 8);  // copy 1: 8 rows on
+  for (int n = 0; n < G::COPIES; ++n) {
+    const int row = copy_row(n);
+    koff[n] = 2u * (uint32_t)(row * ld + (HD == 64 ? k_chunk(row) : chunk72(n)) * 8);
+  }
+  voff = 2u * (uint32_t)(copy_row(0) * ld + v_chunk(copy_row(0)) * 8);  // head_dim 64; copy 1: 8 rows on
   auto copy_k = [&](int kbase, int buf) {
     const bf16* base = Kg + (int64_t)kbase * ld;
     if (kbase + AK <= L) {
 #pragma unroll
-      for (int n = 0; n < 2; ++n) lds_dma16_at(base, koff[n], sm.k[buf] + (2 * wave + n) * 1024);
+      for (int n = 0; n < G::COPIES; ++n)
+        if (active(n)) lds_dma16_at(base, koff[n], dst(sm.k[buf], n));
     } else {
 #pragma unroll
-      for (int n = 0; n < 2; ++n) {
+      for (int n = 0; n < G::COPIES; ++n) {
         const int row = copy_row(n);
-        const uint32_t off = 2u * (uint32_t)(min(row, L - 1 - kbase) * ld + k_chunk(row) * 8);
-        lds_dma16_at(base, off, sm.k[buf] + (2 * wave + n) * 1024);
+        const int c = HD == 64 ? k_chunk(row) : chunk72(n);
+        const uint32_t off = 2u * (uint32_t)(min(row, L - 1 - kbase) * ld + c * 8);
+        if (active(n)) lds_dma16_at(base, off, dst(sm.k[buf], n));
       }
     }
   };
@@ -639,13 +742,19 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     const bf16* base = Vg + (int64_t)kbase * ld;
     if (kbase + AK <= L) {
 #pragma unroll
-      for (int n = 0; n < 2; ++n) lds_dma16_at(base + n * 8 * ld, voff, sm.v[buf] + (2 * wave + n) * 1024);
+      for (int n = 0; n < G::COPIES; ++n) {
+        if constexpr (HD == 64)
+          lds_dma16_at(base + n * 8 * ld, voff, dst(sm.v[buf], n));
+        else if (active(n))
+          lds_dma16_at(base, koff[n], dst(sm.v[buf], n));  // same layout as K
+      }
     } else {
 #pragma unroll
-      for (int n = 0; n < 2; ++n) {
+      for (int n = 0; n < G::COPIES; ++n) {
         const int row = copy_row(n);
-        const uint32_t off = 2u * (uint32_t)(min(row, L - 1 - kbase) * ld + v_chunk(row) * 8);
-        lds_dma16_at(base, off, sm.v[buf] + (2 * wave + n) * 1024);
+        const int c = HD == 64 ? v_chunk(row) : chunk72(n);
+        const uint32_t off = 2u * (uint32_t)(min(row, L - 1 - kbase) * ld + c * 8);
+        if (active(n)) lds_dma16_at(base, off, dst(sm.v[buf], n));
       }
     }
   };
@@ -657,17 +766,21 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   auto land = [&](auto keep) {
     if (decltype(keep)::value == 4)
       __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4) lgkmcnt(0)
+    else if (decltype(keep)::value == 6)
+      __builtin_amdgcn_s_waitcnt(0x0076);  // vmcnt(6) lgkmcnt(0)
     else
       __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0) lgkmcnt(0)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
-  using Keep4 = std::integral_constant<int, 4>;
+  using Keep4 = std::integral_constant<int, 2 * G::COPIES>;  // this iteration's copies stay in flight
   using Keep0 = std::integral_constant<int, 0>;
 
-  const dma::LaneOff lo = dma::lane_offsets(lane);
-  f32x16 oacc[2] = {f32x16{}, f32x16{}};
+  const dma::LaneOff<HD> lo = dma::lane_offsets<HD>(lane);
+  f32x16 oacc[G::DB];
+#pragma unroll
+  for (int db = 0; db < G::DB; ++db) oacc[db] = f32x16{};
   float m_run, l_run = 0.0f;
   const int nkt = (L + AK - 1) / AK;
 
@@ -680,8 +793,8 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   float alpha = 1.0f;
   auto rescale_o = [&]() {
     if (__ballot(alpha != 1.0f) != 0) {
-      oacc[0] *= alpha;
-      oacc[1] *= alpha;
+#pragma unroll
+      for (int db = 0; db < G::DB; ++db) oacc[db] *= alpha;
     }
   };
   int slot = 0;  // t % 3
@@ -704,7 +817,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
         c0[r] -= delta;
         c1[r] -= delta;
       }
-    dma::region(sm.k[s1], sm.v[s2], lo, qf, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
+    dma::region<HD>(sm.k[s1], sm.v[s2], lo, qf, q4, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
     land(Keep4{});
     slot = s1;
   };
@@ -715,7 +828,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   copy_v(0, 0);
   land(Keep4{});
   f32x16 a0, a1, b0, b1;
-  dma::qk(sm.k[0], lo, qf, a0, a1);
+  dma::qk<HD>(sm.k[0], lo, qf, q4, a0, a1);
   {  // the running max starts at tile 0's (keys past L masked)
     m_run = tile_max<true>(a0, a1, g, 0, L);
 #pragma unroll
@@ -751,31 +864,39 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     rescale_o();
     alpha = a_new;
     dma::last_probs(a0, a1, delta, l_run, pb);
-    dma::pv(sm.v[sprev], lo, pa, oacc);
+    dma::pv<HD>(sm.v[sprev], lo, pa, oacc);
     rescale_o();
     land(Keep0{});
-    dma::pv(sm.v[slot], lo, pb, oacc);
+    dma::pv<HD>(sm.v[slot], lo, pb, oacc);
   }
   l_run += __shfl_xor(l_run, 32, kWave);
   if (ql < Lq) {
     const float inv = 1.0f / l_run;
     bf16* orow = static_cast<bf16*>(io.o) + (int64_t)(seg0 + ql) * D + head * HD;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+    for (int db = 0; db < G::DB; ++db)
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        bf16x4 ov;
+      for (int rr = 0; rr < 4; ++rr)
+        if (db * 32 + rr * 8 < HD) {  // head_dim 72: of the third block only dims 64..71
+          bf16x4 ov;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) ov[q] = (bf16)(oacc[db][rr * 4 + q] * inv);
-        *reinterpret_cast<bf16x4*>(orow + db * 32 + rr * 8 + g * 4) = ov;
-      }
+          for (int q = 0; q < 4; ++q) ov[q] = (bf16)(oacc[db][rr * 4 + q] * inv);
+          *reinterpret_cast<bf16x4*>(orow + db * 32 + rr * 8 + g * 4) = ov;
+        }
   }
 }
 
 __global__ __launch_bounds__(256, 3) void k_attn_bf16_dma(AttnIO io, int D, int heads, float scale_log2,
                                                           SegTable S) {
-  __shared__ __attribute__((aligned(1024))) dma::Smem sm;
-  attn_body_dma(io, D, heads, scale_log2, S, sm);
+  __shared__ __attribute__((aligned(1024))) dma::Smem<64> sm;
+  attn_body_dma<64>(io, D, heads, scale_log2, S, sm);
+}
+
+// head_dim 72: 55 KB of LDS and about 190 VGPRs, two workgroups per CU.
+__global__ __launch_bounds__(256, 2) void k_attn_bf16_dma72(AttnIO io, int D, int heads, float scale_log2,
+                                                            SegTable S) {
+  __shared__ __attribute__((aligned(1024))) dma::Smem<72> sm;
+  attn_body_dma<72>(io, D, heads, scale_log2, S, sm);
 }
 
 constexpr int kF32Max = 64;
@@ -830,10 +951,13 @@ hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads,
     // the copy kernel addresses a segment's keys and values with 32-bit element offsets
     int64_t kv_max = 0;
     for (int i = 0; i < S.nseg; ++i) kv_max = std::max<int64_t>(kv_max, S.kv_len[i]);
-    if (head_dim == 64 && kv_max * io.ldkv < ((int64_t)1 << 31))
+    const bool small = kv_max * io.ldkv < ((int64_t)1 << 31);
+    if (head_dim == 64 && small)
       k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else if (head_dim == 64)
       k_attn_bf16<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
+    else if (small)
+      k_attn_bf16_dma72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else
       k_attn_bf16_d72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
   } else {
