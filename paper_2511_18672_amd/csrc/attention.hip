@@ -383,19 +383,21 @@ template <int HD>
 struct Geo;
 template <>
 struct Geo<64> {
-  static constexpr int RB = 128, DB = 2, KS = 4, NPV = 8, NQK = 8, TILE = AK * RB, PAD = 0, COPIES = 2;
+  static constexpr int RB = 128, DB = 2, KS = 4, NPV = 8, NQK = 8, TILE = AK * RB, PAD = 0, COPIES = 2, VR = 3;
 };
 template <>
 struct Geo<72> {
   // PAD: a third-block V^T read of the last key row runs up to 40 bytes past
   // its tile (into dims that are dropped); the pad keeps it inside the ring.
-  static constexpr int RB = 144, DB = 3, KS = 5, NPV = 12, NQK = 10, TILE = AK * RB, PAD = 64, COPIES = 3;
+  // VR: V ring of two slots (46 KB of LDS, three workgroups per CU); V(t) is
+  // copied in the iteration before its PV and waited for at its end.
+  static constexpr int RB = 144, DB = 3, KS = 5, NPV = 12, NQK = 10, TILE = AK * RB, PAD = 64, COPIES = 3, VR = 2;
 };
 
 template <int HD>
 struct Smem {
   char k[kRing][Geo<HD>::TILE];
-  char v[kRing][Geo<HD>::TILE];
+  char v[Geo<HD>::VR][Geo<HD>::TILE];
   char pad[Geo<HD>::PAD + 16];
 };
 
@@ -673,7 +675,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   // V buffer 2 (that of "tile -1") starts all zero: the first iteration's PV
   // multiplies it by zero probabilities.  (So does the pad behind it, which
   // third-block reads of head_dim 72 run into.)
-  for (int i = tid; i < G::TILE / 16; i += 256) reinterpret_cast<bf16x8*>(sm.v[2])[i] = zero8;
+  for (int i = tid; i < G::TILE / 16; i += 256) reinterpret_cast<bf16x8*>(sm.v[G::VR - 1])[i] = zero8;
   if (G::PAD > 0 && tid < (G::PAD + 16) / 16) reinterpret_cast<bf16x8*>(sm.pad)[tid] = zero8;
 
   const int ql = qt * AQ + wave * 32 + r32;
@@ -766,6 +768,8 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   auto land = [&](auto keep) {
     if (decltype(keep)::value == 4)
       __builtin_amdgcn_s_waitcnt(0x0074);  // vmcnt(4) lgkmcnt(0)
+    else if (decltype(keep)::value == 3)
+      __builtin_amdgcn_s_waitcnt(0x0073);  // vmcnt(3) lgkmcnt(0)
     else if (decltype(keep)::value == 6)
       __builtin_amdgcn_s_waitcnt(0x0076);  // vmcnt(6) lgkmcnt(0)
     else
@@ -774,7 +778,10 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
-  using Keep4 = std::integral_constant<int, 2 * G::COPIES>;  // this iteration's copies stay in flight
+  // copies that stay in flight at the end of an iteration: head_dim 64 both
+  // of its copies (K(t+3), V(t+1)), head_dim 72 only K(t+3) (V(t) is needed
+  // in the next iteration)
+  using Keep4 = std::integral_constant<int, HD == 64 ? 4 : 3>;
   using Keep0 = std::integral_constant<int, 0>;
 
   const dma::LaneOff<HD> lo = dma::lane_offsets<HD>(lane);
@@ -805,8 +812,16 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   auto iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, bf16x8 (&pp)[2][2],
                   bf16x8 (&pn)[2][2]) {
     const int s1 = slot == 2 ? 0 : slot + 1, s2 = slot == 0 ? 2 : slot - 1;  // (t+1) % 3, (t-1) % 3
-    copy_k(min(t + 3, nkt - 1) * AK, slot);
-    copy_v((t + 1) * AK, s1);
+    int vs;  // V slot of PV(t-1)
+    if constexpr (HD == 64) {
+      copy_k(min(t + 3, nkt - 1) * AK, slot);
+      copy_v((t + 1) * AK, s1);
+      vs = s2;
+    } else {
+      copy_v(t * AK, t & 1);  // first, so that the end-of-iteration wait can leave K(t+3) in flight
+      copy_k(min(t + 3, nkt - 1) * AK, slot);
+      vs = (t + 1) & 1;
+    }
     float delta;
     const float a_new = dma::raise_max_shifted(tile_max<false>(c0, c1, g, t * AK, L), m_run, l_run, delta);
     rescale_o();
@@ -817,7 +832,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
         c0[r] -= delta;
         c1[r] -= delta;
       }
-    dma::region<HD>(sm.k[s1], sm.v[s2], lo, qf, q4, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
+    dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
     land(Keep4{});
     slot = s1;
   };
@@ -825,8 +840,12 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   copy_k(0, 0);
   copy_k(min(1, nkt - 1) * AK, 1);
   copy_k(min(2, nkt - 1) * AK, 2);
-  copy_v(0, 0);
-  land(Keep4{});
+  if constexpr (HD == 64) {
+    copy_v(0, 0);
+    land(Keep4{});  // K(0) and K(1) have landed
+  } else {
+    land(std::integral_constant<int, 6>{});  // K(0) has landed
+  }
   f32x16 a0, a1, b0, b1;
   dma::qk<HD>(sm.k[0], lo, qf, q4, a0, a1);
   {  // the running max starts at tile 0's (keys past L masked)
@@ -838,6 +857,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     }
   }
   // iteration 0 copies K(3) into slot 0: every wave must be done reading K(0)
+  // (and, at head_dim 72, K(1) must have landed)
   land(Keep4{});
   bf16x8 pa[2][2] = {{zero8, zero8}, {zero8, zero8}}, pb[2][2];
   int t = 0;
@@ -855,8 +875,16 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
       for (int hf = 0; hf < 2; ++hf) pa[kb][hf] = pb[kb][hf];
     ++t;
   }
-  {  // last tile t = nkt - 1 (possibly partial); V(t) was copied in iteration t-1
-    const int sprev = slot == 0 ? 2 : slot - 1;
+  {  // last tile t = nkt - 1 (possibly partial); head_dim 64: V(t) was copied in iteration t-1
+    int sprev, scur;
+    if constexpr (HD == 64) {
+      sprev = slot == 0 ? 2 : slot - 1;
+      scur = slot;
+    } else {
+      copy_v(t * AK, t & 1);
+      sprev = (t + 1) & 1;
+      scur = t & 1;
+    }
     const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L)
                                    : tile_max<false>(a0, a1, g, t * AK, L);
     float delta;
@@ -867,7 +895,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     dma::pv<HD>(sm.v[sprev], lo, pa, oacc);
     rescale_o();
     land(Keep0{});
-    dma::pv<HD>(sm.v[slot], lo, pb, oacc);
+    dma::pv<HD>(sm.v[scur], lo, pb, oacc);
   }
   l_run += __shfl_xor(l_run, 32, kWave);
   if (ql < Lq) {
@@ -892,8 +920,8 @@ __global__ __launch_bounds__(256, 3) void k_attn_bf16_dma(AttnIO io, int D, int 
   attn_body_dma<64>(io, D, heads, scale_log2, S, sm);
 }
 
-// head_dim 72: 55 KB of LDS and about 190 VGPRs, two workgroups per CU.
-__global__ __launch_bounds__(256, 2) void k_attn_bf16_dma72(AttnIO io, int D, int heads, float scale_log2,
+// head_dim 72: 46 KB of LDS, three workgroups per CU.
+__global__ __launch_bounds__(256, 3) void k_attn_bf16_dma72(AttnIO io, int D, int heads, float scale_log2,
                                                             SegTable S) {
   __shared__ __attribute__((aligned(1024))) dma::Smem<72> sm;
   attn_body_dma<72>(io, D, heads, scale_log2, S, sm);
