@@ -26,9 +26,10 @@
 // workgroup order is remapped so that each XCD works on whole heads.
 // head_dim 72 pads QK^T to 5 k-steps of 16 (d 72..79 zero) and computes O^T in
 // three 32-row blocks (rows 72..95 are computed from zero V^T rows and dropped).
-// head_dim 64 runs a software-pipelined form of the same computation with
-// direct global->LDS copies (k_attn_bf16_dma, described with its code); the
-// kernel above remains for head_dim 64 inputs too large for its 32-bit offsets.
+// Both head dims normally run a software-pipelined form of the same
+// computation with direct global->LDS copies (k_attn_bf16_dma and
+// k_attn_bf16_dma72, described with their code); the staged kernels above
+// remain for inputs too large for their 32-bit offsets.
 //
 // fp32 path (fp32 models, head_dim <= 64): one thread per (query, head).
 
