@@ -331,6 +331,33 @@ def test_frame_region_small_end_to_end_d72():
     check_end_to_end(wl, teacher_forced=False)
 
 
+MID72 = W.ModelCfg(D=1152, heads=16, head_dim=72, mlp=1152, L=1, dtype="bf16")
+
+
+def test_ragged_d72_tile_edges():
+    """The pipelined head_dim-72 attention at its tile edges: four requests
+    whose segments hold one partial key tile, exactly the two-tile path (one
+    loop iteration and the last tile), and longer ragged tails, with staggered
+    starts; every step teacher-forced against the oracle."""
+    wl = W.custom("ragged72", MID72, [W.Request(3, 24, 20), W.Request(2, 16, 16), W.Request(2, 10, 14),
+                                      W.Request(1, 4, 4)],
+                  [0.6, 0.75, 0.9, 0.5], [("uniform", 0.3, 0.7), 0.5, 0.5, 0.2], [4, 3, 3, 2])
+    R, states, sels = run_gpu(wl, trace=True)
+    lens = sorted({int(x) for _, _, cu in sels for x in np.diff(cu) if x > 0})
+    print(f"[ragged72] segment lengths seen: {lens}")
+    assert any(x < 64 for x in lens) and any(64 < x <= 128 for x in lens) and any(x > 128 for x in lens)
+    model = O.model_from_workload(wl)
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    info = O.token_info(wl.requests)
+    worst = 0.0
+    for i, p in enumerate(plans):
+        res = O.step(wl, model, states[i], p, "model", info=info)
+        assert np.array_equal(sels[i][1], res.idx), i
+        worst = max(worst, np.abs(states[i + 1] - res.state).max())
+    print(f"[ragged72] teacher-forced per-step max_abs = {worst:.3e}")
+    assert worst <= TOL["bf16"]
+
+
 def test_frame_region_full_shape_one_block_step():
     """Frame+region at its full shape (21 x 64x64 latent) with a one-block
     head_dim-72 denoiser: run until every frame is active, then compare the
