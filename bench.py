@@ -376,7 +376,7 @@ def main():
                         cache_period=args.cache_period, per_frame_grid=args.per_frame_grid)
     R.reset()
     stream = torch.cuda.current_stream()
-    D, L, mlp = wl.model.D, wl.model.L, wl.model.mlp
+    D, L, mlp, hd = wl.model.D, wl.model.L, wl.model.mlp, wl.model.head_dim
     req_tokens = np.diff(np.asarray(wl.tok_offset)).astype(np.float64)
     force = bool(args.select_every_step)
     for i in range(args.warmup):
@@ -389,19 +389,34 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     refined = 0
-    attn_flop_timed = 0.0  # latent cache: queries x all keys of the request, summed over the timed steps
+
+    def joint_flop():  # one block's joint attention FLOPs of the step just run: 4 D sum_r n_r^2
+        seg = np.diff(np.asarray(R.cu_host)).astype(np.float64)
+        return 4.0 * D * float((seg ** 2).sum())
+
+    # Attention FLOPs and selected tokens summed over the timed steps (the
+    # selection can change from step to step, e.g. as frames reach their
+    # start times); host-side values only, no extra synchronisation.
+    attn_flop_timed = 0.0  # latent cache: queries x all keys of the request
+    n_timed = 0.0
     for i in range(args.warmup, args.warmup + args.steps):
         refined += R.step(i, force_select=force)
+        n_timed += R.n_sel
         if args.cache_period > 0:
             attn_flop_timed += 4.0 * D * float((np.diff(R.cu_fwd).astype(np.float64) * req_tokens).sum())
+        else:
+            attn_flop_timed += joint_flop()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     attn_timing = S.sphinx_timing_read()["attention"]
     # per-class breakdown from a few further, untimed steps with every class bracketed
     S.sphinx_timing_enable(True)
     n_breakdown = min(args.steps, 5)
+    attn_flop_bd, n_bd = 0.0, 0.0
     for i in range(args.warmup + args.steps, args.warmup + args.steps + n_breakdown):
         R.step(i, force_select=force)
+        attn_flop_bd += joint_flop()
+        n_bd += R.n_sel
     torch.cuda.synchronize()
     timing = S.sphinx_timing_read()
     S.sphinx_timing_enable(False)
@@ -409,9 +424,10 @@ def main():
     ms_per_step = 1e3 * wall / args.steps
     value = refined / wall
     n = R.n_sel
-    cu = R.cu_host
-    seg = np.diff(cu).astype(np.float64)
-    attn_flop = 4.0 * D * float((seg ** 2).sum())
+    # FLOPs per attention launch, averaged over the timed steps (each step
+    # launches attention once per block)
+    attn_flop = attn_flop_timed * L / max(attn_timing[0], 1)
+    bd_launch_flop = attn_flop_bd / n_breakdown  # the same for the breakdown steps
     if args.attention == "factorised":  # spatial (per frame) and temporal (per position) launches alternate
         idx = R.idx[:n].cpu().numpy().astype(np.int64)
         toff = np.asarray(wl.tok_offset)
@@ -420,28 +436,33 @@ def main():
         loc = idx - toff[r_of]
         frame_cnt = np.unique(np.stack([r_of, loc // tpf], 1), axis=0, return_counts=True)[1].astype(np.float64)
         col_cnt = np.unique(np.stack([r_of, loc % tpf], 1), axis=0, return_counts=True)[1].astype(np.float64)
-        attn_flop = 4.0 * D * float((frame_cnt ** 2).sum() + (col_cnt ** 2).sum()) / 2.0
-    if args.cache_period > 0:  # launches differ between full and partial steps: average FLOPs per launch
-        attn_flop = attn_flop_timed * L / attn_timing[0]
-    gemm_flop = {"gemm_qkv": 2.0 * n * D * 3 * D, "gemm_out": 2.0 * n * D * D, "gemm_mlp1": 2.0 * n * D * mlp,
-                 "gemm_mlp2": 2.0 * n * mlp * D}
+        # (from the last step's selection; the headline selection is the same every step)
+        attn_flop = bd_launch_flop = 4.0 * D * float((frame_cnt ** 2).sum() + (col_cnt ** 2).sum()) / 2.0
+
+    def gemm_flops(nn):
+        return {"gemm_qkv": 2.0 * nn * D * 3 * D, "gemm_out": 2.0 * nn * D * D, "gemm_mlp1": 2.0 * nn * D * mlp,
+                "gemm_mlp2": 2.0 * nn * mlp * D}
+
+    gemm_flop = gemm_flops(n_timed / args.steps)  # per launch, averaged over the timed steps
+    gemm_flop_bd = gemm_flops(n_bd / n_breakdown)
     kernels = {}
     for k, (cnt, ms) in timing.items():
         if cnt == 0:
             continue
         avg_us = 1e3 * ms / cnt
         e = {"launches": cnt, "avg_us": round(avg_us, 2), "ms_per_step": round(ms / n_breakdown, 4)}
-        if k == "attention":
-            e["tflops"] = round(attn_flop / (avg_us * 1e-6) / 1e12, 1)
-        if k in gemm_flop:
-            e["tflops"] = round(gemm_flop[k] / (avg_us * 1e-6) / 1e12, 1)
+        if k == "attention" and args.cache_period == 0:
+            e["tflops"] = round(bd_launch_flop / (avg_us * 1e-6) / 1e12, 1)
+        if k in gemm_flop_bd:
+            e["tflops"] = round(gemm_flop_bd[k] / (avg_us * 1e-6) / 1e12, 1)
         kernels[k] = e
     cnt, ms = attn_timing
     avg_s = ms / cnt / 1e3
     achieved = attn_flop / avg_s / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic_entry("attention", args.config) if args.cache_period == 0 else None,
-                "kernel": "k_attn_bf16_dma (varlen flash attention, head_dim 64)" if args.attention == "joint"
+                "kernel": (f"k_attn_bf16_dma{'' if hd == 64 else hd} (varlen flash attention, head_dim {hd})"
+                           if wl.model.dtype == "bf16" else "k_attn_f32") if args.attention == "joint"
                 else "attention class: k_attn_bf16_dma per frame and k_attn_temporal per position, alternating",
                 "algorithmic_flop_per_launch": attn_flop}
     step_flop = L * (attn_flop + sum(gemm_flop.values()))
