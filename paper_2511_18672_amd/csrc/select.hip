@@ -104,34 +104,57 @@ __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, co
   }
 }
 
-// Exclusive scan of nblk chunk counts by one workgroup of 1024 threads.
+// Exclusive scan of nblk chunk counts by one workgroup of 1024 threads, in
+// blocks of kScanBlk counts staged in LDS: coalesced loads and stores, and
+// each thread scans 16 consecutive counts from LDS (a strided walk through
+// global memory would serialise 16 load latencies per thread).
+constexpr int kScanBlk = 16384;
 __global__ __launch_bounds__(1024) void k_select_scan(const int32_t* __restrict__ blk_cnt, int nblk,
                                                      int32_t* __restrict__ blk_off, int32_t* __restrict__ cu_sel,
                                                      int R) {
+  __shared__ int32_t s_v[kScanBlk];
   __shared__ int s_part[1024 / kWave];
-  const int per = (nblk + 1023) / 1024;
-  const int b0 = threadIdx.x * per;
-  int local = 0;
-  for (int i = 0; i < per; ++i)
-    if (b0 + i < nblk) local += blk_cnt[b0 + i];
-  const int lane = lane_id();
-  const int incl = wave_incl_scan(local, lane);
-  if (lane == kWave - 1) s_part[threadIdx.x / kWave] = incl;
-  __syncthreads();
-  int wave_base = 0;
-  for (int w = 0; w < (int)(threadIdx.x / kWave); ++w) wave_base += s_part[w];
-  int run = wave_base + incl - local;
-  for (int i = 0; i < per; ++i) {
-    if (b0 + i < nblk) {
-      blk_off[b0 + i] = run;
-      run += blk_cnt[b0 + i];
+  const int tid = (int)threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  constexpr int per = kScanBlk / 1024;  // 16 consecutive counts per thread
+  int carry = 0;                        // counts of the blocks before this one
+  for (int base = 0; base < nblk; base += kScanBlk) {
+    const int m = min(kScanBlk, nblk - base);
+    {  // all 16 loads issued before the first LDS store
+      int v[per];
+#pragma unroll
+      for (int k = 0; k < per; ++k) v[k] = (tid + 1024 * k < m) ? blk_cnt[base + tid + 1024 * k] : 0;
+#pragma unroll
+      for (int k = 0; k < per; ++k) s_v[tid + 1024 * k] = v[k];
     }
+    __syncthreads();
+    int local = 0;
+#pragma unroll
+    for (int j = 0; j < per; ++j)
+      if (tid * per + j < m) local += s_v[tid * per + j];
+    const int incl = wave_incl_scan(local, lane);
+    if (lane == kWave - 1) s_part[wave] = incl;
+    __syncthreads();
+    int wave_base = 0, total = 0;
+    for (int w = 0; w < 1024 / kWave; ++w) {
+      if (w < wave) wave_base += s_part[w];
+      total += s_part[w];
+    }
+    int run = carry + wave_base + incl - local;
+#pragma unroll
+    for (int j = 0; j < per; ++j)
+      if (tid * per + j < m) {
+        const int v = s_v[tid * per + j];
+        s_v[tid * per + j] = run;
+        run += v;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < per; ++k)
+      if (tid + 1024 * k < m) blk_off[base + tid + 1024 * k] = s_v[tid + 1024 * k];
+    carry += total;
+    __syncthreads();  // s_v and s_part are reused by the next block
   }
-  if (threadIdx.x == 1023) {
-    int tot = 0;
-    for (int w = 0; w < 1024 / kWave; ++w) tot += s_part[w];
-    cu_sel[R] = tot;
-  }
+  if (tid == 0) cu_sel[R] = carry;
 }
 
 __global__ __launch_bounds__(kTPB) void k_select_write(ReqTable T, int64_t N, const uint8_t* __restrict__ mask,
