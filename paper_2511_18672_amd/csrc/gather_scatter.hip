@@ -113,6 +113,10 @@ __global__ __launch_bounds__(kTPB) void k_gather_nchw(ReqTable T, const ST* __re
 }
 
 // Token-major gather: lane i moves values 4*(i%4) .. 4*(i%4)+3 of token i/4.
+// Token-major gather: four lanes per token, 16 bytes each, and two tokens per
+// thread (j and j + half): the second token's index, state and noise loads
+// are in flight together with the first's, which doubles the bytes each
+// thread keeps in flight (the kernel is bound by load latency, not by HBM).
 template <typename ST, typename ET>
 __global__ __launch_bounds__(kTPB) void k_gather_tok(ReqTable T, const ST* __restrict__ state,
                                                      const ET* __restrict__ eps, const int32_t* __restrict__ idx,
@@ -120,22 +124,42 @@ __global__ __launch_bounds__(kTPB) void k_gather_tok(ReqTable T, const ST* __res
                                                      const float* __restrict__ b, GatherCtx C,
                                                      float* __restrict__ x) {
   const int64_t i = (int64_t)blockIdx.x * kTPB + threadIdx.x;
-  const int64_t j = i >> 2;
-  if (j >= n) return;
+  const int64_t half = ((int64_t)n + 1) >> 1;
+  const int64_t j1 = i >> 2;
+  if (j1 >= half) return;
   const int q = (int)(i & 3);
-  const int32_t t = idx[j];
-  if (t < 0 || t >= T.tok_off[T.R]) return;  // out-of-range index: nothing is read
-  const int g = frame_of_token(T, t);
-  const bool ctx = C.wmask != nullptr && C.wmask[t] == 0;
-  const float av = ctx ? C.a[g] : a[g], bv = ctx ? C.b[g] : b[g];
-  const int64_t e = 16 * (int64_t)t + 4 * q;
-  const float4 z = Vec<ST>::load4nt(state, e);
-  float4 v = make_float4(av * z.x, av * z.y, av * z.z, av * z.w);
-  if (eps != nullptr && bv != 0.0f) {
-    const float4 nz = Vec<ET>::load4(eps, e);
-    v = make_float4(fmaf(bv, nz.x, v.x), fmaf(bv, nz.y, v.y), fmaf(bv, nz.z, v.z), fmaf(bv, nz.w, v.w));
+  const int64_t js[2] = {j1, j1 + half};
+  const int64_t Ntok = T.tok_off[T.R];
+  int32_t ts[2];
+  bool ok[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    ts[u] = js[u] < n ? idx[js[u]] : -1;
+    ok[u] = ts[u] >= 0 && ts[u] < Ntok;  // out-of-range index: nothing is read
   }
-  Vec<float>::store4nt(x, 4 * i, v);
+  float4 z[2], nz[2];
+  float av[2], bv[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    if (!ok[u]) continue;
+    const int32_t t = ts[u];
+    const int g = frame_of_token(T, t);
+    const bool ctx = C.wmask != nullptr && C.wmask[t] == 0;
+    av[u] = ctx ? C.a[g] : a[g];
+    bv[u] = ctx ? C.b[g] : b[g];
+    const int64_t e = 16 * (int64_t)t + 4 * q;
+    z[u] = Vec<ST>::load4nt(state, e);
+    if (eps != nullptr && bv[u] != 0.0f) nz[u] = Vec<ET>::load4(eps, e);  // noise only where injected
+  }
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    if (!ok[u]) continue;
+    float4 v = make_float4(av[u] * z[u].x, av[u] * z[u].y, av[u] * z[u].z, av[u] * z[u].w);
+    if (eps != nullptr && bv[u] != 0.0f)
+      v = make_float4(fmaf(bv[u], nz[u].x, v.x), fmaf(bv[u], nz[u].y, v.y), fmaf(bv[u], nz[u].z, v.z),
+                      fmaf(bv[u], nz[u].w, v.w));
+    Vec<float>::store4nt(x, 16 * js[u] + 4 * q, v);
+  }
 }
 
 template <typename OT>
@@ -242,8 +266,8 @@ template <typename ST, typename ET>
 void gather_typed(const ReqTable& T, sphinx_layout lay, const void* state, const void* eps, const int32_t* idx,
                   int n, const float* a, const float* b, const GatherCtx& C, float* x, hipStream_t s) {
   if (lay == SPHINX_LAYOUT_TOKENS)
-    k_gather_tok<ST, ET><<<grid_for(4 * (int64_t)n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a,
-                                                                   b, C, x);
+    k_gather_tok<ST, ET><<<grid_for(4 * (((int64_t)n + 1) >> 1)), kTPB, 0, s>>>(T, (const ST*)state,
+                                                                                (const ET*)eps, idx, n, a, b, C, x);
   else
     k_gather_nchw<ST, ET><<<grid_for(n), kTPB, 0, s>>>(T, (const ST*)state, (const ET*)eps, idx, n, a, b, C, x);
 }
