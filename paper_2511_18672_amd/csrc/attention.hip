@@ -384,7 +384,7 @@ template <int HD>
 struct Geo;
 template <>
 struct Geo<64> {
-  static constexpr int RB = 128, DB = 2, KS = 4, NPV = 8, NQK = 8, TILE = AK * RB, PAD = 0, COPIES = 2, VR = 3;
+  static constexpr int RB = 128, DB = 2, NPV = 8, NQK = 8, TILE = AK * RB, PAD = 0, COPIES = 2, VR = 3;
 };
 template <>
 struct Geo<72> {
@@ -392,7 +392,7 @@ struct Geo<72> {
   // its tile (into dims that are dropped); the pad keeps it inside the ring.
   // VR: V ring of two slots (46 KB of LDS, three workgroups per CU); V(t) is
   // copied in the iteration before its PV and waited for at its end.
-  static constexpr int RB = 144, DB = 3, KS = 5, NPV = 12, NQK = 10, TILE = AK * RB, PAD = 64, COPIES = 3, VR = 2;
+  static constexpr int RB = 144, DB = 3, NPV = 12, NQK = 10, TILE = AK * RB, PAD = 64, COPIES = 3, VR = 2;
 };
 
 template <int HD>

@@ -127,28 +127,6 @@ __global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int
   }
 }
 
-// Loads the row into registers and returns (mean, rstd).
-__device__ __forceinline__ void row_stats(const float* __restrict__ hr, int D, int lane, float (&v)[kMaxPer],
-                                          float& mu, float& rstd) {
-  const int per = D / kWave;
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < kMaxPer; ++i)
-    if (i < per) {
-      v[i] = hr[i * kWave + lane];
-      s += v[i];
-    }
-  mu = wave_sum(s) / (float)D;
-  float s2 = 0.f;
-#pragma unroll
-  for (int i = 0; i < kMaxPer; ++i)
-    if (i < per) {
-      const float d = v[i] - mu;
-      s2 = fmaf(d, d, s2);
-    }
-  rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
-}
-
 template <int V> struct VecF;
 template <> struct VecF<1> {
   typedef float T;
