@@ -179,7 +179,8 @@ template <> struct VecStore<bf16, 4> {
 // One wave per row; lane handles V consecutive values per 64*V-wide chunk, so
 // every load and store of a wave is one contiguous 256*V- (fp32) or 128*V-byte run.
 // CH: chunks of 64 V columns per row when known at compile time (then all
-// row loads issue back to back), 0 for any D.
+// row loads issue back to back; instantiated for D = 512, 1024, 2048 with
+// V = 4 and D = 1152 with V = 2), 0 for any D.
 template <typename OT, int V, int CH>
 __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, int n, int D,
                                                  const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
@@ -363,12 +364,14 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
   const bool v4 = (D % (kWave * 4) == 0) && (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
   const bool v2 = (D % (kWave * 2) == 0) && (ldm % 2 == 0) && (sh_off % 2 == 0) && (sc_off % 2 == 0);
   const int ch4 = v4 ? D / (kWave * 4) : 0;
+  const int ch2 = (!v4 && v2) ? D / (kWave * 2) : 0;  // 9 at D = 1152
   if (odt == SPHINX_BF16) {
     bf16* o = (bf16*)out;
     if (ch4 == 4) k_ln_mod<bf16, 4, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 2) k_ln_mod<bf16, 4, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 8) k_ln_mod<bf16, 4, 8><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v4) k_ln_mod<bf16, 4, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch2 == 9) k_ln_mod<bf16, 2, 9><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v2) k_ln_mod<bf16, 2, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else k_ln_mod<bf16, 1, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
   } else {
@@ -377,6 +380,7 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
     else if (ch4 == 2) k_ln_mod<float, 4, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 8) k_ln_mod<float, 4, 8><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v4) k_ln_mod<float, 4, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch2 == 9) k_ln_mod<float, 2, 9><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v2) k_ln_mod<float, 2, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else k_ln_mod<float, 1, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
   }
