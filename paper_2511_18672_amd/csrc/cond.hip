@@ -11,6 +11,8 @@
 //  * k_pos_tables  fp64 sinusoid tables for patch rows, columns and frames.
 //  * k_token_meta  per selected row: global frame, conditioning row, packed
 //                  (frame, y, x) position.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -74,7 +76,11 @@ struct WVec<float> {
 };
 
 constexpr int kGemvMaxVec = 4;  // K <= 4 * 64 * (elements per vector)
-template <typename WT, bool SILU_OUT>
+// NV = ceil(K / (64 * elements per vector)) vectors per lane, known at compile
+// time: every lane issues its NV loads back to back (an out-of-range vector
+// reloads the row's last one and is zeroed), instead of waiting after each
+// guarded load.
+template <typename WT, bool SILU_OUT, int NV>
 __global__ __launch_bounds__(kTPB) void k_rowgemm(const float* __restrict__ X, int ldx, const int32_t* __restrict__ Up,
                                                   int K, int N, const WT* __restrict__ W, const WT* __restrict__ bias,
                                                   float* __restrict__ out, int ldo) {
@@ -84,33 +90,30 @@ __global__ __launch_bounds__(kTPB) void k_rowgemm(const float* __restrict__ X, i
   const int lane = lane_id();
   const int U = *Up;
   const int nvec = K / VN;
-  float w[kGemvMaxVec][VN];
+  const float bv = load_as_f32(bias, n);
+  float w[NV][VN];
   const WT* wr = W + (int64_t)n * K;
 #pragma unroll
-  for (int i = 0; i < kGemvMaxVec; ++i) {
-    const int v = lane + kWave * i;
-    if (v < nvec)
-      WVec<WT>::get(wr + v * VN, w[i]);
-    else
+  for (int i = 0; i < NV; ++i) WVec<WT>::get(wr + min(lane + kWave * i, nvec - 1) * VN, w[i]);
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (lane + kWave * i >= nvec)
 #pragma unroll
       for (int e = 0; e < VN; ++e) w[i][e] = 0.0f;
-  }
-  const float bv = load_as_f32(bias, n);
   for (int u = 0; u < U; ++u) {
     const float* xr = X + (int64_t)u * ldx;
     float acc = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kGemvMaxVec; ++i) {
-      const int v = lane + kWave * i;
-      if (v < nvec)
+    for (int i = 0; i < NV; ++i) {
+      const int v = min(lane + kWave * i, nvec - 1);  // zero weights past the row
 #pragma unroll
-        for (int e = 0; e < VN; e += 4) {
-          const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + v * VN + e);
-          acc = fmaf(w[i][e], xv[0], acc);
-          acc = fmaf(w[i][e + 1], xv[1], acc);
-          acc = fmaf(w[i][e + 2], xv[2], acc);
-          acc = fmaf(w[i][e + 3], xv[3], acc);
-        }
+      for (int e = 0; e < VN; e += 4) {
+        const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + v * VN + e);
+        acc = fmaf(w[i][e], xv[0], acc);
+        acc = fmaf(w[i][e + 1], xv[1], acc);
+        acc = fmaf(w[i][e + 2], xv[2], acc);
+        acc = fmaf(w[i][e + 3], xv[3], acc);
+      }
     }
     acc = wave_sum(acc);
     if (lane == 0) {
@@ -176,16 +179,24 @@ hipError_t launch_temb(const int32_t* utau, const int32_t* U, int Gmax, float* t
 hipError_t launch_rowgemm(const float* X, int ldx, const int32_t* U, int K, const void* W, const void* b,
                           sphinx_dtype wdt, int N, bool silu_out, float* out, int ldo, hipStream_t s) {
   const int g = (N + kTPB / kWave - 1) / (kTPB / kWave);
+  const int nv = (K / (wdt == SPHINX_BF16 ? 8 : 4) + kWave - 1) / kWave;  // vectors per lane, 1..4
+  auto go = [&](auto wt, auto silu, auto nvc) {
+    typedef decltype(wt) WT;
+    k_rowgemm<WT, decltype(silu)::value, decltype(nvc)::value>
+        <<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const WT*)W, (const WT*)b, out, ldo);
+  };
+  auto by_nv = [&](auto wt, auto silu) {
+    if (nv <= 1) go(wt, silu, std::integral_constant<int, 1>{});
+    else if (nv == 2) go(wt, silu, std::integral_constant<int, 2>{});
+    else if (nv == 3) go(wt, silu, std::integral_constant<int, 3>{});
+    else go(wt, silu, std::integral_constant<int, 4>{});
+  };
   if (wdt == SPHINX_BF16) {
-    if (silu_out)
-      k_rowgemm<bf16, true><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const bf16*)W, (const bf16*)b, out, ldo);
-    else
-      k_rowgemm<bf16, false><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const bf16*)W, (const bf16*)b, out, ldo);
+    if (silu_out) by_nv(bf16{}, std::true_type{});
+    else by_nv(bf16{}, std::false_type{});
   } else {
-    if (silu_out)
-      k_rowgemm<float, true><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const float*)W, (const float*)b, out, ldo);
-    else
-      k_rowgemm<float, false><<<g, kTPB, 0, s>>>(X, ldx, U, K, N, (const float*)W, (const float*)b, out, ldo);
+    if (silu_out) by_nv(float{}, std::true_type{});
+    else by_nv(float{}, std::false_type{});
   }
   return hipGetLastError();
 }
