@@ -88,6 +88,30 @@ def test_select_edge_cases():
     print(f"[select] big N={big.N} n_sel={n}")
 
 
+def test_select_stale_workspace_many_chunks():
+    """Selection on a workspace full of stale bytes, three calls in a row on
+    it: 150 chunks of 4096 tokens, a 3-chunk input, then 2301 chunks."""
+    big = W.custom("lookback", MICRO_BF16, [W.Request(150, 128, 128), W.Request(2, 6, 4)], [0.3, 0.6], [0.5, 0.5],
+                   [1, 1], u_recipe="uniform", with_weights=False)
+    small = W.custom("lookback2", MICRO_BF16, [W.Request(9, 64, 66)], [0.5], [0.5], [1], u_recipe="uniform",
+                     with_weights=False)
+    huge = W.custom("lookback3", MICRO_BF16, [W.Request(3, 6, 10), W.Request(1150, 128, 128),
+                                              W.Request(1150, 128, 128)], [0.5, 0.3, 0.6], [0.5] * 3, [1] * 3,
+                    u_recipe="uniform", with_weights=False)
+    ws = torch.full((S.sphinx_select_workspace_bytes(huge.N),), 0xAB, dtype=torch.uint8, device="cuda")
+    for wl in (big, small, huge):
+        info = O.token_info(wl.requests)
+        mask, idx, cu, n = O.select(wl.u, wl.thr[info.gframe], np.ones(wl.N, bool), wl.tok_offset[:-1])
+        gm = torch.empty(wl.N, dtype=torch.uint8, device="cuda")
+        gi = torch.full((wl.N,), -7, dtype=torch.int32, device="cuda")
+        gc = torch.empty(wl.R + 1, dtype=torch.int32, device="cuda")
+        cu_host = S.sphinx_select_mask(S.make_requests(wl.requests), _dev(wl.u), _dev(wl.thr), None, gm, gi, gc, ws)
+        assert np.array_equal(gm.cpu().numpy().astype(bool), mask)
+        assert np.array_equal(gi[:n].cpu().numpy(), idx)
+        assert list(cu_host) == list(cu) + [n]
+        print(f"[select] stale-workspace N={wl.N} chunks={(wl.N + 4095) // 4096} n_sel={n}")
+
+
 def _in_layout(nchw, tokens_2d, layout):
     """The same latents in `layout` (tokens_2d: [N][16] in patch order)."""
     return nchw if layout == S.NCHW else np.ascontiguousarray(tokens_2d).ravel()
