@@ -238,23 +238,15 @@ struct DmaCfg {
   static_assert(EH == 1 || EH == 2, "whole tile or two halves (one per wave row)");
 };
 
-template <int EPI, int BM, int BN, int NS, int EH = 1>
-__device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const bf16* __restrict__ W,
-                                              const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e,
-                                              unsigned char* smem) {
-  typedef DmaCfg<BM, BN, NS, EH> C;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  const int g = lane >> 5, r32 = lane & 31;
-  // One-dimensional grid; workgroups are dealt to the 8 XCDs round-robin.
-  // Wide N (more than 8 column tiles): tiles in plain N-fastest order, so XCD
-  // x always gets the column tiles n = x (mod 8) and keeps that eighth of W in
-  // its L2 for the whole kernel.  Narrow N: renumbered (xcd_tile) so that each
-  // XCD takes consecutive row blocks of A with all their column tiles, and A is
-  // fetched into one L2 instead of eight.
+// Tile of a one-dimensional grid of BM x BN tiles; workgroups are dealt to the
+// 8 XCDs round-robin.  Wide N (more than 8 column tiles): tiles in plain
+// N-fastest order, so XCD x always gets the column tiles n = x (mod 8) and
+// keeps that eighth of W in its L2 for the whole kernel.  Narrow N: renumbered
+// (xcd_tile) so that each XCD takes consecutive row blocks of A with all their
+// column tiles, and A is fetched into one L2 instead of eight.
+template <int BM, int BN>
+__device__ __forceinline__ void grid_tile(int N, int& m0, int& n0) {
   const int nt = N / BN;
-  int m0, n0;
   if (nt > 8) {
     m0 = ((int)blockIdx.x / nt) * BM;
     n0 = ((int)blockIdx.x % nt) * BN;
@@ -263,6 +255,17 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     m0 = (tile / nt) * BM;
     n0 = (tile % nt) * BN;
   }
+}
+
+template <int EPI, int BM, int BN, int NS, int EH = 1>
+__device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                              const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e,
+                                              unsigned char* smem, int m0, int n0) {
+  typedef DmaCfg<BM, BN, NS, EH> C;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int g = lane >> 5, r32 = lane & 31;
 
   // copy sources: instruction i of this wave fills rows 8q .. 8q+7 of the
   // stage (q = wave * COPIES + i; rows < BM are A rows, the rest W rows)
@@ -435,7 +438,9 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   __global__ __launch_bounds__(256, 2) void NAME(const bf16* __restrict__ A, const bf16* __restrict__ W,          \
                                                  const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {  \
     __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<BM, 128, 2, EH>::SMEM];                   \
-    gemm_dma_body<EPI, BM, 128, 2, EH>(A, W, bias, M, N, K, e, smem);                                            \
+    int m0, n0;                                                                                                  \
+    grid_tile<BM, 128>(N, m0, n0);                                                                               \
+    gemm_dma_body<EPI, BM, 128, 2, EH>(A, W, bias, M, N, K, e, smem, m0, n0);                                    \
   }
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_bias, EPI_BIAS, 128, 1)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_gelu, EPI_GELU, 128, 1)
@@ -447,6 +452,31 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_bias, EPI_BIAS, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
+
+// Mixed row tiles for narrow outputs (at most 8 column tiles) that fit in one
+// round of two workgroups per CU.  XCD x takes the row band [x B, (x+1) B),
+// B = 192 nb + 128 ns, as nb 192-row and ns 128-row tiles per column tile; its
+// first nb * nt workgroups (at most one per CU) are the 192-row ones.  With
+// only 192-row tiles a CU can hold two of them (384 rows) while others hold
+// one; here a CU holds at most 192 + 128 rows.  Same results as either tile.
+template <int EPI>
+__global__ __launch_bounds__(256, 2) void k_gemm_dma_mix(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                                         const bf16* __restrict__ bias, int M, int N, int K,
+                                                         GemmEpi e, int nb, int ns) {
+  constexpr int S192 = DmaCfg<192, 128, 2, 2>::SMEM, S128 = DmaCfg<128, 128, 2, 1>::SMEM;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[S192 > S128 ? S192 : S128];
+  const int nt = N / 128;
+  const int x = (int)blockIdx.x & 7, k = (int)blockIdx.x >> 3;
+  const int band = x * (192 * nb + 128 * ns);
+  if (k < nb * nt) {
+    const int m0 = band + (k / nt) * 192;
+    if (m0 < M) gemm_dma_body<EPI, 192, 128, 2, 2>(A, W, bias, M, N, K, e, smem, m0, (k % nt) * 128);
+  } else {
+    const int j = k - nb * nt;
+    const int m0 = band + 192 * nb + (j / nt) * 128;
+    if (m0 < M) gemm_dma_body<EPI, 128, 128, 2, 1>(A, W, bias, M, N, K, e, smem, m0, (j % nt) * 128);
+  }
+}
 }  // namespace dma
 
 template <int EPI>
@@ -572,8 +602,22 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
     if ((int64_t)M * K < lim && (int64_t)N * K < lim) {
       const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
       const int64_t t128 = nt * ((M + 127) / 128), t192 = nt * ((M + 191) / 192);
-      // a 192-row tile does 1.5x the work of a 128-row one in 1.41x the time
-      if (tile_rounds(t192, slots, 1.41) < tile_rounds(t128, slots, 1.0)) {
+      // mixed tiles: narrow N, 192-row tiles filling more than half of one round
+      int nb = -1, ns = 0;
+      if (nt <= 8 && slots % 16 == 0 && t192 * 2 > slots && t192 <= slots) {
+        const int per = (int)(slots / 8 / nt);  // slots per XCD and column tile
+        const int need = (M + 7) / 8;           // rows per XCD band
+        nb = std::max(0, (need - 128 * per + 63) / 64);
+        ns = per - nb;
+        if (nb * 2 > per) nb = -1;  // some CU would hold two 192-row tiles
+      }
+      if (nb >= 0) {
+        const int grid = 8 * (nb + ns) * (int)nt;
+        if (epi == EPI_BIAS) dma::k_gemm_dma_mix<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
+        else if (epi == EPI_GELU) dma::k_gemm_dma_mix<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
+        else dma::k_gemm_dma_mix<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
+      } else if (tile_rounds(t192, slots, 1.41) < tile_rounds(t128, slots, 1.0)) {
+        // a 192-row tile does 1.5x the work of a 128-row one in 1.41x the time
         const int tiles = (int)t192;
         if (epi == EPI_BIAS) dma::k_gemm_dma192_bias<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
         else if (epi == EPI_GELU) dma::k_gemm_dma192_gelu<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
