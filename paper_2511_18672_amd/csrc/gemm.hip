@@ -453,28 +453,44 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
 
-// Mixed row tiles for narrow outputs (at most 8 column tiles) that fit in one
-// round of two workgroups per CU.  XCD x takes the row band [x B, (x+1) B),
-// B = 192 nb + 128 ns, as nb 192-row and ns 128-row tiles per column tile; its
-// first nb * nt workgroups (at most one per CU) are the 192-row ones.  With
-// only 192-row tiles a CU can hold two of them (384 rows) while others hold
-// one; here a CU holds at most 192 + 128 rows.  Same results as either tile.
-template <int EPI>
+// Mixed row tiles: nb 192-row and ns 128-row tiles per column tile.  Same
+// results as either tile.
+//  * Narrow outputs (at most 8 column tiles) that fit in one round of two
+//    workgroups per CU: XCD x takes the row band [x B, (x+1) B),
+//    B = 192 nb + 128 ns, with all column tiles; its first nb * nt workgroups
+//    (at most one per CU) are the 192-row ones.  With only 192-row tiles a CU
+//    can hold two of them (384 rows) while others hold one; here a CU holds at
+//    most 192 + 128 rows.
+//  * Wide outputs: column-fastest order (XCD x keeps the column tiles
+//    n = x mod 8), the 192-row tiles first and the 128-row ones last, so that
+//    the last round is made of the smaller tiles.
+template <int EPI, bool WIDE>
 __global__ __launch_bounds__(256, 2) void k_gemm_dma_mix(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                          const bf16* __restrict__ bias, int M, int N, int K,
                                                          GemmEpi e, int nb, int ns) {
   constexpr int S192 = DmaCfg<192, 128, 2, 2>::SMEM, S128 = DmaCfg<128, 128, 2, 1>::SMEM;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S192 > S128 ? S192 : S128];
   const int nt = N / 128;
-  const int x = (int)blockIdx.x & 7, k = (int)blockIdx.x >> 3;
-  const int band = x * (192 * nb + 128 * ns);
-  if (k < nb * nt) {
-    const int m0 = band + (k / nt) * 192;
-    if (m0 < M) gemm_dma_body<EPI, 192, 128, 2, 2>(A, W, bias, M, N, K, e, smem, m0, (k % nt) * 128);
-  } else {
-    const int j = k - nb * nt;
-    const int m0 = band + 192 * nb + (j / nt) * 128;
-    if (m0 < M) gemm_dma_body<EPI, 128, 128, 2, 1>(A, W, bias, M, N, K, e, smem, m0, (j % nt) * 128);
+  if constexpr (WIDE) {  // nb row tiles of 192 rows, then ns of 128, column-fastest
+    const int k = (int)blockIdx.x;
+    if (k < nb * nt) {
+      gemm_dma_body<EPI, 192, 128, 2, 2>(A, W, bias, M, N, K, e, smem, (k / nt) * 192, (k % nt) * 128);
+    } else {
+      const int j = k - nb * nt;
+      const int m0 = 192 * nb + (j / nt) * 128;
+      if (m0 < M) gemm_dma_body<EPI, 128, 128, 2, 1>(A, W, bias, M, N, K, e, smem, m0, (j % nt) * 128);
+    }
+  } else {  // XCD bands
+    const int x = (int)blockIdx.x & 7, k = (int)blockIdx.x >> 3;
+    const int band = x * (192 * nb + 128 * ns);
+    if (k < nb * nt) {
+      const int m0 = band + (k / nt) * 192;
+      if (m0 < M) gemm_dma_body<EPI, 192, 128, 2, 2>(A, W, bias, M, N, K, e, smem, m0, (k % nt) * 128);
+    } else {
+      const int j = k - nb * nt;
+      const int m0 = band + 192 * nb + (j / nt) * 128;
+      if (m0 < M) gemm_dma_body<EPI, 128, 128, 2, 1>(A, W, bias, M, N, K, e, smem, m0, (j % nt) * 128);
+    }
   }
 }
 }  // namespace dma
@@ -611,11 +627,24 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
         ns = per - nb;
         if (nb * 2 > per) nb = -1;  // some CU would hold two 192-row tiles
       }
+      // wide N needing more than three rounds of 192-row tiles: the last round
+      // all 128-row tiles (ns per column tile), 192-row tiles before it
+      if (nt > 8 && t192 > 3 * slots) {
+        const int ws = (int)(slots / nt);
+        const int wb = (M - 128 * ws + 191) / 192;
+        if (ws > 0 && wb > 0) {
+          const int grid = (wb + ws) * (int)nt;
+          if (epi == EPI_BIAS) dma::k_gemm_dma_mix<EPI_BIAS, true><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, wb, ws);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_mix<EPI_GELU, true><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, wb, ws);
+          else dma::k_gemm_dma_mix<EPI_GATED, true><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, wb, ws);
+          return hipGetLastError();
+        }
+      }
       if (nb >= 0) {
         const int grid = 8 * (nb + ns) * (int)nt;
-        if (epi == EPI_BIAS) dma::k_gemm_dma_mix<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
-        else if (epi == EPI_GELU) dma::k_gemm_dma_mix<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
-        else dma::k_gemm_dma_mix<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
+        if (epi == EPI_BIAS) dma::k_gemm_dma_mix<EPI_BIAS, false><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
+        else if (epi == EPI_GELU) dma::k_gemm_dma_mix<EPI_GELU, false><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
+        else dma::k_gemm_dma_mix<EPI_GATED, false><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e, nb, ns);
       } else if (tile_rounds(t192, slots, 1.41) < tile_rounds(t128, slots, 1.0)) {
         // a 192-row tile does 1.5x the work of a 128-row one in 1.41x the time
         const int tiles = (int)t192;
