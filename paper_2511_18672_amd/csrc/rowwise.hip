@@ -1,6 +1,6 @@
 // Row-wise kernels of the denoiser:
 //  * k_embed   h = x W_pe^T + b_pe + [Ty(y) || Tx(x)] + Tf(f)          (fp32)
-//  * k_ln_mod  a = LN(h) * (1 + scale[row]) + shift[row]  -> bf16/fp32  (one wave per row)
+//  * k_ln_mod  a = LN(h) * (1 + scale[row]) + shift[row]  -> bf16/fp32  (one wave per row, or per two rows)
 //  * k_final   eps_hat = (LN(h) (1 + scale) + shift) W_out^T + b_out, then the
 //              DDIM update x <- c1 x + c2 eps_hat in place (one wave per row;
 //              the 16 outputs are reduced with a butterfly reduce-scatter).
@@ -181,53 +181,64 @@ template <> struct VecStore<bf16, 4> {
 // CH: chunks of 64 V columns per row when known at compile time (then all
 // row loads issue back to back; instantiated for D = 512, 1024, 2048 with
 // V = 4 and D = 1152 with V = 2), 0 for any D.
-template <typename OT, int V, int CH>
+template <typename OT, int V, int CH, int R = 1>
 __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, int n, int D,
                                                  const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
                                                  const int32_t* __restrict__ crow, OT* __restrict__ out) {
   typedef typename VecF<V>::T VT;
+  static_assert(R == 1 || CH > 0, "several rows per wave need a compile-time chunk count");
   constexpr int kMaxChunks = CH > 0 ? CH : kMaxPer / V;
-  const int row = blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave);
-  if (row >= n) return;
+  const int row0 = (blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave)) * R;
+  if (row0 >= n) return;
   const int lane = lane_id();
   const int chunks = CH > 0 ? CH : D / (kWave * V);
-  const float* hr = h + (int64_t)row * D;
-  const float* m = mod + (int64_t)crow[row] * ldm;
-  VT v[kMaxChunks];
-  float s = 0.f;
+  // all rows' loads first; a row past n repeats row n - 1 and is not stored
+  VT v[R][kMaxChunks];
+  const float* m[R];
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i)
-    if (CH > 0 || i < chunks) v[i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+  for (int j = 0; j < R; ++j) {
+    const int row = min(row0 + j, n - 1);
+    const float* hr = h + (int64_t)row * D;
+    m[j] = mod + (int64_t)crow[row] * ldm;
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i)
-    if (CH > 0 || i < chunks)
+    for (int i = 0; i < kMaxChunks; ++i)
+      if (CH > 0 || i < chunks) v[j][i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+  }
 #pragma unroll
-      for (int e = 0; e < V; ++e) s += VecF<V>::get(v[i], e);
-  const float mu = wave_sum(s) / (float)D;
-  float s2 = 0.f;
+  for (int j = 0; j < R; ++j) {
+    float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i)
-    if (CH > 0 || i < chunks) {
+    for (int i = 0; i < kMaxChunks; ++i)
+      if (CH > 0 || i < chunks)
 #pragma unroll
-      for (int e = 0; e < V; ++e) {
-        const float d = VecF<V>::get(v[i], e) - mu;
-        s2 = fmaf(d, d, s2);
+        for (int e = 0; e < V; ++e) s += VecF<V>::get(v[j][i], e);
+    const float mu = wave_sum(s) / (float)D;
+    float s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxChunks; ++i)
+      if (CH > 0 || i < chunks) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          const float d = VecF<V>::get(v[j][i], e) - mu;
+          s2 = fmaf(d, d, s2);
+        }
       }
-    }
-  const float rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
-  OT* o = out + (int64_t)row * D;
+    const float rstd = rsqrtf(wave_sum(s2) / (float)D + 1e-6f);
+    if (row0 + j >= n) break;
+    OT* o = out + (int64_t)(row0 + j) * D;
 #pragma unroll
-  for (int i = 0; i < kMaxChunks; ++i)
-    if (CH > 0 || i < chunks) {
-      const int c = (i * kWave + lane) * V;
-      const VT sh = *reinterpret_cast<const VT*>(m + sh_off + c);
-      const VT sc = *reinterpret_cast<const VT*>(m + sc_off + c);
-      float r[V];
+    for (int i = 0; i < kMaxChunks; ++i)
+      if (CH > 0 || i < chunks) {
+        const int c = (i * kWave + lane) * V;
+        const VT sh = *reinterpret_cast<const VT*>(m[j] + sh_off + c);
+        const VT sc = *reinterpret_cast<const VT*>(m[j] + sc_off + c);
+        float r[V];
 #pragma unroll
-      for (int e = 0; e < V; ++e)
-        r[e] = fmaf((VecF<V>::get(v[i], e) - mu) * rstd, 1.0f + VecF<V>::get(sc, e), VecF<V>::get(sh, e));
-      VecStore<OT, V>::put(o + c, r);
-    }
+        for (int e = 0; e < V; ++e)
+          r[e] = fmaf((VecF<V>::get(v[j][i], e) - mu) * rstd, 1.0f + VecF<V>::get(sc, e), VecF<V>::get(sh, e));
+        VecStore<OT, V>::put(o + c, r);
+      }
+  }
 }
 
 // One wave per row; lane owns the column quads lane + 64 i.  The output
@@ -360,6 +371,10 @@ hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const vo
 hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
                          const int32_t* crow, void* out, sphinx_dtype odt, hipStream_t s) {
   const int g = (n + kRowsPerBlock - 1) / kRowsPerBlock;
+  // two rows per wave where a lane holds four float4 chunks of a row (D = 1024:
+  // 13.2 -> 12.3 us at 9677 rows); at D = 1152 (nine float2 chunks) two rows
+  // per wave measured slower (15.2 -> 16.2 us)
+  const int g2 = (n + 2 * kRowsPerBlock - 1) / (2 * kRowsPerBlock);
   // 16-byte vectors need every row and every modulation chunk on a 16-byte boundary
   const bool v4 = (D % (kWave * 4) == 0) && (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
   const bool v2 = (D % (kWave * 2) == 0) && (ldm % 2 == 0) && (sh_off % 2 == 0) && (sc_off % 2 == 0);
@@ -367,7 +382,7 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
   const int ch2 = (!v4 && v2) ? D / (kWave * 2) : 0;  // 9 at D = 1152
   if (odt == SPHINX_BF16) {
     bf16* o = (bf16*)out;
-    if (ch4 == 4) k_ln_mod<bf16, 4, 4><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    if (ch4 == 4) k_ln_mod<bf16, 4, 4, 2><<<g2, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 2) k_ln_mod<bf16, 4, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 8) k_ln_mod<bf16, 4, 8><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v4) k_ln_mod<bf16, 4, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
