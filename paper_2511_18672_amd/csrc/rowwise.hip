@@ -6,6 +6,8 @@
 //              the 16 outputs are reduced with a butterfly reduce-scatter).
 // LayerNorm: biased variance, eps 1e-6, no affine; statistics in fp32 from the
 // row held in registers (two passes over registers, one read of HBM).
+#include <algorithm>
+
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -405,14 +407,26 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
 hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
                         const int32_t* crow, const int32_t* gframe, const void* out_w, const void* out_b,
                         sphinx_dtype wdt, const float* c1, const float* c2, float* x, hipStream_t s) {
+  // Grid-stride over rows: as many workgroups as fit on the device at once
+  // (each fills its LDS weight table once), so that all of them run in one
+  // round.  (A fixed 1024 left a quarter of them for a second round at three
+  // workgroups per CU.)
   const int rows_blocks = (n + kRowsPerBlock - 1) / kRowsPerBlock;
-  const int g = rows_blocks < 1024 ? rows_blocks : 1024;
+  const size_t lds = 16 * (size_t)D * (wdt == SPHINX_BF16 ? sizeof(bf16) : sizeof(float));
+  int per_cu = 0, dev = 0, cus = 0;
+  hipError_t err = wdt == SPHINX_BF16
+                       ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_final<bf16>, kTPB, lds)
+                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_final<float>, kTPB, lds);
+  if (err != hipSuccess || per_cu <= 0) per_cu = 2;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  const int g = std::min(rows_blocks, per_cu * cus);
   if (wdt == SPHINX_BF16)
-    k_final<bf16><<<g, kTPB, 16 * D * sizeof(bf16), s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe,
-                                                         (const bf16*)out_w, (const bf16*)out_b, c1, c2, x);
+    k_final<bf16><<<g, kTPB, lds, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, (const bf16*)out_w,
+                                       (const bf16*)out_b, c1, c2, x);
   else
-    k_final<float><<<g, kTPB, 16 * D * sizeof(float), s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe,
-                                                           (const float*)out_w, (const float*)out_b, c1, c2, x);
+    k_final<float><<<g, kTPB, lds, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, (const float*)out_w,
+                                        (const float*)out_b, c1, c2, x);
   return hipGetLastError();
 }
 
