@@ -7,7 +7,7 @@
 //  * k_rowgemm     out[u][n] = act(sum_k X[u][k] W[n][k] + b[n]) for the U rows:
 //                  the timestep MLP and the adaLN projections of all blocks in
 //                  one pass over the weights (weight-read bound; one wave per
-//                  output column, fp32 math).
+//                  two output columns, fp32 math).
 //  * k_pos_tables  fp64 sinusoid tables for patch rows, columns and frames.
 //  * k_token_meta  per selected row: global frame, conditioning row, packed
 //                  (frame, y, x) position.
@@ -80,46 +80,69 @@ constexpr int kGemvMaxVec = 4;  // K <= 4 * 64 * (elements per vector)
 // time: every lane issues its NV loads back to back (an out-of-range vector
 // reloads the row's last one and is zeroed), instead of waiting after each
 // guarded load.
+constexpr int kRowgemmCols = 2;  // output columns per wave
+
 template <typename WT, bool SILU_OUT, int NV>
 __global__ __launch_bounds__(kTPB) void k_rowgemm(const float* __restrict__ X, int ldx, const int32_t* __restrict__ Up,
                                                   int K, int N, const WT* __restrict__ W, const WT* __restrict__ bias,
                                                   float* __restrict__ out, int ldo) {
   constexpr int VN = WVec<WT>::N;
-  const int n = blockIdx.x * (kTPB / kWave) + (int)(threadIdx.x / kWave);
-  if (n >= N) return;
+  constexpr int C = kRowgemmCols;
+  // C output columns per wave: their weight loads are in flight together and
+  // each X load serves all of them (a column past N repeats column N - 1 and
+  // is not stored)
+  const int n0 = (blockIdx.x * (kTPB / kWave) + (int)(threadIdx.x / kWave)) * C;
+  if (n0 >= N) return;
   const int lane = lane_id();
   const int U = *Up;
   const int nvec = K / VN;
-  const float bv = load_as_f32(bias, n);
-  float w[NV][VN];
-  const WT* wr = W + (int64_t)n * K;
+  float bv[C];
+  float w[C][NV][VN];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) WVec<WT>::get(wr + min(lane + kWave * i, nvec - 1) * VN, w[i]);
+  for (int c = 0; c < C; ++c) {
+    const int n = min(n0 + c, N - 1);
+    bv[c] = load_as_f32(bias, n);
+    const WT* wr = W + (int64_t)n * K;
 #pragma unroll
-  for (int i = 0; i < NV; ++i)
-    if (lane + kWave * i >= nvec)
+    for (int i = 0; i < NV; ++i) WVec<WT>::get(wr + min(lane + kWave * i, nvec - 1) * VN, w[c][i]);
+  }
 #pragma unroll
-      for (int e = 0; e < VN; ++e) w[i][e] = 0.0f;
+  for (int c = 0; c < C; ++c)
+#pragma unroll
+    for (int i = 0; i < NV; ++i)
+      if (lane + kWave * i >= nvec)
+#pragma unroll
+        for (int e = 0; e < VN; ++e) w[c][i][e] = 0.0f;
   for (int u = 0; u < U; ++u) {
     const float* xr = X + (int64_t)u * ldx;
-    float acc = 0.0f;
+    float acc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] = 0.0f;
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int v = min(lane + kWave * i, nvec - 1);  // zero weights past the row
 #pragma unroll
       for (int e = 0; e < VN; e += 4) {
         const f32x4 xv = *reinterpret_cast<const f32x4*>(xr + v * VN + e);
-        acc = fmaf(w[i][e], xv[0], acc);
-        acc = fmaf(w[i][e + 1], xv[1], acc);
-        acc = fmaf(w[i][e + 2], xv[2], acc);
-        acc = fmaf(w[i][e + 3], xv[3], acc);
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+          acc[c] = fmaf(w[c][i][e], xv[0], acc[c]);
+          acc[c] = fmaf(w[c][i][e + 1], xv[1], acc[c]);
+          acc[c] = fmaf(w[c][i][e + 2], xv[2], acc[c]);
+          acc[c] = fmaf(w[c][i][e + 3], xv[3], acc[c]);
+        }
       }
     }
-    acc = wave_sum(acc);
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[c] = wave_sum(acc[c]);
     if (lane == 0) {
-      float v = acc + bv;
-      if (SILU_OUT) v = silu(v);
-      out[(int64_t)u * ldo + n] = v;
+#pragma unroll
+      for (int c = 0; c < C; ++c)
+        if (n0 + c < N) {
+          float v = acc[c] + bv[c];
+          if (SILU_OUT) v = silu(v);
+          out[(int64_t)u * ldo + n0 + c] = v;
+        }
     }
   }
 }
@@ -178,7 +201,8 @@ hipError_t launch_temb(const int32_t* utau, const int32_t* U, int Gmax, float* t
 
 hipError_t launch_rowgemm(const float* X, int ldx, const int32_t* U, int K, const void* W, const void* b,
                           sphinx_dtype wdt, int N, bool silu_out, float* out, int ldo, hipStream_t s) {
-  const int g = (N + kTPB / kWave - 1) / (kTPB / kWave);
+  const int cols = kRowgemmCols * (kTPB / kWave);  // output columns per workgroup
+  const int g = (N + cols - 1) / cols;
   const int nv = (K / (wdt == SPHINX_BF16 ? 8 : 4) + kWave - 1) / kWave;  // vectors per lane, 1..4
   auto go = [&](auto wt, auto silu, auto nvc) {
     typedef decltype(wt) WT;
