@@ -833,7 +833,11 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
         c0[r] -= delta;
         c1[r] -= delta;
       }
+    // head_dim 64: the wave in its MFMA region goes first, ahead of the
+    // serial tile-max and rescale work of the other waves on its SIMD
+    if constexpr (HD == 64) __builtin_amdgcn_s_setprio(1);
     dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
+    if constexpr (HD == 64) __builtin_amdgcn_s_setprio(0);
     land(Keep4{});
     slot = s1;
   };

@@ -7,6 +7,7 @@
 // LayerNorm: biased variance, eps 1e-6, no affine; statistics in fp32 from the
 // row held in registers (two passes over registers, one read of HBM).
 #include <algorithm>
+#include <atomic>
 
 #include "kernels.hpp"
 
@@ -411,16 +412,30 @@ hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm,
   // (each fills its LDS weight table once), so that all of them run in one
   // round.  (A fixed 1024 left a quarter of them for a second round at three
   // workgroups per CU.)
+  // The resident count is queried once per device, weight type and D (the
+  // query is not cheap enough to repeat every step).
   const int rows_blocks = (n + kRowsPerBlock - 1) / kRowsPerBlock;
   const size_t lds = 16 * (size_t)D * (wdt == SPHINX_BF16 ? sizeof(bf16) : sizeof(float));
-  int per_cu = 0, dev = 0, cus = 0;
-  hipError_t err = wdt == SPHINX_BF16
-                       ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_final<bf16>, kTPB, lds)
-                       : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_final<float>, kTPB, lds);
-  if (err != hipSuccess || per_cu <= 0) per_cu = 2;
-  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    cus = 256;
-  const int g = std::min(rows_blocks, per_cu * cus);
+  struct Entry {
+    std::atomic<int> key{-1}, blocks{0};
+  };
+  static Entry cache[64][2];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  Entry& ent = cache[dev][wdt == SPHINX_BF16 ? 0 : 1];
+  int resident = ent.key.load(std::memory_order_acquire) == D ? ent.blocks.load(std::memory_order_relaxed) : 0;
+  if (resident <= 0) {
+    int per_cu = 0, cus = 0;
+    const hipError_t err = wdt == SPHINX_BF16
+                               ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_final<bf16>, kTPB, lds)
+                               : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_final<float>, kTPB, lds);
+    if (err != hipSuccess || per_cu <= 0) per_cu = 2;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    resident = per_cu * cus;
+    ent.blocks.store(resident, std::memory_order_relaxed);
+    ent.key.store(D, std::memory_order_release);
+  }
+  const int g = std::min(rows_blocks, resident);
   if (wdt == SPHINX_BF16)
     k_final<bf16><<<g, kTPB, lds, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, (const bf16*)out_w,
                                        (const bf16*)out_b, c1, c2, x);
