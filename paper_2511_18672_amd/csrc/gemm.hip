@@ -384,8 +384,24 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n);
     bv = make_float4((float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]);
   }
+  constexpr int NP = C::EROWS / RPP;  // row passes per staged half
 #pragma unroll
   for (int h = 0; h < EH; ++h) {
+    // gated residual: every pass's residual and gate loads are issued before
+    // the staging (rows past M read row M - 1 and are not stored), so their
+    // latencies overlap instead of following one another pass by pass
+    float4 hres[EPI == EPI_GATED ? NP : 1], gres[EPI == EPI_GATED ? NP : 1];
+    if constexpr (EPI == EPI_GATED) {
+      int cr[NP];
+#pragma unroll
+      for (int p = 0; p < NP; ++p) cr[p] = e.crow[min(m0 + h * C::EROWS + p * RPP + rsub, M - 1)];
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        const int mc = min(m0 + h * C::EROWS + p * RPP + rsub, M - 1);
+        hres[p] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(e.out) + (int64_t)mc * e.ldo + n);
+        gres[p] = *reinterpret_cast<const float4*>(e.gate + (int64_t)cr[p] * e.ldg + n);
+      }
+    }
     if (EH == 1 || wm == h) {
       const int r0 = a_row0 - h * C::EROWS;
 #pragma unroll
@@ -397,8 +413,23 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
             sC[(r0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
     }
     __syncthreads();
+    if constexpr (EPI == EPI_GATED) {
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        const int row = p * RPP + rsub;
+        const int m = m0 + h * C::EROWS + row;
+        float4 v = *reinterpret_cast<const float4*>(&sC[row * C::CLD + c4]);
+        const float4 gv = gres[p];
+        float4 hv = hres[p];
+        hv.x = fmaf(1.0f + gv.x, v.x + bv.x, hv.x);
+        hv.y = fmaf(1.0f + gv.y, v.y + bv.y, hv.y);
+        hv.z = fmaf(1.0f + gv.z, v.z + bv.z, hv.z);
+        hv.w = fmaf(1.0f + gv.w, v.w + bv.w, hv.w);
+        if (m < M) *reinterpret_cast<float4*>(reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n) = hv;
+      }
+    }
 #pragma unroll 4
-    for (int p = 0; p < C::EROWS / RPP; ++p) {
+    for (int p = 0; p < (EPI == EPI_GATED ? 0 : NP); ++p) {
       const int row = p * RPP + rsub;
       const int m = m0 + h * C::EROWS + row;
       if (m >= M) continue;
@@ -407,29 +438,18 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
       v.y += bv.y;
       v.z += bv.z;
       v.w += bv.w;
-      if constexpr (EPI == EPI_GATED) {
-        float* hp = reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n;
-        const float4 gv = *reinterpret_cast<const float4*>(e.gate + (int64_t)e.crow[m] * e.ldg + n);
-        float4 hv = *reinterpret_cast<const float4*>(hp);
-        hv.x = fmaf(1.0f + gv.x, v.x, hv.x);
-        hv.y = fmaf(1.0f + gv.y, v.y, hv.y);
-        hv.z = fmaf(1.0f + gv.z, v.z, hv.z);
-        hv.w = fmaf(1.0f + gv.w, v.w, hv.w);
-        *reinterpret_cast<float4*>(hp) = hv;
-      } else {
-        if constexpr (EPI == EPI_GELU) {
-          v.x = gelu_tanh(v.x);
-          v.y = gelu_tanh(v.y);
-          v.z = gelu_tanh(v.z);
-          v.w = gelu_tanh(v.w);
-        }
-        bf16x4 o;
-        o[0] = (bf16)v.x;
-        o[1] = (bf16)v.y;
-        o[2] = (bf16)v.z;
-        o[3] = (bf16)v.w;
-        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
+      if constexpr (EPI == EPI_GELU) {
+        v.x = gelu_tanh(v.x);
+        v.y = gelu_tanh(v.y);
+        v.z = gelu_tanh(v.z);
+        v.w = gelu_tanh(v.w);
       }
+      bf16x4 o;
+      o[0] = (bf16)v.x;
+      o[1] = (bf16)v.y;
+      o[2] = (bf16)v.z;
+      o[3] = (bf16)v.w;
+      *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
     }
     if (h + 1 < EH) __syncthreads();  // the next half reuses the staging rows
   }
