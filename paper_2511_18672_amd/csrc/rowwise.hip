@@ -184,17 +184,21 @@ template <> struct VecStore<bf16, 4> {
 // CH: chunks of 64 V columns per row when known at compile time (then all
 // row loads issue back to back; instantiated for D = 512, 1024, 2048 with
 // V = 4 and D = 1152 with V = 2), 0 for any D.
-template <typename OT, int V, int CH, int R = 1>
+// HALF: the last of the CH chunks covers only lanes 0..31 (D = 64 V (CH - 1) + 32 V,
+// e.g. D = 1152 in float4 chunks).
+template <typename OT, int V, int CH, int R = 1, bool HALF = false>
 __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, int n, int D,
                                                  const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
                                                  const int32_t* __restrict__ crow, OT* __restrict__ out) {
   typedef typename VecF<V>::T VT;
   static_assert(R == 1 || CH > 0, "several rows per wave need a compile-time chunk count");
+  static_assert(!HALF || CH > 0, "a half last chunk needs a compile-time chunk count");
   constexpr int kMaxChunks = CH > 0 ? CH : kMaxPer / V;
   const int row0 = (blockIdx.x * kRowsPerBlock + (int)(threadIdx.x / kWave)) * R;
   if (row0 >= n) return;
   const int lane = lane_id();
   const int chunks = CH > 0 ? CH : D / (kWave * V);
+  auto live = [&](int i) { return CH > 0 ? (!HALF || i + 1 < CH || lane < kWave / 2) : i < chunks; };
   // all rows' loads first; a row past n repeats row n - 1 and is not stored
   VT v[R][kMaxChunks];
   const float* m[R];
@@ -204,22 +208,26 @@ __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, in
     const float* hr = h + (int64_t)row * D;
     m[j] = mod + (int64_t)crow[row] * ldm;
 #pragma unroll
-    for (int i = 0; i < kMaxChunks; ++i)
-      if (CH > 0 || i < chunks) v[j][i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+    for (int i = 0; i < kMaxChunks; ++i) {
+      if (HALF && i + 1 == CH)  // lanes 32..63 load a duplicate of lanes 0..31 and drop it
+        v[j][i] = *reinterpret_cast<const VT*>(hr + (i * kWave + (lane & (kWave / 2 - 1))) * V);
+      else if (CH > 0 || i < chunks)
+        v[j][i] = *reinterpret_cast<const VT*>(hr + (i * kWave + lane) * V);
+    }
   }
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < kMaxChunks; ++i)
-      if (CH > 0 || i < chunks)
+      if (live(i))
 #pragma unroll
         for (int e = 0; e < V; ++e) s += VecF<V>::get(v[j][i], e);
     const float mu = wave_sum(s) / (float)D;
     float s2 = 0.f;
 #pragma unroll
     for (int i = 0; i < kMaxChunks; ++i)
-      if (CH > 0 || i < chunks) {
+      if (live(i)) {
 #pragma unroll
         for (int e = 0; e < V; ++e) {
           const float d = VecF<V>::get(v[j][i], e) - mu;
@@ -231,7 +239,7 @@ __global__ __launch_bounds__(kTPB) void k_ln_mod(const float* __restrict__ h, in
     OT* o = out + (int64_t)(row0 + j) * D;
 #pragma unroll
     for (int i = 0; i < kMaxChunks; ++i)
-      if (CH > 0 || i < chunks) {
+      if (live(i)) {
         const int c = (i * kWave + lane) * V;
         const VT sh = *reinterpret_cast<const VT*>(m[j] + sh_off + c);
         const VT sc = *reinterpret_cast<const VT*>(m[j] + sc_off + c);
@@ -375,20 +383,24 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
                          const int32_t* crow, void* out, sphinx_dtype odt, hipStream_t s) {
   const int g = (n + kRowsPerBlock - 1) / kRowsPerBlock;
   // two rows per wave where a lane holds four float4 chunks of a row (D = 1024:
-  // 13.2 -> 12.3 us at 9677 rows); at D = 1152 (nine float2 chunks) two rows
-  // per wave measured slower (15.2 -> 16.2 us)
+  // 13.2 -> 12.3 us at 9677 rows); at D = 1152 two rows per wave measured
+  // slower (15.2 -> 16.2 us with float2 chunks), and float4 chunks with a half
+  // last one beat nine float2 chunks (15.4 -> 14.8 us)
   const int g2 = (n + 2 * kRowsPerBlock - 1) / (2 * kRowsPerBlock);
   // 16-byte vectors need every row and every modulation chunk on a 16-byte boundary
   const bool v4 = (D % (kWave * 4) == 0) && (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
   const bool v2 = (D % (kWave * 2) == 0) && (ldm % 2 == 0) && (sh_off % 2 == 0) && (sc_off % 2 == 0);
   const int ch4 = v4 ? D / (kWave * 4) : 0;
   const int ch2 = (!v4 && v2) ? D / (kWave * 2) : 0;  // 9 at D = 1152
+  // D = 1152 in float4 chunks: four full, the fifth on half the lanes
+  const bool v4h = (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
   if (odt == SPHINX_BF16) {
     bf16* o = (bf16*)out;
     if (ch4 == 4) k_ln_mod<bf16, 4, 4, 2><<<g2, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 2) k_ln_mod<bf16, 4, 2><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch4 == 8) k_ln_mod<bf16, 4, 8><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v4) k_ln_mod<bf16, 4, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
+    else if (ch2 == 9 && v4h) k_ln_mod<bf16, 4, 5, 1, true><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (ch2 == 9) k_ln_mod<bf16, 2, 9><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else if (v2) k_ln_mod<bf16, 2, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
     else k_ln_mod<bf16, 1, 0><<<g, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, o);
