@@ -164,6 +164,41 @@ def pin_patch_layout(O):
     assert np.array_equal(O.unpatchify(P, reqs), lat)
 
 
+def pin_token_coordinates(O):
+    """token_info against the token layout written out by loops (token t of a
+    request = f (h/2)(w/2) + y (w/2) + x, requests concatenated, frames
+    numbered globally), and against the NCHW element each token covers: the
+    patch of token (f, y, x) holds latent rows 2y, 2y+1 and columns 2x, 2x+1
+    of frame f.  Non-square latents (h != w) so that a y/x mix-up shows."""
+    reqs = [W.Request(3, 4, 10), W.Request(2, 6, 2), W.Request(1, 8, 12)]
+    info = O.token_info(reqs)
+    t = g0 = 0
+    for r, q in enumerate(reqs):
+        hp, wp = q.h // 2, q.w // 2
+        for f in range(q.frames):
+            for y in range(hp):
+                for x in range(wp):
+                    assert (info.req[t], info.gframe[t], info.f[t], info.y[t], info.x[t]) == (r, g0 + f, f, y, x), t
+                    t += 1
+        g0 += q.frames
+    assert t == len(info.req)
+    # coordinates carried by the latent itself: each element holds its own
+    # frame, row and column; the patch of every token must hold its own (f, y, x)
+    n = sum(q.frames * 4 * q.h * q.w for q in reqs)
+    lf, ly, lx = (np.zeros(n) for _ in range(3))
+    e = 0
+    for q in reqs:
+        for f in range(q.frames):
+            for c in range(4):
+                for yy in range(q.h):
+                    for xx in range(q.w):
+                        lf[e], ly[e], lx[e] = f, yy // 2, xx // 2
+                        e += 1
+    for lat, want in ((lf, info.f), (ly, info.y), (lx, info.x)):
+        P = O.patchify(lat, reqs)
+        assert np.array_equal(P, np.repeat(want[:, None], 16, axis=1).astype(np.float64))
+
+
 def brute_select(u, thr, active, tok_offset):
     mask = [bool(a) and (float(x) > float(t)) for x, t, a in zip(u, thr, active)]
     idx = [t for t, m in enumerate(mask) if m]
@@ -615,7 +650,7 @@ def pin_per_frame_grid(O):
 
 
 ALL_PINS = [pin_alpha_bar_exact, pin_grid, pin_ddim_true_noise, pin_ddim_zero_noise, pin_alg1_active_counts,
-            pin_patch_layout, pin_select_bruteforce, pin_select_threshold_count, pin_round_bf16,
+            pin_patch_layout, pin_token_coordinates, pin_select_bruteforce, pin_select_threshold_count, pin_round_bf16,
             pin_layer_norm, pin_activations, pin_linear, pin_embeddings, pin_attention_bruteforce,
             pin_attention_sdpa, pin_attention_special, pin_denoiser_torch, pin_empty_mask_identity,
             pin_all_selected_dense, pin_unselected_independence, pin_packed_equals_separate,

@@ -110,6 +110,16 @@ def _pos_x_uses_y(f, y, x, D):
     return _orig["position_embedding"](f, y, y, D)
 
 
+def _token_info_yx_swapped(requests):
+    ti = _orig["token_info"](requests)
+    return O.TokenInfo(ti.req, ti.gframe, ti.f, ti.x, ti.y)
+
+
+def _token_info_local_frames(requests):
+    ti = _orig["token_info"](requests)
+    return O.TokenInfo(ti.req, ti.f, ti.f, ti.y, ti.x)
+
+
 def _denoise_raw_gate(model, x, f, y, xx, tau, seg, precision="model", **kw):
     w = dict(model.weights)
     D = model.D
@@ -234,6 +244,8 @@ MUTANTS = {
     "patch_order_swapped": ("patchify", _patchify_swapped),
     "temb_sin_cos_swapped": ("timestep_embedding", _temb_swapped),
     "pos_x_uses_y": ("position_embedding", _pos_x_uses_y),
+    "token_info_yx_swapped": ("token_info", _token_info_yx_swapped),
+    "token_info_frames_not_global": ("token_info", _token_info_local_frames),
     "gate_without_one": ("denoise", _denoise_raw_gate),
     "reinject_every_step": ("plan_steps", _plan_always_new),
     "scatter_without_update": ("step", _step_skips_update),
