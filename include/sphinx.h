@@ -237,7 +237,9 @@ sphinx_status sphinx_refine_workspace_bytes(const sphinx_model_desc* m, const sp
  * c1, c2: dev float [G]; x_sel: dev float [n_sel][16] in/out; cu_sel_host:
  * host int32 [R+1] with cu_sel_host[R] = n_sel.  n_sel = 0 is a no-op.
  * bf16 models compute GEMMs and attention with bf16 operands and fp32
- * accumulation; residual stream, statistics, softmax and the update are fp32. */
+ * accumulation; residual stream, statistics, softmax and the update are fp32.
+ * SPHINX_E_UNSUPPORTED when n_sel * max(3 D, mlp) >= 2^31 (the activation
+ * matrices are addressed with 32-bit element offsets). */
 sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_request* reqs, int32_t R,
                                  const int32_t* idx, int32_t n_sel, const int32_t* cu_sel_host,
                                  const int32_t* tau, const float* c1, const float* c2, float* x_sel, void* ws,

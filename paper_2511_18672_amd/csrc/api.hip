@@ -572,6 +572,10 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
     if (len < 0 || len > T.tok_off[r + 1] - T.tok_off[r]) return SPHINX_E_INVALID;
   }
   if (n_sel == 0) return SPHINX_OK;
+  // GEMM operand tiles are addressed with 32-bit element offsets: the widest
+  // activation matrix (n x max(3D, mlp)) must stay below 2^31 elements
+  if ((int64_t)n_sel * std::max(3 * (int64_t)m->D, (int64_t)m->mlp) >= ((int64_t)1 << 31))
+    return SPHINX_E_UNSUPPORTED;
   if (!idx || !tau || !c1 || !c2 || !x_sel || !ws || m->weights == nullptr) return SPHINX_E_INVALID;
   if (!aligned(idx, 16) || !aligned(x_sel, 16) || !aligned(ws, 256) || !aligned(m->weights, 256))
     return SPHINX_E_INVALID;

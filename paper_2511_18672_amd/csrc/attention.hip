@@ -4,32 +4,27 @@
 //
 // bf16 path, head_dim 64 or 72, gfx950 MFMA (flash-attention style, online softmax):
 //  * one workgroup = 128 queries of one segment and one head, 4 waves x 32
-//    queries; K/V tiles of 64 keys are staged in LDS (K row-major, V
-//    transposed to [d][key]);
+//    queries; K/V tiles of 64 keys are copied global->LDS directly;
 //  * scores are computed transposed, S^T = K Q^T with v_mfma_f32_32x32x16_bf16:
 //    every lane then owns one query and 16 of each 32 keys, so the row max and
 //    row sum need no cross-lane traffic except one exchange with lane^32;
 //  * P^T stays in registers and is fed directly as the B operand of
-//    O^T = V^T P^T.  The MFMA sums over k-slots; a slot (g = lane/32, j) of
-//    P^T holds key 16*half + 8*(j/4) + 4*g + j%4 of the 32-key block, and the
-//    V^T tile is stored with the same key permutation inside each 16-key group,
-//    so each A-operand fragment is one 16-byte LDS read;
+//    O^T = V^T P^T; the V^T fragments come from LDS transpose reads in the
+//    key order of the P^T k-slots;
 //  * the output O^T lands with the query on the lane, so the final 1/l
 //    normalisation is lane-local;
 //  * softmax in base 2 with the 1/sqrt(d) scale folded into log2(e)/sqrt(d);
 //    the running max is only moved (and O, l rescaled) when a tile raises it
 //    by more than 8 in log2 units, so P <= 2^8; P is rounded to bf16 for the PV
 //    product and the row sum adds the same rounded values (v_dot2 with ones);
-//  * only the last key tile of a segment is masked; K/V tiles are double
-//    buffered in LDS, the next tile's global loads overlapping this tile.
+//  * only the last key tile of a segment is masked.
 // Workgroups of the longest segment are scheduled first, and the linear
 // workgroup order is remapped so that each XCD works on whole heads.
-// head_dim 72 pads QK^T to 5 k-steps of 16 (d 72..79 zero) and computes O^T in
-// three 32-row blocks (rows 72..95 are computed from zero V^T rows and dropped).
-// Both head dims normally run a software-pipelined form of the same
-// computation with direct global->LDS copies (k_attn_bf16_dma and
-// k_attn_bf16_dma72, described with their code); the staged kernels above
-// remain for inputs too large for their 32-bit offsets.
+// head_dim 72 pads QK^T with one 8-deep k-step and computes O^T in three
+// 32-row blocks (rows 72..95 are dropped).  Both head dims run the
+// software-pipelined kernels k_attn_bf16_dma and k_attn_bf16_dma72 (described
+// with their code).  Row bases are 64-bit and per-lane copy offsets stay
+// within one 64-key tile, so any segment the ABI accepts is addressable.
 //
 // fp32 path (fp32 models, head_dim <= 64): one thread per (query, head).
 
@@ -42,258 +37,10 @@ namespace sphinx {
 namespace {
 constexpr int AQ = 128;  // queries per workgroup
 constexpr int AK = 64;   // keys per LDS tile
-constexpr int VLD = AK + 8;
 constexpr float kRescaleLog2 = 8.0f;  // rescale only when the running max grows by > 2^8
 static_assert(AQ == kAttnQueryTile, "host tile size must match the kernel");
 
-// Head-dimension dependent shape: HD = 64 or 72.
-template <int HD>
-struct AttnShape {
-  static constexpr int KS = (HD + 15) / 16;  // 16-deep k steps of QK^T (d padded with zeros)
-  static constexpr int DB = (HD + 31) / 32;  // 32-row blocks of O^T (rows past HD unused)
-  static constexpr int KCH = HD / 8;         // 16-byte chunks of one q/k/v row
-  static constexpr int KLD = KS * 16 + 8;    // K tile row stride (bf16)
-  static constexpr int VROWS = DB * 32;      // rows of the V^T tile
-  static constexpr int KLOADS = (AK * KCH + 255) / 256;       // K chunks per thread
-  static constexpr int VLOADS = ((AK / 2) * KCH + 255) / 256;  // V key-pair chunks per thread
-};
-
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Column of key k in a V^T row.  Inside each group of 16 keys the order is
-// 0-3, 8-11, 4-7, 12-15, so the eight keys that lane group g feeds to one
-// PV k-step (4g..4g+3 and 8+4g..8+4g+3) are contiguous: one 16-byte read.
-__device__ __forceinline__ int vcol(int k) { return (k & ~15) | (k & 3) | ((k & 8) >> 1) | ((k & 4) << 1); }
-
-template <int HD>
-struct AttnSmem {
-  bf16 k[2][AK * AttnShape<HD>::KLD];        // K tile, [key][d], d >= HD zero
-  bf16 v[2][AttnShape<HD>::VROWS * VLD];     // V tile transposed, [d][vcol(key)], d >= HD zero
-};
-
-// One 64-key tile for the 32 queries of this wave.  Scores are S^T = K Q^T:
-// s[kb][r] is key 32*kb + 8*(r/4) + 4*g + r%4 against query r32 of the wave.
-template <int HD, bool MASK>
-__device__ __forceinline__ void attn_tile(const bf16* __restrict__ sK, const bf16* __restrict__ sV,
-                                          const bf16x8 (&qf)[AttnShape<HD>::KS], int g, int r32, int kbase, int L,
-                                          float scale_log2, float& m_run, float& l_run,
-                                          f32x16 (&oacc)[AttnShape<HD>::DB]) {
-  typedef AttnShape<HD> SH;
-  f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-  for (int ks = 0; ks < SH::KS; ++ks) {
-    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(&sK[r32 * SH::KLD + ks * 16 + g * 8]);
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(&sK[(32 + r32) * SH::KLD + ks * 16 + g * 8]);
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], s1, 0, 0, 0);
-  }
-  if (MASK) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = kbase + (r >> 2) * 8 + g * 4 + (r & 3);
-      if (key >= L) s0[r] = -INFINITY;
-      if (key + 32 >= L) s1[r] = -INFINITY;
-    }
-  }
-  float m4[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    float t = fmaxf(fmaxf(s0[4 * q], s0[4 * q + 1]), s0[4 * q + 2]);
-    t = fmaxf(fmaxf(t, s0[4 * q + 3]), s1[4 * q]);
-    t = fmaxf(fmaxf(t, s1[4 * q + 1]), s1[4 * q + 2]);
-    m4[q] = fmaxf(t, s1[4 * q + 3]);
-  }
-  float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
-  // lanes l and l^32 hold the same query and see the same mx: same decision
-  if (mx > m_run + kRescaleLog2) {
-    const float alpha = fast_exp2(m_run - mx);
-    l_run *= alpha;
-#pragma unroll
-    for (int db = 0; db < SH::DB; ++db) oacc[db] *= alpha;
-    m_run = mx;
-  }
-  const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
-  bf16x8 pf[2][2];
-  float psum = 0.0f;
-#pragma unroll
-  for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = hf * 8 + 2 * i;
-      bf16x2 a, b;
-      a[0] = (bf16)fast_exp2(fmaf(s0[r], scale_log2, -m_run));
-      a[1] = (bf16)fast_exp2(fmaf(s0[r + 1], scale_log2, -m_run));
-      b[0] = (bf16)fast_exp2(fmaf(s1[r], scale_log2, -m_run));
-      b[1] = (bf16)fast_exp2(fmaf(s1[r + 1], scale_log2, -m_run));
-      psum = __builtin_amdgcn_fdot2_f32_bf16(a, ones, psum, false);
-      psum = __builtin_amdgcn_fdot2_f32_bf16(b, ones, psum, false);
-      pf[0][hf][2 * i] = a[0];
-      pf[0][hf][2 * i + 1] = a[1];
-      pf[1][hf][2 * i] = b[0];
-      pf[1][hf][2 * i + 1] = b[1];
-    }
-  l_run += psum;
-  // O^T += V^T P^T; P^T k-slot (g, j) of half hf is key 16*hf + 8*(j/4) + 4*g + j%4
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-      for (int db = 0; db < SH::DB; ++db) {
-        const bf16x8 vf =
-            *reinterpret_cast<const bf16x8*>(&sV[(db * 32 + r32) * VLD + kb * 32 + hf * 16 + g * 8]);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][hf], oacc[db], 0, 0, 0);
-      }
-}
-
-template <int HD>
-__device__ __forceinline__ void attn_body(const AttnIO& io, int D, int heads, float scale_log2, const SegTable& S,
-                                          AttnSmem<HD>& sm) {
-  typedef AttnShape<HD> SH;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int g = lane >> 5, r32 = lane & 31;
-  // Workgroups are dealt to the 8 XCDs round-robin by linear id.  Renumber them
-  // so that each XCD receives a contiguous range of (head, query tile) work,
-  // i.e. whole heads, keeping a head's K and V in that XCD's L2.
-  const int ntiles = S.tile_prefix[S.nseg];
-  const int work = ntiles * heads;
-  int lid = (int)blockIdx.x;
-  if (work % 8 == 0) lid = (lid & 7) * (work >> 3) + (lid >> 3);
-  const int head = lid / ntiles, tile = lid - head * ntiles;
-  int s = 0;
-  while (s + 1 < S.nseg && S.tile_prefix[s + 1] <= tile) ++s;
-  const int qt = tile - S.tile_prefix[s];
-  const int seg0 = S.start[s], Lq = S.len[s];
-  const int kv0 = S.kv_start[s], L = S.kv_len[s];  // L: keys of the segment
-  const int64_t ldq = io.ldq, ld = io.ldkv;
-  const bf16* Qg = static_cast<const bf16*>(io.q) + head * HD;
-  const bf16* Kg = static_cast<const bf16*>(io.k) + head * HD;
-  const bf16* Vg = static_cast<const bf16*>(io.v) + head * HD;
-  const bf16x8 zero8 = {};
-
-  // d columns past HD stay zero in both LDS buffers for the whole kernel
-  if (SH::KS * 16 != HD) {
-    for (int i = tid; i < 2 * AK; i += 256) {
-      const int b = i / AK, key = i % AK;
-#pragma unroll
-      for (int d = HD; d < SH::KS * 16; ++d) sm.k[b][key * SH::KLD + d] = (bf16)0.0f;
-    }
-  }
-  if (SH::VROWS != HD) {
-    for (int i = tid; i < 2 * (SH::VROWS - HD) * VLD; i += 256) {
-      const int b = i / ((SH::VROWS - HD) * VLD), rem = i % ((SH::VROWS - HD) * VLD);
-      sm.v[b][HD * VLD + rem] = (bf16)0.0f;
-    }
-  }
-
-  const int ql = qt * AQ + wave * 32 + r32;
-  bf16x8 qf[SH::KS];
-#pragma unroll
-  for (int ks = 0; ks < SH::KS; ++ks) {
-    const int d0 = ks * 16 + g * 8;
-    qf[ks] = (ql < Lq && d0 < HD) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)(seg0 + ql) * ldq + d0) : zero8;
-  }
-
-  // Loaders: K as (key, 16-byte chunk) and V as (key pair, chunk) work items
-  // spread over the 256 threads.  Rows past the segment end are clamped to its
-  // last key: their scores are masked to -inf, so they get weight exactly 0 and
-  // their (finite) values never contribute.
-  const bf16* kptr = Kg + (int64_t)kv0 * ld;
-  const bf16* vptr = Vg + (int64_t)kv0 * ld;
-  bf16x8 rk[SH::KLOADS], rv[2 * SH::VLOADS];
-  auto gload = [&](int kbase) {
-#pragma unroll
-    for (int i = 0; i < SH::KLOADS; ++i) {
-      const int c = tid + 256 * i;
-      if (c < AK * SH::KCH) {
-        const int key = min(kbase + c / SH::KCH, L - 1);
-        rk[i] = *reinterpret_cast<const bf16x8*>(kptr + (int64_t)key * ld + (c % SH::KCH) * 8);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < SH::VLOADS; ++i) {
-      const int c = tid + 256 * i;
-      if (c < (AK / 2) * SH::KCH) {
-        const int p = c % 32, vc = c / 32;
-        const int k0 = min(kbase + 2 * p, L - 1), k1 = min(kbase + 2 * p + 1, L - 1);
-        rv[2 * i] = *reinterpret_cast<const bf16x8*>(vptr + (int64_t)k0 * ld + vc * 8);
-        rv[2 * i + 1] = *reinterpret_cast<const bf16x8*>(vptr + (int64_t)k1 * ld + vc * 8);
-      }
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < SH::KLOADS; ++i) {
-      const int c = tid + 256 * i;
-      if (c < AK * SH::KCH)
-        *reinterpret_cast<bf16x8*>(&sm.k[buf][(c / SH::KCH) * SH::KLD + (c % SH::KCH) * 8]) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < SH::VLOADS; ++i) {
-      const int c = tid + 256 * i;
-      if (c < (AK / 2) * SH::KCH) {
-        const int p = c % 32, vc = c / 32;
-        const int col = vcol(2 * p);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          bf16x2 pr;
-          pr[0] = rv[2 * i][e];
-          pr[1] = rv[2 * i + 1][e];
-          *reinterpret_cast<bf16x2*>(&sm.v[buf][(vc * 8 + e) * VLD + col]) = pr;
-        }
-      }
-    }
-  };
-
-  f32x16 oacc[SH::DB];
-#pragma unroll
-  for (int db = 0; db < SH::DB; ++db) oacc[db] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.0f;
-  const int nkt = (L + AK - 1) / AK;
-  const int nfull = L / AK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nkt) gload((kt + 1) * AK);
-    if (kt < nfull)
-      attn_tile<HD, false>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
-    else
-      attn_tile<HD, true>(sm.k[buf], sm.v[buf], qf, g, r32, kt * AK, L, scale_log2, m_run, l_run, oacc);
-    if (kt + 1 < nkt) sstore(buf ^ 1);
-    __syncthreads();
-  }
-  l_run += __shfl_xor(l_run, 32, kWave);
-  if (ql < Lq) {
-    const float inv = 1.0f / l_run;
-    bf16* orow = static_cast<bf16*>(io.o) + (int64_t)(seg0 + ql) * D + head * HD;
-#pragma unroll
-    for (int db = 0; db < SH::DB; ++db)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int d = db * 32 + rr * 8 + g * 4;  // output rows d .. d+3 of this register group
-        if (d < HD) {
-          bf16x4 ov;
-#pragma unroll
-          for (int t = 0; t < 4; ++t) ov[t] = (bf16)(oacc[db][rr * 4 + t] * inv);
-          *reinterpret_cast<bf16x4*>(orow + d) = ov;
-        }
-      }
-  }
-}
-
-__global__ __launch_bounds__(256, 2) void k_attn_bf16(AttnIO io, int D, int heads, float scale_log2, SegTable S) {
-  __shared__ __attribute__((aligned(16))) AttnSmem<64> sm;
-  attn_body<64>(io, D, heads, scale_log2, S, sm);
-}
-
-__global__ __launch_bounds__(256, 2) void k_attn_bf16_d72(AttnIO io, int D, int heads, float scale_log2,
-                                                          SegTable S) {
-  __shared__ __attribute__((aligned(16))) AttnSmem<72> sm;
-  attn_body<72>(io, D, heads, scale_log2, S, sm);
-}
 
 // Three-way max as one instruction.  Written out because the compiler
 // otherwise first quiets each MFMA result that enters a two-operand max (an
@@ -347,9 +94,7 @@ __device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kba
 //    steps of one MFMA and one pair of probabilities, fenced so the compiler
 //    keeps the order.  The running max moves branch-free; O is rescaled (a
 //    wave-uniform branch taken only when some lane's max moved) between
-//    PV(t-1) and PV(t), at the start of the next iteration.  The floating-point
-//    operations and their order are those of attn_body<64>: results are
-//    bit-identical.
+//    PV(t-1) and PV(t), at the start of the next iteration.
 //  * K and V tiles are stored unpadded, 64 rows of 128 B, with the 16-byte
 //    chunks of row r permuted: K chunk c at c ^ ((r >> 1) & 7), V chunk c at
 //    c ^ 2(r & 3).  LDS has 64 four-byte banks and serves a 16-byte read to 16
@@ -981,18 +726,10 @@ hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads,
   if (dt == SPHINX_BF16) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
     const int grid = S.tile_prefix[S.nseg] * heads;
-    // the copy kernel addresses a segment's keys and values with 32-bit element offsets
-    int64_t kv_max = 0;
-    for (int i = 0; i < S.nseg; ++i) kv_max = std::max<int64_t>(kv_max, S.kv_len[i]);
-    const bool small = kv_max * io.ldkv < ((int64_t)1 << 31);
-    if (head_dim == 64 && small)
+    if (head_dim == 64)
       k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
-    else if (head_dim == 64)
-      k_attn_bf16<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
-    else if (small)
-      k_attn_bf16_dma72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
     else
-      k_attn_bf16_d72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
+      k_attn_bf16_dma72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
   } else {
     const float scale = 1.0f / sqrtf((float)head_dim);
     k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>(io, D, head_dim, heads, n, scale, S);

@@ -5,18 +5,8 @@
 //   EPI_GATED : h  += (1 + gate[row]) * C       (out-proj, MLP second layer; fp32 residual)
 // M = selected tokens (ragged), N, K multiples of the tile sizes.
 //
-// bf16 path (gfx950 MFMA): block tile 128x128, K step 64, 256 threads = 4 waves
-// in a 2x2 grid, each wave a 64x64 tile of 2x2 v_mfma_f32_32x32x16_bf16.  A and
-// W are both K-contiguous, so every operand fragment is one 16-byte LDS read.
-// LDS rows are padded by 16 bytes against bank conflicts.  Global loads run
-// two K steps ahead (two register sets, two LDS buffers, K loop unrolled by
-// two), which hides the L2/HBM latency behind the MFMAs.  Rows past M are
-// clamped to the last row and not stored.  The epilogue stages the fp32
-// tile in LDS and finishes it with 16-byte row-contiguous loads and stores.
-//
-// That register-staged kernel (k_gemm_bf16) is the fallback for operands beyond
-// 32-bit element offsets;
-// otherwise the bf16 path runs k_gemm_dma_* (described with its code).
+// bf16 path (gfx950 MFMA): k_gemm_dma_* (described with their code).  Operand
+// offsets are 32-bit: the caller guarantees M*K and N*K below 2^31 elements.
 //
 // fp32 path: a plain 64x64 SIMT tile (used by fp32 models only).
 #include <atomic>
@@ -39,164 +29,8 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
   }
 }
 
-constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;
-constexpr int CLD = BN + 4;  // fp32 staging row of the epilogue
-constexpr int kGemmSmem = 2 * (BM + BN) * LDK * 2;
-static_assert(BM * CLD * 4 <= kGemmSmem, "epilogue staging must fit in the operand buffers");
-
-template <int EPI>
-__global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A, const bf16* __restrict__ W,
-                                                      const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {
-  // one LDS block: two A and two B operand buffers, reused as the fp32 C tile
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kGemmSmem];
-  bf16(*sA)[BM * LDK] = reinterpret_cast<bf16(*)[BM * LDK]>(smem);
-  bf16(*sB)[BN * LDK] = reinterpret_cast<bf16(*)[BN * LDK]>(smem + 2 * BM * LDK * sizeof(bf16));
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int lrow = tid >> 3, lch = (tid & 7) * 8;
-  const int g = lane >> 5, r32 = lane & 31;
-  // Row pointers of this thread's four A and four W rows.  Rows past M are
-  // clamped to M-1: they are computed like any other row and never stored.
-  const bf16* pa[4];
-  const bf16* pw[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = lrow + 32 * i;
-    pa[i] = A + (int64_t)min(m0 + r, M - 1) * K + lch;
-    pw[i] = W + (int64_t)(n0 + r) * K + lch;
-  }
-  // Two register sets: the global loads run two K steps ahead of the MFMAs.
-  bf16x8 ra0[4], rb0[4], ra1[4], rb1[4];
-  auto gload = [&](int k0, bf16x8 (&ra)[4], bf16x8 (&rb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra[i] = *reinterpret_cast<const bf16x8*>(pa[i] + k0);
-      rb[i] = *reinterpret_cast<const bf16x8*>(pw[i] + k0);
-    }
-  };
-  auto sstore = [&](int buf, const bf16x8 (&ra)[4], const bf16x8 (&rb)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = lrow + 32 * i;
-      *reinterpret_cast<bf16x8*>(&sA[buf][r * LDK + lch]) = ra[i];
-      *reinterpret_cast<bf16x8*>(&sB[buf][r * LDK + lch]) = rb[i];
-    }
-  };
-
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  auto compute = [&](int buf) {
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[2], bw[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&sA[buf][(wm * 64 + i * 32 + r32) * LDK + ks * 16 + g * 8]);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bw[j] = *reinterpret_cast<const bf16x8*>(&sB[buf][(wn * 64 + j * 32 + r32) * LDK + ks * 16 + g * 8]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);
-    }
-  };
-
-  // K loop unrolled by two so that LDS buffers and register sets are static:
-  // even steps read LDS buffer 0 (register set 0 was stored there), odd steps
-  // buffer 1 (set 1).
-  const int KT = K / BK;
-  gload(0, ra0, rb0);
-  if (KT > 1) gload(BK, ra1, rb1);
-  sstore(0, ra0, rb0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; kt += 2) {
-    if (kt + 2 < KT) gload((kt + 2) * BK, ra0, rb0);
-    compute(0);
-    if (kt + 1 < KT) sstore(1, ra1, rb1);
-    __syncthreads();
-    if (kt + 1 >= KT) break;
-    if (kt + 3 < KT) gload((kt + 3) * BK, ra1, rb1);
-    compute(1);
-    if (kt + 2 < KT) sstore(0, ra0, rb0);
-    __syncthreads();
-  }
-
-  // Epilogue through LDS: each wave parks its 64x64 fp32 tile (register r of
-  // block (i, j) is row 8*(r/4) + 4*g + r%4, column r32), then every thread
-  // finishes 4-wide row segments with coalesced 16-byte loads and stores.
-  float* sC = reinterpret_cast<float*>(smem);  // [BM][CLD], reuses the operand buffers
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        sC[(wm * 64 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * CLD + wn * 64 + j * 32 + r32] = acc[i][j][r];
-  __syncthreads();
-  const int c4 = (tid & 31) * 4;  // column inside the tile
-  const int n = n0 + c4;
-  float4 bv;
-  {
-    const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n);
-    bv = make_float4((float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]);
-  }
-#pragma unroll
-  for (int q0 = 0; q0 < BM / 8; q0 += 4) {
-    float4 v[4], hv[4], gv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int row = (q0 + u) * 8 + (tid >> 5);
-      const int m = m0 + row;
-      v[u] = *reinterpret_cast<const float4*>(&sC[row * CLD + c4]);
-      v[u].x += bv.x;
-      v[u].y += bv.y;
-      v[u].z += bv.z;
-      v[u].w += bv.w;
-      if constexpr (EPI == EPI_GATED) {
-        if (m < M) {
-          hv[u] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(e.out) + (int64_t)m * e.ldo + n);
-          gv[u] = *reinterpret_cast<const float4*>(e.gate + (int64_t)e.crow[m] * e.ldg + n);
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int m = m0 + (q0 + u) * 8 + (tid >> 5);
-      if (m >= M) continue;
-      if constexpr (EPI == EPI_GATED) {
-        float4 h = hv[u];
-        h.x = fmaf(1.0f + gv[u].x, v[u].x, h.x);
-        h.y = fmaf(1.0f + gv[u].y, v[u].y, h.y);
-        h.z = fmaf(1.0f + gv[u].z, v[u].z, h.z);
-        h.w = fmaf(1.0f + gv[u].w, v[u].w, h.w);
-        *reinterpret_cast<float4*>(reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n) = h;
-      } else {
-        if constexpr (EPI == EPI_GELU) {
-          v[u].x = gelu_tanh(v[u].x);
-          v[u].y = gelu_tanh(v[u].y);
-          v[u].z = gelu_tanh(v[u].z);
-          v[u].w = gelu_tanh(v[u].w);
-        }
-        bf16x4 o;
-        o[0] = (bf16)v[u].x;
-        o[1] = (bf16)v[u].y;
-        o[2] = (bf16)v[u].z;
-        o[3] = (bf16)v[u].w;
-        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
-      }
-    }
-  }
-}
-
 // ---------------------------------------------------------------------------
-// bf16 GEMM with direct global->LDS copies (global_load_lds_dwordx4), used
-// whenever A and W are addressable with 32-bit element offsets.
+// bf16 GEMM with direct global->LDS copies (global_load_lds_dwordx4).
 //  * Block tile 128x128x64, 4 waves in 2x2, each a 64x64 tile of 2x2
 //    v_mfma_f32_32x32x16_bf16; two workgroups per CU.
 //  * Operand tiles are unpadded 128-byte rows (A rows, then W rows, of one
@@ -213,8 +47,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const bf16* __restrict__ A
 //    step each k-step's fragment reads are issued before the previous
 //    k-step's MFMAs.  Barriers carry no memory fence: each wave waits for its
 //    own copies (vmcnt) and LDS reads (lgkmcnt) first.
-//  * The accumulation order per output (k-steps of 16 in ascending k, then the
-//    same epilogue) equals k_gemm_bf16's, so the results are bit-identical.
+//  * Every output accumulates its k-steps of 16 in ascending k, whatever the
+//    tile shape, so all variants give bit-identical results.
 //  * A 192-row variant (wave tiles 96x64, 80 KB of LDS, epilogue staged one
 //    wave row at a time) is launched where its smaller tile count packs into
 //    fewer rounds of two workgroups per CU; same results.
@@ -632,10 +466,8 @@ double tile_rounds(int64_t tiles, int64_t slots, double w) {
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
                        const GemmEpi& e, hipStream_t s) {
   if (dt == SPHINX_BF16) {
-    const dim3 grid(N / BN, (M + BM - 1) / BM);
     const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
-    const int64_t lim = (int64_t)1 << 31;  // the copy kernel uses 32-bit element offsets
-    if ((int64_t)M * K < lim && (int64_t)N * K < lim) {
+    {
       const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
       const int64_t t128 = nt * ((M + 127) / 128), t192 = nt * ((M + 191) / 192);
       // mixed tiles: narrow N, 192-row tiles filling more than half of one round
@@ -677,12 +509,6 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
         else if (epi == EPI_GELU) dma::k_gemm_dma_gelu<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
         else dma::k_gemm_dma_gated<<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
       }
-    } else if (epi == EPI_BIAS) {
-      k_gemm_bf16<EPI_BIAS><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
-    } else if (epi == EPI_GELU) {
-      k_gemm_bf16<EPI_GELU><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
-    } else {
-      k_gemm_bf16<EPI_GATED><<<grid, 256, 0, s>>>(a, w, b, M, N, K, e);
     }
   } else {
     const dim3 grid(N / 64, (M + 63) / 64);

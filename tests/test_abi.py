@@ -126,6 +126,18 @@ def test_refine_validation(L):
     assert L.sphinx_refine_step(*args(40, over, need.value)) == INVALID
 
 
+def test_refine_size_limit(L):
+    """The activation matrices are addressed with 32-bit element offsets: a
+    step with n * max(3 D, mlp) >= 2^31 is refused before any HIP call."""
+    P = ctypes.c_void_p
+    d = S.model_desc(W.ModelCfg(D=1024, heads=16, head_dim=64, mlp=8192, L=1, dtype="bf16"), 256)
+    reqs = _reqs([(1024, 1024, 1024)])  # 268M tokens
+    for n, code in [((1 << 31) // 8192, UNSUPPORTED), ((1 << 31) // 8192 - 1, WORKSPACE)]:
+        cu = (ctypes.c_int32 * 2)(0, n)
+        assert L.sphinx_refine_step(ctypes.byref(d), reqs, 1, P(256), n, cu, P(256), P(256), P(256), P(256), P(256),
+                                    0, None) == code, n
+
+
 @pytest.mark.parametrize("cfg", [W.TINY_MODEL, W.SMALL_MODEL, W.HEADLINE_MODEL])
 def test_blob_layout(L, cfg):
     d = S.model_desc(cfg, 256)
