@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "kernels.hpp"
+#include "sphinx_prof.h"
 
 using namespace sphinx;
 

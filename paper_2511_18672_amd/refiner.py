@@ -143,6 +143,18 @@ class Refiner:
         self._pending = None
         self._slot_key = [None, None]
 
+    def load_state(self, state_nchw, stream=None):
+        """state <- the given fp32 NCHW latents of all requests (host array or
+        tensor), converted into the state's layout by the library."""
+        src = torch.as_tensor(np.ascontiguousarray(state_nchw, dtype=np.float32)
+                              if not isinstance(state_nchw, torch.Tensor) else state_nchw)
+        src = src.to(device=self.z.device, dtype=torch.float32).contiguous()
+        if src.numel() != self.z.numel():
+            raise ValueError(f"state has {src.numel()} values, expected {self.z.numel()}")
+        B.sphinx_scatter_blend(self.reqs, None, None, 0, src, B.F32, B.NCHW, self.z, B.F32, self.layout, stream)
+        self._pending = None
+        self._slot_key = [None, None]
+
     def _enqueue_select(self, k: int, slot: int, stream=None):
         """Selection of schedule step k into `slot`; cu_sel reaches pinned host
         memory asynchronously (no host synchronization)."""

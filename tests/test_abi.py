@@ -1,8 +1,9 @@
 """C-ABI checks that need no GPU: the library loads, exports every entry point
-declared in include/sphinx.h, validates arguments before any HIP call, lays
+declared in include/*.h, validates arguments before any HIP call, lays
 out the weight blob consistently, and its host-side step schedule equals the
 oracle's."""
 import ctypes
+import glob
 import os
 import re
 
@@ -25,8 +26,13 @@ def L():
 
 
 def header_functions():
-    text = open(os.path.join(ROOT, "include", "sphinx.h")).read()
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(sphinx_\w+)\s*\(", text, re.M)))
+    """Every function declared in include/*.h (the method's calls in sphinx.h,
+    the measurement aids in sphinx_prof.h)."""
+    names = set()
+    for h in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))):
+        text = open(h).read()
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(sphinx_\w+)\s*\(", text, re.M))
+    return sorted(names)
 
 
 def test_exports_every_declared_symbol(L):

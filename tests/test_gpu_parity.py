@@ -13,6 +13,7 @@ import pytest
 
 import oracle as O
 import workloads as W
+from golden_states import forward_state
 from pins import MICRO_BF16
 
 torch = pytest.importorskip("torch")
@@ -205,7 +206,7 @@ def _report(tag, got, ref, truth=None):
 
 
 def check_end_to_end(wl, teacher_forced=True):
-    R, states, sels = run_gpu(wl, trace=teacher_forced)
+    R, _, sels = run_gpu(wl)
     got = R.state.cpu().numpy().astype(np.float64)
     ref, trace = O.refine(wl, precision="model", trace=True)
     for i, (res, (n, idx, cu)) in enumerate(zip(trace, sels)):
@@ -216,16 +217,25 @@ def check_end_to_end(wl, teacher_forced=True):
     assert err <= TOL[wl.model.dtype]
     assert np.isfinite(got).all()
     if teacher_forced:
-        model = O.model_from_workload(wl)
-        plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
-        info = O.token_info(wl.requests)
-        worst = 0.0
-        for i, p in enumerate(plans):
-            res = O.step(wl, model, states[i], p, "model", info=info)
-            worst = max(worst, np.abs(states[i + 1] - res.state).max())
+        worst = teacher_forced_steps(R, wl, trace)
         print(f"[{wl.name}] teacher-forced per-step max_abs = {worst:.3e}")
         assert worst <= TOL[wl.model.dtype]
     return R
+
+
+def teacher_forced_steps(R, wl, trace):
+    """Every step once more from the oracle's state before it (loaded into the
+    GPU state), against the oracle's state after it; returns the worst error."""
+    worst = 0.0
+    before = np.asarray(wl.z0, np.float64)
+    R.reset()
+    for i, res in enumerate(trace):
+        R.load_state(before)
+        n = R.step(i, force_select=True)
+        assert n == res.n_sel and np.array_equal(R.idx[:n].cpu().numpy(), res.idx), i
+        worst = max(worst, float(np.abs(R.state.cpu().numpy() - res.state).max()))
+        before = res.state
+    return worst
 
 
 def test_tiny_end_to_end():
@@ -366,34 +376,33 @@ def test_ragged_d72_tile_edges():
     wl = W.custom("ragged72", MID72, [W.Request(3, 24, 20), W.Request(2, 16, 16), W.Request(2, 10, 14),
                                       W.Request(1, 4, 4)],
                   [0.6, 0.75, 0.9, 0.5], [("uniform", 0.3, 0.7), 0.5, 0.5, 0.2], [4, 3, 3, 2])
-    R, states, sels = run_gpu(wl, trace=True)
+    R, _, sels = run_gpu(wl)
     lens = sorted({int(x) for _, _, cu in sels for x in np.diff(cu) if x > 0})
     print(f"[ragged72] segment lengths seen: {lens}")
     assert any(x < 64 for x in lens) and any(64 < x <= 128 for x in lens) and any(x > 128 for x in lens)
-    model = O.model_from_workload(wl)
-    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
-    info = O.token_info(wl.requests)
-    worst = 0.0
-    for i, p in enumerate(plans):
-        res = O.step(wl, model, states[i], p, "model", info=info)
-        assert np.array_equal(sels[i][1], res.idx), i
-        worst = max(worst, np.abs(states[i + 1] - res.state).max())
+    _, trace = O.refine(wl, precision="model", trace=True)
+    worst = teacher_forced_steps(R, wl, trace)
     print(f"[ragged72] teacher-forced per-step max_abs = {worst:.3e}")
     assert worst <= TOL["bf16"]
 
 
 def test_frame_region_full_shape_one_block_step():
     """Frame+region at its full shape (21 x 64x64 latent) with a one-block
-    head_dim-72 denoiser: run until every frame is active, then compare the
-    next step teacher-forced with the oracle."""
+    head_dim-72 denoiser, at the first step with every frame active, from the
+    oracle's forward-process state before it (its loop run with the true
+    injected noise as the denoiser output)."""
     wl = W.frame_region(model=XL1)
     plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
     k = next(i for i, p in enumerate(plans) if p.active.all())
-    R, states, sels = run_gpu(wl, trace=True, steps=k + 1)
-    assert sels[k][0] == 10194
-    res = O.step(wl, O.model_from_workload(wl), states[k], plans[k], "model")
-    assert np.array_equal(sels[k][1], res.idx)
-    assert _report(f"frame_region L=1 step {k} (teacher-forced)", states[k + 1], res.state) <= TOL["bf16"]
+    before = forward_state(wl, k)
+    R = S.from_workload(wl)
+    R.reset()
+    R.load_state(before)
+    assert R.step(k, force_select=True) == 10194
+    res = O.step(wl, O.model_from_workload(wl), before, plans[k], "model")
+    assert np.array_equal(R.idx[:10194].cpu().numpy(), res.idx)
+    got = R.state.cpu().numpy().astype(np.float64)
+    assert _report(f"frame_region L=1 step {k} (teacher-forced)", got, res.state) <= TOL["bf16"]
 
 
 def test_frame_region_full_depth_properties():
