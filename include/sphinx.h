@@ -214,6 +214,21 @@ sphinx_status sphinx_select_mask(const sphinx_request* reqs, int32_t R, const fl
                                  const uint8_t* active, uint8_t* mask, int32_t* idx, int32_t* cu_sel,
                                  int32_t* cu_sel_host, void* ws, size_t ws_bytes, void* stream);
 
+/* sphinx_select_mask without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * sphinx_select_mask, bit-identical outputs.  Its scratch (per-chunk counts
+ * and offsets, 512 KB) is a static array of the library, one per GPU, held
+ * until the process ends; the call allocates nothing.  N (all requests'
+ * tokens) is limited to SPHINX_SELECT_STATIC_MAX_TOKENS; larger inputs return
+ * SPHINX_E_UNSUPPORTED before any HIP call.  Calls on the same GPU share the
+ * array: calls that overlap in time on one GPU (other streams, other threads)
+ * race and must be serialised by the caller. */
+#define SPHINX_SELECT_STATIC_MAX_TOKENS (1LL << 28)
+sphinx_status sphinx_select_mask_static(const sphinx_request* reqs, int32_t R, const float* uncert,
+                                        const float* thr, const uint8_t* active, uint8_t* mask, int32_t* idx,
+                                        int32_t* cu_sel, int32_t* cu_sel_host, void* stream);
+
 /* Gather with noise injection (Alg. 1 add_noise on the selected tokens).
  *   x_sel[j][k] = a[g] * z[k] + b[g] * eps[k]   for token idx[j] of frame g,
  * z and eps read from the latents `state` / `eps` (dtype f32 or bf16), both in

@@ -32,7 +32,7 @@ EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_par
             "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
             "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_kv_cache_bytes", "sphinx_gather_ctx",
             "sphinx_refine_step_cached", "sphinx_scatter_masked", "sphinx_mask_frontend_workspace_bytes",
-            "sphinx_mask_frontend", "sphinx_adaptive_start"]
+            "sphinx_mask_frontend", "sphinx_adaptive_start", "sphinx_select_mask_static"]
 PEAK_BLOCKS = 2048
 PEAK_CONSTANT, PEAK_RANDOM = 0, 1
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
         "sphinx_plan_step_grid": (c_int32, [POINTER(Request), c_int32, P, P, c_int32, c_int32, P, P, P, P, P, P, P]),
         "sphinx_select_workspace_bytes": (c_int32, [c_int64, POINTER(c_size_t)]),
         "sphinx_select_mask": (c_int32, [POINTER(Request), c_int32, P, P, P, P, P, P, P, P, c_size_t, P]),
+        "sphinx_select_mask_static": (c_int32, [POINTER(Request), c_int32, P, P, P, P, P, P, P, P]),
         "sphinx_gather": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P, P,
                                     P]),
         "sphinx_refine_workspace_bytes": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, c_int64,
@@ -224,6 +225,16 @@ def sphinx_select_mask(reqs, uncert, thr, active, mask, idx, cu_sel, ws, readbac
     _check("sphinx_select_mask", lib().sphinx_select_mask(
         reqs, len(reqs), _ptr(uncert), _ptr(thr), _ptr(active), _ptr(mask), _ptr(idx), _ptr(cu_sel),
         _ptr(host), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    return host
+
+
+def sphinx_select_mask_static(reqs, uncert, thr, active, mask, idx, cu_sel, readback: bool = True, stream=None):
+    """sphinx_select_mask on the library's static scratch (no workspace, no
+    device allocation).  With readback=True returns cu_sel on the host."""
+    host = np.zeros(len(reqs) + 1, np.int32) if readback else None
+    _check("sphinx_select_mask_static", lib().sphinx_select_mask_static(
+        reqs, len(reqs), _ptr(uncert), _ptr(thr), _ptr(active), _ptr(mask), _ptr(idx), _ptr(cu_sel),
+        _ptr(host), _stream(stream)))
     return host
 
 

@@ -485,6 +485,32 @@ sphinx_status sphinx_select_mask(const sphinx_request* reqs, int32_t R, const fl
   return SPHINX_OK;
 }
 
+sphinx_status sphinx_select_mask_static(const sphinx_request* reqs, int32_t R, const float* uncert,
+                                        const float* thr, const uint8_t* active, uint8_t* mask, int32_t* idx,
+                                        int32_t* cu_sel, int32_t* cu_sel_host, void* stream) {
+  ReqTable T;
+  int64_t N;
+  int32_t G;
+  sphinx_status st = build_table(reqs, R, &T, &N, &G);
+  if (st != SPHINX_OK) return st;
+  if (!uncert || !thr || !mask || !idx || !cu_sel) return SPHINX_E_INVALID;
+  if (!aligned(uncert, 16) || !aligned(mask, 16) || !aligned(idx, 16) || !aligned(cu_sel, 16))
+    return SPHINX_E_INVALID;
+  if (N > select_static_max_tokens()) return SPHINX_E_UNSUPPORTED;
+  hipStream_t s = (hipStream_t)stream;
+  void* ws = nullptr;
+  SPHINX_TRY(select_static_ws(&ws));
+  {
+    Bracket br(SPHINX_K_SELECT, s);
+    SPHINX_TRY(launch_select(T, N, uncert, thr, active, mask, idx, cu_sel, ws, s));
+  }
+  if (cu_sel_host != nullptr) {
+    SPHINX_TRY(hipMemcpyAsync(cu_sel_host, cu_sel, (size_t)(R + 1) * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    SPHINX_TRY(hipStreamSynchronize(s));
+  }
+  return SPHINX_OK;
+}
+
 sphinx_status sphinx_gather(const sphinx_request* reqs, int32_t R, sphinx_layout layout, const void* state,
                             sphinx_dtype state_dtype, const void* eps, sphinx_dtype eps_dtype, const int32_t* idx,
                             int32_t n_sel, const float* a, const float* b, float* x_sel, void* stream) {

@@ -53,6 +53,11 @@ constexpr int kAttnQueryTile = 128;
 
 // select.hip
 size_t select_ws_bytes(int64_t N);
+// The library's static selection scratch: the largest N it serves, and its
+// device address on the current device (looked up once per device).
+constexpr int kMaxDevices = 64;
+int64_t select_static_max_tokens();
+hipError_t select_static_ws(void** ptr);
 hipError_t launch_select(const ReqTable& T, int64_t N, const float* u, const float* thr, const uint8_t* active,
                          uint8_t* mask, int32_t* idx, int32_t* cu_sel, void* ws, hipStream_t s);
 

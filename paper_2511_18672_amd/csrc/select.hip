@@ -15,6 +15,8 @@
 // Thread order is token order, so idx comes out ascending without a sort and
 // the result is deterministic.  (Non-temporal loads and stores measured slower
 // here than ordinary ones, unlike in gather/scatter.)
+#include <mutex>
+
 #include "kernels.hpp"
 
 namespace sphinx {
@@ -203,6 +205,39 @@ __global__ __launch_bounds__(kTPB) void k_select_write(ReqTable T, int64_t N, co
   for (int i = threadIdx.x; i < btot; i += kTPB) idx[boff + i] = s_idx[i];
 }
 }  // namespace
+
+// Scratch of the allocation-free selection (sphinx_select_mask_static): the
+// chunk counts and offsets of up to kStaticChunks chunks, 512 KB, one copy per
+// GPU for the life of the process.  Every call fully rewrites the entries it
+// reads (counts of all its chunks, then their offsets), so nothing needs
+// clearing between calls; calls that overlap on one GPU share the array and
+// race.  In host code `scratch` is only a symbol: its device address comes
+// from hipGetSymbolAddress, resolved once per device.
+constexpr int64_t kStaticChunks = (int64_t)1 << 16;
+static __device__ __align__(256) int32_t scratch[2 * kStaticChunks];
+
+static_assert(kStaticChunks * kChunk == SPHINX_SELECT_STATIC_MAX_TOKENS, "the header states the static limit");
+
+int64_t select_static_max_tokens() { return kStaticChunks * kChunk; }
+
+hipError_t select_static_ws(void** ptr) {
+  static std::mutex mu;
+  static void* dev_ptr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(mu);
+  if (dev_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    dev_ptr[dev] = p;
+  }
+  *ptr = dev_ptr[dev];
+  return hipSuccess;
+}
 
 size_t select_ws_bytes(int64_t N) {
   const int64_t nblk = (N + kChunk - 1) / kChunk;

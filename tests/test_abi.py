@@ -132,6 +132,19 @@ def test_refine_validation(L):
     assert L.sphinx_refine_step(*args(40, over, need.value)) == INVALID
 
 
+def test_select_static_validation(L):
+    """The allocation-free selection validates like sphinx_select_mask and
+    refuses inputs beyond its static scratch, all before any HIP call."""
+    P = ctypes.c_void_p
+    reqs = _reqs([(2, 8, 8)])
+    f = L.sphinx_select_mask_static
+    assert f(reqs, 1, None, P(256), None, P(256), P(256), P(256), None, None) == INVALID
+    assert f(reqs, 1, P(258), P(256), None, P(256), P(256), P(256), None, None) == INVALID  # misaligned
+    assert f(reqs, 0, P(256), P(256), None, P(256), P(256), P(256), None, None) == INVALID
+    big = _reqs([(1100, 1024, 1024)])  # 288 M tokens > 2^28
+    assert f(big, 1, P(256), P(256), None, P(256), P(256), P(256), None, None) == UNSUPPORTED
+
+
 def test_refine_size_limit(L):
     """The activation matrices are addressed with 32-bit element offsets: a
     step with n * max(3 D, mlp) >= 2^31 is refused before any HIP call."""
