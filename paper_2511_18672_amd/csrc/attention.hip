@@ -14,8 +14,9 @@
 //  * the output O^T lands with the query on the lane, so the final 1/l
 //    normalisation is lane-local;
 //  * softmax in base 2 with the 1/sqrt(d) scale folded into log2(e)/sqrt(d);
-//    the running max is only moved (and O, l rescaled) when a tile raises it
-//    by more than 8 in log2 units, so P <= 2^8; P is rounded to bf16 for the PV
+//    the running max starts at the first tile's and is only moved (and O, l
+//    rescaled) when a tile's probabilities would sum past 2^64, so no tile
+//    max is computed in the common case; P is rounded to bf16 for the PV
 //    product and the row sum adds the same rounded values (v_dot2 with ones);
 //  * only the last key tile of a segment is masked.
 // Workgroups of the longest segment are scheduled first, and the linear
@@ -37,7 +38,11 @@ namespace sphinx {
 namespace {
 constexpr int AQ = 128;  // queries per workgroup
 constexpr int AK = 64;   // keys per LDS tile
-constexpr float kRescaleLog2 = 8.0f;  // rescale only when the running max grows by > 2^8
+// A tile's probabilities are exp2 of its scores minus the running max, with
+// no per-tile max in the common case; the max is moved (and O, l rescaled)
+// only when a tile's row sum of probabilities exceeds this bound, so every
+// probability stays below 2^64 and every accumulator far from overflow.
+constexpr float kPsumMax = 18446744073709551616.0f;  // 2^64
 static_assert(AQ == kAttnQueryTile, "host tile size must match the kernel");
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -56,20 +61,22 @@ __device__ __forceinline__ float max_across_halves(float x) {
   return max3(__uint_as_float(r[0]), __uint_as_float(r[1]), __uint_as_float(r[1]));
 }
 
-// Row max of one 64-key tile (scores s0: keys 0..31, s1: keys 32..63 of the
-// tile, slot r = key 8*(r/4) + 4*g + r%4; lanes l and l^32 hold the two
-// halves of the same query's keys).  With MASK, keys past L are set to -inf
-// first.
+// Scores of keys at or past L set to -inf (scores s0: keys 0..31, s1: keys
+// 32..63 of the tile starting at key kbase, slot r = key 8*(r/4) + 4*g + r%4).
+__device__ __forceinline__ void mask_tail(f32x16& s0, f32x16& s1, int g, int kbase, int L) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int key = kbase + (r >> 2) * 8 + g * 4 + (r & 3);
+    if (key >= L) s0[r] = -INFINITY;
+    if (key + 32 >= L) s1[r] = -INFINITY;
+  }
+}
+
+// Row max of one 64-key tile (lanes l and l^32 hold the two halves of the
+// same query's keys).  With MASK, keys past L are set to -inf first.
 template <bool MASK>
 __device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kbase, int L) {
-  if (MASK) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = kbase + (r >> 2) * 8 + g * 4 + (r & 3);
-      if (key >= L) s0[r] = -INFINITY;
-      if (key + 32 >= L) s1[r] = -INFINITY;
-    }
-  }
+  if (MASK) mask_tail(s0, s1, g, kbase, L);
   // four independent chains of four max3 over the 32 values, then one max3 and a max
   float m4[4];
 #pragma unroll
@@ -277,7 +284,7 @@ __device__ __forceinline__ bf16x8 step_frag(const char* sK, const char* sV, cons
 template <int HD>
 __device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff<HD>& lo,
                                        const bf16x8 (&qf)[4], const v4s& q4, float m_run, const f32x16& c0,
-                                       const f32x16& c1, float& l_run, const bf16x8 (&pp)[2][2],
+                                       const f32x16& c1, float& psum_out, const bf16x8 (&pp)[2][2],
                                        bf16x8 (&pn)[2][2], f32x16& n0, f32x16& n1,
                                        f32x16 (&oacc)[Geo<HD>::DB]) {
   constexpr int NPV = Geo<HD>::NPV, NSTEP = NPV + Geo<HD>::NQK;
@@ -343,7 +350,6 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
     }
     __builtin_amdgcn_sched_barrier(0);
   }
-  l_run += psum;
   // Pin the probabilities here: otherwise the compiler sinks their whole
   // computation past the next iteration's branches, next to their use,
   // undoing the interleaving with this iteration's MFMAs.
@@ -351,13 +357,13 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
   for (int w = 0; w < 2; ++w)
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) asm volatile("" : "+v"(pn[w][hf]));
-  asm volatile("" : "+v"(l_run));
+  asm volatile("" : "+v"(psum));
+  psum_out = psum;
 }
 
-// Probabilities exp2(s - delta) of the last tile's shifted scores, rounded to
-// bf16 in P^T operand order; their row sum is added to l_run.
-__device__ __forceinline__ void last_probs(const f32x16& s0, const f32x16& s1, float delta, float& l_run,
-                                           bf16x8 (&pf)[2][2]) {
+// Probabilities exp2(s - delta) of a tile's shifted scores, rounded to bf16 in
+// P^T operand order; returns their row sum (of the rounded values).
+__device__ __forceinline__ float probs(const f32x16& s0, const f32x16& s1, float delta, bf16x8 (&pf)[2][2]) {
   const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
 #pragma unroll
@@ -377,21 +383,7 @@ __device__ __forceinline__ void last_probs(const f32x16& s0, const f32x16& s1, f
       pf[1][hf][2 * i] = b[0];
       pf[1][hf][2 * i + 1] = b[1];
     }
-  l_run += psum;
-}
-
-// Running max for scores that arrive shifted by it: mx is the tile max
-// relative to m_run.  The max moves, to m_run + mx, only where mx exceeds
-// 2^kRescaleLog2; returns the factor for O (exactly 1 elsewhere) and, in
-// delta, by how much the max moved, i.e. the shift the tile's scores still
-// need.
-__device__ __forceinline__ float raise_max_shifted(float mx, float& m_run, float& l_run, float& delta) {
-  const float m_new = (mx > kRescaleLog2) ? m_run + mx : m_run;
-  delta = m_new - m_run;
-  const float alpha = fast_exp2(-delta);
-  l_run *= alpha;
-  m_run = m_new;
-  return alpha;
+  return psum;
 }
 }  // namespace dma
 
@@ -540,21 +532,73 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   // Tile j of K and of V lives in ring slot j % 3.  Iteration t: softmax of
   // tile t, QK(t+1), PV(t-1); copies K(t+3) (clamped to the last tile: a
   // harmless duplicate near the end) and V(t+1), which land by the end of
-  // iteration t+1.  The running max moves branch-free; the factor for O
-  // (exactly 1 unless some lane's max moved) is applied at the start of the
-  // next iteration, i.e. after PV(t-1) and before PV(t).
-  float alpha = 1.0f;
-  auto rescale_o = [&]() {
-    if (__ballot(alpha != 1.0f) != 0) {
-#pragma unroll
-      for (int db = 0; db < G::DB; ++db) oacc[db] *= alpha;
-    }
-  };
+  // iteration t+1.
   int slot = 0;  // t % 3
   // The scores of every tile arrive shifted by the running max as it stood
-  // when their QK was issued (tile 0: shifted here by its own max).  Unless
-  // the max moved since, the probabilities are exp2 of the MFMA output with
-  // no further arithmetic.
+  // when their QK was issued (tile 0: shifted here by its own max), so the
+  // probabilities are exp2 of the MFMA output with no further arithmetic and
+  // no per-tile max.  Only when a tile's row sum exceeds kPsumMax (some score
+  // more than about 64 above the running max) does `rebase` move the max to
+  // the tile's, rescale O (which then holds the tiles up to t-1) and l, and
+  // recompute the tile's probabilities.  The next tile's QK was already issued
+  // with the old max: `pend` is what its scores still owe, subtracted at the
+  // start of the next iteration (`moved` is wave-uniform).
+  bool moved = false;
+  float pend = 0.0f;
+  auto rebase = [&](f32x16& c0, f32x16& c1, bf16x8 (&pf)[2][2]) -> float {
+    const float mx = tile_max<false>(c0, c1, g, 0, L);  // the same in lanes l and l^32
+    const float delta = mx > 0.0f ? mx : 0.0f;
+    const float alpha = fast_exp2(-delta);
+#pragma unroll
+    for (int db = 0; db < G::DB; ++db) oacc[db] *= alpha;
+    l_run *= alpha;
+    m_run += delta;
+    pend = delta;
+    moved = true;
+    return dma::probs(c0, c1, delta, pf);
+  };
+  // The scores of tile t once more, shifted by the current max, for the rare
+  // rebase (their registers are reused as soon as the probabilities are made,
+  // and a loop tile's K slot in LDS has been refilled by then): the rows are
+  // read from global memory in the fragment layout of the LDS reads (row r32
+  // of each 32-key block, dims 16 ks + 8 g .. + 7; head_dim 72: dims 64 + 4 g
+  // .. + 3 for the 8-deep step).  Rows past the segment repeat its last key
+  // and their scores are masked.
+  auto rescore = [&](int t, f32x16& c0, f32x16& c1) {
+    const bf16* r0 = Kg + (int64_t)min(t * AK + r32, L - 1) * ld;
+    const bf16* r1 = Kg + (int64_t)min(t * AK + 32 + r32, L - 1) * ld;
+    c0 = f32x16{};
+    c1 = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(r0 + ks * 16 + g * 8);
+      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(r1 + ks * 16 + g * 8);
+      c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], c1, 0, 0, 0);
+    }
+    if constexpr (HD == 72) {
+      const dma::v4s k0 = *reinterpret_cast<const dma::v4s*>(r0 + 64 + g * 4);
+      const dma::v4s k1 = *reinterpret_cast<const dma::v4s*>(r1 + 64 + g * 4);
+      c0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(k0, q4, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(k1, q4, c1, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      c0[r] -= m_run;
+      c1[r] -= m_run;
+    }
+    if (t * AK + AK > L) mask_tail(c0, c1, g, t * AK, L);
+  };
+  auto settle = [&](f32x16& c0, f32x16& c1) {  // scores shifted by an older max
+    if (moved) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        c0[r] -= pend;
+        c1[r] -= pend;
+      }
+      moved = false;
+    }
+  };
   auto iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, bf16x8 (&pp)[2][2],
                   bf16x8 (&pn)[2][2]) {
     const int s1 = slot == 2 ? 0 : slot + 1, s2 = slot == 0 ? 2 : slot - 1;  // (t+1) % 3, (t-1) % 3
@@ -568,21 +612,18 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
       copy_k(min(t + 3, nkt - 1) * AK, slot);
       vs = (t + 1) & 1;
     }
-    float delta;
-    const float a_new = dma::raise_max_shifted(tile_max<false>(c0, c1, g, t * AK, L), m_run, l_run, delta);
-    rescale_o();
-    alpha = a_new;
-    if (__ballot(delta != 0.0f) != 0)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        c0[r] -= delta;
-        c1[r] -= delta;
-      }
+    settle(c0, c1);
     // head_dim 64: the wave in its MFMA region goes first, ahead of the
-    // serial tile-max and rescale work of the other waves on its SIMD
+    // serial work of the other waves on its SIMD
     if constexpr (HD == 64) __builtin_amdgcn_s_setprio(1);
-    dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, m_run, c0, c1, l_run, pp, pn, n0, n1, oacc);
+    float psum;
+    dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, m_run, c0, c1, psum, pp, pn, n0, n1, oacc);
     if constexpr (HD == 64) __builtin_amdgcn_s_setprio(0);
+    if (__ballot(!(psum <= kPsumMax)) != 0) {
+      rescore(t, c0, c1);
+      psum = rebase(c0, c1, pn);
+    }
+    l_run += psum;
     land(Keep4{});
     slot = s1;
   };
@@ -635,15 +676,15 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
       sprev = (t + 1) & 1;
       scur = t & 1;
     }
-    const float mx = (L % AK != 0) ? tile_max<true>(a0, a1, g, t * AK, L)
-                                   : tile_max<false>(a0, a1, g, t * AK, L);
-    float delta;
-    const float a_new = dma::raise_max_shifted(mx, m_run, l_run, delta);
-    rescale_o();
-    alpha = a_new;
-    dma::last_probs(a0, a1, delta, l_run, pb);
-    dma::pv<HD>(sm.v[sprev], lo, pa, oacc);
-    rescale_o();
+    settle(a0, a1);
+    if (L % AK != 0) mask_tail(a0, a1, g, t * AK, L);
+    float psum = dma::probs(a0, a1, 0.0f, pb);
+    dma::pv<HD>(sm.v[sprev], lo, pa, oacc);  // PV(t-1) before a rebase, which rescales it too
+    if (__ballot(!(psum <= kPsumMax)) != 0) {
+      rescore(t, a0, a1);
+      psum = rebase(a0, a1, pb);
+    }
+    l_run += psum;
     land(Keep0{});
     dma::pv<HD>(sm.v[scur], lo, pb, oacc);
   }
