@@ -41,8 +41,11 @@ Precision modes:
   ``precision="model"`` -- float64 arithmetic, but for a bf16 model the
       operands that the model declares as bf16 are rounded to bf16
       (round-to-nearest-even) exactly where the model stores them: the
-      adaLN-modulated LayerNorm outputs fed to the QKV and MLP1 GEMMs, q, k, v,
-      the attention output, and the GELU output fed to MLP2.  Weights and
+      adaLN-modulated LayerNorm outputs fed to the QKV and MLP1 GEMMs, the
+      query scaled by log2(e)/sqrt(d) (the model keeps its queries in the
+      units of a base-2 softmax, so the 1/sqrt(d) of the attention is applied
+      before the query is stored, not after), k, v, the attention output, and
+      the GELU output fed to MLP2.  Weights and
       latents are bf16 values already.  Residual stream, statistics, softmax,
       conditioning, noise prediction and the DDIM update stay float64.
 """
@@ -325,15 +328,17 @@ def position_embedding(f, y, x, D: int) -> np.ndarray:
     return spatial + np.concatenate([np.sin(af), np.cos(af)], axis=1)
 
 
-def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048, kv_seg: Optional[np.ndarray] = None):
-    """Non-causal softmax(q k^T / sqrt(d)) v per head, each query attending to
-    the keys of its own segment only (segments = contiguous row ranges seg[r]..seg[r+1]).
+def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048, kv_seg: Optional[np.ndarray] = None,
+              scale: Optional[float] = None):
+    """Non-causal softmax(scale q k^T) v per head, scale = 1/sqrt(d) unless
+    given, each query attending to the keys of its own segment only (segments
+    = contiguous row ranges seg[r]..seg[r+1]).
 
     With kv_seg, the queries of segment r attend to the key/value rows
     kv_seg[r]..kv_seg[r+1] instead (k and v then have their own row count)."""
     n, D = q.shape
     d = D // heads
-    scale = 1.0 / np.sqrt(d)
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
     out = np.zeros((n, D))
     for r in range(len(seg) - 1):
         s0, s1 = int(seg[r]), int(seg[r + 1])
@@ -353,12 +358,13 @@ def attention(q, k, v, heads: int, seg: np.ndarray, chunk: int = 2048, kv_seg: O
     return out
 
 
-def attention_groups(q, k, v, heads: int, gq: np.ndarray, gk: np.ndarray):
-    """Non-causal softmax(q k^T / sqrt(d)) v per head where query row i attends
-    to the key rows j with gk[j] == gq[i] (groups need not be contiguous)."""
+def attention_groups(q, k, v, heads: int, gq: np.ndarray, gk: np.ndarray, scale: Optional[float] = None):
+    """Non-causal softmax(scale q k^T) v per head (scale = 1/sqrt(d) unless
+    given) where query row i attends to the key rows j with gk[j] == gq[i]
+    (groups need not be contiguous)."""
     n, D = q.shape
     d = D // heads
-    scale = 1.0 / np.sqrt(d)
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
     out = np.zeros((n, D))
     for g in np.unique(gq):
         qi = np.flatnonzero(gq == g)
@@ -434,6 +440,9 @@ def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.
     w = model.weights
     D, H = model.D, model.heads
     rnd = round_bf16 if (precision == "model" and model.dtype == "bf16") else (lambda a: a)
+    # queries are kept in base-2 softmax units: q' = q log2(e)/sqrt(d), and
+    # softmax(q k^T / sqrt(d)) = softmax(ln(2) q' k^T)
+    qscale, sscale = np.log2(np.e) / np.sqrt(D // H), np.log(2.0)
     # conditioning, per distinct timestep (identical for equal timesteps)
     taus, inv = np.unique(np.asarray(tau_tok), return_inverse=True)
     c = silu(conditioning(model, taus))
@@ -443,20 +452,20 @@ def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.
         sh1, sc1, g1, sh2, sc2, g2 = (mod[:, i * D:(i + 1) * D] for i in range(6))
         a = rnd(layer_norm(h) * (1.0 + sc1) + sh1)
         qkv = linear(a, w[f"b{l}.qkv_w"], w[f"b{l}.qkv_b"])
-        q, k, v = rnd(qkv[:, :D]), rnd(qkv[:, D:2 * D]), rnd(qkv[:, 2 * D:])
+        q, k, v = rnd(qkv[:, :D] * qscale), rnd(qkv[:, D:2 * D]), rnd(qkv[:, 2 * D:])
         kind = block_attention(model.attention, l)
         if cache is None:
             if kind == "joint":
-                o = rnd(attention(q, k, v, H, seg))
+                o = rnd(attention(q, k, v, H, seg, scale=sscale))
             else:
                 req = np.searchsorted(seg, np.arange(x.shape[0]), side="right") - 1
                 grp = attention_group_ids(kind, req, f, y, xx)
-                o = rnd(attention_groups(q, k, v, H, grp, grp))
+                o = rnd(attention_groups(q, k, v, H, grp, grp, scale=sscale))
         else:
             cache[l][0][rows] = k
             cache[l][1][rows] = v
             if kind == "joint":
-                o = rnd(attention(q, cache[l][0], cache[l][1], H, seg, kv_seg=kv_seg))
+                o = rnd(attention(q, cache[l][0], cache[l][1], H, seg, kv_seg=kv_seg, scale=sscale))
             else:
                 n_all = cache[l][0].shape[0]
                 req_q = np.searchsorted(seg, np.arange(x.shape[0]), side="right") - 1
@@ -464,7 +473,7 @@ def denoise(model: Model, x: np.ndarray, f, y, xx, tau_tok: np.ndarray, seg: np.
                 both = attention_group_ids(kind, np.concatenate([req_q, req_k]), np.concatenate([f, kv_pos[0]]),
                                            np.concatenate([y, kv_pos[1]]), np.concatenate([xx, kv_pos[2]]))
                 gq, gk = both[:x.shape[0]], both[x.shape[0]:]
-                o = rnd(attention_groups(q, cache[l][0], cache[l][1], H, gq, gk))
+                o = rnd(attention_groups(q, cache[l][0], cache[l][1], H, gq, gk, scale=sscale))
         h = h + (1.0 + g1) * linear(o, w[f"b{l}.o_w"], w[f"b{l}.o_b"])
         a2 = rnd(layer_norm(h) * (1.0 + sc2) + sh2)
         m = rnd(gelu_tanh(linear(a2, w[f"b{l}.fc1_w"], w[f"b{l}.fc1_b"])))

@@ -15,6 +15,7 @@ using namespace sphinx;
 namespace {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr float kLog2e = 1.4426950408889634f;
 inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 inline size_t esize(sphinx_dtype d) { return d == SPHINX_BF16 ? 2 : 4; }
 inline bool valid_dtype(sphinx_dtype d) { return d == SPHINX_F32 || d == SPHINX_BF16; }
@@ -724,7 +725,9 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
     }
     {
       Bracket br(SPHINX_K_GEMM_QKV, s);
-      GemmEpi e_qkv{qkv, 3 * D, nullptr, 0, nullptr};
+      // q leaves the projection scaled by log2(e)/sqrt(head_dim), rounded once:
+      // attention scores then come out of q k^T in base-2 units
+      GemmEpi e_qkv{qkv, 3 * D, nullptr, 0, nullptr, D, kLog2e / std::sqrt((float)m->head_dim)};
       SPHINX_TRY(launch_gemm(EPI_BIAS, dt, abuf, P(SPHINX_P_QKV_W, l), P(SPHINX_P_QKV_B, l), n, 3 * D, D, e_qkv, s));
     }
     AttnIO io{qkv, static_cast<const unsigned char*>(qkv) + (size_t)D * esize(dt),

@@ -13,7 +13,8 @@
 //    key order of the P^T k-slots;
 //  * the output O^T lands with the query on the lane, so the final 1/l
 //    normalisation is lane-local;
-//  * softmax in base 2 with the 1/sqrt(d) scale folded into log2(e)/sqrt(d);
+//  * softmax in base 2: q arrives from the QKV projection already multiplied
+//    by log2(e)/sqrt(d) (rounded to bf16 once, after the scale);
 //    the running max starts at the first tile's and is only moved (and O, l
 //    rescaled) when a tile's probabilities would sum past 2^64, so no tile
 //    max is computed in the common case; P is rounded to bf16 for the PV
@@ -99,9 +100,7 @@ __device__ __forceinline__ float tile_max(f32x16& s0, f32x16& s1, int g, int kba
 //    the previous iteration.  Neither MFMA group depends on that softmax, so
 //    the region is one straight-line block: all fragment reads first, then 16
 //    steps of one MFMA and one pair of probabilities, fenced so the compiler
-//    keeps the order.  The running max moves branch-free; O is rescaled (a
-//    wave-uniform branch taken only when some lane's max moved) between
-//    PV(t-1) and PV(t), at the start of the next iteration.
+//    keeps the order.
 //  * K and V tiles are stored unpadded, 64 rows of 128 B, with the 16-byte
 //    chunks of row r permuted: K chunk c at c ^ ((r >> 1) & 7), V chunk c at
 //    c ^ 2(r & 3).  LDS has 64 four-byte banks and serves a 16-byte read to 16
@@ -388,7 +387,7 @@ __device__ __forceinline__ float probs(const f32x16& s0, const f32x16& s1, float
 }  // namespace dma
 
 template <int HD>
-__device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads, float scale_log2, const SegTable& S,
+__device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads, const SegTable& S,
                                               dma::Smem<HD>& sm) {
   typedef dma::Geo<HD> G;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -420,18 +419,13 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   bf16x8 qf[4];
   dma::v4s q4 = {};  // head_dim 72: dims 64 + 4 g .. + 3
   const bf16* Qg = static_cast<const bf16*>(io.q) + (int64_t)seg0 * ldq + head * HD;
+  // q is stored scaled by log2(e)/sqrt(d): scores come out of the MFMAs in base-2 units
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
+  for (int ks = 0; ks < 4; ++ks)
     qf[ks] = (ql < Lq) ? *reinterpret_cast<const bf16x8*>(Qg + (int64_t)ql * ldq + ks * 16 + g * 8) : zero8;
-    // scores come out of the MFMAs already scaled: q * log2(e) / sqrt(d), rounded to bf16
-#pragma unroll
-    for (int e = 0; e < 8; ++e) qf[ks][e] = (bf16)((float)qf[ks][e] * scale_log2);
-  }
   if constexpr (HD == 72) {
     bf16x4 v = {};
     if (ql < Lq) v = *reinterpret_cast<const bf16x4*>(Qg + (int64_t)ql * ldq + 64 + g * 4);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = (bf16)((float)v[e] * scale_log2);
     q4 = __builtin_bit_cast(dma::v4s, v);
   }
 
@@ -545,8 +539,44 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   // start of the next iteration (`moved` is wave-uniform).
   bool moved = false;
   float pend = 0.0f;
-  auto rebase = [&](f32x16& c0, f32x16& c1, bf16x8 (&pf)[2][2]) -> float {
-    const float mx = tile_max<false>(c0, c1, g, 0, L);  // the same in lanes l and l^32
+  // The scores of one 32-key block w of tile t once more, shifted by the
+  // current max (rare path: the tile's score registers are reused as soon as
+  // its probabilities are made, and a loop tile's K slot in LDS is refilled by
+  // then).  K rows are read from global memory in the fragment layout of the
+  // LDS reads (row r32 of the block, dims 16 ks + 8 g .. + 7; head_dim 72:
+  // dims 64 + 4 g .. + 3 for the 8-deep step).  Rows past the segment repeat
+  // its last key and their scores are masked.
+  auto rescore = [&](int t, int w) -> f32x16 {
+    const int key = t * AK + 32 * w + r32;
+    const bf16* row = Kg + (int64_t)min(key, L - 1) * ld;
+    f32x16 c = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*reinterpret_cast<const bf16x8*>(row + ks * 16 + g * 8), qf[ks], c,
+                                                  0, 0, 0);
+    if constexpr (HD == 72)
+      c = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(*reinterpret_cast<const dma::v4s*>(row + 64 + g * 4), q4, c, 0, 0,
+                                                    0);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int k = t * AK + 32 * w + (r >> 2) * 8 + g * 4 + (r & 3);
+      c[r] = k < L ? c[r] - m_run : -INFINITY;
+    }
+    return c;
+  };
+  // Rebase for tile t, whose probabilities passed the bound: the running max
+  // moves to the tile's max where that is larger, O (which then holds the tiles
+  // up to t-1) and l are rescaled, and the tile's probabilities are made again
+  // from rescored scores, one 32-key block at a time.  Returns their row sum.
+  auto rebase = [&](int t, bf16x8 (&pf)[2][2]) -> float {
+    float mx = -INFINITY;
+#pragma unroll 1
+    for (int w = 0; w < 2; ++w) {  // one block at a time: few registers on this rare path
+      const f32x16 c = rescore(t, w);
+#pragma unroll
+      for (int r = 0; r < 16; r += 2) mx = max3(mx, c[r], c[r + 1]);
+    }
+    mx = max_across_halves(mx);  // the same in lanes l and l^32
     const float delta = mx > 0.0f ? mx : 0.0f;
     const float alpha = fast_exp2(-delta);
 #pragma unroll
@@ -555,39 +585,37 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     m_run += delta;
     pend = delta;
     moved = true;
-    return dma::probs(c0, c1, delta, pf);
-  };
-  // The scores of tile t once more, shifted by the current max, for the rare
-  // rebase (their registers are reused as soon as the probabilities are made,
-  // and a loop tile's K slot in LDS has been refilled by then): the rows are
-  // read from global memory in the fragment layout of the LDS reads (row r32
-  // of each 32-key block, dims 16 ks + 8 g .. + 7; head_dim 72: dims 64 + 4 g
-  // .. + 3 for the 8-deep step).  Rows past the segment repeat its last key
-  // and their scores are masked.
-  auto rescore = [&](int t, f32x16& c0, f32x16& c1) {
-    const bf16* r0 = Kg + (int64_t)min(t * AK + r32, L - 1) * ld;
-    const bf16* r1 = Kg + (int64_t)min(t * AK + 32 + r32, L - 1) * ld;
-    c0 = f32x16{};
-    c1 = f32x16{};
+    const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+    float psum = 0.0f;
+    bf16x8 q0[2], q1[2];  // probabilities of blocks 0 and 1
+#pragma unroll 1
+    for (int w = 0; w < 2; ++w) {
+      const f32x16 c = rescore(t, w);  // now shifted by the new max
+      bf16x8 h[2];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(r0 + ks * 16 + g * 8);
-      const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(r1 + ks * 16 + g * 8);
-      c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[ks], c0, 0, 0, 0);
-      c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[ks], c1, 0, 0, 0);
-    }
-    if constexpr (HD == 72) {
-      const dma::v4s k0 = *reinterpret_cast<const dma::v4s*>(r0 + 64 + g * 4);
-      const dma::v4s k1 = *reinterpret_cast<const dma::v4s*>(r1 + 64 + g * 4);
-      c0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(k0, q4, c0, 0, 0, 0);
-      c1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(k1, q4, c1, 0, 0, 0);
-    }
+      for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      c0[r] -= m_run;
-      c1[r] -= m_run;
+        for (int i = 0; i < 4; ++i) {
+          bf16x2 pr;
+          pr[0] = (bf16)fast_exp2(c[hf * 8 + 2 * i]);
+          pr[1] = (bf16)fast_exp2(c[hf * 8 + 2 * i + 1]);
+          psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, psum, false);
+          h[hf][2 * i] = pr[0];
+          h[hf][2 * i + 1] = pr[1];
+        }
+      if (w == 0) {
+        q0[0] = h[0];
+        q0[1] = h[1];
+      } else {
+        q1[0] = h[0];
+        q1[1] = h[1];
+      }
     }
-    if (t * AK + AK > L) mask_tail(c0, c1, g, t * AK, L);
+    pf[0][0] = q0[0];
+    pf[0][1] = q0[1];
+    pf[1][0] = q1[0];
+    pf[1][1] = q1[1];
+    return psum;
   };
   auto settle = [&](f32x16& c0, f32x16& c1) {  // scores shifted by an older max
     if (moved) {
@@ -619,10 +647,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     float psum;
     dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, m_run, c0, c1, psum, pp, pn, n0, n1, oacc);
     if constexpr (HD == 64) __builtin_amdgcn_s_setprio(0);
-    if (__ballot(!(psum <= kPsumMax)) != 0) {
-      rescore(t, c0, c1);
-      psum = rebase(c0, c1, pn);
-    }
+    if (__ballot(!(psum <= kPsumMax)) != 0) psum = rebase(t, pn);
     l_run += psum;
     land(Keep4{});
     slot = s1;
@@ -680,10 +705,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     if (L % AK != 0) mask_tail(a0, a1, g, t * AK, L);
     float psum = dma::probs(a0, a1, 0.0f, pb);
     dma::pv<HD>(sm.v[sprev], lo, pa, oacc);  // PV(t-1) before a rebase, which rescales it too
-    if (__ballot(!(psum <= kPsumMax)) != 0) {
-      rescore(t, a0, a1);
-      psum = rebase(a0, a1, pb);
-    }
+    if (__ballot(!(psum <= kPsumMax)) != 0) psum = rebase(t, pb);
     l_run += psum;
     land(Keep0{});
     dma::pv<HD>(sm.v[scur], lo, pb, oacc);
@@ -705,23 +727,21 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
 }
 
-__global__ __launch_bounds__(256, 3) void k_attn_bf16_dma(AttnIO io, int D, int heads, float scale_log2,
-                                                          SegTable S) {
+__global__ __launch_bounds__(256, 3) void k_attn_bf16_dma(AttnIO io, int D, int heads, SegTable S) {
   __shared__ __attribute__((aligned(1024))) dma::Smem<64> sm;
-  attn_body_dma<64>(io, D, heads, scale_log2, S, sm);
+  attn_body_dma<64>(io, D, heads, S, sm);
 }
 
 // head_dim 72: 46 KB of LDS, three workgroups per CU.
-__global__ __launch_bounds__(256, 3) void k_attn_bf16_dma72(AttnIO io, int D, int heads, float scale_log2,
-                                                            SegTable S) {
+__global__ __launch_bounds__(256, 3) void k_attn_bf16_dma72(AttnIO io, int D, int heads, SegTable S) {
   __shared__ __attribute__((aligned(1024))) dma::Smem<72> sm;
-  attn_body_dma<72>(io, D, heads, scale_log2, S, sm);
+  attn_body_dma<72>(io, D, heads, S, sm);
 }
 
 constexpr int kF32Max = 64;
 
-__global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int heads, int n, float scale,
-                                                  SegTable S) {
+// q is stored scaled by log2(e)/sqrt(d): base-2 online softmax.
+__global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int heads, int n, SegTable S) {
   const int gid = blockIdx.x * 128 + threadIdx.x;
   if (gid >= n * heads) return;
   const int j = gid / heads, h = gid % heads;
@@ -746,10 +766,9 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int h
 #pragma unroll
     for (int c = 0; c < kF32Max; ++c)
       if (c < d) sc = fmaf(q[c], kr[c], sc);
-    sc *= scale;
     const float mn = fmaxf(m, sc);
-    const float corr = expf(m - mn);
-    const float p = expf(sc - mn);
+    const float corr = exp2f(m - mn);
+    const float p = exp2f(sc - mn);
     l = fmaf(l, corr, p);
 #pragma unroll
     for (int c = 0; c < kF32Max; ++c)
@@ -765,15 +784,13 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnIO io, int D, int d, int h
 hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads, int head_dim, int n,
                             const SegTable& S, hipStream_t s) {
   if (dt == SPHINX_BF16) {
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)head_dim);
     const int grid = S.tile_prefix[S.nseg] * heads;
     if (head_dim == 64)
-      k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
+      k_attn_bf16_dma<<<grid, 256, 0, s>>>(io, D, heads, S);
     else
-      k_attn_bf16_dma72<<<grid, 256, 0, s>>>(io, D, heads, scale_log2, S);
+      k_attn_bf16_dma72<<<grid, 256, 0, s>>>(io, D, heads, S);
   } else {
-    const float scale = 1.0f / sqrtf((float)head_dim);
-    k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>(io, D, head_dim, heads, n, scale, S);
+    k_attn_f32<<<(n * heads + 127) / 128, 128, 0, s>>>(io, D, head_dim, heads, n, S);
   }
   return hipGetLastError();
 }
@@ -788,7 +805,8 @@ hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads,
 // workgroup per column (members found with one ballot), one wave per head,
 // one lane per query.  Each wave stages its head's key and value rows in LDS
 // in chunks with 16-byte loads; the lanes then read them as broadcasts.  fp32
-// math with an online softmax.
+// math with an online softmax in base 2 (q is stored scaled by
+// log2(e)/sqrt(d)).
 // ---------------------------------------------------------------------------
 namespace sphinx {
 namespace {
@@ -818,7 +836,7 @@ struct TempVec<float> {
 // (fp32 models); a multiple of the 16-byte vector.
 template <typename T, int HD, bool EXACT>
 __global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, int D, int d_rt, int heads,
-                                                       float scale, const int32_t* __restrict__ pos, int cached) {
+                                                       const int32_t* __restrict__ pos, int cached) {
   constexpr int VN = TempVec<T>::N;             // elements per 16-byte vector
   constexpr int NV = HD / VN;                   // vectors per head row (upper bound)
   constexpr int KC = sizeof(T) == 2 ? 32 : 16;  // keys per staged chunk
@@ -878,10 +896,7 @@ __global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, i
         for (int i = 0; i < VN; ++i) q[v * VN + i] = 0.0f;
     }
 #pragma unroll
-    for (int e = 0; e < HD; ++e) {
-      q[e] *= scale;
-      acc[e] = 0.0f;
-    }
+    for (int e = 0; e < HD; ++e) acc[e] = 0.0f;
     float m = -INFINITY, l = 0.0f;
     for (int k0 = 0; k0 < nk; k0 += KC) {
       const int cnt = min(KC, nk - k0);
@@ -908,7 +923,7 @@ __global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, i
           }
           const float sc = (part[0] + part[1]) + (part[2] + part[3]);
           const float mn = fmaxf(m, sc);
-          const float corr = __expf(m - mn), p = __expf(sc - mn);
+          const float corr = exp2f(m - mn), p = exp2f(sc - mn);
           l = fmaf(l, corr, p);
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
@@ -938,14 +953,13 @@ hipError_t launch_attn_temporal(sphinx_dtype dt, const ReqTable& T, const AttnIO
                                 int head_dim, const int32_t* pos, bool cached, hipStream_t s) {
   int64_t cols = 0;
   for (int r = 0; r < T.R; ++r) cols += (int64_t)(T.h[r] >> 1) * (T.w[r] >> 1);
-  const float scale = 1.0f / sqrtf((float)head_dim);
   const int cf = cached ? 1 : 0;
   if (dt == SPHINX_BF16 && head_dim == 64)
-    k_attn_temporal<bf16, 64, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cf);
+    k_attn_temporal<bf16, 64, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, pos, cf);
   else if (dt == SPHINX_BF16)
-    k_attn_temporal<bf16, 72, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cf);
+    k_attn_temporal<bf16, 72, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, pos, cf);
   else
-    k_attn_temporal<float, 64, false><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, scale, pos, cf);
+    k_attn_temporal<float, 64, false><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, pos, cf);
   return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
     h[o] = fmaf(1.0f + e.gate[(int64_t)e.crow[m] * e.ldg + n], v, h[o]);
   } else {
     if constexpr (EPI == EPI_GELU) v = gelu_tanh(v);
+    if constexpr (EPI == EPI_BIAS) v = n < e.qcols ? v * e.qscale : v;
     reinterpret_cast<OT*>(e.out)[(int64_t)m * e.ldo + n] = store_from_f32<OT>(v);
   }
 }
@@ -277,6 +278,14 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
         v.y = gelu_tanh(v.y);
         v.z = gelu_tanh(v.z);
         v.w = gelu_tanh(v.w);
+      }
+      if constexpr (EPI == EPI_BIAS) {
+        if (n < e.qcols) {  // four columns of one thread are all queries or all not (qcols % 4 == 0)
+          v.x *= e.qscale;
+          v.y *= e.qscale;
+          v.z *= e.qscale;
+          v.w *= e.qscale;
+        }
       }
       bf16x4 o;
       o[0] = (bf16)v.x;

@@ -15,6 +15,8 @@ struct GemmEpi {
   const float* gate;     // EPI_GATED: gate rows (conditioning row of each token)
   int ldg;
   const int32_t* crow;   // EPI_GATED: conditioning row of each token
+  int qcols;             // EPI_BIAS: columns [0, qcols) are multiplied by qscale before the store
+  float qscale;          //   (the queries of the QKV projection, scaled by log2(e)/sqrt(head_dim))
 };
 
 // Attention segments (one per request with forwarded tokens): the queries of

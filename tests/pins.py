@@ -384,9 +384,12 @@ def torch_denoiser(O, model, x, f, y, xx, tau, seg, precision, attention="joint"
         mask = allowed if attention == "joint" else (same_frame if l % 2 == 0 else same_column)
         mod = F.linear(c, wt[f"b{l}.ada_w"], wt[f"b{l}.ada_b"]).chunk(6, dim=1)
         a = rnd(ln(h) * (1 + mod[1]) + mod[0])
-        q, k, v = (rnd(z) for z in F.linear(a, wt[f"b{l}.qkv_w"], wt[f"b{l}.qkv_b"]).chunk(3, dim=1))
+        q, k, v = F.linear(a, wt[f"b{l}.qkv_w"], wt[f"b{l}.qkv_b"]).chunk(3, dim=1)
+        # the model stores q already multiplied by log2(e)/sqrt(d) (rounded after
+        # the scale) and runs the softmax in base 2: scale ln(2) on q' k^T
+        q, k, v = rnd(q * (math.log2(math.e) / math.sqrt(d))), rnd(k), rnd(v)
         heads = lambda z: z.reshape(n, H, d).transpose(0, 1)
-        o = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), attn_mask=mask)
+        o = F.scaled_dot_product_attention(heads(q), heads(k), heads(v), attn_mask=mask, scale=math.log(2.0))
         o = rnd(o.transpose(0, 1).reshape(n, D))
         h = h + (1 + mod[2]) * F.linear(o, wt[f"b{l}.o_w"], wt[f"b{l}.o_b"])
         a2 = rnd(ln(h) * (1 + mod[4]) + mod[3])

@@ -38,27 +38,27 @@ def _alpha_bar_off(*_):
     return np.cumprod(1.0 - (1e-4 + (2e-2 - 1e-4) * i / 1000))
 
 
-def _attention_no_scale(q, k, v, heads, seg, chunk=2048, kv_seg=None):
-    d = q.shape[1] // heads
-    return _orig["attention"](q * np.sqrt(d), k, v, heads, seg, chunk, kv_seg)
+def _attention_no_scale(q, k, v, heads, seg, chunk=2048, kv_seg=None, scale=None):
+    return _orig["attention"](q, k, v, heads, seg, chunk, kv_seg, 1.0)
 
 
-def _attention_no_segments(q, k, v, heads, seg, chunk=2048, kv_seg=None):
+def _attention_no_segments(q, k, v, heads, seg, chunk=2048, kv_seg=None, scale=None):
     kv = None if kv_seg is None else np.array([kv_seg[0], kv_seg[-1]])
-    return _orig["attention"](q, k, v, heads, np.array([seg[0], seg[-1]]), chunk, kv)
+    return _orig["attention"](q, k, v, heads, np.array([seg[0], seg[-1]]), chunk, kv, scale)
 
 
-def _attention_wrong_axis(q, k, v, heads, seg, chunk=2048, kv_seg=None):
+def _attention_wrong_axis(q, k, v, heads, seg, chunk=2048, kv_seg=None, scale=None):
     if kv_seg is not None:
         raise NotImplementedError
     n, D = q.shape
     d = D // heads
+    sc = 1.0 / np.sqrt(d) if scale is None else scale
     out = np.zeros((n, D))
     for r in range(len(seg) - 1):
         s0, s1 = int(seg[r]), int(seg[r + 1])
         for h in range(heads):
             c = slice(h * d, (h + 1) * d)
-            s = q[s0:s1, c] @ k[s0:s1, c].T / np.sqrt(d)
+            s = q[s0:s1, c] @ k[s0:s1, c].T * sc
             p = np.exp(s - s.max(axis=0, keepdims=True))
             p /= p.sum(axis=0, keepdims=True)
             out[s0:s1, c] = p @ v[s0:s1, c]
@@ -162,10 +162,10 @@ def _denoise_stale(model, x, f, y, xx, tau, seg, precision, cache, rows, kv_seg)
     orig_attention = O.attention
     calls = {"l": 0}
 
-    def attention_on_old(q, k, v, heads, seg_, chunk=2048, kv_seg=None):
+    def attention_on_old(q, k, v, heads, seg_, chunk=2048, kv_seg=None, scale=None):
         l = calls["l"]
         calls["l"] += 1
-        return orig_attention(q, before[l][0], before[l][1], heads, seg_, chunk, kv_seg)
+        return orig_attention(q, before[l][0], before[l][1], heads, seg_, chunk, kv_seg, scale)
 
     O.attention = attention_on_old
     try:
