@@ -86,18 +86,42 @@ def traffic_entry(kernel: str, workload: str):
         return None
 
 
+def _oracle_e2e(O, wl, threads=None, min_s=1.0):
+    """Refined tokens·steps/s of the unmodified oracle's whole loop on wl,
+    repeated until at least min_s seconds have passed (tiny runs in ms)."""
+    from threadpoolctl import threadpool_limits
+
+    reps, n, t0 = 0, 0, time.perf_counter()
+    while True:
+        with threadpool_limits(limits=threads):
+            _, trace = O.refine(wl, precision="model", trace=True)
+        n += sum(r.n_sel for r in trace)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s:
+            return {"value": round(n / dt, 2), "runs": reps, "seconds": round(dt, 2),
+                    "threads": "all" if threads is None else threads}
+
+
 def cpu_baseline(wl) -> dict:
-    """The oracle (numpy fp64, unmodified) on a bounded sample: one step of the
-    same workload through a one-block denoiser, scaled to the full depth."""
+    """The oracle (numpy fp64, unmodified) on the host.  value: a bounded sample
+    of the headline workload, one step through a one-block denoiser scaled to
+    the full depth.  Also measured: the whole loop of the tiny and small
+    workloads end to end, on all threads and on one."""
     import oracle as O
     import workloads as W
 
     try:
         from threadpoolctl import threadpool_info
 
-        cores = max([d.get("num_threads", 1) for d in threadpool_info()] or [os.cpu_count() or 1])
+        blas = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     except Exception:
-        cores = os.cpu_count() or 1
+        blas = 1
+    nproc = os.cpu_count() or 1
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except Exception:
+        affinity = nproc
     m = wl.model
     one = W.ModelCfg(D=m.D, heads=m.heads, head_dim=m.head_dim, mlp=m.mlp, L=1, dtype=m.dtype)
     sample = W.Workload(name=wl.name, model=one, requests=wl.requests, u=wl.u, thr=wl.thr, s_start=wl.s_start,
@@ -109,10 +133,18 @@ def cpu_baseline(wl) -> dict:
     res = O.step(sample, model, wl.z0, plans[0], "model")
     dt = time.perf_counter() - t0
     per_step = dt * m.L  # blocks dominate; embedding and final projection counted L times (conservative)
-    return {"value": res.n_sel / per_step, "unit": "refined tokens·steps/s", "cores": int(cores),
-            "kind": "oracle",
-            "sample": f"one step ({res.n_sel} selected tokens) through a 1-block copy of the denoiser, "
-                      f"{dt:.1f} s, scaled x{m.L} blocks"}
+    out = {"value": res.n_sel / per_step, "unit": "refined tokens·steps/s", "cores": int(blas),
+           "kind": "oracle",
+           "sample": f"one headline step ({res.n_sel} selected tokens) through a 1-block copy of the denoiser, "
+                     f"{dt:.1f} s, scaled x{m.L} blocks (BLAS threads {blas}; elementwise numpy is one thread)",
+           "nproc": int(nproc), "affinity_cpus": int(affinity), "blas_threads": int(blas)}
+    runs = {}
+    for name, ctor in (("tiny", W.tiny), ("small", W.small)):
+        w = ctor()
+        runs[name] = {"all_threads": _oracle_e2e(O, w), "one_thread": _oracle_e2e(O, w, threads=1)}
+    out["end_to_end"] = runs
+    out["end_to_end_unit"] = "refined tokens·steps/s over the whole loop (tiny: 1 step, small: 10 steps)"
+    return out
 
 
 def copy_mode(args):
