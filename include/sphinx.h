@@ -260,6 +260,27 @@ sphinx_status sphinx_refine_step(const sphinx_model_desc* m, const sphinx_reques
                                  const int32_t* tau, const float* c1, const float* c2, float* x_sel, void* ws,
                                  size_t ws_bytes, void* stream);
 
+/* Varlen non-causal attention, the attention step of the denoiser blocks
+ * (Alg. 1 D.partial_step on the masked tokens; joint attention over each
+ * request's selected tokens), on its own.  Per segment i and head h:
+ *   o[j] = sum_t 2^(q[j].k[t]) v[t] / sum_t 2^(q[j].k[t])
+ * for query rows j in [cu_q[i], cu_q[i+1]) and key/value rows t in
+ * [cu_kv[i], cu_kv[i+1]), head h using columns [h d, (h+1) d).  The softmax
+ * is in base 2: q must already be multiplied by log2(e)/sqrt(d) (the layout
+ * the denoiser's QKV projection writes), which makes this softmax(q k^T /
+ * sqrt(d)) of the unscaled queries.
+ *   dtype: SPHINX_BF16 (head_dim 64 or 72; P is rounded to bf16, accumulation
+ *          fp32, o rounded to bf16) or SPHINX_F32 (head_dim <= 64).
+ *   q: dev [rows][ldq] elements; k, v: dev [rows][ldkv]; o: dev, row j at
+ *   element j * heads * head_dim (written for the query rows of the segments
+ *   only).  cu_q, cu_kv: host int32 [nseg+1], non-decreasing from 0; empty
+ *   segments are skipped; 1 <= nseg <= SPHINX_MAX_REQUESTS.  ldq, ldkv >=
+ *   heads * head_dim and multiples of 8; pointers 16-byte aligned.  A segment
+ *   with queries needs at least one key (SPHINX_E_INVALID otherwise). */
+sphinx_status sphinx_varlen_attention(sphinx_dtype dtype, int32_t heads, int32_t head_dim, const void* q,
+                                      int32_t ldq, const void* k, const void* v, int32_t ldkv, void* o,
+                                      const int32_t* cu_q, const int32_t* cu_kv, int32_t nseg, void* stream);
+
 /* Scatter and blend (Sec. 3 and 5.3: confident regions keep their values).
  *   z_out = z_in with token idx[j] replaced by x_sel[j]   (j < n_sel)
  * z_in == z_out scatters in place (dtype and layout must match); otherwise

@@ -10,7 +10,7 @@ from .binding import (ATTN_FACTORISED, ATTN_JOINT, GRID_PER_FRAME, GRID_SHARED, 
                       sphinx_mask_frontend_workspace_bytes, sphinx_model_blob_bytes, sphinx_model_param,
                       sphinx_peak_mfma, sphinx_plan_cache, sphinx_plan_step, sphinx_refine_step,
                       sphinx_refine_step_cached, sphinx_refine_workspace_bytes, sphinx_scatter_blend,
-                      sphinx_scatter_masked, sphinx_select_mask, sphinx_select_mask_static, sphinx_select_workspace_bytes,
+                      sphinx_scatter_masked, sphinx_select_mask, sphinx_select_mask_static, sphinx_select_workspace_bytes, sphinx_varlen_attention,
                       sphinx_status_string, sphinx_timing_enable, sphinx_timing_read)
 from .refiner import Refiner, from_workload, pack_weights
 
@@ -20,6 +20,6 @@ __all__ = ["ATTN_FACTORISED", "ATTN_JOINT", "GRID_PER_FRAME", "GRID_SHARED", "sp
            "sphinx_mask_frontend_workspace_bytes", "sphinx_model_blob_bytes", "sphinx_model_param",
            "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_plan_step", "sphinx_refine_step",
            "sphinx_refine_step_cached", "sphinx_refine_workspace_bytes", "sphinx_scatter_blend",
-           "sphinx_scatter_masked", "sphinx_select_mask", "sphinx_select_mask_static", "sphinx_select_workspace_bytes", "sphinx_status_string",
+           "sphinx_scatter_masked", "sphinx_select_mask", "sphinx_select_mask_static", "sphinx_select_workspace_bytes", "sphinx_varlen_attention", "sphinx_status_string",
            "sphinx_timing_enable", "sphinx_timing_read", "select_mask", "gather", "refine_step", "scatter_blend",
            "plan_step"]

@@ -32,7 +32,7 @@ EXPORTED = ["sphinx_status_string", "sphinx_model_blob_bytes", "sphinx_model_par
             "sphinx_refine_step", "sphinx_scatter_blend", "sphinx_timing_enable", "sphinx_timing_read",
             "sphinx_peak_mfma", "sphinx_plan_cache", "sphinx_kv_cache_bytes", "sphinx_gather_ctx",
             "sphinx_refine_step_cached", "sphinx_scatter_masked", "sphinx_mask_frontend_workspace_bytes",
-            "sphinx_mask_frontend", "sphinx_adaptive_start", "sphinx_select_mask_static"]
+            "sphinx_mask_frontend", "sphinx_adaptive_start", "sphinx_select_mask_static", "sphinx_varlen_attention"]
 PEAK_BLOCKS = 2048
 PEAK_CONSTANT, PEAK_RANDOM = 0, 1
 KERNEL_CLASSES = ["select", "gather", "cond", "embed", "ln", "gemm_qkv", "attention", "gemm_out", "gemm_mlp1",
@@ -92,6 +92,8 @@ def lib() -> ctypes.CDLL:
         "sphinx_select_workspace_bytes": (c_int32, [c_int64, POINTER(c_size_t)]),
         "sphinx_select_mask": (c_int32, [POINTER(Request), c_int32, P, P, P, P, P, P, P, P, c_size_t, P]),
         "sphinx_select_mask_static": (c_int32, [POINTER(Request), c_int32, P, P, P, P, P, P, P, P]),
+        "sphinx_varlen_attention": (c_int32, [c_int32, c_int32, c_int32, P, c_int32, P, P, c_int32, P, P, P, c_int32,
+                                              P]),
         "sphinx_gather": (c_int32, [POINTER(Request), c_int32, c_int32, P, c_int32, P, c_int32, P, c_int32, P, P, P,
                                     P]),
         "sphinx_refine_workspace_bytes": (c_int32, [POINTER(ModelDesc), POINTER(Request), c_int32, c_int64,
@@ -236,6 +238,18 @@ def sphinx_select_mask_static(reqs, uncert, thr, active, mask, idx, cu_sel, read
         reqs, len(reqs), _ptr(uncert), _ptr(thr), _ptr(active), _ptr(mask), _ptr(idx), _ptr(cu_sel),
         _ptr(host), _stream(stream)))
     return host
+
+
+def sphinx_varlen_attention(dtype: int, heads: int, head_dim: int, q, ldq: int, k, v, ldkv: int, o, cu_q, cu_kv,
+                            stream=None):
+    """Varlen attention (base-2 softmax; q already scaled by log2(e)/sqrt(d)).
+    cu_q, cu_kv: host int sequences of segment bounds."""
+    cq = np.ascontiguousarray(cu_q, dtype=np.int32)
+    ck = np.ascontiguousarray(cu_kv, dtype=np.int32)
+    assert cq.size == ck.size and cq.size >= 2
+    _check("sphinx_varlen_attention", lib().sphinx_varlen_attention(
+        dtype, heads, head_dim, _ptr(q), ldq, _ptr(k), _ptr(v), ldkv, _ptr(o), _ptr(cq), _ptr(ck), cq.size - 1,
+        _stream(stream)))
 
 
 def sphinx_gather(reqs, layout: int, state, state_dtype: int, eps, eps_dtype: int, idx, n_sel: int, a, b, x_sel,

@@ -793,6 +793,48 @@ sphinx_status sphinx_refine_step_cached(const sphinx_model_desc* m, const sphinx
   return refine_impl(m, reqs, R, idx, n, cu_host, tau, c1, c2, x, kv_cache, ws, ws_bytes, stream);
 }
 
+sphinx_status sphinx_varlen_attention(sphinx_dtype dtype, int32_t heads, int32_t head_dim, const void* q,
+                                      int32_t ldq, const void* k, const void* v, int32_t ldkv, void* o,
+                                      const int32_t* cu_q, const int32_t* cu_kv, int32_t nseg, void* stream) {
+  if (!valid_dtype(dtype)) return SPHINX_E_UNSUPPORTED;
+  if (heads < 1 || head_dim < 1 || nseg < 1 || !cu_q || !cu_kv) return SPHINX_E_INVALID;
+  if (nseg > SPHINX_MAX_REQUESTS) return SPHINX_E_UNSUPPORTED;
+  if (dtype == SPHINX_BF16 ? (head_dim != 64 && head_dim != 72) : head_dim > 64) return SPHINX_E_UNSUPPORTED;
+  const int64_t D = (int64_t)heads * head_dim;
+  if (D > 4096 || ldq < D || ldkv < D || ldq % 8 != 0 || ldkv % 8 != 0) return SPHINX_E_INVALID;
+  if (cu_q[0] != 0 || cu_kv[0] != 0) return SPHINX_E_INVALID;
+  for (int i = 0; i < nseg; ++i) {
+    if (cu_q[i + 1] < cu_q[i] || cu_kv[i + 1] < cu_kv[i]) return SPHINX_E_INVALID;
+    if (cu_q[i + 1] > cu_q[i] && cu_kv[i + 1] == cu_kv[i]) return SPHINX_E_INVALID;
+  }
+  const int64_t nq = cu_q[nseg], nkv = cu_kv[nseg];
+  if (nq == 0) return SPHINX_OK;
+  if (!q || !k || !v || !o || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
+    return SPHINX_E_INVALID;
+  if (nq * ldq >= ((int64_t)1 << 31) || nkv * ldkv >= ((int64_t)1 << 31) || nq * D >= ((int64_t)1 << 31))
+    return SPHINX_E_UNSUPPORTED;
+  SegTable S;
+  std::memset(&S, 0, sizeof(S));
+  std::vector<int> order;
+  for (int i = 0; i < nseg; ++i)
+    if (cu_q[i + 1] > cu_q[i]) order.push_back(i);
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int x, int y) { return cu_kv[x + 1] - cu_kv[x] > cu_kv[y + 1] - cu_kv[y]; });
+  S.nseg = (int)order.size();
+  for (int j = 0; j < S.nseg; ++j) {
+    const int i = order[j];
+    S.start[j] = cu_q[i];
+    S.len[j] = cu_q[i + 1] - cu_q[i];
+    S.kv_start[j] = cu_kv[i];
+    S.kv_len[j] = cu_kv[i + 1] - cu_kv[i];
+    S.tile_prefix[j + 1] = S.tile_prefix[j] + (S.len[j] + kAttnQueryTile - 1) / kAttnQueryTile;
+  }
+  const AttnIO io{q, k, v, o, ldq, ldkv};
+  hipStream_t s = (hipStream_t)stream;
+  Bracket br(SPHINX_K_ATTENTION, s);
+  return hip_status(launch_attention(dtype, io, (int)D, heads, head_dim, (int)nq, S, s));
+}
+
 sphinx_status sphinx_scatter_blend(const sphinx_request* reqs, int32_t R, const float* x_sel, const int32_t* idx,
                                    int32_t n_sel, const void* z_in, sphinx_dtype in_dtype, sphinx_layout in_layout,
                                    void* z_out, sphinx_dtype out_dtype, sphinx_layout out_layout, void* stream) {

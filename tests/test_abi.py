@@ -145,6 +145,25 @@ def test_select_static_validation(L):
     assert f(big, 1, P(256), P(256), None, P(256), P(256), P(256), None, None) == UNSUPPORTED
 
 
+def test_varlen_attention_validation(L):
+    P = ctypes.c_void_p
+    f = L.sphinx_varlen_attention
+    cu = lambda *v: (ctypes.c_int32 * len(v))(*v)
+    args = lambda dt, hd, cq, ck, n, q=256, ld=64: (dt, 1, hd, P(q), ld, P(256), P(256), ld, P(256), cq, ck, n, None)
+    assert f(*args(1, 32, cu(0, 4), cu(0, 4), 1)) == UNSUPPORTED  # bf16 head_dim 32
+    assert f(*args(0, 80, cu(0, 4), cu(0, 4), 1, ld=80)) == UNSUPPORTED  # fp32 head_dim > 64
+    assert f(*args(5, 64, cu(0, 4), cu(0, 4), 1)) == UNSUPPORTED  # dtype
+    assert f(*args(1, 64, cu(0, 4), cu(0, 0), 1)) == INVALID  # queries without keys
+    assert f(*args(1, 64, cu(1, 4), cu(0, 4), 1)) == INVALID  # does not start at 0
+    assert f(*args(1, 64, cu(0, 4, 2), cu(0, 4, 8), 2)) == INVALID  # decreasing
+    assert f(*args(1, 64, cu(0, 4), cu(0, 4), 1, ld=60)) == INVALID  # stride below heads * head_dim
+    assert f(*args(1, 64, cu(0, 4), cu(0, 4), 1, q=258)) == INVALID  # misaligned
+    assert f(*args(1, 64, cu(0, 4), cu(0, 4), 0)) == INVALID
+    assert f(*args(1, 64, cu(0, 0), cu(0, 9), 1)) == OK  # no queries: nothing to do
+    many = (ctypes.c_int32 * 66)(*range(66))
+    assert f(*args(1, 64, many, many, 65)) == UNSUPPORTED
+
+
 def test_refine_size_limit(L):
     """The activation matrices are addressed with 32-bit element offsets: a
     step with n * max(3 D, mlp) >= 2^31 is refused before any HIP call."""
