@@ -15,8 +15,9 @@
 //    normalisation is lane-local;
 //  * softmax in base 2: q arrives from the QKV projection already multiplied
 //    by log2(e)/sqrt(d) (rounded to bf16 once, after the scale);
-//    the running max starts at the first tile's and is only moved (and O, l
-//    rescaled) when a tile's probabilities would sum past 2^64, so no tile
+//    the running max starts at zero (head_dim 64, when the first tile's
+//    maxima are moderate) or at the first tile's, and is only moved (and O,
+//    l rescaled) when a tile's probabilities would sum past 2^64, so no tile
 //    max is computed in the common case; P is rounded to bf16 for the PV
 //    product and the row sum adds the same rounded values (v_dot2 with ones);
 //  * only the last key tile of a segment is masked.
@@ -153,6 +154,14 @@ struct Smem {
   char pad[Geo<HD>::PAD + 16];
 };
 
+// acc + p.x + p.y as one v_dot2c with (1, 1) in bf16.  A volatile statement,
+// so that each step's dot product stays in its step: as plain arithmetic the
+// compiler gathers the sixteen of a tile into one chain after the last MFMA.
+__device__ __forceinline__ float rowsum_add(float acc, bf16x2 p) {
+  asm volatile("v_dot2c_f32_bf16_e32 %0, 0x3f803f80, %1" : "+v"(acc) : "v"(__builtin_bit_cast(unsigned, p)));
+  return acc;
+}
+
 __device__ __forceinline__ bf16x8 tr_pair(const char* p0, const char* p1) {
   const v4s a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p0);
   const v4s b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p1);
@@ -236,8 +245,9 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff<HD>& lo, const 
 // One iteration's MFMA work interleaved by hand with the softmax of the
 // previous tile: one MFMA per step (PV(t-1) first: 8 steps at head_dim 64,
 // 12 at 72; then QK(t+1), the head-dim k-steps of the two 32-key blocks
-// alternately, the first of them accumulating onto -max, so that the scores
-// arrive scaled and shifted) and, in the first 16 steps, softmax work on two
+// alternately, the first of them accumulating from zero (head_dim 64) or
+// onto -max (head_dim 72, so that the scores arrive shifted)) and, in the
+// first 16 steps, softmax work on two
 // consecutive probability
 // pairs, software-pipelined so that no instruction of a step waits on another
 // of the same step: the exponentials of pair st+1 and the bf16 pack and
@@ -301,7 +311,7 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
   __builtin_amdgcn_sched_barrier(0);
   const bf16x2 ones2 = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
-  f32x16 negm;  // -m_run in every element, built just before the first QK step
+  f32x16 negm;  // head_dim 72: -m_run in every element, built just before the first QK step
 #pragma unroll
   for (int st = 0; st < NSTEP; ++st) {
     if (st + 2 < NSTEP) fr[(st + 2) % 3] = step_frag<HD>(sK, sV, lo, st + 2);
@@ -309,7 +319,7 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
       int kb, hf, db;
       pv_step<HD>(st, kb, hf, db);
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], pp[kb][hf], oacc[db], 0, 0, 0);
-      if (st == NPV - 1)
+      if (HD == 72 && st == NPV - 1)
 #pragma unroll
         for (int r = 0; r < 16; r += 2) {  // eight 64-bit moves of the (-m, -m) pair
           const unsigned u = __float_as_uint(-m_run);
@@ -320,9 +330,11 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
           negm[r + 1] = __uint_as_float((unsigned)(d >> 32));
         }
     } else {
-      // the first k-step accumulates onto -max (every element of a lane
-      // belongs to its query), so the scores arrive shifted
+      // the first k-step accumulates onto -max (head_dim 72: every element
+      // of a lane belongs to its query, so the scores arrive shifted) or
+      // from zero (head_dim 64)
       const int ks = (st - NPV) >> 1;
+      const f32x16 zero16 = {};
       if (HD == 72 && ks == 4) {
         const v4s a = *reinterpret_cast<const v4s*>(&fr[st % 3]);
         if ((st - NPV) & 1)
@@ -330,9 +342,9 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
         else
           n0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, q4, n0, 0, 0, 0);
       } else if ((st - NPV) & 1) {
-        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? negm : n1, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? (HD == 72 ? negm : zero16) : n1, 0, 0, 0);
       } else {
-        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? negm : n0, 0, 0, 0);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? (HD == 72 ? negm : zero16) : n0, 0, 0, 0);
       }
     }
     if (st + 1 < 16)
@@ -343,7 +355,10 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
       bf16x2 pr;
       pr[0] = (bf16)ex[st][0];
       pr[1] = (bf16)ex[st][1];
-      psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones2, psum, false);
+      if constexpr (HD == 64)
+        psum = rowsum_add(psum, pr);
+      else  // head_dim 72: fencing them costs registers that the copy offsets need
+        psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones2, psum, false);
       pn[w][hf][2 * i] = pr[0];
       pn[w][hf][2 * i + 1] = pr[1];
     }
@@ -528,15 +543,24 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   // harmless duplicate near the end) and V(t+1), which land by the end of
   // iteration t+1.
   int slot = 0;  // t % 3
-  // The scores of every tile arrive shifted by the running max as it stood
-  // when their QK was issued (tile 0: shifted here by its own max), so the
-  // probabilities are exp2 of the MFMA output with no further arithmetic and
-  // no per-tile max.  Only when a tile's row sum exceeds kPsumMax (some score
+  // No per-tile max: a tile's probabilities are exp2 of its scores minus the
+  // running max.  Only when a tile's row sum exceeds kPsumMax (some score
   // more than about 64 above the running max) does `rebase` move the max to
   // the tile's, rescale O (which then holds the tiles up to t-1) and l, and
-  // recompute the tile's probabilities.  The next tile's QK was already issued
-  // with the old max: `pend` is what its scores still owe, subtracted at the
-  // start of the next iteration (`moved` is wave-uniform).
+  // recompute the tile's probabilities.
+  //  * head_dim 64: QK accumulates from zero.  A wave whose first-tile maxima
+  //    all lie in [-64, 32] keeps the running max at zero (exp2 of such
+  //    scores neither overflows nor loses the row sum to underflow), so its
+  //    probabilities are exp2 of the MFMA output with no further arithmetic.
+  //    Otherwise, and after a rebase, the wave is `shifted` (wave-uniform):
+  //    each tile's scores have the running max subtracted before their
+  //    exponentials.
+  //  * head_dim 72: the scores of every tile arrive shifted by the running max
+  //    as it stood when their QK was issued (tile 0: shifted here by its own
+  //    max).  After a rebase the next tile's QK has already been issued with
+  //    the old max: `pend` is what its scores still owe, subtracted at the
+  //    start of the next iteration (`moved` is wave-uniform).
+  bool shifted = HD == 72;
   bool moved = false;
   float pend = 0.0f;
   // The scores of one 32-key block w of tile t once more, shifted by the
@@ -585,6 +609,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     m_run += delta;
     pend = delta;
     moved = true;
+    shifted = true;
     const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
     float psum = 0.0f;
     bf16x8 q0[2], q1[2];  // probabilities of blocks 0 and 1
@@ -617,8 +642,15 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     pf[1][1] = q1[1];
     return psum;
   };
-  auto settle = [&](f32x16& c0, f32x16& c1) {  // scores shifted by an older max
-    if (moved) {
+  auto settle = [&](f32x16& c0, f32x16& c1) {  // what a tile's scores still owe
+    if constexpr (HD == 64) {
+      if (shifted)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          c0[r] -= m_run;
+          c1[r] -= m_run;
+        }
+    } else if (moved) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         c0[r] -= pend;
@@ -664,12 +696,18 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
   f32x16 a0, a1, b0, b1;
   dma::qk<HD>(sm.k[0], lo, qf, q4, a0, a1);
-  {  // the running max starts at tile 0's (keys past L masked)
-    m_run = tile_max<true>(a0, a1, g, 0, L);
+  {  // the running max starts at zero or at tile 0's (keys past L masked)
+    const float m0 = tile_max<true>(a0, a1, g, 0, L);
+    if constexpr (HD == 64) {  // tile 0's scores are settled like every other tile's
+      shifted = __ballot(!(m0 >= -64.0f && m0 <= 32.0f)) != 0;
+      m_run = shifted ? m0 : 0.0f;
+    } else {
+      m_run = m0;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      a0[r] -= m_run;
-      a1[r] -= m_run;
+      for (int r = 0; r < 16; ++r) {
+        a0[r] -= m_run;
+        a1[r] -= m_run;
+      }
     }
   }
   // iteration 0 copies K(3) into slot 0: every wave must be done reading K(0)

@@ -6,9 +6,12 @@ The kernels take q already multiplied by log2(e)/sqrt(d) and run a base-2
 softmax, i.e. softmax(ln(2) q k^T) in the oracle's terms.  Covered: ragged
 segments around the 64-key tile and 128-query tile edges, queries and keys of
 different lengths (the latent-cache layout), strided rows as in the QKV
-buffer, both bf16 head dims, the fp32 path, and inputs whose scores rise by
+buffer, both bf16 head dims, the fp32 path, inputs whose scores rise by
 far more than 2^64 above the first tile's maximum, so that the kernel's rare
-rebase path runs: once, in the last (partial) tile, and repeatedly.
+rebase path runs: once, in the last (partial) tile, and repeatedly, and
+inputs whose first-tile maxima lie far above or below zero (at head_dim 64
+the running max starts at zero only for maxima in [-64, 32]; these waves
+start shifted, in some cases next to unshifted waves of the same tile).
 
 Bound for bf16: every probability is rounded to bf16 (relative 2^-9), which
 moves an output by at most 2^-8 max|v|; o itself is rounded to bf16
@@ -135,6 +138,32 @@ def test_rebase_path(hd, case):
     print(f"[attention rebase {case} hd{hd}] scores rise {gap:.0f} above the first tile's max (log2 units)")
     assert gap > 128
     check(q, k, v, heads, hd, cu, cu, tag=f"rebase {case} hd{hd}")
+
+
+@pytest.mark.parametrize("hd", [64, 72])
+@pytest.mark.parametrize("case", ["high", "low", "mixed"])
+def test_shifted_from_start(hd, case):
+    """Every score near +512 ("high": exp2 overflows without the shift), near
+    -512 ("low": the row sum underflows to zero without it), or the queries
+    32..63 of every 128-query tile near -512 and the rest moderate ("mixed":
+    one shifted wave per workgroup)."""
+    rng = np.random.default_rng(6)
+    heads = 2
+    D = heads * hd
+    n = 300
+    e = np.ones((1, D), np.float32)
+    k = rand(rng, n, D, 0.3) + 4.0 * e
+    q = rand(rng, n, D, 0.3) + (2.0 if case == "high" else -2.0) * e
+    if case == "mixed":
+        moderate = (np.arange(n) % 128 < 32) | (np.arange(n) % 128 >= 64)
+        q[moderate] = rand(rng, int(moderate.sum()), D, 0.3)
+    v = rand(rng, n, D)
+    cu = np.array([0, n], np.int32)
+    qe, ke = bf16(q).double().numpy(), bf16(k).double().numpy()
+    m0 = np.stack([qe[:, h * hd:(h + 1) * hd] @ ke[:64, h * hd:(h + 1) * hd].T for h in range(heads)]).max(axis=2)
+    print(f"[attention shifted {case} hd{hd}] first-tile maxima in [{m0.min():.0f}, {m0.max():.0f}]")
+    assert (m0.max() > 256) if case == "high" else (m0.min() < -256)
+    check(q, k, v, heads, hd, cu, cu, tag=f"shifted {case} hd{hd}")
 
 
 def test_fp32_path():
