@@ -113,6 +113,44 @@ def test_select_stale_workspace_many_chunks():
         print(f"[select] stale-workspace N={wl.N} chunks={(wl.N + 4095) // 4096} n_sel={n}")
 
 
+@pytest.mark.parametrize("case", ["two_scan_blocks", "ragged_requests"])
+def test_select_large(case):
+    """Large selections: 2^26 + 2^16 tokens (16 400 chunks of 4096 tokens, so
+    the chunk-count scan runs two of its 16 384-count blocks and carries
+    between them), and 21.3 M tokens in four requests (requests starting
+    inside chunks, a ragged last chunk).  Per-frame thresholds and active
+    flags, uniform-random u; the workspace (full of stale bytes) and the static
+    entry point, both against the oracle."""
+    if case == "two_scan_blocks":
+        shapes = [W.Request(1025, 512, 512)]
+    else:
+        shapes = [W.Request(3, 6, 10), W.Request(325, 512, 512), W.Request(1, 2, 2), W.Request(3, 130, 98)]
+    rng = np.random.default_rng(31)
+    info = O.token_info(shapes)
+    N, G = len(info.gframe), sum(r.frames for r in shapes)
+    tok_off = np.concatenate([[0], np.cumsum([r.frames * (r.h // 2) * (r.w // 2) for r in shapes])])
+    u = rng.random(N, dtype=np.float32)
+    thr = (0.5 + 0.4 * rng.random(G)).astype(np.float32)
+    active = (rng.random(G) < 0.7).astype(np.uint8)
+    mask, idx, cu, n = O.select(u, thr[info.gframe], active.astype(bool)[info.gframe], tok_off[:-1])
+    print(f"[select large] {case} N={N} chunks={(N + 4095) // 4096} n_sel={n}", flush=True)
+    reqs = S.make_requests(shapes)
+    ud, td, ad = _dev(u), _dev(thr), _dev(active)
+    ws = torch.full((S.sphinx_select_workspace_bytes(N),), 0xAB, dtype=torch.uint8, device="cuda")
+    for static in (False, True):
+        gm = torch.empty(N, dtype=torch.uint8, device="cuda")
+        gi = torch.full((N,), -7, dtype=torch.int32, device="cuda")
+        gc = torch.empty(len(shapes) + 1, dtype=torch.int32, device="cuda")
+        if static:
+            cu_host = S.sphinx_select_mask_static(reqs, ud, td, ad, gm, gi, gc)
+        else:
+            cu_host = S.sphinx_select_mask(reqs, ud, td, ad, gm, gi, gc, ws)
+        assert list(cu_host) == list(cu) + [n]
+        assert np.array_equal(gm.cpu().numpy().astype(bool), mask)
+        assert np.array_equal(gi[:n].cpu().numpy(), idx)
+        assert (gi[n:] == -7).all().item()
+
+
 def _in_layout(nchw, tokens_2d, layout):
     """The same latents in `layout` (tokens_2d: [N][16] in patch order)."""
     return nchw if layout == S.NCHW else np.ascontiguousarray(tokens_2d).ravel()
