@@ -15,8 +15,10 @@ For frame+region and batched the state before a late step is the oracle's
 loop run with the true injected noise as denoiser output, recomputed here.
 Masks and indices are compared bit-exact, latents element by element at the
 bf16 bar (2e-2 max-abs); tokens outside the step's selection must keep the
-state they had before it bit for bit.  Runs in the launch configuration the
-benchmark times (Refiner, token-major state).
+state they had before it bit for bit, i.e. the oracle's state as loaded (rounded
+once to the GPU state's storage type: requests that finished earlier hold fp64
+values there).  Runs in the launch configuration the benchmark times (Refiner,
+token-major state).
 """
 import os
 
@@ -66,7 +68,8 @@ def _refiner(wl):
 def _compare(tag, R, wl, before, idx, x):
     """GPU state after the step vs `before` with the oracle's rows idx <- x."""
     got = R.state.cpu().numpy().astype(np.float64)
-    expect = state_from_rows(wl, before, idx, x)
+    loaded = torch.from_numpy(np.ascontiguousarray(before)).to(R.state.dtype).double().numpy()
+    expect = state_from_rows(wl, loaded, idx, x)
     Pg, Pe = O.patchify(got, wl.requests), O.patchify(expect, wl.requests)
     keep = np.ones(wl.N, bool)
     keep[idx] = False
