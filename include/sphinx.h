@@ -49,12 +49,22 @@
 extern "C" {
 #endif
 
+/* The enumerations below are 32-bit values at the ABI.  In C++ they take
+ * int32_t as their fixed underlying type, so every int32 a caller passes is a
+ * representable value that the library can reject (out-of-range values return
+ * SPHINX_E_INVALID or "unknown status"), never an undefined enum load. */
+#ifdef __cplusplus
+#define SPHINX_ENUM enum : int32_t
+#else
+#define SPHINX_ENUM enum
+#endif
+
 #define SPHINX_MAX_REQUESTS 64
 #define SPHINX_TOKEN_DIM 16 /* 4 latent channels x 2 x 2 patch */
 #define SPHINX_TEMB_DIM 256 /* sinusoidal timestep embedding width */
 #define SPHINX_TRAIN_STEPS 1000
 
-typedef enum {
+typedef SPHINX_ENUM {
   SPHINX_OK = 0,
   SPHINX_E_INVALID = 1,     /* null required pointer, bad size, misalignment, inconsistent offsets */
   SPHINX_E_UNSUPPORTED = 2, /* valid but not implemented (head_dim, dtype, sizes) */
@@ -62,9 +72,9 @@ typedef enum {
   SPHINX_E_HIP = 4          /* a HIP launch or copy failed */
 } sphinx_status;
 
-typedef enum { SPHINX_F32 = 0, SPHINX_BF16 = 1 } sphinx_dtype;
+typedef SPHINX_ENUM { SPHINX_F32 = 0, SPHINX_BF16 = 1 } sphinx_dtype;
 
-typedef enum { SPHINX_LAYOUT_NCHW = 0, SPHINX_LAYOUT_TOKENS = 1 } sphinx_layout;
+typedef SPHINX_ENUM { SPHINX_LAYOUT_NCHW = 0, SPHINX_LAYOUT_TOKENS = 1 } sphinx_layout;
 
 /* Attention of the denoiser blocks.  JOINT: every block attends over the
  * request's tokens.  FACTORISED (the spatial / temporal split of the paper's
@@ -75,13 +85,13 @@ typedef enum { SPHINX_LAYOUT_NCHW = 0, SPHINX_LAYOUT_TOKENS = 1 } sphinx_layout;
  * blocks need the forwarded rows per frame on the host: a refine call on a
  * factorised model synchronizes its stream once to read them, and requires
  * idx in ascending order (as sphinx_select_mask produces). */
-typedef enum { SPHINX_ATTN_JOINT = 0, SPHINX_ATTN_FACTORISED = 1 } sphinx_attention;
+typedef SPHINX_ENUM { SPHINX_ATTN_JOINT = 0, SPHINX_ATTN_FACTORISED = 1 } sphinx_attention;
 
 /* Timestep grids of frames with different start indices (Alg. 1 per-frame
  * start): SHARED walks one grid per request from the largest start and lets a
  * frame join when the grid reaches its start; PER_FRAME walks every frame's
  * own n-step grid from its own start, all frames active from the first step. */
-typedef enum { SPHINX_GRID_SHARED = 0, SPHINX_GRID_PER_FRAME = 1 } sphinx_grid;
+typedef SPHINX_ENUM { SPHINX_GRID_SHARED = 0, SPHINX_GRID_PER_FRAME = 1 } sphinx_grid;
 
 typedef struct {
   int32_t frames;       /* F >= 1 */
@@ -108,7 +118,7 @@ typedef struct {
  * projection are stored as one matrix COND_W [(6L+2)D][D]: rows
  * [6D*l, 6D*(l+1)) belong to block l and give (shift1, scale1, gate1, shift2,
  * scale2, gate2); the last 2D rows give the final (shift, scale). */
-typedef enum {
+typedef SPHINX_ENUM {
   SPHINX_P_PE_W = 0,  /* [D][16]     patch embedding */
   SPHINX_P_PE_B,      /* [D] */
   SPHINX_P_T1_W,      /* [D][256]    timestep MLP, first layer */

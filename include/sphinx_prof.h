@@ -26,7 +26,7 @@ extern "C" {
  * keeps the events away from the other launches.  Events are created on first
  * use and reused; nothing is allocated on the device.  The timing state is
  * process-wide and guarded by a mutex. */
-typedef enum {
+typedef SPHINX_ENUM {
   SPHINX_K_SELECT = 0, /* mask + compaction (three kernels, one bracket) */
   SPHINX_K_GATHER,
   SPHINX_K_COND,       /* timestep/adaLN conditioning, position tables, token metadata */

@@ -14,7 +14,9 @@ from typing import Dict, Optional, Sequence
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsphinx.so")
+# SPHINX_LIBRARY names another build of the same library (the host-only
+# sanitizer build of the CPU tests); by default the in-tree gfx950 build.
+LIB_PATH = os.environ.get("SPHINX_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsphinx.so")
 
 F32, BF16 = 0, 1
 NCHW, TOKENS = 0, 1  # sphinx_layout

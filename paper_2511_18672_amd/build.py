@@ -4,6 +4,12 @@ Every ``csrc/*.hip`` file is compiled for gfx950 with hipcc (in parallel) into
 ``_build/`` at the repository root and linked into
 ``paper_2511_18672_amd/libsphinx.so``.  Packed-fp32 instruction selection is
 switched off for all device code.
+
+``build_sanitized()`` builds a second copy, ``_build/sanitize/libsphinx.so``,
+whose host code is compiled with AddressSanitizer and UndefinedBehaviorSanitizer
+(``-Xarch_host`` before each ``-fsanitize=``: the device code is the ordinary
+gfx950 code).  The CPU tests load it through ``SPHINX_LIBRARY`` with the
+sanitizer runtime preloaded (``sanitizer_runtime()``).
 """
 from __future__ import annotations
 
@@ -33,9 +39,13 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *FLAGS, "-c", src, "-o", obj]
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-Xarch_host", "-g"]
+
+
+def _compile(src: str, verbose: bool, out_dir: str = BUILD, extra=()) -> str:
+    obj = os.path.join(out_dir, os.path.basename(src) + ".o")
+    cmd = [_hipcc(), *FLAGS, *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = "\n".join(l for l in (r.stdout + r.stderr).splitlines() if "packed-fp32-ops" not in l)
     if r.returncode != 0:
@@ -57,6 +67,34 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     os.replace(tmp, LIB)
     return LIB
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """Host-sanitized copy of the library (see the module docstring)."""
+    out_dir = os.path.join(BUILD, "sanitize")
+    os.makedirs(out_dir, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose, out_dir, SANITIZE), srcs))
+    lib = os.path.join(out_dir, "libsphinx.so")
+    r = subprocess.run([_hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", *SANITIZE[:4], "-shared-libasan",
+                        "-o", lib + ".tmp", *objs], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
+    os.replace(lib + ".tmp", lib)
+    return lib
+
+
+def sanitizer_runtime() -> str:
+    """The compiler's shared AddressSanitizer runtime (to preload)."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(_hipcc())), "..", "llvm", "bin", "clang")
+    for c in (clang, "/opt/rocm/llvm/bin/clang"):
+        if os.path.exists(c):
+            r = subprocess.run([c, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+            path = r.stdout.strip()
+            if r.returncode == 0 and os.path.isabs(path) and os.path.exists(path):
+                return path
+    raise RuntimeError("the AddressSanitizer runtime was not found")
 
 
 if __name__ == "__main__":
