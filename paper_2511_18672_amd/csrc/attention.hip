@@ -15,10 +15,10 @@
 //    normalisation is lane-local;
 //  * softmax in base 2: q arrives from the QKV projection already multiplied
 //    by log2(e)/sqrt(d) (rounded to bf16 once, after the scale);
-//    the running max starts at zero (head_dim 64, when the first tile's
-//    maxima are moderate) or at the first tile's, and is only moved (and O,
-//    l rescaled) when a tile's probabilities would sum past 2^64, so no tile
-//    max is computed in the common case; P is rounded to bf16 for the PV
+//    the running max starts at zero (when the first tile's maxima are
+//    moderate) or at the first tile's, and is only moved (and O, l rescaled)
+//    when a tile's probabilities would sum past 2^64, so no tile max is
+//    computed in the common case; P is rounded to bf16 for the PV
 //    product and the row sum adds the same rounded values (v_dot2 with ones);
 //  * only the last key tile of a segment is masked.
 // Workgroups of the longest segment are scheduled first, and the linear
@@ -245,9 +245,8 @@ __device__ __forceinline__ void pv(const char* sV, const LaneOff<HD>& lo, const 
 // One iteration's MFMA work interleaved by hand with the softmax of the
 // previous tile: one MFMA per step (PV(t-1) first: 8 steps at head_dim 64,
 // 12 at 72; then QK(t+1), the head-dim k-steps of the two 32-key blocks
-// alternately, the first of them accumulating from zero (head_dim 64) or
-// onto -max (head_dim 72, so that the scores arrive shifted)) and, in the
-// first 16 steps, softmax work on two
+// alternately, from a zero accumulator) and, in the first 16 steps, softmax
+// work on two
 // consecutive probability
 // pairs, software-pipelined so that no instruction of a step waits on another
 // of the same step: the exponentials of pair st+1 and the bf16 pack and
@@ -292,7 +291,7 @@ __device__ __forceinline__ bf16x8 step_frag(const char* sK, const char* sV, cons
 
 template <int HD>
 __device__ __forceinline__ void region(const char* sK, const char* sV, const LaneOff<HD>& lo,
-                                       const bf16x8 (&qf)[4], const v4s& q4, float m_run, const f32x16& c0,
+                                       const bf16x8 (&qf)[4], const v4s& q4, const f32x16& c0,
                                        const f32x16& c1, float& psum_out, const bf16x8 (&pp)[2][2],
                                        bf16x8 (&pn)[2][2], f32x16& n0, f32x16& n1,
                                        f32x16 (&oacc)[Geo<HD>::DB]) {
@@ -311,7 +310,7 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
   __builtin_amdgcn_sched_barrier(0);
   const bf16x2 ones2 = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
-  f32x16 negm;  // head_dim 72: -m_run in every element, built just before the first QK step
+  const f32x16 zero16 = {};
 #pragma unroll
   for (int st = 0; st < NSTEP; ++st) {
     if (st + 2 < NSTEP) fr[(st + 2) % 3] = step_frag<HD>(sK, sV, lo, st + 2);
@@ -319,22 +318,9 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
       int kb, hf, db;
       pv_step<HD>(st, kb, hf, db);
       oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], pp[kb][hf], oacc[db], 0, 0, 0);
-      if (HD == 72 && st == NPV - 1)
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {  // eight 64-bit moves of the (-m, -m) pair
-          const unsigned u = __float_as_uint(-m_run);
-          const uint64_t pair = ((uint64_t)u << 32) | u;
-          uint64_t d;
-          asm volatile("v_mov_b64 %0, %1" : "=v"(d) : "v"(pair));
-          negm[r] = __uint_as_float((unsigned)d);
-          negm[r + 1] = __uint_as_float((unsigned)(d >> 32));
-        }
     } else {
-      // the first k-step accumulates onto -max (head_dim 72: every element
-      // of a lane belongs to its query, so the scores arrive shifted) or
-      // from zero (head_dim 64)
+      // the first k-step accumulates from zero: the scores arrive unshifted
       const int ks = (st - NPV) >> 1;
-      const f32x16 zero16 = {};
       if (HD == 72 && ks == 4) {
         const v4s a = *reinterpret_cast<const v4s*>(&fr[st % 3]);
         if ((st - NPV) & 1)
@@ -342,9 +328,9 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
         else
           n0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, q4, n0, 0, 0, 0);
       } else if ((st - NPV) & 1) {
-        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? (HD == 72 ? negm : zero16) : n1, 0, 0, 0);
+        n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? zero16 : n1, 0, 0, 0);
       } else {
-        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? (HD == 72 ? negm : zero16) : n0, 0, 0, 0);
+        n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fr[st % 3], qf[ks], ks == 0 ? zero16 : n0, 0, 0, 0);
       }
     }
     if (st + 1 < 16)
@@ -547,22 +533,14 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   // running max.  Only when a tile's row sum exceeds kPsumMax (some score
   // more than about 64 above the running max) does `rebase` move the max to
   // the tile's, rescale O (which then holds the tiles up to t-1) and l, and
-  // recompute the tile's probabilities.
-  //  * head_dim 64: QK accumulates from zero.  A wave whose first-tile maxima
-  //    all lie in [-64, 32] keeps the running max at zero (exp2 of such
-  //    scores neither overflows nor loses the row sum to underflow), so its
-  //    probabilities are exp2 of the MFMA output with no further arithmetic.
-  //    Otherwise, and after a rebase, the wave is `shifted` (wave-uniform):
-  //    each tile's scores have the running max subtracted before their
-  //    exponentials.
-  //  * head_dim 72: the scores of every tile arrive shifted by the running max
-  //    as it stood when their QK was issued (tile 0: shifted here by its own
-  //    max).  After a rebase the next tile's QK has already been issued with
-  //    the old max: `pend` is what its scores still owe, subtracted at the
-  //    start of the next iteration (`moved` is wave-uniform).
-  bool shifted = HD == 72;
-  bool moved = false;
-  float pend = 0.0f;
+  // recompute the tile's probabilities.  QK accumulates from zero.  A wave
+  // whose first-tile maxima all lie in [-64, 32] keeps the running max at
+  // zero (exp2 of such scores neither overflows nor loses the row sum to
+  // underflow), so its probabilities are exp2 of the MFMA output with no
+  // further arithmetic.  Otherwise, and after a rebase, the wave is `shifted`
+  // (wave-uniform): each tile's scores have the running max subtracted
+  // before their exponentials.
+  bool shifted = false;
   // The scores of one 32-key block w of tile t once more, shifted by the
   // current max (rare path: the tile's score registers are reused as soon as
   // its probabilities are made, and a loop tile's K slot in LDS is refilled by
@@ -607,8 +585,6 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     for (int db = 0; db < G::DB; ++db) oacc[db] *= alpha;
     l_run *= alpha;
     m_run += delta;
-    pend = delta;
-    moved = true;
     shifted = true;
     const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
     float psum = 0.0f;
@@ -643,21 +619,12 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     return psum;
   };
   auto settle = [&](f32x16& c0, f32x16& c1) {  // what a tile's scores still owe
-    if constexpr (HD == 64) {
-      if (shifted)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          c0[r] -= m_run;
-          c1[r] -= m_run;
-        }
-    } else if (moved) {
+    if (shifted)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        c0[r] -= pend;
-        c1[r] -= pend;
+        c0[r] -= m_run;
+        c1[r] -= m_run;
       }
-      moved = false;
-    }
   };
   auto iter = [&](int t, f32x16& c0, f32x16& c1, f32x16& n0, f32x16& n1, bf16x8 (&pp)[2][2],
                   bf16x8 (&pn)[2][2]) {
@@ -677,7 +644,7 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
     // serial work of the other waves on its SIMD
     if constexpr (HD == 64) __builtin_amdgcn_s_setprio(1);
     float psum;
-    dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, m_run, c0, c1, psum, pp, pn, n0, n1, oacc);
+    dma::region<HD>(sm.k[s1], sm.v[vs], lo, qf, q4, c0, c1, psum, pp, pn, n0, n1, oacc);
     if constexpr (HD == 64) __builtin_amdgcn_s_setprio(0);
     if (__ballot(!(psum <= kPsumMax)) != 0) psum = rebase(t, pn);
     l_run += psum;
@@ -696,19 +663,11 @@ __device__ __forceinline__ void attn_body_dma(const AttnIO& io, int D, int heads
   }
   f32x16 a0, a1, b0, b1;
   dma::qk<HD>(sm.k[0], lo, qf, q4, a0, a1);
-  {  // the running max starts at zero or at tile 0's (keys past L masked)
+  {  // the running max starts at zero or at tile 0's (keys past L masked);
+     // tile 0's scores are settled like every other tile's
     const float m0 = tile_max<true>(a0, a1, g, 0, L);
-    if constexpr (HD == 64) {  // tile 0's scores are settled like every other tile's
-      shifted = __ballot(!(m0 >= -64.0f && m0 <= 32.0f)) != 0;
-      m_run = shifted ? m0 : 0.0f;
-    } else {
-      m_run = m0;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        a0[r] -= m_run;
-        a1[r] -= m_run;
-      }
-    }
+    shifted = __ballot(!(m0 >= -64.0f && m0 <= 32.0f)) != 0;
+    m_run = shifted ? m0 : 0.0f;
   }
   // iteration 0 copies K(3) into slot 0: every wave must be done reading K(0)
   // (and, at head_dim 72, K(1) must have landed)
