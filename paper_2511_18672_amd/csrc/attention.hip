@@ -308,7 +308,6 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
 #pragma unroll
   for (int e = 0; e < 2; ++e) ex[0][e] = fast_exp2(score(0, e));
   __builtin_amdgcn_sched_barrier(0);
-  const bf16x2 ones2 = {(bf16)1.0f, (bf16)1.0f};
   float psum = 0.0f;
   const f32x16 zero16 = {};
 #pragma unroll
@@ -341,10 +340,7 @@ __device__ __forceinline__ void region(const char* sK, const char* sV, const Lan
       bf16x2 pr;
       pr[0] = (bf16)ex[st][0];
       pr[1] = (bf16)ex[st][1];
-      if constexpr (HD == 64)
-        psum = rowsum_add(psum, pr);
-      else  // head_dim 72: fencing them costs registers that the copy offsets need
-        psum = __builtin_amdgcn_fdot2_f32_bf16(pr, ones2, psum, false);
+      psum = rowsum_add(psum, pr);
       pn[w][hf][2 * i] = pr[0];
       pn[w][hf][2 * i + 1] = pr[1];
     }
