@@ -106,55 +106,68 @@ __global__ __launch_bounds__(kTPB) void k_select_count(ReqTable T, int64_t N, co
   }
 }
 
-// Exclusive scan of nblk chunk counts by one workgroup of 1024 threads, in
-// blocks of kScanBlk counts staged in LDS: coalesced loads and stores, and
-// each thread scans 16 consecutive counts from LDS (a strided walk through
-// global memory would serialise 16 load latencies per thread).
-constexpr int kScanBlk = 16384;
+// Exclusive scan of nblk chunk counts by one workgroup of 1024 threads,
+// 16384 counts per pass: thread i owns counts 16 i .. 16 i + 15 of the pass
+// and moves them with four 16-byte loads and stores (both arrays are 16-byte
+// aligned), so no count is staged in LDS; a wave64 scan of the per-thread
+// sums and the 16 wave totals (read by every lane of a wave at one address)
+// give each thread its base.
+constexpr int kScanPer = 16;
+constexpr int kScanBlk = 1024 * kScanPer;
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(1024) void k_select_scan(const int32_t* __restrict__ blk_cnt, int nblk,
                                                      int32_t* __restrict__ blk_off, int32_t* __restrict__ cu_sel,
                                                      int R) {
-  __shared__ int32_t s_v[kScanBlk];
   __shared__ int s_part[1024 / kWave];
   const int tid = (int)threadIdx.x, lane = lane_id(), wave = tid / kWave;
-  constexpr int per = kScanBlk / 1024;  // 16 consecutive counts per thread
-  int carry = 0;                        // counts of the blocks before this one
+  int carry = 0;  // counts of the passes before this one
   for (int base = 0; base < nblk; base += kScanBlk) {
-    const int m = min(kScanBlk, nblk - base);
-    {  // all 16 loads issued before the first LDS store
-      int v[per];
+    const int i0 = base + tid * kScanPer;
+    const bool full = i0 + kScanPer <= nblk;
+    int v[kScanPer];
+    if (full) {
 #pragma unroll
-      for (int k = 0; k < per; ++k) v[k] = (tid + 1024 * k < m) ? blk_cnt[base + tid + 1024 * k] : 0;
+      for (int q = 0; q < kScanPer / 4; ++q) {
+        const i32x4 x = reinterpret_cast<const i32x4*>(blk_cnt + i0)[q];
+        v[4 * q] = x[0];
+        v[4 * q + 1] = x[1];
+        v[4 * q + 2] = x[2];
+        v[4 * q + 3] = x[3];
+      }
+    } else {
 #pragma unroll
-      for (int k = 0; k < per; ++k) s_v[tid + 1024 * k] = v[k];
+      for (int j = 0; j < kScanPer; ++j) v[j] = (i0 + j < nblk) ? blk_cnt[i0 + j] : 0;
     }
-    __syncthreads();
     int local = 0;
 #pragma unroll
-    for (int j = 0; j < per; ++j)
-      if (tid * per + j < m) local += s_v[tid * per + j];
+    for (int j = 0; j < kScanPer; ++j) local += v[j];
     const int incl = wave_incl_scan(local, lane);
     if (lane == kWave - 1) s_part[wave] = incl;
     __syncthreads();
     int wave_base = 0, total = 0;
     for (int w = 0; w < 1024 / kWave; ++w) {
-      if (w < wave) wave_base += s_part[w];
-      total += s_part[w];
+      const int p = s_part[w];
+      if (w < wave) wave_base += p;
+      total += p;
     }
     int run = carry + wave_base + incl - local;
 #pragma unroll
-    for (int j = 0; j < per; ++j)
-      if (tid * per + j < m) {
-        const int v = s_v[tid * per + j];
-        s_v[tid * per + j] = run;
-        run += v;
-      }
-    __syncthreads();
+    for (int j = 0; j < kScanPer; ++j) {
+      const int c = v[j];
+      v[j] = run;
+      run += c;
+    }
+    if (full) {
 #pragma unroll
-    for (int k = 0; k < per; ++k)
-      if (tid + 1024 * k < m) blk_off[base + tid + 1024 * k] = s_v[tid + 1024 * k];
+      for (int q = 0; q < kScanPer / 4; ++q)
+        reinterpret_cast<i32x4*>(blk_off + i0)[q] = i32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+    } else {
+#pragma unroll
+      for (int j = 0; j < kScanPer; ++j)
+        if (i0 + j < nblk) blk_off[i0 + j] = v[j];
+    }
     carry += total;
-    __syncthreads();  // s_v and s_part are reused by the next block
+    __syncthreads();  // s_part is rewritten by the next pass
   }
   if (tid == 0) cu_sel[R] = carry;
 }
@@ -217,6 +230,7 @@ constexpr int64_t kStaticChunks = (int64_t)1 << 16;
 static __device__ __align__(256) int32_t scratch[2 * kStaticChunks];
 
 static_assert(kStaticChunks * kChunk == SPHINX_SELECT_STATIC_MAX_TOKENS, "the header states the static limit");
+static_assert(kStaticChunks % 4 == 0, "the offsets start at a multiple of 4 entries");
 
 int64_t select_static_max_tokens() { return kStaticChunks * kChunk; }
 
@@ -239,6 +253,8 @@ hipError_t select_static_ws(void** ptr) {
   return hipSuccess;
 }
 
+// Chunk counts, then their offsets from the next multiple of 4 entries on
+// (at most 12 bytes of the 256 spare).
 size_t select_ws_bytes(int64_t N) {
   const int64_t nblk = (N + kChunk - 1) / kChunk;
   return (size_t)(2 * nblk * sizeof(int32_t) + 256);
@@ -248,7 +264,7 @@ hipError_t launch_select(const ReqTable& T, int64_t N, const float* u, const flo
                          uint8_t* mask, int32_t* idx, int32_t* cu_sel, void* ws, hipStream_t s) {
   const int nblk = (int)((N + kChunk - 1) / kChunk);
   int32_t* blk_cnt = reinterpret_cast<int32_t*>(ws);
-  int32_t* blk_off = blk_cnt + nblk;
+  int32_t* blk_off = blk_cnt + ((nblk + 3) & ~3);  // 16-byte aligned, like blk_cnt
   k_select_count<<<nblk, kTPB, 0, s>>>(T, N, u, thr, active, mask, blk_cnt);
   k_select_scan<<<1, 1024, 0, s>>>(blk_cnt, nblk, blk_off, cu_sel, T.R);
   k_select_write<<<nblk, kTPB, 0, s>>>(T, N, mask, blk_off, idx, cu_sel);
