@@ -2,8 +2,10 @@
 //  * k_embed   h = x W_pe^T + b_pe + [Ty(y) || Tx(x)] + Tf(f)          (fp32)
 //  * k_ln_mod  a = LN(h) * (1 + scale[row]) + shift[row]  -> bf16/fp32  (one wave per row, or per two rows)
 //  * k_final   eps_hat = (LN(h) (1 + scale) + shift) W_out^T + b_out, then the
-//              DDIM update x <- c1 x + c2 eps_hat in place (one wave per row;
-//              the 16 outputs are reduced with a butterfly reduce-scatter).
+//              DDIM update x <- c1 x + c2 eps_hat in place.  bf16 weights at
+//              D = 128, 512, 1024, 1152: k_final_mfma, 16 rows per workgroup on the matrix
+//              cores; otherwise one wave per row, the 16 outputs reduced with a
+//              butterfly reduce-scatter.
 // LayerNorm: biased variance, eps 1e-6, no affine; statistics in fp32 from the
 // row held in registers (two passes over registers, one read of HBM).
 #include <algorithm>
@@ -366,6 +368,132 @@ __global__ __launch_bounds__(kTPB) void k_final(const float* __restrict__ h, int
     if ((lane & 3) == 0) *xp = fmaf(c2g, e + bout, c1g * xold);
   }
 }
+
+// k_final on the matrix cores (bf16 weights, D = 128 KPW): the output
+// projection is a GEMM with 16 columns, so a workgroup takes 16 rows and
+// v_mfma_f32_16x16x32_bf16 does the 16 x D x 16 product.  Wave w owns the
+// D/4 columns [32 KPW w, 32 KPW (w+1)); lane l holds row r = l % 16 at columns
+// 32 (KPW w + kb) + 8 (l / 16) + 0..7, which is the A-operand layout of the
+// MFMA (and its B operand, the weights of output r at the same columns, is 16
+// contiguous bytes of out_w).
+//  * LayerNorm statistics: each wave's mean and squared deviations over its
+//    columns (the four lanes of a row reduced with two shuffles), combined
+//    across the waves through LDS as equal-size groups (Chan et al.).
+//  * The modulated value a is fp32; it enters the MFMA as a_hi = bf16(a) and
+//    a_lo = bf16(a - a_hi), two MFMAs per 32 columns, so the products keep
+//    about 17 significant bits of a (bf16 x bf16 products are exact in fp32
+//    and the MFMA accumulates in fp32).
+//  * Rows, weights and modulation are loaded up front (PF of the KPW column
+//    blocks' modulation; the rest one block at a time, PF blocks ahead), so a
+//    workgroup waits on memory about once.
+//  * The four waves' 16 x 16 partial sums meet in LDS; thread t finishes row
+//    t / 16, output t % 16 with the bias and the DDIM update.
+// Modulation blocks loaded ahead at D = 1024 and 1152: 3 (162 and 176 VGPRs)
+// measured 17.0 and 19.6 us at 9677 and 10194 rows, all of them up front (238
+// and 256 VGPRs, fewer waves per SIMD) 17.9 and 24.6 us.
+constexpr int kFinalAhead = 3;
+
+template <int KPW, int PF>
+__global__ __launch_bounds__(kTPB) void k_final_mfma(const float* __restrict__ h, int n, int D,
+                                                     const float* __restrict__ mod, int ldm, int sh_off, int sc_off,
+                                                     const int32_t* __restrict__ crow,
+                                                     const int32_t* __restrict__ gframe, const bf16* __restrict__ out_w,
+                                                     const bf16* __restrict__ out_b, const float* __restrict__ c1,
+                                                     const float* __restrict__ c2, float* __restrict__ x) {
+  static_assert(PF >= 1 && PF <= KPW, "modulation blocks loaded ahead");
+  constexpr int WCOLS = 32 * KPW;  // columns per wave
+  __shared__ float s_stat[4][16][2];
+  __shared__ float s_acc[4][16][17];
+  const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int row0 = (int)blockIdx.x * 16;
+  const int row = min(row0 + r, n - 1);  // rows past n repeat row n - 1 and are not stored
+  const int cb = WCOLS * wave + 8 * g;   // the lane's column at kb = 0
+  const float* hr = h + (int64_t)row * D + cb;
+  const float* m = mod + (int64_t)crow[row] * ldm + cb;
+  const bf16* wr = out_w + (int64_t)r * D + cb;
+  f32x4 hv[KPW][2], sc[KPW][2], sh[KPW][2];
+  bf16x8 wv[KPW];
+#pragma unroll
+  for (int kb = 0; kb < KPW; ++kb) {
+    hv[kb][0] = *reinterpret_cast<const f32x4*>(hr + 32 * kb);
+    hv[kb][1] = *reinterpret_cast<const f32x4*>(hr + 32 * kb + 4);
+  }
+#pragma unroll
+  for (int kb = 0; kb < KPW; ++kb) wv[kb] = *reinterpret_cast<const bf16x8*>(wr + 32 * kb);
+  auto load_mod = [&](int kb) {
+    sc[kb][0] = *reinterpret_cast<const f32x4*>(m + sc_off + 32 * kb);
+    sc[kb][1] = *reinterpret_cast<const f32x4*>(m + sc_off + 32 * kb + 4);
+    sh[kb][0] = *reinterpret_cast<const f32x4*>(m + sh_off + 32 * kb);
+    sh[kb][1] = *reinterpret_cast<const f32x4*>(m + sh_off + 32 * kb + 4);
+  };
+#pragma unroll
+  for (int kb = 0; kb < PF; ++kb) load_mod(kb);
+  // statistics of the wave's columns of the row, then of the whole row
+  float s = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < KPW; ++kb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s += hv[kb][0][e] + hv[kb][1][e];
+  s += __shfl_xor(s, 16, kWave);
+  s += __shfl_xor(s, 32, kWave);
+  const float mw = s / (float)WCOLS;
+  float q = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < KPW; ++kb)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float d0 = hv[kb][0][e] - mw, d1 = hv[kb][1][e] - mw;
+      q = fmaf(d0, d0, q);
+      q = fmaf(d1, d1, q);
+    }
+  q += __shfl_xor(q, 16, kWave);
+  q += __shfl_xor(q, 32, kWave);
+  if (g == 0) {
+    s_stat[wave][r][0] = mw;
+    s_stat[wave][r][1] = q;
+  }
+  __syncthreads();
+  float mu = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) mu += s_stat[w][r][0];
+  mu *= 0.25f;
+  float m2 = 0.f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float d = s_stat[w][r][0] - mu;
+    m2 += fmaf((float)WCOLS * d, d, s_stat[w][r][1]);
+  }
+  const float rstd = rsqrtf(m2 / (float)D + 1e-6f);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < KPW; ++kb) {
+    if (kb + PF < KPW) load_mod(kb + PF);
+    bf16x8 ahi, alo;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int hf = e >> 2, i = e & 3;
+      const float a = fmaf((hv[kb][hf][i] - mu) * rstd, 1.0f + sc[kb][hf][i], sh[kb][hf][i]);
+      const bf16 hi = (bf16)a;
+      ahi[e] = hi;
+      alo[e] = (bf16)(a - (float)hi);
+    }
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, wv[kb], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, wv[kb], acc, 0, 0, 0);
+  }
+  // lane l holds rows 4 (l / 16) + i, output l % 16 of the wave's partial sum
+#pragma unroll
+  for (int i = 0; i < 4; ++i) s_acc[wave][4 * g + i][r] = acc[i];
+  __syncthreads();
+  const int orow = tid >> 4, on = tid & 15;
+  const int grow = row0 + orow;
+  if (grow < n) {
+    const float e = (s_acc[0][orow][on] + s_acc[1][orow][on]) + (s_acc[2][orow][on] + s_acc[3][orow][on]);
+    const int gf = gframe[grow];
+    float* xp = x + (int64_t)grow * 16 + on;
+    *xp = fmaf(c2[gf], e + (float)out_b[on], c1[gf] * *xp);
+  }
+}
 }  // namespace
 
 hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const void* pe_b, sphinx_dtype wdt,
@@ -420,6 +548,29 @@ hipError_t launch_ln_mod(const float* h, int n, int D, const float* mod, int ldm
 hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm, int sh_off, int sc_off,
                         const int32_t* crow, const int32_t* gframe, const void* out_w, const void* out_b,
                         sphinx_dtype wdt, const float* c1, const float* c2, float* x, hipStream_t s) {
+  // bf16 weights at D = 128 KPW (KPW 1, 4, 8, 9: the widths the tests cover) with 16-byte aligned
+  // modulation rows: the matrix-core kernel, one workgroup per 16 rows
+  const bool mod4 = (ldm % 4 == 0) && (sh_off % 4 == 0) && (sc_off % 4 == 0);
+  if (wdt == SPHINX_BF16 && mod4 && D % 128 == 0) {
+    const unsigned gb = (unsigned)((n + 15) / 16);
+    const bf16 *w = (const bf16*)out_w, *b = (const bf16*)out_b;
+    switch (D / 128) {
+      case 1:
+        k_final_mfma<1, 1><<<gb, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, w, b, c1, c2, x);
+        return hipGetLastError();
+      case 4:
+        k_final_mfma<4, 4><<<gb, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, w, b, c1, c2, x);
+        return hipGetLastError();
+      case 8:
+        k_final_mfma<8, kFinalAhead><<<gb, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, w, b, c1, c2, x);
+        return hipGetLastError();
+      case 9:
+        k_final_mfma<9, kFinalAhead><<<gb, kTPB, 0, s>>>(h, n, D, mod, ldm, sh_off, sc_off, crow, gframe, w, b, c1, c2, x);
+        return hipGetLastError();
+      default:
+        break;
+    }
+  }
   // Grid-stride over rows: as many workgroups as fit on the device at once
   // (each fills its LDS weight table once), so that all of them run in one
   // round.  (A fixed 1024 left a quarter of them for a second round at three
