@@ -1,5 +1,6 @@
 // Row-wise kernels of the denoiser:
-//  * k_embed   h = x W_pe^T + b_pe + [Ty(y) || Tx(x)] + Tf(f)          (fp32)
+//  * k_embed   h = x W_pe^T + b_pe + [Ty(y) || Tx(x)] + Tf(f)          (fp32;
+//              k_embed_mfma on the matrix cores for bf16 weights at D = 128 k)
 //  * k_ln_mod  a = LN(h) * (1 + scale[row]) + shift[row]  -> bf16/fp32  (one wave per row, or per two rows)
 //  * k_final   eps_hat = (LN(h) (1 + scale) + shift) W_out^T + b_out, then the
 //              DDIM update x <- c1 x + c2 eps_hat in place.  bf16 weights at
@@ -81,7 +82,7 @@ __device__ __forceinline__ void load16_at(const unsigned char* tab, const int (&
 }
 
 // One thread per four consecutive columns and a block of kEmbedRows rows,
-// grid (column blocks, row blocks): the thread's 4 x 16 weights stay in
+// grid (row blocks, column blocks): the thread's 4 x 16 weights stay in
 // registers across the rows (the weight matrix is read once per row block,
 // not once per row); per row 16-byte loads of the position tables and one
 // 16-byte store of h (x and the packed position are wave-uniform).
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int
                                                 const float* __restrict__ Tx, const float* __restrict__ Tf,
                                                 const int32_t* __restrict__ posc, float* __restrict__ h) {
   const int quads = D >> 2;
-  const int qd = (int)blockIdx.x * kTPB + (int)threadIdx.x;
+  const int qd = (int)blockIdx.y * kTPB + (int)threadIdx.x;
   if (qd >= quads) return;
   const int c0 = 4 * qd;
   float w[4][16], b[4];
@@ -103,7 +104,7 @@ __global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int
     b[e] = load_as_f32(pe_b, c0 + e);
   }
   const int half = D / 2;
-  const int j0 = (int)blockIdx.y * kEmbedRows, j1 = min(j0 + kEmbedRows, n);
+  const int j0 = (int)blockIdx.x * kEmbedRows, j1 = min(j0 + kEmbedRows, n);
 #pragma unroll 2
   for (int j = j0; j < j1; ++j) {
     const int pc = posc[j];
@@ -129,6 +130,63 @@ __global__ __launch_bounds__(kTPB) void k_embed(const float* __restrict__ x, int
       out[e] = v + pos[e] + tf[e];
     }
     *reinterpret_cast<f32x4*>(h + (int64_t)j * D + c0) = out;
+  }
+}
+
+// k_embed on the matrix cores (bf16 weights, D a multiple of 128).  The patch
+// embedding is a GEMM with a 16-deep contraction: a wave computes a 32 x 32
+// tile of h with v_mfma_f32_32x32x16_bf16 (K = 16, one MFMA per operand) on a
+// hi/lo bf16 split of the fp32 latents, x = bf16(x) + bf16(x - bf16(x)), two
+// MFMAs (bf16 products are exact in fp32, accumulation is fp32).  Lane l holds
+// latent row l % 32, values 8 (l / 32) .. + 7 (the A layout) and column
+// c0 + l % 32's weights at the same 8 positions (the B layout: 16 contiguous
+// bytes of W_pe); the result gives lane l column c0 + l % 32 of rows
+// 8 (i / 4) + 4 (l / 32) + i % 4, i < 16, to which it adds the bias and the
+// position tables.  The 32 columns of a wave lie on one side of D / 2 (D is a
+// multiple of 128), so the y or x table is a wave-uniform choice.  Workgroup:
+// 32 rows x 128 columns, four waves side by side.
+__global__ __launch_bounds__(kTPB) void k_embed_mfma(const float* __restrict__ x, int n, int D,
+                                                     const bf16* __restrict__ pe_w, const bf16* __restrict__ pe_b,
+                                                     const float* __restrict__ Ty, const float* __restrict__ Tx,
+                                                     const float* __restrict__ Tf, const int32_t* __restrict__ posc,
+                                                     float* __restrict__ h) {
+  const int lane = (int)threadIdx.x & 63, wave = (int)threadIdx.x >> 6;
+  const int l32 = lane & 31, g = lane >> 5;
+  const int row0 = (int)blockIdx.x * 32;
+  const int c = (int)blockIdx.y * 128 + wave * 32 + l32;
+  const float* xr = x + (int64_t)min(row0 + l32, n - 1) * 16 + 8 * g;  // rows past n repeat row n - 1
+  const f32x4 x0 = reinterpret_cast<const f32x4*>(xr)[0], x1 = reinterpret_cast<const f32x4*>(xr)[1];
+  const bf16x8 wv = *reinterpret_cast<const bf16x8*>(pe_w + (int64_t)c * 16 + 8 * g);
+  bf16x8 xhi, xlo;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float v = e < 4 ? x0[e] : x1[e - 4];
+    const bf16 hi = (bf16)v;
+    xhi[e] = hi;
+    xlo[e] = (bf16)(v - (float)hi);
+  }
+  f32x16 acc = {};
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xhi, wv, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xlo, wv, acc, 0, 0, 0);
+  const float bc = (float)pe_b[c];
+  const int half = D >> 1;
+  const bool left = c < half;
+  const float* tp = left ? Ty + c : Tx + (c - half);
+  // every row's position and table loads first, then the sums and stores
+  int pc[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) pc[i] = posc[min(row0 + 8 * (i >> 2) + 4 * g + (i & 3), n - 1)];
+  float pos[16], tf[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int f = pc[i] >> 20, y = (pc[i] >> 10) & 1023, xx = pc[i] & 1023;
+    pos[i] = tp[(int64_t)(left ? y : xx) * half];
+    tf[i] = Tf[(int64_t)f * D + c];
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int row = row0 + 8 * (i >> 2) + 4 * g + (i & 3);
+    if (row < n) h[(int64_t)row * D + c] = ((acc[i] + bc) + pos[i]) + tf[i];
   }
 }
 
@@ -499,7 +557,12 @@ __global__ __launch_bounds__(kTPB) void k_final_mfma(const float* __restrict__ h
 hipError_t launch_embed(const float* x, int n, int D, const void* pe_w, const void* pe_b, sphinx_dtype wdt,
                         const float* Ty, const float* Tx, const float* Tf, const int32_t* posc, float* h,
                         hipStream_t s) {
-  const dim3 g((unsigned)((D / 4 + kTPB - 1) / kTPB), (unsigned)((n + kEmbedRows - 1) / kEmbedRows));
+  if (wdt == SPHINX_BF16 && D % 128 == 0) {  // matrix cores: 32 rows x 128 columns per workgroup
+    const dim3 gm((unsigned)((n + 31) / 32), (unsigned)(D / 128));  // rows in x: no 65535 limit
+    k_embed_mfma<<<gm, kTPB, 0, s>>>(x, n, D, (const bf16*)pe_w, (const bf16*)pe_b, Ty, Tx, Tf, posc, h);
+    return hipGetLastError();
+  }
+  const dim3 g((unsigned)((n + kEmbedRows - 1) / kEmbedRows), (unsigned)((D / 4 + kTPB - 1) / kTPB));
   if (wdt == SPHINX_BF16)
     k_embed<bf16><<<g, kTPB, 0, s>>>(x, n, D, (const bf16*)pe_w, (const bf16*)pe_b, Ty, Tx, Tf, posc, h);
   else
