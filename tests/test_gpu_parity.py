@@ -424,6 +424,20 @@ def test_ragged_d72_tile_edges():
     assert worst <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("width", ["d128", "d1152_h72"])
+@pytest.mark.parametrize("n", [1, 3, 17, 33])
+def test_few_selected_tokens(width, n):
+    """Selections smaller than one row block of the matrix-core embedding (32
+    rows) and final projection (16 rows): 1, 3, 17 and 33 tokens, at D 128 and
+    at D 1152 with heads of 72, end to end and teacher-forced per step."""
+    model = MID_BF16 if width == "d128" else MID72
+    req = W.Request(1, 8, 8) if n < 16 else W.Request(1, 16, 16)
+    tokens = (req.h // 2) * (req.w // 2) * req.frames
+    wl = W.custom(f"few{n}_{width}", model, [req], [n / tokens], [0.5], [2])
+    R = check_end_to_end(wl)
+    assert R.n_sel == n
+
+
 def test_frame_region_full_shape_one_block_step():
     """Frame+region at its full shape (21 x 64x64 latent) with a one-block
     head_dim-72 denoiser, at the first step with every frame active, from the
