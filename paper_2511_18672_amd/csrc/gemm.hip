@@ -104,8 +104,10 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
 
   // copy sources: instruction i of this wave fills rows 8q .. 8q+7 of the
   // stage (q = wave * COPIES + i; rows < BM are A rows, the rest W rows)
+  // (the operand, A or W, is wave-uniform: a scalar base; the lane's byte
+  // offset from it is fixed, so moving to the next K step is scalar arithmetic)
   const bf16* src[C::COPIES];
-  int soff[C::COPIES];
+  uint32_t voff[C::COPIES];
 #pragma unroll
   for (int i = 0; i < C::COPIES; ++i) {
     const int q = wave * C::COPIES + i;
@@ -113,17 +115,17 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     const int c = (lane & 7) ^ ((row >> 1) & 7);
     if (8 * q < BM) {
       src[i] = A;
-      soff[i] = min(m0 + row, M - 1) * K + c * 8;
+      voff[i] = 2u * (uint32_t)(min(m0 + row, M - 1) * K + c * 8);
     } else {
       src[i] = W;
-      soff[i] = (n0 + row - BM) * K + c * 8;
+      voff[i] = 2u * (uint32_t)((n0 + row - BM) * K + c * 8);
     }
   }
   auto copy_stage = [&](int kt, int slot) {
     unsigned char* base = smem + slot * C::STAGE;
 #pragma unroll
     for (int i = 0; i < C::COPIES; ++i)
-      lds_dma16(src[i] + soff[i] + kt * C::BK, base + (wave * C::COPIES + i) * 1024);
+      lds_dma16_at(src[i] + kt * C::BK, voff[i], base + (wave * C::COPIES + i) * 1024);
   };
   // fragment offsets inside a stage (k-step ks of 16)
   int foff[4];
