@@ -139,33 +139,23 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
 #pragma unroll
     for (int j = 0; j < C::TJ; ++j) acc[i][j] = f32x16{};
 
-  const int KT = K / C::BK;
-  static_assert(NS == 2 || NS == 3, "ring of 2 or 3 stages");
-  // Stage j lives in slot j % NS.  The wait for stage kt+1 and the barrier sit
+  const int KT = K / C::BK;  // even (K is a multiple of 128)
+  static_assert(NS == 2, "ring of 2 stages");
+  // Stage j lives in slot j % 2.  The wait for stage kt+1 and the barrier sit
   // inside the last k-step of tile kt: after it every wave has read all of
-  // stage kt (so its slot can be refilled with stage kt+NS) and stage kt+1 has
+  // stage kt (so its slot can be refilled with stage kt+2) and stage kt+1 has
   // landed (so its first fragments can be read while the last MFMAs of tile
-  // kt run).  With 3 slots the copies of stage kt+2 may stay in flight.
-  auto sync_stage = [&](int next) {  // next = the stage that must have landed
-    if (NS == 3 && next + 1 < KT)
-      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(C::COPIES));
-    else
-      __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+  // kt run).
+  auto sync_stage = [&]() {
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
-#pragma unroll
-  for (int s = 0; s < NS; ++s)
-    if (s < KT) copy_stage(s, s);
-  // the first min(NS, KT) stages are issued; stage 0 must land before the
-  // first reads, the later ones may stay in flight
-  if (NS == 3 && KT > 2)
-    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(2 * C::COPIES));
-  else if (KT > 1)
-    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(C::COPIES));
-  else
-    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+  copy_stage(0, 0);
+  copy_stage(1, 1);
+  // stage 0 must land before the first reads; stage 1 may stay in flight
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(C::COPIES));
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
@@ -179,17 +169,17 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     for (int j = 0; j < C::TJ; ++j)
       fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + (b_row0 + 32 * j) * 128 + foff[ks]);
   };
-  int slot = 0;
-  read(smem, 0, 0);
-  for (int kt = 0; kt < KT; ++kt) {
+  // One K step in ring slot SLOT (a compile-time constant, so that every
+  // fragment address is a loop-invariant base plus an immediate offset).
+  auto step = [&](int kt, auto SLOT) {
+    constexpr int slot = decltype(SLOT)::value, nslot = slot + 1 == NS ? 0 : slot + 1;
     const unsigned char* st = smem + slot * C::STAGE;
-    const int nslot = slot + 1 == NS ? 0 : slot + 1;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       if (ks < 3) {
         read(st, ks + 1, ks + 1);
       } else if (kt + 1 < KT) {
-        sync_stage(kt + 1);
+        sync_stage();
         if (kt + NS < KT) copy_stage(kt + NS, slot);
         read(smem + nslot * C::STAGE, 0, 0);
       }
@@ -202,7 +192,12 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
-    slot = nslot;
+  };
+  read(smem, 0, 0);
+  // K is a multiple of 128 (launch_gemm checks it), so KT is even
+  for (int kt = 0; kt < KT; kt += 2) {
+    step(kt, std::integral_constant<int, 0>{});
+    step(kt + 1, std::integral_constant<int, 1>{});
   }
   __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
   asm volatile("" ::: "memory");
@@ -477,6 +472,7 @@ double tile_rounds(int64_t tiles, int64_t slots, double w) {
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
                        const GemmEpi& e, hipStream_t s) {
   if (dt == SPHINX_BF16) {
+    if (K % 128 != 0 || N % 128 != 0) return hipErrorInvalidValue;  // the kernels' K loop takes two 64-deep steps at a time
     const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
     {
       const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
