@@ -133,11 +133,17 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   for (int ks = 0; ks < 4; ++ks) foff[ks] = r32 * 128 + (((2 * ks + g) ^ ((r32 >> 1) & 7)) << 4);
   const int a_row0 = wm * C::WM, b_row0 = BM + wn * C::WN;
 
+  // the accumulators start at the bias of their column (lane column
+  // wn WN + 32 j + r32 of the tile), so the epilogue adds no bias
   f32x16 acc[C::TI][C::TJ];
 #pragma unroll
-  for (int i = 0; i < C::TI; ++i)
+  for (int j = 0; j < C::TJ; ++j) {
+    const float bj = (float)bias[n0 + wn * C::WN + j * 32 + r32];
 #pragma unroll
-    for (int j = 0; j < C::TJ; ++j) acc[i][j] = f32x16{};
+    for (int i = 0; i < C::TI; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = bj;
+  }
 
   const int KT = K / C::BK;  // even (K is a multiple of 128)
   static_assert(NS == 2, "ring of 2 stages");
@@ -205,93 +211,106 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   asm volatile("" ::: "memory");
 
   // epilogue: fp32 tile staged in LDS (whole, or one wave row's half at a
-  // time), then 16-byte row-contiguous I/O
+  // time), then 16-byte row-contiguous I/O.  Outputs and the residual are
+  // addressed as a wave-uniform tile base plus the thread's 32-bit byte offset
+  // (at most EROWS rows of ldo elements), which grows by a fixed stride per
+  // pass; tiles wholly inside M skip the per-row checks, and the query scale
+  // is a tile-uniform branch.
   float* sC = reinterpret_cast<float*>(smem);
   constexpr int TPR = BN / 4;          // threads per row (one float4 each)
   constexpr int RPP = 256 / TPR;       // rows per pass
+  constexpr int NP = C::EROWS / RPP;   // row passes per staged half
+  constexpr int OSZ = EPI == EPI_GATED ? 4 : 2;  // output bytes: fp32 residual or bf16 activation
   const int c4 = (tid % TPR) * 4, rsub = tid / TPR;
-  const int n = n0 + c4;
-  float4 bv;
-  {
-    const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n);
-    bv = make_float4((float)b4[0], (float)b4[1], (float)b4[2], (float)b4[3]);
-  }
-  constexpr int NP = C::EROWS / RPP;  // row passes per staged half
+  const uint32_t off0 = (uint32_t)(rsub * e.ldo + c4) * OSZ, ostep = (uint32_t)(RPP * e.ldo) * OSZ;
+  auto epilogue = [&](auto FULL, auto QT) {
+    constexpr bool kFull = decltype(FULL)::value, kQ = decltype(QT)::value;
 #pragma unroll
-  for (int h = 0; h < EH; ++h) {
-    // gated residual: every pass's residual and gate loads are issued before
-    // the staging (rows past M read row M - 1 and are not stored), so their
-    // latencies overlap instead of following one another pass by pass
-    float4 hres[EPI == EPI_GATED ? NP : 1], gres[EPI == EPI_GATED ? NP : 1];
-    if constexpr (EPI == EPI_GATED) {
-      int cr[NP];
+    for (int h = 0; h < EH; ++h) {
+      const int mh = m0 + h * C::EROWS;  // first row of this half
+      char* obase = reinterpret_cast<char*>(e.out) + ((int64_t)mh * e.ldo + n0) * OSZ;
+      // gated residual: every pass's residual and gate loads are issued before
+      // the staging (rows past M read row M - 1 and are not stored), so their
+      // latencies overlap instead of following one another pass by pass
+      float4 hres[EPI == EPI_GATED ? NP : 1], gres[EPI == EPI_GATED ? NP : 1];
+      if constexpr (EPI == EPI_GATED) {
+        int cr[NP];
 #pragma unroll
-      for (int p = 0; p < NP; ++p) cr[p] = e.crow[min(m0 + h * C::EROWS + p * RPP + rsub, M - 1)];
+        for (int p = 0; p < NP; ++p) {
+          const int m = mh + p * RPP + rsub;
+          cr[p] = e.crow[kFull ? m : min(m, M - 1)];
+        }
 #pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        const int mc = min(m0 + h * C::EROWS + p * RPP + rsub, M - 1);
-        hres[p] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(e.out) + (int64_t)mc * e.ldo + n);
-        gres[p] = *reinterpret_cast<const float4*>(e.gate + (int64_t)cr[p] * e.ldg + n);
-      }
-    }
-    if (EH == 1 || wm == h) {
-      const int r0 = a_row0 - h * C::EROWS;
-#pragma unroll
-      for (int i = 0; i < C::TI; ++i)
-#pragma unroll
-        for (int j = 0; j < C::TJ; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            sC[(r0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
-    }
-    __syncthreads();
-    if constexpr (EPI == EPI_GATED) {
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        const int row = p * RPP + rsub;
-        const int m = m0 + h * C::EROWS + row;
-        float4 v = *reinterpret_cast<const float4*>(&sC[row * C::CLD + c4]);
-        const float4 gv = gres[p];
-        float4 hv = hres[p];
-        hv.x = fmaf(1.0f + gv.x, v.x + bv.x, hv.x);
-        hv.y = fmaf(1.0f + gv.y, v.y + bv.y, hv.y);
-        hv.z = fmaf(1.0f + gv.z, v.z + bv.z, hv.z);
-        hv.w = fmaf(1.0f + gv.w, v.w + bv.w, hv.w);
-        if (m < M) *reinterpret_cast<float4*>(reinterpret_cast<float*>(e.out) + (int64_t)m * e.ldo + n) = hv;
-      }
-    }
-#pragma unroll 4
-    for (int p = 0; p < (EPI == EPI_GATED ? 0 : NP); ++p) {
-      const int row = p * RPP + rsub;
-      const int m = m0 + h * C::EROWS + row;
-      if (m >= M) continue;
-      float4 v = *reinterpret_cast<const float4*>(&sC[row * C::CLD + c4]);
-      v.x += bv.x;
-      v.y += bv.y;
-      v.z += bv.z;
-      v.w += bv.w;
-      if constexpr (EPI == EPI_GELU) {
-        v.x = gelu_tanh(v.x);
-        v.y = gelu_tanh(v.y);
-        v.z = gelu_tanh(v.z);
-        v.w = gelu_tanh(v.w);
-      }
-      if constexpr (EPI == EPI_BIAS) {
-        if (n < e.qcols) {  // four columns of one thread are all queries or all not (qcols % 4 == 0)
-          v.x *= e.qscale;
-          v.y *= e.qscale;
-          v.z *= e.qscale;
-          v.w *= e.qscale;
+        for (int p = 0; p < NP; ++p) {
+          // in a tile that crosses M the clamped row may lie before this half
+          // (a whole half past M reads row M - 1): address it absolutely there
+          if constexpr (kFull)
+            hres[p] = *reinterpret_cast<const float4*>(obase + off0 + p * ostep);
+          else
+            hres[p] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(e.out) +
+                                                       (int64_t)min(mh + p * RPP + rsub, M - 1) * e.ldo + n0 + c4);
+          gres[p] = *reinterpret_cast<const float4*>(e.gate + (int64_t)cr[p] * e.ldg + n0 + c4);
         }
       }
-      bf16x4 o;
-      o[0] = (bf16)v.x;
-      o[1] = (bf16)v.y;
-      o[2] = (bf16)v.z;
-      o[3] = (bf16)v.w;
-      *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(e.out) + (int64_t)m * e.ldo + n) = o;
+      if (EH == 1 || wm == h) {
+        const int r0 = a_row0 - h * C::EROWS;
+#pragma unroll
+        for (int i = 0; i < C::TI; ++i)
+#pragma unroll
+          for (int j = 0; j < C::TJ; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              sC[(r0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
+      }
+      __syncthreads();
+      if constexpr (EPI == EPI_GATED) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const float4 v = *reinterpret_cast<const float4*>(&sC[(p * RPP + rsub) * C::CLD + c4]);
+          const float4 gv = gres[p];
+          float4 hv = hres[p];
+          hv.x = fmaf(1.0f + gv.x, v.x, hv.x);
+          hv.y = fmaf(1.0f + gv.y, v.y, hv.y);
+          hv.z = fmaf(1.0f + gv.z, v.z, hv.z);
+          hv.w = fmaf(1.0f + gv.w, v.w, hv.w);
+          if (kFull || mh + p * RPP + rsub < M) *reinterpret_cast<float4*>(obase + off0 + p * ostep) = hv;
+        }
+      } else {
+#pragma unroll 4
+        for (int p = 0; p < NP; ++p) {
+          if (!kFull && mh + p * RPP + rsub >= M) continue;
+          float4 v = *reinterpret_cast<const float4*>(&sC[(p * RPP + rsub) * C::CLD + c4]);
+          if constexpr (EPI == EPI_GELU) {
+            v.x = gelu_tanh(v.x);
+            v.y = gelu_tanh(v.y);
+            v.z = gelu_tanh(v.z);
+            v.w = gelu_tanh(v.w);
+          }
+          if constexpr (kQ) {
+            v.x *= e.qscale;
+            v.y *= e.qscale;
+            v.z *= e.qscale;
+            v.w *= e.qscale;
+          }
+          bf16x4 o;
+          o[0] = (bf16)v.x;
+          o[1] = (bf16)v.y;
+          o[2] = (bf16)v.z;
+          o[3] = (bf16)v.w;
+          *reinterpret_cast<bf16x4*>(obase + off0 + p * ostep) = o;
+        }
+      }
+      if (h + 1 < EH) __syncthreads();  // the next half reuses the staging rows
     }
-    if (h + 1 < EH) __syncthreads();  // the next half reuses the staging rows
+  };
+  // a column tile is all queries or none (qcols is a multiple of 128)
+  const bool qtile = EPI == EPI_BIAS && n0 < e.qcols;
+  if (m0 + BM <= M) {
+    if (qtile) epilogue(std::true_type{}, std::true_type{});
+    else epilogue(std::true_type{}, std::false_type{});
+  } else {
+    if (qtile) epilogue(std::false_type{}, std::true_type{});
+    else epilogue(std::false_type{}, std::false_type{});
   }
 }
 #define SPHINX_GEMM_DMA_KERNEL(NAME, EPI, BM, EH)                                                            \
@@ -472,7 +491,8 @@ double tile_rounds(int64_t tiles, int64_t slots, double w) {
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
                        const GemmEpi& e, hipStream_t s) {
   if (dt == SPHINX_BF16) {
-    if (K % 128 != 0 || N % 128 != 0) return hipErrorInvalidValue;  // the kernels' K loop takes two 64-deep steps at a time
+    // the K loop takes two 64-deep steps at a time; the query scale is applied per 128-column tile
+    if (K % 128 != 0 || N % 128 != 0 || (epi == EPI_BIAS && e.qcols % 128 != 0)) return hipErrorInvalidValue;
     const bf16 *a = (const bf16*)A, *w = (const bf16*)W, *b = (const bf16*)bias;
     {
       const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
