@@ -156,9 +156,9 @@ __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z));
 // keeps the MLP epilogue cheap next to its MFMAs.  Large negative z gives
 // z / inf = -0, large positive z gives z.
 __device__ __forceinline__ float gelu_tanh(float z) {
-  const float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
-  const float u = z * fmaf(0.044715f * z, z, 1.0f);                     // z + 0.044715 z^3
-  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(c * u));
+  constexpr float c = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float a = z * fmaf(c * 0.044715f, z * z, c);                         // c (z + 0.044715 z^3)
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(a));
 }
 
 }  // namespace sphinx
