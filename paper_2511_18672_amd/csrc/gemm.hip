@@ -3,7 +3,7 @@
 //   EPI_BIAS  : out = C                         (QKV projection)      -> bf16/fp32
 //   EPI_GELU  : out = GELU_tanh(C)              (MLP first layer)     -> bf16/fp32
 //   EPI_GATED : h  += (1 + gate[row]) * C       (out-proj, MLP second layer; fp32 residual)
-// M = selected tokens (ragged), N, K multiples of the tile sizes.
+// M = selected tokens (ragged); N and K multiples of 128 on the bf16 path.
 //
 // bf16 path (gfx950 MFMA): k_gemm_dma_* (described with their code).  Operand
 // offsets are 32-bit: the caller guarantees M*K and N*K below 2^31 elements.
@@ -39,8 +39,12 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 //    the 16 rows of one ds_read_b128 pass (same chunk) over all 64 LDS banks.
 //    Each wave copies 8 rows per instruction: lane i of copy q writes slot i%8
 //    of row 8q + i/8 and reads the global chunk the permutation puts there, so
-//    the copy needs no registers, no LDS stores and no address VALU beyond one
-//    add per copy.
+//    the copy needs no registers and no LDS stores; its source is a
+//    wave-uniform scalar base (A or W, moved by scalar adds per K step) plus a
+//    fixed per-lane byte offset, so it needs no VALU either.
+//  * On gfx950 VALU work does not overlap other waves' MFMAs, so the loop is
+//    kept free of it: the K loop is unrolled over the ring, making every
+//    fragment address a loop-invariant base plus an immediate offset.
 //  * K steps live in a 2-slot ring.  The wait for the next step's copies and
 //    the workgroup barrier sit inside the last 16-deep k-step of the current
 //    one, so the next step's first fragments are read (and the following
@@ -48,8 +52,9 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 //    step each k-step's fragment reads are issued before the previous
 //    k-step's MFMAs.  Barriers carry no memory fence: each wave waits for its
 //    own copies (vmcnt) and LDS reads (lgkmcnt) first.
-//  * Every output accumulates its k-steps of 16 in ascending k, whatever the
-//    tile shape, so all variants give bit-identical results.
+//  * Every output starts at its bias and accumulates its k-steps of 16 in
+//    ascending k, whatever the tile shape, so all variants give bit-identical
+//    results.
 //  * A 192-row variant (wave tiles 96x64, 80 KB of LDS, epilogue staged one
 //    wave row at a time) is launched where its smaller tile count packs into
 //    fewer rounds of two workgroups per CU; same results.
