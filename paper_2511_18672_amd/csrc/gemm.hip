@@ -138,17 +138,22 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   for (int ks = 0; ks < 4; ++ks) foff[ks] = r32 * 128 + (((2 * ks + g) ^ ((r32 >> 1) & 7)) << 4);
   const int a_row0 = wm * C::WM, b_row0 = BM + wn * C::WN;
 
-  // the accumulators start at the bias of their column (lane column
-  // wn WN + 32 j + r32 of the tile), so the epilogue adds no bias
+  // acc[i][j] is the transposed output block: the MFMA takes the W fragment
+  // as its A operand, so lane l holds row a_row0 + 32 i + l%32 of the tile and,
+  // in registers 4q .. 4q+3, its four consecutive columns wn WN + 32 j + 8q +
+  // 4(l/32) .. +3.  The accumulators start at the bias of their column, so the
+  // epilogue adds no bias.
   f32x16 acc[C::TI][C::TJ];
 #pragma unroll
-  for (int j = 0; j < C::TJ; ++j) {
-    const float bj = (float)bias[n0 + wn * C::WN + j * 32 + r32];
+  for (int j = 0; j < C::TJ; ++j)
 #pragma unroll
-    for (int i = 0; i < C::TI; ++i)
+    for (int q = 0; q < 4; ++q) {
+      const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + n0 + wn * C::WN + j * 32 + 8 * q + 4 * g);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = bj;
-  }
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < C::TI; ++i) acc[i][j][4 * q + t] = (float)b4[t];
+    }
 
   const int KT = K / C::BK;  // even (K is a multiple of 128)
   static_assert(NS == 2, "ring of 2 stages");
@@ -200,7 +205,7 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
       for (int i = 0; i < C::TI; ++i)
 #pragma unroll
         for (int j = 0; j < C::TJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ks][i], fb[ks][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -257,15 +262,16 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
           gres[p] = *reinterpret_cast<const float4*>(e.gate + (int64_t)cr[p] * e.ldg + n0 + c4);
         }
       }
-      if (EH == 1 || wm == h) {
-        const int r0 = a_row0 - h * C::EROWS;
+      if (EH == 1 || wm == h) {  // four consecutive columns per 16-byte LDS store
+        float* srow = sC + (a_row0 - h * C::EROWS + r32) * C::CLD + wn * C::WN + 4 * g;
 #pragma unroll
         for (int i = 0; i < C::TI; ++i)
 #pragma unroll
           for (int j = 0; j < C::TJ; ++j)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              sC[(r0 + i * 32 + (r >> 2) * 8 + g * 4 + (r & 3)) * C::CLD + wn * C::WN + j * 32 + r32] = acc[i][j][r];
+            for (int q = 0; q < 4; ++q)
+              *reinterpret_cast<float4*>(srow + i * 32 * C::CLD + j * 32 + 8 * q) =
+                  make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
       }
       __syncthreads();
       if constexpr (EPI == EPI_GATED) {
