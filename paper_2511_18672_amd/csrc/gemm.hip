@@ -58,6 +58,9 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 //  * A 192-row variant (wave tiles 96x64, 80 KB of LDS, epilogue staged one
 //    wave row at a time) is launched where its smaller tile count packs into
 //    fewer rounds of two workgroups per CU; same results.
+//  * Launches whose 128-row tiles all fit on the CUs at once (few selected
+//    tokens) run one workgroup per CU with a ring of 3 or 4 stages instead;
+//    same results.
 namespace dma {
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
@@ -156,22 +159,24 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     }
 
   const int KT = K / C::BK;  // even (K is a multiple of 128)
-  static_assert(NS == 2, "ring of 2 stages");
-  // Stage j lives in slot j % 2.  The wait for stage kt+1 and the barrier sit
+  static_assert(NS >= 2 && NS <= 4, "ring of 2 to 4 stages");
+  // Stage j lives in slot j % NS.  The wait for stage kt+1 and the barrier sit
   // inside the last k-step of tile kt: after it every wave has read all of
-  // stage kt (so its slot can be refilled with stage kt+2) and stage kt+1 has
+  // stage kt (so its slot can be refilled with stage kt+NS) and stage kt+1 has
   // landed (so its first fragments can be read while the last MFMAs of tile
-  // kt run).
+  // kt run).  With NS > 2 every K step refills its slot, near the end with a
+  // copy of the last stage into a slot that is not read again, so that at
+  // each wait exactly the NS - 2 newest stages may still be in flight.
   auto sync_stage = [&]() {
-    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
+    __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((NS - 2) * C::COPIES));
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
   };
-  copy_stage(0, 0);
-  copy_stage(1, 1);
-  // stage 0 must land before the first reads; stage 1 may stay in flight
-  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(C::COPIES));
+#pragma unroll
+  for (int st = 0; st < NS; ++st) copy_stage(NS == 2 ? st : min(st, KT - 1), st);
+  // stage 0 must land before the first reads; the later ones may stay in flight
+  __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0((NS - 1) * C::COPIES));
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
@@ -196,7 +201,11 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
         read(st, ks + 1, ks + 1);
       } else if (kt + 1 < KT) {
         sync_stage();
-        if (kt + NS < KT) copy_stage(kt + NS, slot);
+        if constexpr (NS == 2) {
+          if (kt + NS < KT) copy_stage(kt + NS, slot);
+        } else {
+          copy_stage(min(kt + NS, KT - 1), slot);
+        }
         read(smem + nslot * C::STAGE, 0, 0);
       }
       // the next k-step's reads are issued before this k-step's MFMAs
@@ -210,10 +219,13 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     }
   };
   read(smem, 0, 0);
-  // K is a multiple of 128 (launch_gemm checks it), so KT is even
-  for (int kt = 0; kt < KT; kt += 2) {
+  // KT is a multiple of NS (launch_gemm checks it: K is a multiple of 128,
+  // and the deeper rings are launched only where KT divides)
+  for (int kt = 0; kt < KT; kt += NS) {
     step(kt, std::integral_constant<int, 0>{});
     step(kt + 1, std::integral_constant<int, 1>{});
+    if constexpr (NS > 2) step(kt + 2, std::integral_constant<int, 2>{});
+    if constexpr (NS > 3) step(kt + 3, std::integral_constant<int, 3>{});
   }
   __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
   asm volatile("" ::: "memory");
@@ -342,6 +354,21 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_bias, EPI_BIAS, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
+
+// 128-row tiles with a ring of NS stages (NS x 32 KB of LDS, so one
+// workgroup per CU), for launches whose 128-row tiles all fit on the CUs at
+// once.  A lone workgroup waits out the copy latency of every K step when only
+// the next stage is in flight; here NS - 1 are.  Same results as the other
+// tiles.
+template <int EPI, int NS>
+__global__ __launch_bounds__(256, 1) void k_gemm_dma_deep(const bf16* __restrict__ A, const bf16* __restrict__ W,
+                                                          const bf16* __restrict__ bias, int M, int N, int K,
+                                                          GemmEpi e) {
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, NS, 1>::SMEM];
+  int m0, n0;
+  grid_tile<128, 128>(N, m0, n0);
+  gemm_dma_body<EPI, 128, 128, NS, 1>(A, W, bias, M, N, K, e, smem, m0, n0);
+}
 
 // Mixed row tiles: nb 192-row and ns 128-row tiles per column tile.  Same
 // results as either tile.
@@ -508,6 +535,21 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
     {
       const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
       const int64_t t128 = nt * ((M + 127) / 128), t192 = nt * ((M + 191) / 192);
+      // few tiles: every 128-row tile on a CU of its own, with a deeper ring
+      const int KT = K / 64;
+      if (t128 * 2 <= slots && (KT % 4 == 0 || KT % 3 == 0)) {
+        const int tiles = (int)t128;
+        if (KT % 4 == 0) {
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 4><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+        } else {
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 3><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 3><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+        }
+        return hipGetLastError();
+      }
       // mixed tiles: narrow N, 192-row tiles filling more than half of one round
       int nb = -1, ns = 0;
       if (nt <= 8 && slots % 16 == 0 && t192 * 2 > slots && t192 <= slots) {
