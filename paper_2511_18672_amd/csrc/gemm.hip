@@ -59,8 +59,8 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 //    wave row at a time) is launched where its smaller tile count packs into
 //    fewer rounds of two workgroups per CU; same results.
 //  * Launches whose 128-row tiles all fit on the CUs at once (few selected
-//    tokens) run one workgroup per CU with a ring of 3 or 4 stages instead;
-//    same results.
+//    tokens) run one eight-wave workgroup per CU with a ring of 3 or 4 stages
+//    instead; same results.
 namespace dma {
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
@@ -68,17 +68,21 @@ namespace dma {
 constexpr int wait_vm_lgkm0(int vm) { return 0x0070 | (vm & 15) | ((vm >> 4) << 14); }
 
 // EH: the fp32 epilogue tile is staged in EH row halves (EH = 2 when the
-// whole tile would need more LDS than the operand ring).
-template <int BM, int BN, int NS, int EH = 1>
+// whole tile would need more LDS than the operand ring).  NW waves in 2 rows
+// of NW/2 (4: 2x2, 8: 2x4).
+template <int BM, int BN, int NS, int EH = 1, int NW = 4>
 struct DmaCfg {
   static constexpr int BK = 64;
-  static constexpr int WM = BM / 2, WN = BN / 2, TI = WM / 32, TJ = WN / 32;
+  static constexpr int NT = 64 * NW, WGN = NW / 2;  // threads; waves along N
+  static constexpr int WM = BM / 2, WN = BN / WGN, TI = WM / 32, TJ = WN / 32;
   static constexpr int STAGE = (BM + BN) * 128;     // bytes per K-step
-  static constexpr int COPIES = (BM + BN) / 32;     // copy instructions per wave per stage
+  static constexpr int COPIES = (BM + BN) / 8 / NW; // copy instructions per wave per stage
   static constexpr int CLD = BN + 4;                // epilogue staging row (fp32)
   static constexpr int EROWS = BM / EH;             // tile rows staged at once
   static constexpr int SMEM = NS * STAGE > EROWS * CLD * 4 ? NS * STAGE : EROWS * CLD * 4;
   static_assert(EH == 1 || EH == 2, "whole tile or two halves (one per wave row)");
+  static_assert(NW == 4 || NW == 8, "2x2 or 2x4 waves");
+  static_assert(COPIES * 8 * NW == BM + BN && BM % 8 == 0, "each copy instruction moves 8 rows of A or of W");
 };
 
 // Tile of a one-dimensional grid of BM x BN tiles; workgroups are dealt to the
@@ -100,14 +104,14 @@ __device__ __forceinline__ void grid_tile(int N, int& m0, int& n0) {
   }
 }
 
-template <int EPI, int BM, int BN, int NS, int EH = 1>
+template <int EPI, int BM, int BN, int NS, int EH = 1, int NW = 4>
 __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                               const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e,
                                               unsigned char* smem, int m0, int n0) {
-  typedef DmaCfg<BM, BN, NS, EH> C;
+  typedef DmaCfg<BM, BN, NS, EH, NW> C;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / C::WGN, wn = wave % C::WGN;
   const int g = lane >> 5, r32 = lane & 31;
 
   // copy sources: instruction i of this wave fills rows 8q .. 8q+7 of the
@@ -240,7 +244,7 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
   // is a tile-uniform branch.
   float* sC = reinterpret_cast<float*>(smem);
   constexpr int TPR = BN / 4;          // threads per row (one float4 each)
-  constexpr int RPP = 256 / TPR;       // rows per pass
+  constexpr int RPP = C::NT / TPR;     // rows per pass
   constexpr int NP = C::EROWS / RPP;   // row passes per staged half
   constexpr int OSZ = EPI == EPI_GATED ? 4 : 2;  // output bytes: fp32 residual or bf16 activation
   const int c4 = (tid % TPR) * 4, rsub = tid / TPR;
@@ -358,16 +362,17 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 // 128-row tiles with a ring of NS stages (NS x 32 KB of LDS, so one
 // workgroup per CU), for launches whose 128-row tiles all fit on the CUs at
 // once.  A lone workgroup waits out the copy latency of every K step when only
-// the next stage is in flight; here NS - 1 are.  Same results as the other
-// tiles.
+// the next stage is in flight; here NS - 1 are.  Eight waves of 64x32 (two per
+// SIMD), so that each SIMD has a second wave to issue while one waits.  Same
+// results as the other tiles.
 template <int EPI, int NS>
-__global__ __launch_bounds__(256, 1) void k_gemm_dma_deep(const bf16* __restrict__ A, const bf16* __restrict__ W,
+__global__ __launch_bounds__(512, 1) void k_gemm_dma_deep(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                           const bf16* __restrict__ bias, int M, int N, int K,
                                                           GemmEpi e) {
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, NS, 1>::SMEM];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, NS, 1, 8>::SMEM];
   int m0, n0;
   grid_tile<128, 128>(N, m0, n0);
-  gemm_dma_body<EPI, 128, 128, NS, 1>(A, W, bias, M, N, K, e, smem, m0, n0);
+  gemm_dma_body<EPI, 128, 128, NS, 1, 8>(A, W, bias, M, N, K, e, smem, m0, n0);
 }
 
 // Mixed row tiles: nb 192-row and ns 128-row tiles per column tile.  Same
@@ -540,13 +545,13 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
       if (t128 * 2 <= slots && (KT % 4 == 0 || KT % 3 == 0)) {
         const int tiles = (int)t128;
         if (KT % 4 == 0) {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 4><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 4><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         } else {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 3><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 3><<<tiles, 256, 0, s>>>(a, w, b, M, N, K, e);
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         }
         return hipGetLastError();
       }
