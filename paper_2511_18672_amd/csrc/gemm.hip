@@ -86,15 +86,16 @@ struct DmaCfg {
 };
 
 // Tile of a one-dimensional grid of BM x BN tiles; workgroups are dealt to the
-// 8 XCDs round-robin.  Wide N (more than 8 column tiles): tiles in plain
-// N-fastest order, so XCD x always gets the column tiles n = x (mod 8) and
-// keeps that eighth of W in its L2 for the whole kernel.  Narrow N: renumbered
-// (xcd_tile) so that each XCD takes consecutive row blocks of A with all their
-// column tiles, and A is fetched into one L2 instead of eight.
+// 8 XCDs round-robin.  Wide N (more than 8 column tiles, and W at least a
+// quarter of A): tiles in plain N-fastest order, so XCD x always gets the
+// column tiles n = x (mod 8) and keeps that eighth of W in its L2 for the
+// whole kernel.  Otherwise renumbered (xcd_tile) so that each XCD takes
+// consecutive row blocks of A with all their column tiles: A is fetched into
+// one L2 instead of eight, W into all eight.
 template <int BM, int BN>
-__device__ __forceinline__ void grid_tile(int N, int& m0, int& n0) {
+__device__ __forceinline__ void grid_tile(int M, int N, int& m0, int& n0) {
   const int nt = N / BN;
-  if (nt > 8) {
+  if (nt > 8 && M < 4 * N) {
     m0 = ((int)blockIdx.x / nt) * BM;
     n0 = ((int)blockIdx.x % nt) * BN;
   } else {
@@ -345,7 +346,7 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
                                                  const bf16* __restrict__ bias, int M, int N, int K, GemmEpi e) {  \
     __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<BM, 128, 2, EH>::SMEM];                   \
     int m0, n0;                                                                                                  \
-    grid_tile<BM, 128>(N, m0, n0);                                                                               \
+    grid_tile<BM, 128>(M, N, m0, n0);                                                                               \
     gemm_dma_body<EPI, BM, 128, 2, EH>(A, W, bias, M, N, K, e, smem, m0, n0);                                    \
   }
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma_bias, EPI_BIAS, 128, 1)
@@ -371,7 +372,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_dma_deep(const bf16* __restrict
                                                           GemmEpi e) {
   __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, NS, 1, 8>::SMEM];
   int m0, n0;
-  grid_tile<128, 128>(N, m0, n0);
+  grid_tile<128, 128>(M, N, m0, n0);
   gemm_dma_body<EPI, 128, 128, NS, 1, 8>(A, W, bias, M, N, K, e, smem, m0, n0);
 }
 
