@@ -58,9 +58,9 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 //  * A 192-row variant (wave tiles 96x64, 80 KB of LDS, epilogue staged one
 //    wave row at a time) is launched where its smaller tile count packs into
 //    fewer rounds of two workgroups per CU; same results.
-//  * Launches whose 128-row tiles all fit on the CUs at once (few selected
-//    tokens) run one eight-wave workgroup per CU with a ring of 3 or 4 stages
-//    instead; same results.
+//  * Launches whose 128-row (else 192-row) tiles all fit on the CUs at once
+//    (few selected tokens) run one eight-wave workgroup per CU with a ring of
+//    3 or 4 stages instead; same results.
 namespace dma {
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
@@ -360,20 +360,21 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
 
-// 128-row tiles with a ring of NS stages (NS x 32 KB of LDS, so one
-// workgroup per CU), for launches whose 128-row tiles all fit on the CUs at
-// once.  A lone workgroup waits out the copy latency of every K step when only
-// the next stage is in flight; here NS - 1 are.  Eight waves of 64x32 (two per
-// SIMD), so that each SIMD has a second wave to issue while one waits.  Same
-// results as the other tiles.
-template <int EPI, int NS>
+// BM-row tiles (128 or 192) with a ring of NS stages (NS x 32 or 40 KB of
+// LDS, so one workgroup per CU), for launches whose tiles all fit on the CUs
+// at once.  A lone workgroup waits out the copy latency of every K step when
+// only the next stage is in flight; here NS - 1 are.  Eight waves of 64x32 or
+// 96x32 (two per SIMD), so that each SIMD has a second wave to issue while one
+// waits.  Same results as the other tiles.
+template <int EPI, int NS, int BM = 128>
 __global__ __launch_bounds__(512, 1) void k_gemm_dma_deep(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                           const bf16* __restrict__ bias, int M, int N, int K,
                                                           GemmEpi e) {
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<128, 128, NS, 1, 8>::SMEM];
+  constexpr int EH = BM == 128 ? 1 : 2;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<BM, 128, NS, EH, 8>::SMEM];
   int m0, n0;
-  grid_tile<128, 128>(M, N, m0, n0);
-  gemm_dma_body<EPI, 128, 128, NS, 1, 8>(A, W, bias, M, N, K, e, smem, m0, n0);
+  grid_tile<BM, 128>(M, N, m0, n0);
+  gemm_dma_body<EPI, BM, 128, NS, EH, 8>(A, W, bias, M, N, K, e, smem, m0, n0);
 }
 
 // Mixed row tiles: nb 192-row and ns 128-row tiles per column tile.  Same
@@ -554,6 +555,15 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
           else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
           else dma::k_gemm_dma_deep<EPI_GATED, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         }
+        return hipGetLastError();
+      }
+      // the 192-row tiles fit on the CUs where the 128-row ones do not: one
+      // per CU with a ring of four stages (160 KB of LDS)
+      if (t192 * 2 <= slots && KT % 4 == 0) {
+        const int tiles = (int)t192;
+        if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+        else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+        else dma::k_gemm_dma_deep<EPI_GATED, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         return hipGetLastError();
       }
       // mixed tiles: narrow N, 192-row tiles filling more than half of one round
