@@ -58,9 +58,9 @@ __device__ __forceinline__ void epi_store(const GemmEpi& e, int m, int n, float 
 //  * A 192-row variant (wave tiles 96x64, 80 KB of LDS, epilogue staged one
 //    wave row at a time) is launched where its smaller tile count packs into
 //    fewer rounds of two workgroups per CU; same results.
-//  * Launches whose 128-row (else 192-row) tiles all fit on the CUs at once
-//    (few selected tokens) run one eight-wave workgroup per CU with a ring of
-//    3 or 4 stages instead; same results.
+//  * Launches whose 128-, 192- or 256-row tiles all fit on the CUs at once
+//    (few selected tokens) run the smallest such tile, one eight-wave
+//    workgroup per CU with a ring of 3 or 4 stages; same results.
 namespace dma {
 
 // s_waitcnt immediate: vmcnt(vm) expcnt(7) lgkmcnt(0) (gfx9 encoding: vmcnt in
@@ -224,13 +224,25 @@ __device__ __forceinline__ void gemm_dma_body(const bf16* __restrict__ A, const 
     }
   };
   read(smem, 0, 0);
-  // KT is a multiple of NS (launch_gemm checks it: K is a multiple of 128,
-  // and the deeper rings are launched only where KT divides)
-  for (int kt = 0; kt < KT; kt += NS) {
-    step(kt, std::integral_constant<int, 0>{});
-    step(kt + 1, std::integral_constant<int, 1>{});
-    if constexpr (NS > 2) step(kt + 2, std::integral_constant<int, 2>{});
-    if constexpr (NS > 3) step(kt + 3, std::integral_constant<int, 3>{});
+  // whole trips over the ring, then (NS > 2) the last KT % NS stages; with two
+  // slots KT is even (K is a multiple of 128, which launch_gemm checks)
+  if constexpr (NS == 2) {
+    for (int kt = 0; kt < KT; kt += 2) {
+      step(kt, std::integral_constant<int, 0>{});
+      step(kt + 1, std::integral_constant<int, 1>{});
+    }
+  } else {
+    int kt = 0;
+    for (; kt + NS <= KT; kt += NS) {
+      step(kt, std::integral_constant<int, 0>{});
+      step(kt + 1, std::integral_constant<int, 1>{});
+      step(kt + 2, std::integral_constant<int, 2>{});
+      if constexpr (NS > 3) step(kt + 3, std::integral_constant<int, 3>{});
+    }
+    if (kt < KT) step(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 < KT) step(kt + 1, std::integral_constant<int, 1>{});
+    if constexpr (NS > 3)
+      if (kt + 2 < KT) step(kt + 2, std::integral_constant<int, 2>{});
   }
   __builtin_amdgcn_s_waitcnt(wait_vm_lgkm0(0));
   asm volatile("" ::: "memory");
@@ -360,12 +372,12 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
 
-// BM-row tiles (128 or 192) with a ring of NS stages (NS x 32 or 40 KB of
-// LDS, so one workgroup per CU), for launches whose tiles all fit on the CUs
-// at once.  A lone workgroup waits out the copy latency of every K step when
-// only the next stage is in flight; here NS - 1 are.  Eight waves of 64x32 or
-// 96x32 (two per SIMD), so that each SIMD has a second wave to issue while one
-// waits.  Same results as the other tiles.
+// BM-row tiles (128, 192 or 256) with a ring of NS stages (4 x 32 KB, 4 x 40
+// KB or 3 x 48 KB of LDS, so one workgroup per CU), for launches whose tiles
+// all fit on the CUs at once.  A lone workgroup waits out the copy latency of
+// every K step when only the next stage is in flight; here NS - 1 are.  Eight
+// waves of 64x32, 96x32 or 128x32 (two per SIMD), so that each SIMD has a
+// second wave to issue while one waits.  Same results as the other tiles.
 template <int EPI, int NS, int BM = 128>
 __global__ __launch_bounds__(512, 1) void k_gemm_dma_deep(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                           const bf16* __restrict__ bias, int M, int N, int K,
@@ -542,28 +554,26 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
     {
       const int64_t nt = N / 128, slots = 2 * (int64_t)cu_count();
       const int64_t t128 = nt * ((M + 127) / 128), t192 = nt * ((M + 191) / 192);
-      // few tiles: every 128-row tile on a CU of its own, with a deeper ring
-      const int KT = K / 64;
-      if (t128 * 2 <= slots && (KT % 4 == 0 || KT % 3 == 0)) {
-        const int tiles = (int)t128;
-        if (KT % 4 == 0) {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 4><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+      // few tiles: the smallest row tile (128, 192 or 256 rows) whose tiles
+      // all fit on the CUs at once, one per CU with a deeper ring (128, 160
+      // or 144 KB of LDS)
+      const int64_t cus = slots / 2, t256 = nt * ((M + 255) / 256);
+      if (t128 <= cus || t192 <= cus || t256 <= cus) {
+        const int bm = t128 <= cus ? 128 : t192 <= cus ? 192 : 256;
+        const int tiles = (int)(bm == 128 ? t128 : bm == 192 ? t192 : t256);
+        if (bm == 128) {
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4, 128><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4, 128><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 4, 128><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+        } else if (bm == 192) {
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         } else {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 3><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 3, 256><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3, 256><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+          else dma::k_gemm_dma_deep<EPI_GATED, 3, 256><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         }
-        return hipGetLastError();
-      }
-      // the 192-row tiles fit on the CUs where the 128-row ones do not: one
-      // per CU with a ring of four stages (160 KB of LDS)
-      if (t192 * 2 <= slots && KT % 4 == 0) {
-        const int tiles = (int)t192;
-        if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-        else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-        else dma::k_gemm_dma_deep<EPI_GATED, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
         return hipGetLastError();
       }
       // mixed tiles: narrow N, 192-row tiles filling more than half of one round
