@@ -340,6 +340,36 @@ def test_headline_shape_one_block_step():
     assert _report("headline L=1 step 0", states[1], res.state) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("rho", [0.05, 0.07, 0.15, 0.2])
+def test_headline_width_few_tile_gemms(rho):
+    """One block of the headline width (D 1024, MLP 4096) at selections whose
+    GEMMs have at most one tile per CU, so that they run one workgroup per CU
+    with a deeper operand ring: on a 256-CU device 1613 and 2258 selected
+    tokens put the QKV projection on 192- and 256-row tiles and MLP1 on
+    256-row ones, 4838 and 6451 tokens the out-projection and MLP2 on 192- and
+    256-row ones (K = 1024 and 4096, so the rings end with a partial trip)."""
+    model = W.ModelCfg(D=1024, heads=16, head_dim=64, mlp=4096, L=1, dtype="bf16")
+    wl = W.headline(model=model, rho=rho)
+    R, states, sels = run_gpu(wl, trace=True, steps=1)
+    plans = O.plan_steps([r.frames for r in wl.requests], wl.s_start, wl.nsteps)
+    res = O.step(wl, O.model_from_workload(wl), wl.z0, plans[0], "model")
+    assert sels[0][0] == res.n_sel and np.array_equal(sels[0][1], res.idx)
+    assert _report(f"headline width L=1, {res.n_sel} selected", states[1], res.state) <= TOL["bf16"]
+
+
+def test_few_tile_gemms_match_packed():
+    """The deep-ring GEMM tiles give bit-identical results to the two-workgroup
+    tiles: three headline-shape requests (1613, 4838 and 6451 selected tokens)
+    each alone run on the deep-ring kernels, and packed into one launch (12902
+    rows) on the two-workgroup kernels."""
+    model = W.ModelCfg(D=1024, heads=16, head_dim=64, mlp=4096, L=1, dtype="bf16")
+    req = W.Request(14, 72, 128)
+    wl = W.custom("few_tile_packed", model, [req, req, req], [0.05, 0.15, 0.2], [0.5, 0.5, 0.5], [25, 25, 25])
+    worst = _packed_vs_separate(wl)
+    print(f"[few-tile GEMMs] packed vs separate max_abs = {worst:.3e}")
+    assert worst == 0.0
+
+
 def test_headline_full_depth_properties():
     """12-block headline step: deterministic, unselected tokens untouched,
     finite, and only selected tokens move."""
