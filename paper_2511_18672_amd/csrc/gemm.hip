@@ -543,6 +543,15 @@ double tile_rounds(int64_t tiles, int64_t slots, double w) {
   const int64_t full = tiles / slots, rem = tiles % slots;
   return w * ((double)full + (rem == 0 ? 0.0 : rem * 2 <= slots ? 0.5 : 1.0));
 }
+
+// One eight-wave workgroup per BM-row tile with an NS-stage ring.
+template <int NS, int BM>
+void launch_deep(int epi, int tiles, const bf16* a, const bf16* w, const bf16* b, int M, int N, int K,
+                 const GemmEpi& e, hipStream_t s) {
+  if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, NS, BM><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+  else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, NS, BM><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+  else dma::k_gemm_dma_deep<EPI_GATED, NS, BM><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
+}
 }  // namespace
 
 hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, const void* bias, int M, int N, int K,
@@ -559,21 +568,9 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
       // or 144 KB of LDS)
       const int64_t cus = slots / 2, t256 = nt * ((M + 255) / 256);
       if (t128 <= cus || t192 <= cus || t256 <= cus) {
-        const int bm = t128 <= cus ? 128 : t192 <= cus ? 192 : 256;
-        const int tiles = (int)(bm == 128 ? t128 : bm == 192 ? t192 : t256);
-        if (bm == 128) {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4, 128><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4, 128><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 4, 128><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-        } else if (bm == 192) {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 4, 192><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-        } else {
-          if (epi == EPI_BIAS) dma::k_gemm_dma_deep<EPI_BIAS, 3, 256><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else if (epi == EPI_GELU) dma::k_gemm_dma_deep<EPI_GELU, 3, 256><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-          else dma::k_gemm_dma_deep<EPI_GATED, 3, 256><<<tiles, 512, 0, s>>>(a, w, b, M, N, K, e);
-        }
+        if (t128 <= cus) launch_deep<4, 128>(epi, (int)t128, a, w, b, M, N, K, e, s);
+        else if (t192 <= cus) launch_deep<4, 192>(epi, (int)t192, a, w, b, M, N, K, e, s);
+        else launch_deep<3, 256>(epi, (int)t256, a, w, b, M, N, K, e, s);
         return hipGetLastError();
       }
       // mixed tiles: narrow N, 192-row tiles filling more than half of one round
