@@ -162,6 +162,12 @@ def test_varlen_attention_validation(L):
     assert f(*args(1, 64, cu(0, 0), cu(0, 9), 1)) == OK  # no queries: nothing to do
     many = (ctypes.c_int32 * 66)(*range(66))
     assert f(*args(1, 64, many, many, 65)) == UNSUPPORTED
+    # rows are addressed with 32-bit element offsets: q or k/v of 2^31 elements
+    # (2^25 rows of 64) are refused before any HIP call
+    rows = 1 << 25
+    assert f(*args(1, 64, cu(0, rows), cu(0, 4), 1)) == UNSUPPORTED
+    assert f(*args(1, 64, cu(0, 4), cu(0, rows), 1)) == UNSUPPORTED
+    assert f(*args(0, 64, cu(0, rows // 2), cu(0, 4), 1, ld=128)) == UNSUPPORTED  # via the row stride
 
 
 def test_refine_size_limit(L):
