@@ -153,7 +153,7 @@ RefineWs refine_layout(const sphinx_model_desc& m, const ReqTable& T, int G, int
   w.gframe = take((size_t)n * 4);
   w.crow = take((size_t)n * 4);
   w.posc = take((size_t)n * 4);
-  w.fcnt = take((size_t)G * 4);           // factorised: forwarded rows per frame
+  w.fcnt = take((size_t)(G + 1) * 4);     // factorised: first forwarded row of each frame (and n)
   w.pos = take((size_t)T.tok_off[T.R] * 4);  // factorised: token -> forwarded row
   w.h = take((size_t)n * D * 4);
   w.a = take((size_t)n * D * act);
@@ -664,20 +664,21 @@ sphinx_status refine_impl(const sphinx_model_desc* m, const sphinx_request* reqs
   SegTable Sf;
   std::memset(&Sf, 0, sizeof(Sf));
   if (factorised) {
-    std::vector<int32_t> cnt(G);
-    SPHINX_TRY(launch_frame_counts(T, idx, n, G, I32(W.fcnt), s));
-    SPHINX_TRY(hipMemcpyAsync(cnt.data(), I32(W.fcnt), (size_t)G * 4, hipMemcpyDeviceToHost, s));
+    std::vector<int32_t> first(G + 1);
+    SPHINX_TRY(launch_frame_bounds(T, idx, n, G, I32(W.fcnt), s));
+    SPHINX_TRY(hipMemcpyAsync(first.data(), I32(W.fcnt), (size_t)(G + 1) * 4, hipMemcpyDeviceToHost, s));
     SPHINX_TRY(hipStreamSynchronize(s));
-    SPHINX_TRY(launch_pos_map(N, idx, n, I32(W.pos), s));
+    // an idx outside [0, N) or out of order: rejected before any further launch
+    if (first[0] != 0 || first[G] != n) return SPHINX_E_INVALID;
     std::vector<int> frames;
-    std::vector<int> fstart(G);
-    int run = 0;
+    std::vector<int> fstart(G), cnt(G);
     for (int g = 0; g < G; ++g) {
-      fstart[g] = run;
-      run += cnt[g];
+      if (first[g + 1] < first[g]) return SPHINX_E_INVALID;
+      fstart[g] = first[g];
+      cnt[g] = first[g + 1] - first[g];
       if (cnt[g] > 0) frames.push_back(g);
     }
-    if (run != n) return SPHINX_E_INVALID;  // an idx outside [0, N): rejected before any further launch
+    SPHINX_TRY(launch_pos_map(N, idx, n, I32(W.pos), s));
     auto frame_keys = [&](int g) {
       int r = 0;
       while (r + 1 < R && T.frame_off[r + 1] <= g) ++r;

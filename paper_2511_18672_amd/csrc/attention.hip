@@ -968,11 +968,141 @@ __global__ __launch_bounds__(256) void k_attn_temporal(ReqTable RT, AttnIO io, i
   }
 }
 }  // namespace
+namespace {
+// Sum over the LPH consecutive lanes of a head (LPH = 4 or 8): quad
+// permutations through DPP, then one exchange with lane ^ 4.
+template <int LPH>
+__device__ __forceinline__ float head_sum(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0xB1, 0xF, 0xF, true));  // l ^ 1
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), 0x4E, 0xF, 0xF, true));  // l ^ 2
+  if constexpr (LPH == 8) x += __shfl_xor(x, 4, kWave);
+  return x;
+}
+
+// The same temporal attention for bf16 rows of D = 64 DPL elements and heads
+// of 64 dims, LPH = 64 / heads lanes each (D 1024: 16 heads of 4 lanes; D 512:
+// 8 heads of 8 lanes): one wave per column, lane l owning dims
+// [DPL l, DPL (l + 1)) of every row, so that a row is one coalesced wave load.
+// A score is the lanes' DPL-wide partial dot products (bf16 pairs, fp32 sums)
+// summed over the head's lanes.  Queries go in chunks of four that share each
+// key's loads; fp32 online softmax in base 2 (q is stored scaled by
+// log2(e)/sqrt(d)).  Members and key rows are read from the lanes that found
+// them (readlane with the wave-uniform frame index).
+template <int DPL, int LPH>
+__global__ __launch_bounds__(256) void k_attn_temporal_lanes(ReqTable RT, AttnIO io, int D,
+                                                             const int32_t* __restrict__ pos, int cached, int ncols) {
+  static_assert(DPL == 8 || DPL == 16, "8 or 16 dims per lane");
+  constexpr int NV = DPL / 8;  // 16-byte vectors per lane and row
+  const int lane = threadIdx.x & 63;
+  int c = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);
+  if (c >= ncols) return;  // wave-uniform; the kernel has no barrier
+  int r = 0;
+  for (;; ++r) {
+    const int cols = (RT.h[r] >> 1) * (RT.w[r] >> 1);
+    if (c < cols || r + 1 == RT.R) break;
+    c -= cols;
+  }
+  const int F = RT.frames[r];
+  const int64_t tpf = (int64_t)(RT.h[r] >> 1) * (RT.w[r] >> 1);
+  int p = -1, kr = 0;  // lane f < F: forwarded row of frame f's token, and its key row
+  if (lane < F) {
+    const int64_t t = RT.tok_off[r] + lane * tpf + c;
+    p = pos[t];
+    kr = cached ? (int)t : p;
+  }
+  const uint64_t qmask = __ballot(p >= 0);
+  if (qmask == 0) return;
+  const uint64_t kmask = cached ? (F >= 64 ? ~0ull : (1ull << F) - 1ull) : qmask;
+  const bf16* Q = static_cast<const bf16*>(io.q) + lane * DPL;
+  const bf16* K = static_cast<const bf16*>(io.k) + lane * DPL;
+  const bf16* V = static_cast<const bf16*>(io.v) + lane * DPL;
+  bf16* O = static_cast<bf16*>(io.o) + lane * DPL;
+  uint64_t qm = qmask;
+  while (qm != 0) {  // chunks of up to four queries
+    int qrow[4], nqc = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (qm != 0) {
+        qrow[u] = __builtin_amdgcn_readlane(p, __builtin_ctzll(qm));
+        qm &= qm - 1;
+        nqc = u + 1;
+      } else {
+        qrow[u] = qrow[0];
+      }
+    }
+    bf16x8 q[4][NV];
+    float acc[4][DPL], m[4], l[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int v = 0; v < NV; ++v) q[u][v] = *reinterpret_cast<const bf16x8*>(Q + (int64_t)qrow[u] * io.ldq + 8 * v);
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) acc[u][e] = 0.0f;
+      m[u] = -INFINITY;
+      l[u] = 0.0f;
+    }
+    uint64_t km = kmask;
+    while (km != 0) {
+      const int krow = __builtin_amdgcn_readlane(kr, __builtin_ctzll(km));
+      km &= km - 1;
+      bf16x8 kv[NV], vv[NV];
+#pragma unroll
+      for (int v = 0; v < NV; ++v) {
+        kv[v] = *reinterpret_cast<const bf16x8*>(K + (int64_t)krow * io.ldkv + 8 * v);
+        vv[v] = *reinterpret_cast<const bf16x8*>(V + (int64_t)krow * io.ldkv + 8 * v);
+      }
+      float vf[DPL];
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) vf[e] = (float)vv[e / 8][e % 8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float sc = 0.0f;
+#pragma unroll
+        for (int e = 0; e < DPL; e += 2) {
+          const bf16x2 a = {q[u][e / 8][e % 8], q[u][e / 8][e % 8 + 1]};
+          const bf16x2 b = {kv[e / 8][e % 8], kv[e / 8][e % 8 + 1]};
+          sc = __builtin_amdgcn_fdot2_f32_bf16(a, b, sc, false);
+        }
+        sc = head_sum<LPH>(sc);
+        const float mn = fmaxf(m[u], sc);
+        const float corr = exp2f(m[u] - mn), pr = exp2f(sc - mn);
+        l[u] = fmaf(l[u], corr, pr);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) acc[u][e] = fmaf(acc[u][e], corr, pr * vf[e]);
+        m[u] = mn;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (u < nqc) {
+        const float inv = 1.0f / l[u];
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          bf16x8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = (bf16)(acc[u][8 * v + e] * inv);
+          *reinterpret_cast<bf16x8*>(O + (int64_t)qrow[u] * D + 8 * v) = o;
+        }
+      }
+    }
+  }
+}
+}  // namespace
+
 hipError_t launch_attn_temporal(sphinx_dtype dt, const ReqTable& T, const AttnIO& io, int D, int heads,
                                 int head_dim, const int32_t* pos, bool cached, hipStream_t s) {
   int64_t cols = 0;
   for (int r = 0; r < T.R; ++r) cols += (int64_t)(T.h[r] >> 1) * (T.w[r] >> 1);
   const int cf = cached ? 1 : 0;
+  // lane-parallel kernel: rows of 64 x 16 or 64 x 8 dims, heads of 64 (of 4 or 8 lanes)
+  if (dt == SPHINX_BF16 && head_dim == 64 && (D == 1024 || D == 512)) {
+    const unsigned grid = (unsigned)((cols + 3) / 4);
+    if (D == 1024)
+      k_attn_temporal_lanes<16, 4><<<grid, 256, 0, s>>>(T, io, D, pos, cf, (int)cols);
+    else
+      k_attn_temporal_lanes<8, 8><<<grid, 256, 0, s>>>(T, io, D, pos, cf, (int)cols);
+    return hipGetLastError();
+  }
   if (dt == SPHINX_BF16 && head_dim == 64)
     k_attn_temporal<bf16, 64, true><<<(unsigned)cols, 256, 0, s>>>(T, io, D, head_dim, heads, pos, cf);
   else if (dt == SPHINX_BF16)

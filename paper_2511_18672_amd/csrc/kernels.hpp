@@ -118,7 +118,7 @@ hipError_t launch_attention(sphinx_dtype dt, const AttnIO& io, int D, int heads,
 hipError_t launch_attn_temporal(sphinx_dtype dt, const ReqTable& T, const AttnIO& io, int D, int heads,
                                 int head_dim, const int32_t* pos, bool cached, hipStream_t s);
 // Per-frame counts of the forwarded rows and the token -> row map (rowwise.hip).
-hipError_t launch_frame_counts(const ReqTable& T, const int32_t* idx, int n, int G, int32_t* cnt, hipStream_t s);
+hipError_t launch_frame_bounds(const ReqTable& T, const int32_t* idx, int n, int G, int32_t* first, hipStream_t s);
 hipError_t launch_pos_map(int64_t N, const int32_t* idx, int n, int32_t* pos, hipStream_t s);
 
 }  // namespace sphinx

@@ -671,19 +671,21 @@ hipError_t launch_final(const float* h, int n, int D, const float* mod, int ldm,
   return hipGetLastError();
 }
 
-// Forwarded rows per frame (the spatial segments of a factorised denoiser):
-// cnt[g] = number of rows j with frame(idx[j]) = g.  Integer atomics, so the
-// counts are exact whatever the order.
-__global__ __launch_bounds__(256) void k_zero_i32(int32_t* __restrict__ p, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) p[i] = 0;
-}
-__global__ __launch_bounds__(256) void k_frame_counts(ReqTable T, const int32_t* __restrict__ idx, int n,
-                                                      int32_t* __restrict__ cnt) {
+// Forwarded rows per frame (the spatial segments of a factorised denoiser),
+// as frame boundaries of the forwarded rows (idx ascending): first[g] = the
+// first row whose token lies in frame g or later (g = 0..G; tokens below 0
+// count as frame -1, tokens at or past N as frame G).  Row j writes first[g]
+// for every g after the frame of row j-1 up to its own, so that with idx
+// ascending every entry is written exactly once, without atomics.
+__global__ __launch_bounds__(256) void k_frame_bounds(ReqTable T, const int32_t* __restrict__ idx, int n, int G,
+                                                      int32_t* __restrict__ first) {
   const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= n) return;
-  const int32_t t = idx[j];
-  if (t >= 0 && t < T.tok_off[T.R]) atomicAdd(&cnt[frame_of_token(T, t)], 1);  // others are not counted
+  if (j > n) return;
+  const int64_t N = T.tok_off[T.R];
+  auto frame = [&](int32_t t) { return t < 0 ? -1 : t >= N ? G : frame_of_token(T, t); };
+  const int fp = j == 0 ? -1 : frame(idx[j - 1]);
+  const int fc = j == n ? G : frame(idx[j]);
+  for (int g = max(fp + 1, 0); g <= min(fc, G); ++g) first[g] = j;
 }
 // Token -> forwarded row map: pos[t] = j for t = idx[j], -1 elsewhere.
 __global__ __launch_bounds__(256) void k_fill_neg(int32_t* __restrict__ p, int64_t n) {
@@ -696,9 +698,8 @@ __global__ __launch_bounds__(256) void k_pos_scatter(const int32_t* __restrict__
   if (j < n && idx[j] >= 0 && idx[j] < N) pos[idx[j]] = j;
 }
 
-hipError_t launch_frame_counts(const ReqTable& T, const int32_t* idx, int n, int G, int32_t* cnt, hipStream_t s) {
-  k_zero_i32<<<(unsigned)((G + 255) / 256), 256, 0, s>>>(cnt, G);
-  k_frame_counts<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(T, idx, n, cnt);
+hipError_t launch_frame_bounds(const ReqTable& T, const int32_t* idx, int n, int G, int32_t* first, hipStream_t s) {
+  k_frame_bounds<<<(unsigned)(n / 256 + 1), 256, 0, s>>>(T, idx, n, G, first);
   return hipGetLastError();
 }
 

@@ -119,6 +119,22 @@ def test_per_frame_grid():
     check(wl, period=2, per_frame_grid=True)
 
 
+@pytest.mark.parametrize("D", [512, 1024])
+def test_factorised_lane_parallel_temporal(D):
+    """bf16 rows of 512 or 1024 dims with heads of 64, where the temporal
+    blocks run lane-parallel (a wave per column, a head's dims over 8 or 4
+    lanes): two ragged requests, without and with the latent cache, end to end
+    and teacher-forced per step.  Every frame starts at t = 0.5 (amplification
+    of per-step rounding at most 3.4; with starts up to 0.7 the D = 1024 run
+    ends at 2.1e-2 on this and on the one-lane-per-query kernel alike, at the
+    same 5.8e-3 per step)."""
+    model = W.ModelCfg(D=D, heads=D // 64, head_dim=64, mlp=1024, L=2, dtype="bf16", attention="factorised")
+    wl = W.custom(f"fact_lanes_d{D}", model, [W.Request(6, 16, 16), W.Request(3, 8, 12)], [0.4, 0.6],
+                  [0.5, 0.5], [4, 3])
+    check(wl)
+    check(wl, period=2)
+
+
 def test_factorised_headline_shape_two_blocks():
     """14 frames of 72x128 latent (9677 of 32256 tokens), D 1024, 16 heads of
     64: one spatial and one temporal block against the oracle."""
