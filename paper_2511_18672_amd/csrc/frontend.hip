@@ -13,12 +13,14 @@
 //   iff any of its pixels is.
 // Every stencil reads its input map with replicated borders.
 //
-// Kernels (one pass over each input plus a 1-byte intermediate):
-//   k_front_var<0>  per 64x16 tile: the stencil chain in LDS, tile min/max of Wm;
+// Kernels (one pass over each input, Wm stored as 8 bytes per pixel and inv
+// as 1):
+//   k_front_var     per 64x16 tile: the stencil chain in LDS, Wm stored, tile
+//                   min/max of Wm;
 //   k_front_minmax  per frame: min/max over its tiles; clears the histogram;
-//   k_front_var<1>  the stencil chain again (recomputed rather than stored:
-//                   Wm needs 8 bytes per pixel), inv as bytes, LDS histogram
-//                   merged into the frame's histogram with integer atomics;
+//   k_front_quant   per 64x16 tile: inv as bytes from the stored Wm, LDS
+//                   histogram merged into the frame's histogram with integer
+//                   atomics;
 //   k_front_otsu    per frame: Otsu threshold from the 256-bin histogram;
 //   k_front_pool    per token: OR over its 16 x 16 pixels of both masks.
 #include "kernels.hpp"
@@ -51,7 +53,6 @@ struct FrontSmem {
   };
   int64_t v[kVY * kVX];
   int64_t red[2 * kTPB / kWave];
-  uint32_t hist[256];
 };
 static_assert(sizeof(int64_t) * kVY * kTX <= sizeof(FrontEarly), "row sums of V must fit the early regions");
 
@@ -81,21 +82,16 @@ __device__ __forceinline__ TileLoc locate_tile(const ReqTable& T, const FrontTil
   return L;
 }
 
-// The stencil chain of one 64 x 16 tile in LDS.  MODE 0 writes the tile's
-// min and max of Wm to part[2 tile .. 2 tile + 1]; MODE 1 quantises Wm with
-// the frame's min/max (lohi), stores the inverted bytes and adds the tile's
-// histogram to the frame's.
-template <int MODE>
+// The stencil chain of one 64 x 16 tile in LDS: stores Wm at the tile's
+// in-image pixels and writes the tile's min and max of Wm to
+// part[2 tile .. 2 tile + 1].
 __global__ __launch_bounds__(kTPB) void k_front_var(ReqTable T, FrontTiles F, const uint8_t* __restrict__ rgb,
-                                                    int64_t* __restrict__ part, const int64_t* __restrict__ lohi,
-                                                    uint8_t* __restrict__ inv, uint32_t* __restrict__ hist) {
+                                                    int64_t* __restrict__ part, int64_t* __restrict__ wm) {
   __shared__ FrontSmem sm;
   const int tid = threadIdx.x;
   const TileLoc L = locate_tile(T, F, blockIdx.x);
   const int H = L.H, W = L.W, y0 = L.y0, x0 = L.x0;
   const uint8_t* img = rgb + 3 * L.pix0;
-  if (MODE == 1)
-    for (int i = tid; i < 256; i += kTPB) sm.hist[i] = 0;
   // luma at clamped positions
   for (int i = tid; i < kGY * kGX; i += kTPB) {
     const int ry = i / kGX, rx = i - ry * kGX;
@@ -154,12 +150,6 @@ __global__ __launch_bounds__(kTPB) void k_front_var(ReqTable T, FrontTiles F, co
   __syncthreads();
   // Wm at the tile's in-image pixels
   int64_t lo = INT64_MAX, hi = INT64_MIN;
-  int64_t flo = 0, fhi = 0;
-  if (MODE == 1) {
-    flo = lohi[2 * L.g];
-    fhi = lohi[2 * L.g + 1];
-  }
-  const double span = (double)(fhi - flo);
   for (int i = tid; i < kTY * kTX; i += kTPB) {
     const int ry = i / kTX, rx = i - ry * kTX;
     const int y = y0 + ry, x = x0 + rx;
@@ -168,10 +158,51 @@ __global__ __launch_bounds__(kTPB) void k_front_var(ReqTable T, FrontTiles F, co
     int64_t w = 0;
 #pragma unroll
     for (int d = -kRS; d <= kRS; ++d) w += sm.r5[(yr + d) * kTX + rx];
-    if (MODE == 0) {
-      lo = min(lo, w);
-      hi = max(hi, w);
-    } else {
+    wm[L.pix0 + (int64_t)y * W + x] = w;
+    lo = min(lo, w);
+    hi = max(hi, w);
+  }
+  for (int m = 32; m >= 1; m >>= 1) {
+    lo = min(lo, (int64_t)__shfl_xor(lo, m, kWave));
+    hi = max(hi, (int64_t)__shfl_xor(hi, m, kWave));
+  }
+  if (lane_id() == 0) {
+    sm.red[2 * (tid / kWave)] = lo;
+    sm.red[2 * (tid / kWave) + 1] = hi;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < kTPB / kWave; ++w) {
+      lo = min(lo, sm.red[2 * w]);
+      hi = max(hi, sm.red[2 * w + 1]);
+    }
+    part[2 * blockIdx.x] = lo;
+    part[2 * blockIdx.x + 1] = hi;
+  }
+}
+
+// Quantisation of one 64 x 16 tile's stored Wm with its frame's min/max
+// (lohi), four consecutive pixels of a row per thread: inv as bytes, and the
+// tile's histogram added to the frame's.
+__global__ __launch_bounds__(kTPB) void k_front_quant(ReqTable T, FrontTiles F, const int64_t* __restrict__ wm,
+                                                      const int64_t* __restrict__ lohi, uint8_t* __restrict__ inv,
+                                                      uint32_t* __restrict__ hist) {
+  static_assert(kTX * kTY == 4 * kTPB, "four pixels per thread");
+  __shared__ uint32_t sh[256];
+  const int tid = threadIdx.x;
+  const TileLoc L = locate_tile(T, F, blockIdx.x);
+  const int W = L.W;
+  sh[tid] = 0;
+  const int64_t flo = lohi[2 * L.g], fhi = lohi[2 * L.g + 1];
+  const double span = (double)(fhi - flo);
+  __syncthreads();
+  const int y = L.y0 + tid / (kTX / 4), x = L.x0 + 4 * (tid % (kTX / 4));
+  if (x < W) {  // W is a multiple of 8 pixels, so the four are all in the image or all past it
+    const int64_t pix = L.pix0 + (int64_t)y * W + x;
+    uint32_t packed = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t w = wm[pix + e];
       int q = 0;
       if (fhi > flo) {
         // floor(255 (w - lo) / (hi - lo)): a double quotient corrected to the exact floor
@@ -182,33 +213,13 @@ __global__ __launch_bounds__(kTPB) void k_front_var(ReqTable T, FrontTiles F, co
         q = (int)qq;
       }
       const int iv = 255 - q;
-      inv[L.pix0 + (int64_t)y * W + x] = (uint8_t)iv;
-      atomicAdd(&sm.hist[iv], 1u);
+      packed |= (uint32_t)iv << (8 * e);
+      atomicAdd(&sh[iv], 1u);
     }
+    *reinterpret_cast<uint32_t*>(inv + pix) = packed;
   }
-  if (MODE == 0) {
-    for (int m = 32; m >= 1; m >>= 1) {
-      lo = min(lo, (int64_t)__shfl_xor(lo, m, kWave));
-      hi = max(hi, (int64_t)__shfl_xor(hi, m, kWave));
-    }
-    if (lane_id() == 0) {
-      sm.red[2 * (tid / kWave)] = lo;
-      sm.red[2 * (tid / kWave) + 1] = hi;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      for (int w = 1; w < kTPB / kWave; ++w) {
-        lo = min(lo, sm.red[2 * w]);
-        hi = max(hi, sm.red[2 * w + 1]);
-      }
-      part[2 * blockIdx.x] = lo;
-      part[2 * blockIdx.x + 1] = hi;
-    }
-  } else {
-    __syncthreads();
-    for (int i = tid; i < 256; i += kTPB)
-      if (sm.hist[i] != 0) atomicAdd(&hist[256 * L.g + i], sm.hist[i]);
-  }
+  __syncthreads();
+  if (sh[tid] != 0) atomicAdd(&hist[256 * L.g + tid], sh[tid]);
 }
 
 // Per frame: min and max of Wm over its tiles; clears the frame's histogram.
@@ -390,7 +401,7 @@ size_t front_ws_bytes(const ReqTable& T, int G) {
   const int64_t pixels = 256 * T.tok_off[T.R];
   auto a256 = [](size_t b) { return (b + 255) & ~(size_t)255; };
   return a256((size_t)tiles * 16) + a256((size_t)G * 16) + a256((size_t)G * 1024) + a256((size_t)G * 4) +
-         a256((size_t)pixels);
+         a256((size_t)pixels) + a256((size_t)pixels * 8);
 }
 
 hipError_t launch_front(const ReqTable& T, int G, const uint8_t* rgb, const float* opacity, float tau,
@@ -407,10 +418,13 @@ hipError_t launch_front(const ReqTable& T, int G, const uint8_t* rgb, const floa
   base += a256((size_t)G * 1024);
   int32_t* thr = thr_out != nullptr ? thr_out : reinterpret_cast<int32_t*>(base);
   base += a256((size_t)G * 4);
+  const int64_t pixels = 256 * T.tok_off[T.R];
   uint8_t* inv = base;
-  k_front_var<0><<<tiles, kTPB, 0, s>>>(T, F, rgb, part, nullptr, nullptr, nullptr);
+  base += a256((size_t)pixels);
+  int64_t* wm = reinterpret_cast<int64_t*>(base);
+  k_front_var<<<tiles, kTPB, 0, s>>>(T, F, rgb, part, wm);
   k_front_minmax<<<G, kTPB, 0, s>>>(T, F, part, lohi, hist);
-  k_front_var<1><<<tiles, kTPB, 0, s>>>(T, F, rgb, nullptr, lohi, inv, hist);
+  k_front_quant<<<tiles, kTPB, 0, s>>>(T, F, wm, lohi, inv, hist);
   k_front_otsu<<<G, 256, 0, s>>>(hist, thr);
   const int64_t N = T.tok_off[T.R];
   k_front_pool<<<(unsigned)((N + 15) / 16), kTPB, 0, s>>>(T, opacity, tau, inv, thr, mask, u);
