@@ -135,6 +135,24 @@ def test_factorised_lane_parallel_temporal(D):
     check(wl, period=2)
 
 
+@pytest.mark.parametrize("case", ["one_request_d512", "two_requests_d128"])
+def test_factorised_max_frames(case):
+    """The frame limit of a factorised call (64 frames, which fill every lane
+    of the temporal kernels' member ballots): one request of 64 frames at
+    D 512 (lane-parallel temporal blocks), and two requests of 40 and 24
+    frames at D 128, without and with the latent cache, every frame starting
+    at t = 0.5."""
+    if case == "one_request_d512":
+        model = W.ModelCfg(D=512, heads=8, head_dim=64, mlp=1024, L=2, dtype="bf16", attention="factorised")
+        wl = W.custom("fact_64_frames", model, [W.Request(64, 8, 8)], [0.5], [0.4], [3])
+    else:
+        wl = W.custom("fact_40_24_frames", FACT_BF16, [W.Request(40, 6, 6), W.Request(24, 4, 8)], [0.5, 0.5],
+                      [0.3, 0.6], [3, 2])
+    assert wl.G == 64
+    check(wl)
+    check(wl, period=2)
+
+
 def test_factorised_headline_shape_two_blocks():
     """14 frames of 72x128 latent (9677 of 32256 tokens), D 1024, 16 heads of
     64: one spatial and one temporal block against the oracle."""

@@ -303,6 +303,21 @@ def test_multi_request_ragged_staggered():
     check_end_to_end(wl)
 
 
+def test_max_requests_end_to_end():
+    """The request limit of the ABI (64 requests in one call, the C header's
+    SPHINX_MAX_REQUESTS): ragged shapes of 1-3 frames and 2-12 latent rows and
+    columns, start times 0.2-0.9, selected fractions 0.1-0.9 and 1-4 steps,
+    end to end and teacher-forced per step."""
+    rng = np.random.default_rng(64)
+    R = 64
+    shapes = [W.Request(int(rng.integers(1, 4)), 2 * int(rng.integers(1, 7)), 2 * int(rng.integers(1, 7)))
+              for _ in range(R)]
+    wl = W.custom("max_requests", MID_BF16, shapes, [float(x) for x in rng.uniform(0.2, 0.9, R)],
+                  [float(x) for x in rng.uniform(0.1, 0.9, R)], [int(x) for x in rng.integers(1, 5, R)])
+    assert wl.R == 64
+    check_end_to_end(wl)
+
+
 def test_empty_mask_is_identity():
     wl = W.custom("empty", MID_BF16, [W.Request(2, 16, 16)], [0.3], [0.5], [3])
     wl.thr[:] = np.inf
