@@ -372,17 +372,18 @@ SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gelu, EPI_GELU, 192, 2)
 SPHINX_GEMM_DMA_KERNEL(k_gemm_dma192_gated, EPI_GATED, 192, 2)
 #undef SPHINX_GEMM_DMA_KERNEL
 
-// BM-row tiles (128, 192 or 256) with a ring of NS stages (4 x 32 KB, 4 x 40
-// KB or 3 x 48 KB of LDS, so one workgroup per CU), for launches whose tiles
-// all fit on the CUs at once.  A lone workgroup waits out the copy latency of
-// every K step when only the next stage is in flight; here NS - 1 are.  Eight
-// waves of 64x32, 96x32 or 128x32 (two per SIMD), so that each SIMD has a
-// second wave to issue while one waits.  Same results as the other tiles.
+// BM-row tiles (64, 128, 192 or 256) with a ring of NS stages (4 x 24 KB,
+// 4 x 32 KB, 4 x 40 KB or 3 x 48 KB of LDS, so one workgroup per CU), for
+// launches whose tiles all fit on the CUs at once.  A lone workgroup waits out
+// the copy latency of every K step when only the next stage is in flight; here
+// NS - 1 are.  Eight waves of 32x32, 64x32, 96x32 or 128x32 (two per SIMD), so
+// that each SIMD has a second wave to issue while one waits.  Same results as
+// the other tiles.
 template <int EPI, int NS, int BM = 128>
 __global__ __launch_bounds__(512, 1) void k_gemm_dma_deep(const bf16* __restrict__ A, const bf16* __restrict__ W,
                                                           const bf16* __restrict__ bias, int M, int N, int K,
                                                           GemmEpi e) {
-  constexpr int EH = BM == 128 ? 1 : 2;
+  constexpr int EH = BM <= 128 ? 1 : 2;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[DmaCfg<BM, 128, NS, EH, 8>::SMEM];
   int m0, n0;
   grid_tile<BM, 128>(M, N, m0, n0);
@@ -565,10 +566,12 @@ hipError_t launch_gemm(int epi, sphinx_dtype dt, const void* A, const void* W, c
       const int64_t t128 = nt * ((M + 127) / 128), t192 = nt * ((M + 191) / 192);
       // few tiles: the smallest row tile (128, 192 or 256 rows) whose tiles
       // all fit on the CUs at once, one per CU with a deeper ring (128, 160
-      // or 144 KB of LDS)
-      const int64_t cus = slots / 2, t256 = nt * ((M + 255) / 256);
+      // or 144 KB of LDS; 64-row tiles 96 KB)
+      const int64_t cus = slots / 2, t256 = nt * ((M + 255) / 256), t64 = nt * ((M + 63) / 64);
       if (t128 <= cus || t192 <= cus || t256 <= cus) {
-        if (t128 <= cus) launch_deep<4, 128>(epi, (int)t128, a, w, b, M, N, K, e, s);
+        // 64-row tiles where 128-row ones would leave more than half the CUs idle
+        if (t64 <= cus && 2 * t128 <= cus) launch_deep<4, 64>(epi, (int)t64, a, w, b, M, N, K, e, s);
+        else if (t128 <= cus) launch_deep<4, 128>(epi, (int)t128, a, w, b, M, N, K, e, s);
         else if (t192 <= cus) launch_deep<4, 192>(epi, (int)t192, a, w, b, M, N, K, e, s);
         else launch_deep<3, 256>(epi, (int)t256, a, w, b, M, N, K, e, s);
         return hipGetLastError();
